@@ -1,0 +1,247 @@
+"""Benchmark: one decode step of GrowPage's hot path at the Qwen3-8B layer shape.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
+
+A step is one pass of the whole path over the batch: restore the boundary
+requests' page metadata and summary slots to the step's starting state (small
+device-to-device copies), update both query summaries of every request, paged
+decode attention for every request, then boundary scoring and
+decide/select/compact for the requests at a capacity boundary.  Inputs are
+seeded synthetic tensors resident in HBM before timing starts.
+
+Prints one JSON line.  ``value`` is GB/s of the every-step traffic (summaries
+and decode attention, algorithmic bytes) over the whole step's time,
+boundary work included in the time but not in the bytes.  The ``roofline``
+object covers the dominant kernel (decode attention) timed with HIP events
+around each launch on its own stream; ``cpu_baseline`` times the CPU oracle
+on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU sample")
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "decode_traffic_qwen3_8b.json"))
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the path shards by request or by KV head, see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_03494_amd as gp
+    import workloads as W
+
+    gp.load()
+    dev = "cuda"
+    w = W.qwen3_8b()
+    R, Hq, Hkv, d, b = w.num_reqs, w.num_q_heads, w.num_kv_heads, w.head_dim, w.page_size
+    e = 2
+    dt = torch.bfloat16
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(dt).to(dev)
+
+    def i32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
+
+    shape = (w.pool_pages, Hkv, b, d)
+    k = torch.empty(shape, dtype=dt, device=dev)
+    v = torch.empty(shape, dtype=dt, device=dev)
+    ids = np.nonzero(w.page_row >= 0)[0]
+    idx = torch.from_numpy(ids.astype(np.int64)).to(dev)
+    k.index_copy_(0, idx, bf(w.k_data[w.page_row[ids]]))
+    v.index_copy_(0, idx, bf(w.v_data[w.page_row[ids]]))
+    kv = gp.KVLayer(k, v)
+    pristine = dict(page_table=i32(w.page_table), num_pages=i32(w.num_pages), seq_lens=i32(w.seq_lens),
+                    refcount=i32(w.refcount), free_list=i32(w.free_list), free_count=i32([w.free_count]))
+    ps = gp.PageState(**{n: t.clone() for n, t in pristine.items()})
+    qstate0 = torch.from_numpy(w.qstate).to(dev)
+    qstate = qstate0.clone()
+    slots, positions = i32(w.slot_ids), i32(w.positions)
+    q_pre, q_post = bf(w.q_pre), bf(w.q_post)
+    init = torch.zeros(R, dtype=torch.uint8, device=dev)
+    out = torch.empty_like(q_post)
+    bnd = i32(w.boundary)
+    Rb = int(bnd.shape[0])
+    max_cand = (w.max_pages - 1) * b
+    params = gp.Params(scale=float(np.float32(1 / math.sqrt(d))))
+    counts = torch.zeros((Rb, Hkv, 2), dtype=torch.int32, device=dev)
+    scores = torch.zeros((Rb, Hkv, max_cand), device=dev)
+    decisions = torch.zeros(Rb, dtype=torch.int32, device=dev)
+    delta = torch.zeros(Rb, device=dev)
+    counters = torch.zeros(4, dtype=torch.int64, device=dev)
+    ws_d = gp.workspace(gp.GP_OP_DECODE, R, 0, Hq, Hkv, d, w.max_pages, dt)
+    ws_s = gp.workspace(gp.GP_OP_SCORE, R, Rb, Hq, Hkv, d, w.max_pages, dt)
+    ws_a = gp.workspace(gp.GP_OP_APPLY, R, Rb, Hq, Hkv, d, w.max_pages, dt)
+    stream = torch.cuda.current_stream()
+
+    def restore():
+        for n, t in pristine.items():
+            getattr(ps, n).copy_(t, non_blocking=True)
+        qstate.copy_(qstate0, non_blocking=True)
+
+    ev = {}
+
+    def step(record: bool):
+        restore()
+        gp.gp_update_summaries(q_pre, slots, init, qstate, params.beta_s, params.beta_l)
+        if record:
+            ev["d0"].append(torch.cuda.Event(enable_timing=True))
+            ev["d0"][-1].record(stream)
+        gp.gp_decode_attention(kv, ps, q_post, params.scale, out, ws_d)
+        if record:
+            ev["d1"].append(torch.cuda.Event(enable_timing=True))
+            ev["d1"][-1].record(stream)
+        gp.gp_boundary_score(kv, ps, q_pre, qstate, slots, positions, bnd, params, counts, scores, ws_s)
+        gp.gp_boundary_apply([kv], ps, bnd, counts, scores, params, decisions, delta, counters, ws_a)
+        if record:
+            ev["b1"].append(torch.cuda.Event(enable_timing=True))
+            ev["b1"][-1].record(stream)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    counters.zero_()
+    ev = {"d0": [], "d1": [], "b1": []}
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(args.steps):
+        step(True)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    step_ms = t0.elapsed_time(t1) / args.steps
+    dec_ms = [a.elapsed_time(c) for a, c in zip(ev["d0"], ev["d1"])]
+    bnd_ms = [a.elapsed_time(c) for a, c in zip(ev["d1"], ev["b1"])]
+    decode_ms = float(np.mean(dec_ms))
+    boundary_ms = float(np.mean(bnd_ms))
+    split = counters.cpu().numpy().tolist()
+
+    # algorithmic bytes
+    m = w.seq_lens.astype(np.int64)
+    decode_bytes = int(m.sum()) * Hkv * d * e * 2 + int(w.num_pages.sum()) * 4 + 2 * R * Hq * d * e
+    summary_bytes = R * Hq * d * e + 2 * 2 * R * Hq * d * 4
+    step_bytes = decode_bytes + summary_bytes
+    gbs = step_bytes / (step_ms * 1e-3) / 1e9
+    dec_gbs = decode_bytes / (decode_ms * 1e-3) / 1e9
+
+    traffic = None
+    if os.path.exists(args.traffic_json):
+        with open(args.traffic_json) as f:
+            tj = json.load(f)
+        if tj.get("kernel_source_hash") == _kernel_hash():
+            traffic = tj.get("hbm_bytes_per_launch")
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(w, args.cpu_seconds)
+
+    line = {
+        "metric": "decode attn GB/s (% of HBM peak) + boundary events/s, Qwen3-8B layer shape",
+        "value": round(gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) K/V/q with 1% heavy keys; no model weights)",
+        "config": {"workload": "qwen3_8b_layer: 64 requests, 32 q / 8 kv heads, d 128, page 16, "
+                               "lengths U[1024,8192] under page budgets {64,128,256}, 4 at a boundary, "
+                               "200k free pages",
+                   "resident_tokens": int(m.sum()), "boundary_requests": Rb},
+        "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "decode_attention": {"ms": round(decode_ms, 4), "GB/s": round(dec_gbs, 1),
+                             "hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4), "bytes": decode_bytes},
+        "boundary": {"ms": round(boundary_ms, 4), "events_per_s": round(Rb / (boundary_ms * 1e-3), 1),
+                     "compress_grow_fallback_preempt": split},
+        "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def _kernel_hash() -> str:
+    import hashlib
+    p = os.path.join(ROOT, "paper_2609_03494_amd", "csrc", "gp_decode.hip")
+    with open(p, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def cpu_baseline(w, budget_s: float):
+    """The fp64 NumPy oracle on the host cores, single BLAS thread, over the
+    first requests of the same workload until the time budget is spent, plus
+    one boundary-event scoring pass.  Reported as decode GB/s-equivalent."""
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:           # pragma: no cover
+        threadpool_limits = None
+    import oracle as O
+
+    class View:
+        def __init__(self, data):
+            self.data = data
+
+        def __getitem__(self, pid):
+            return self.data[w.page_row[int(pid)]]
+
+    scale = 1.0 / math.sqrt(w.head_dim)
+    import contextlib
+    ctx = threadpool_limits(limits=1) if threadpool_limits else contextlib.nullcontext()
+    with ctx:
+        t_start = time.perf_counter()
+        done, nbytes = 0, 0
+        for r in range(w.num_reqs):
+            O.decode_attention(View(w.k_data), View(w.v_data), w.dtype, w.page_table, w.seq_lens,
+                               w.q_post, w.num_q_heads, scale, requests=[r])
+            done += 1
+            nbytes += int(w.seq_lens[r]) * w.num_kv_heads * w.head_dim * 2 * 2
+            if time.perf_counter() - t_start > budget_s:
+                break
+        t_dec = time.perf_counter() - t_start
+        r = int(w.boundary[0])
+        P = int(w.num_pages[r])
+        t1 = time.perf_counter()
+        toks = O.gather_tokens(View(w.k_data), w.page_table[r], P * 16, 16)
+        O.score_request(toks, w.dtype, P, 16, w.q_pre[r], w.qstate[w.slot_ids[r]], int(w.positions[r]),
+                        O.Params().as_f32(w.head_dim), scale)
+        t_evt = time.perf_counter() - t1
+    return {"value": round(nbytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"decode attention of the first {done} of {w.num_reqs} requests "
+                      f"({nbytes / 1e6:.0f} MB of K/V) in {t_dec:.1f} s; one boundary scoring pass "
+                      f"({P} pages) in {t_evt:.2f} s",
+            "boundary_score_s_per_event": round(t_evt, 3)}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,211 @@
+/*
+ * growpage.h -- C ABI of the GrowPage decode-step library for MI355X (gfx950).
+ *
+ * GrowPage ("On-Demand KV Budgeting for Efficient LLM Reasoning Serving",
+ * arXiv 2609.03494) decides, each time a request's last KV page fills, whether
+ * to compress its cache in place or to grow it by one page.  This library runs
+ * the per-decode-step path on one GPU:
+ *
+ *   gp_update_summaries  every step: the two EMA query summaries (Sec. 3.2)
+ *   gp_decode_attention  every step: paged GQA decode attention (Sec. 3.1)
+ *   gp_boundary_score    at boundaries: calibrated, rotated summaries scored
+ *                        against the cached keys, top-p working sets (Sec. 3.2,
+ *                        App. E.1) and token importance (Sec. 3.3)
+ *   gp_boundary_apply    at boundaries: demand trend, decision, page allocation,
+ *                        block-local + global selection and in-place compaction
+ *                        (Sec. 3.2, 3.3, 4.2, App. E.2)
+ *
+ * Conventions shared by every call
+ *  - Every data pointer is DEVICE memory owned by the caller.  Structs passed
+ *    by pointer (gp_kv_layer_t, gp_page_state_t, gp_params_t) live in HOST
+ *    memory and are read during the call only.
+ *  - The library allocates and frees nothing, never synchronises the stream
+ *    and keeps no global state: every call only enqueues kernels on `stream`
+ *    and returns.  Results are valid once the stream has reached them.
+ *  - Host-side validation returns a status without launching anything.  A
+ *    launch failure returns GP_ERR_HIP.  Device-side state that breaks the
+ *    layout contract (page ids out of range, seq_len above the pages held) is
+ *    never read out of bounds but gives unspecified results.
+ *  - Workspaces (`ws`) are caller-owned device buffers of at least
+ *    gp_workspace_bytes() bytes, one per operation.  A workspace must be
+ *    zero-filled once after allocation; every call leaves its counters at
+ *    zero on completion, so it can be reused without clearing.  Two calls
+ *    that run concurrently must not share a workspace.
+ *  - Page size b is 16 tokens; head_dim is 64 or 128; num_q_heads is 1, 2, 4
+ *    or 8 times num_kv_heads.  Other shapes return GP_ERR_UNSUPPORTED.
+ *
+ * Layout
+ *  K and V pools     [pool_pages][num_kv_heads][page_size][head_dim], float32
+ *                    or bfloat16; token i of a request lives in page
+ *                    page_table[r][i / page_size], slot i % page_size.
+ *  page_table        [num_reqs][max_pages] int32 physical page ids.
+ *  num_pages, seq_lens  [num_reqs] int32: pages held P_r and resident tokens
+ *                    m_r (m_r <= P_r * page_size).  A request is at a capacity
+ *                    boundary when m_r == P_r * page_size (Sec. 3.3).
+ *  refcount          [pool_pages] int32 references from page tables (pages
+ *                    shared by a common prefix have refcount > 1, App. E.2).
+ *  free_list, free_count  stack of free page ids; the top is
+ *                    free_list[*free_count - 1].
+ *  qstate            [num_slots][2][num_q_heads][head_dim] float32 summary
+ *                    pool (view 0 = short-timescale S, 1 = long-timescale L),
+ *                    the per-layer slice of the paper's query-state pool
+ *                    (App. E.1, query-cache layout).
+ *  q_pre, q_post     [num_reqs][num_q_heads][head_dim] in the KV dtype: the
+ *                    current query before and after RoPE.
+ */
+#ifndef GROWPAGE_H
+#define GROWPAGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    GP_OK = 0,
+    GP_ERR_INVALID = 1,      /* null pointer, negative size, inconsistent shapes */
+    GP_ERR_UNSUPPORTED = 2,  /* page size, head_dim or GQA ratio not built       */
+    GP_ERR_WORKSPACE = 3,    /* ws_bytes below gp_workspace_bytes()              */
+    GP_ERR_HIP = 4           /* a kernel launch failed                           */
+} gp_status_t;
+
+typedef enum { GP_F32 = 0, GP_BF16 = 1 } gp_dtype_t;
+
+/* Per-request decisions written by gp_boundary_apply (Sec. 3.3, 4.2). */
+enum {
+    GP_COMPRESS = 0,      /* Compress & Hold: one page of tokens evicted in place  */
+    GP_GROW = 1,          /* Grow by One Page: a free page appended to the table   */
+    GP_FALLBACK = 2,      /* wanted to grow, no page could be granted: compressed  */
+    GP_PREEMPT = 3,       /* neither possible; state untouched (scheduler decides) */
+    GP_NOT_BOUNDARY = 4   /* m_r != P_r * page_size; state untouched               */
+};
+
+/* Which workspace gp_workspace_bytes() sizes. */
+enum { GP_OP_DECODE = 0, GP_OP_SCORE = 1, GP_OP_APPLY = 2 };
+
+typedef struct {
+    void *k;                 /* [pool_pages][num_kv_heads][page_size][head_dim] */
+    void *v;                 /* same layout as k                                */
+    int32_t pool_pages;
+    int32_t num_kv_heads;
+    int32_t page_size;       /* must be 16                                      */
+    int32_t head_dim;        /* 64 or 128                                       */
+    gp_dtype_t dtype;
+} gp_kv_layer_t;
+
+typedef struct {
+    int32_t *page_table;     /* [num_reqs][max_pages]                           */
+    int32_t *num_pages;      /* [num_reqs] P_r                                  */
+    int32_t *seq_lens;       /* [num_reqs] m_r                                  */
+    int32_t *refcount;       /* [pool_pages]                                    */
+    int32_t *free_list;      /* [pool_pages] stack                              */
+    int32_t *free_count;     /* [1] stack height                                */
+    int32_t num_reqs;
+    int32_t max_pages;
+    int32_t pool_pages;
+} gp_page_state_t;
+
+/* Method constants.  Paper defaults: beta_s 0.9, beta_l 0.999 (Sec. 3.2),
+ * p 0.99 (Sec. 3.2), tau 0 (Sec. 3.2), k_loc a quarter of a block (App. D.2
+ * uses 64 of 256; 4 of 16 here), scale 1/sqrt(head_dim), rope_theta 1e6
+ * (half-split rotary pairs, as in Qwen3).  reserve_pages: a grow is granted
+ * only while more than this many pages are free (Sec. 4.2, "safely"). */
+typedef struct {
+    float beta_s, beta_l;
+    float p;
+    float tau;
+    float scale;
+    float rope_theta;
+    int32_t k_loc;
+    int32_t reserve_pages;
+} gp_params_t;
+
+/* Dual-timescale summaries (Sec. 3.2, EMA equation; App. E.1).
+ * For each request r with slot s = slot_ids[r]: if init[r] != 0 both views of
+ * slot s become q_pre[r] (a new owner overwrites whatever the slot held);
+ * otherwise qbar_x <- beta_x * qbar_x + (1 - beta_x) * q_pre[r] for x in {S, L}.
+ * Arithmetic is fp64, rounded once to float32.  Requests with a slot outside
+ * [0, num_slots) are skipped.  q_pre: [num_reqs][num_q_heads][head_dim] in
+ * `dtype`; slot_ids [num_reqs] int32; init [num_reqs] uint8; qstate updated
+ * in place.  Slots must be distinct across requests. */
+gp_status_t gp_update_summaries(const void *q_pre, gp_dtype_t dtype, int32_t num_reqs,
+                                int32_t num_q_heads, int32_t head_dim,
+                                const int32_t *slot_ids, const uint8_t *init,
+                                float *qstate, int32_t num_slots,
+                                float beta_s, float beta_l, hipStream_t stream);
+
+/* Paged decode attention (Sec. 3.1, attention-output equation):
+ * out[r][g] = sum_{i < m_r} softmax_i(scale * q_post[r][g] . k_i) v_i, with
+ * k_i, v_i read from KV head g / (num_q_heads / num_kv_heads) through the page
+ * table.  fp32 accumulation; output in the KV dtype.  A request with m_r == 0
+ * gets a zero output.  Page slots at or beyond m_r are never used, whatever
+ * they hold.  out: [num_reqs][num_q_heads][head_dim]. */
+gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
+                                const void *q_post, int32_t num_q_heads, float scale,
+                                void *out, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Boundary scoring of one layer (Sec. 3.2 and 3.3; App. E.1).
+ * For boundary request i (r = bnd[i], at a boundary, P = num_pages[r]):
+ * candidates are slots [0, (P-1) * page_size) (the most recent page is left
+ * out).  Each summary x of each query head is scaled to the RMS of q_pre[r]
+ * (RMS calibration), rotated at positions[r], and its softmax over the
+ * candidates' keys is taken; the G query heads of a KV head are averaged.
+ * Outputs, per KV head h:
+ *   k_counts[i][h][x]  top-p working-set size K^x (min k whose k largest
+ *                      weights reach p), x = 0 (S), 1 (L);
+ *   scores[i][h][c]    s_c = max(a^S_c, a^L_c) for c < (P-1) * page_size.
+ * Weights are computed in fp64 and rounded to float32; K^x is decided on the
+ * float32 weights.  Requests not at a boundary get k_counts 0.  Requires
+ * max_cand >= (max_pages - 1) * page_size.  bnd [num_bnd] int32, positions
+ * [num_reqs] int32 (logical index of the current token). */
+gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
+                              const void *q_pre, const float *qstate, int32_t num_slots,
+                              const int32_t *slot_ids, const int32_t *positions,
+                              const int32_t *bnd, int32_t num_bnd, int32_t num_q_heads,
+                              const gp_params_t *params, int32_t *k_counts, float *scores,
+                              int32_t max_cand, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Decision, allocation, selection and compaction for the boundary requests,
+ * over n_layers layers (layers[l], k_counts[l][num_bnd][Hkv][2] and
+ * scores[l][num_bnd][Hkv][max_cand] from gp_boundary_score).
+ *  - Delta = r^S - r^L, the mean over (layer, KV head) of K^x / |C|
+ *    (Sec. 3.2, aggregation equation), evaluated from the integer counts;
+ *    Grow iff Delta > tau.  delta[i] receives Delta as float32.
+ *  - Requests are served in list order.  A grow pops the free-page stack
+ *    (refcount 1, appended at index P); if no page can be granted (stack at or
+ *    below reserve_pages, or the table row full) the request compresses
+ *    (GP_FALLBACK).  P <= 1 cannot compress: grow or GP_PREEMPT.
+ *  - Compress keeps P and sets m = (P-1) * page_size.  Per layer and KV head,
+ *    exactly page_size candidates are evicted: each candidate page keeps its
+ *    min(k_loc, K_t / (P-1)) best tokens, K_t = (P-2) * page_size, and the
+ *    rest of K_t goes to the best remaining candidates (order: score
+ *    descending, slot ascending).  Kept tokens stay in order, followed by the
+ *    protected last page (Sec. 3.3, selection equation).
+ *  - Shared pages (refcount > 1) are never written: a compressing request
+ *    first pops one private page per shared page (GP_PREEMPT if too few), its
+ *    compacted tokens go there, and the shared page loses one reference
+ *    (App. E.2).  Pages whose count reaches zero are pushed on the stack at
+ *    the end of the call, in (boundary index, logical page) order.
+ *  - counters[4] (int64) += number of COMPRESS, GROW, FALLBACK, PREEMPT. */
+gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers,
+                              const gp_page_state_t *ps, const int32_t *bnd, int32_t num_bnd,
+                              const int32_t *k_counts, const float *scores, int32_t max_cand,
+                              const gp_params_t *params, int32_t *decisions, float *delta,
+                              int64_t *counters, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Bytes of workspace an operation needs (op = GP_OP_DECODE / SCORE / APPLY). */
+size_t gp_workspace_bytes(int32_t op, int32_t num_reqs, int32_t num_bnd, int32_t num_q_heads,
+                          int32_t num_kv_heads, int32_t head_dim, int32_t max_pages,
+                          int32_t page_size, gp_dtype_t dtype, int32_t n_layers);
+
+/* Static description of a status code. */
+const char *gp_status_string(gp_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GROWPAGE_H */

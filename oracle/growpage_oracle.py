@@ -346,14 +346,17 @@ def decide_and_allocate(state: PageState, bnd, counts, b: int, params: Params):
     readings: requests earlier in the list win scarce pages; "safely" granted
     means more than ``reserve_pages`` pages are free and the block table has
     room; a request with P <= 1 cannot compress, so it grows if it can and is
-    preempted otherwise; pages whose count reaches zero are pushed back onto
-    the stack after every pop of the call, in (request, logical page) order.
+    preempted otherwise; a page counts as shared if its reference count exceeds
+    one when the call starts; references are dropped after every pop of the
+    call and pages whose count reaches zero are pushed back onto the stack in
+    ascending page-id order.
 
     Mutates ``state``; returns (decisions [Rb] int, delta [Rb] float32)."""
     Rb = len(bnd)
     dec = np.zeros(Rb, dtype=np.int64)
     delta = np.zeros(Rb, dtype=np.float32)
-    released = []
+    ref_at_start = state.refcount.copy()
+    dropped = []
     max_pages = state.page_table.shape[1]
     tau = Fraction(float(params.tau)) if np.isfinite(params.tau) else None
     for i in range(Rb):
@@ -385,22 +388,21 @@ def decide_and_allocate(state: PageState, bnd, counts, b: int, params: Params):
         if P <= 1:
             dec[i] = PREEMPT
             continue
-        shared = [j for j in range(P) if state.refcount[state.page_table[r, j]] > 1]
+        shared = [j for j in range(P) if ref_at_start[state.page_table[r, j]] > 1]
         if len(shared) > state.free_count:
             dec[i] = PREEMPT
             continue
         for j in shared:
             pid = int(state.free_list[state.free_count - 1])
             state.free_count -= 1
-            old = int(state.page_table[r, j])
+            dropped.append(int(state.page_table[r, j]))
             state.page_table[r, j] = pid
             state.refcount[pid] = 1
-            state.refcount[old] -= 1
-            if state.refcount[old] == 0:
-                released.append(old)
         state.seq_lens[r] = (P - 1) * b
         dec[i] = FALLBACK if want_grow else COMPRESS
-    for pid in released:
+    for old in dropped:
+        state.refcount[old] -= 1
+    for pid in sorted({old for old in dropped if state.refcount[old] == 0}):
         state.free_list[state.free_count] = pid
         state.free_count += 1
     return dec, delta
@@ -477,20 +479,29 @@ def boundary_step(layers, dtype, state: PageState, q_pre, qstate, slot_ids, posi
     s_layers = list(qstate) if isinstance(qstate, (list, tuple)) else [qstate] * n_layers
     d = layers[0][0].shape[-1]
     scale = params.scale if params.scale is not None else 1.0 / np.sqrt(d)
-    counts_all, scores_all = [], []
+    counts_all, scores_all, weights_all = [], [], []
     for i, r in enumerate(bnd):
         r = int(r)
         P = int(state.num_pages[r])
-        per_layer_c, per_layer_s = [], []
+        per_layer_c, per_layer_s, per_layer_w = [], [], []
+        at_boundary = int(state.seq_lens[r]) == P * b
         for ell, (kp, vp) in enumerate(layers):
-            toks = gather_tokens(kp, state.page_table[r], P * b, b)
-            c, s, _ = score_request(toks, dtype, P, b, q_layers[ell][r],
-                                    s_layers[ell][int(slot_ids[r])], int(positions[r]),
-                                    params, scale)
+            if at_boundary and P >= 2:
+                toks = gather_tokens(kp, state.page_table[r], P * b, b)
+                c, s, a32 = score_request(toks, dtype, P, b, q_layers[ell][r],
+                                          s_layers[ell][int(slot_ids[r])], int(positions[r]),
+                                          params, scale)
+            else:
+                Hkv = kp.shape[1]
+                c = np.zeros((Hkv, 2), np.int64)
+                s = np.zeros((Hkv, 0), np.float32)
+                a32 = np.zeros((2, Hkv, 0), np.float32)
             per_layer_c.append(c)
             per_layer_s.append(s)
+            per_layer_w.append(a32)
         counts_all.append(np.stack(per_layer_c))
         scores_all.append(per_layer_s)
+        weights_all.append(per_layer_w)
     old_tables = {int(r): state.page_table[int(r)].copy() for r in bnd}
     dec, delta = decide_and_allocate(state, bnd, counts_all, b, params)
     kept_all = {}
@@ -516,4 +527,4 @@ def boundary_step(layers, dtype, state: PageState, q_pre, qstate, slot_ids, posi
         if code < 4:
             counters[code] += 1
     return dict(decisions=dec, delta=delta, counts=counts_all, scores=scores_all,
-                kept=kept_all, counters=counters)
+                weights=weights_all, kept=kept_all, counters=counters)

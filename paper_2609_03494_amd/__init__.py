@@ -1,0 +1,15 @@
+"""GrowPage decode-step hot path on MI355X: a C-ABI HIP library and its binding.
+
+The library (``libgrowpage.so``, header ``include/growpage.h``) runs paged GQA
+decode attention, the dual-timescale query summaries, and the capacity-boundary
+scoring / compress-vs-grow decision / selection / compaction of GrowPage
+(arXiv 2609.03494) as hand-written gfx950 kernels.  PyTorch supplies device
+memory and streams.
+"""
+from ._lib import (  # noqa: F401
+    EXPORTS, GP_BF16, GP_COMPRESS, GP_F32, GP_FALLBACK, GP_GROW, GP_NOT_BOUNDARY,
+    GP_OP_APPLY, GP_OP_DECODE, GP_OP_SCORE, GP_PREEMPT, LIB_PATH, PAGE_SIZE,
+    GrowPageError, KVLayer, PageState, Params, gp_boundary_apply, gp_boundary_score,
+    gp_decode_attention, gp_update_summaries, gp_workspace_bytes, load, status_string,
+    workspace,
+)

@@ -1,0 +1,221 @@
+"""ctypes binding of libgrowpage.so (include/growpage.h).
+
+Argument marshalling only: tensors become device pointers, the current torch
+stream becomes the HIP stream, and a non-zero status becomes GrowPageError.
+Every step of the computation runs in the library's HIP kernels.  If the
+library has not been built, importing a function raises instead of falling
+back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgrowpage.so")
+
+GP_F32, GP_BF16 = 0, 1
+GP_OP_DECODE, GP_OP_SCORE, GP_OP_APPLY = 0, 1, 2
+GP_COMPRESS, GP_GROW, GP_FALLBACK, GP_PREEMPT, GP_NOT_BOUNDARY = 0, 1, 2, 3, 4
+PAGE_SIZE = 16
+
+EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_boundary_score",
+           "gp_boundary_apply", "gp_workspace_bytes", "gp_status_string")
+
+
+class GrowPageError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: status {status} ({status_string(status)})")
+        self.status = status
+
+
+class _KVLayer(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("pool_pages", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int)]
+
+
+class _PageState(ctypes.Structure):
+    _fields_ = [("page_table", ctypes.c_void_p), ("num_pages", ctypes.c_void_p),
+                ("seq_lens", ctypes.c_void_p), ("refcount", ctypes.c_void_p),
+                ("free_list", ctypes.c_void_p), ("free_count", ctypes.c_void_p),
+                ("num_reqs", ctypes.c_int32), ("max_pages", ctypes.c_int32),
+                ("pool_pages", ctypes.c_int32)]
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("beta_s", ctypes.c_float), ("beta_l", ctypes.c_float), ("p", ctypes.c_float),
+                ("tau", ctypes.c_float), ("scale", ctypes.c_float), ("rope_theta", ctypes.c_float),
+                ("k_loc", ctypes.c_int32), ("reserve_pages", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load the built library (raises if it is missing)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_03494_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+    lib.gp_status_string.restype = ctypes.c_char_p
+    lib.gp_status_string.argtypes = [ctypes.c_int]
+    lib.gp_workspace_bytes.restype = sz
+    lib.gp_workspace_bytes.argtypes = [i32] * 8 + [ctypes.c_int, i32]
+    lib.gp_update_summaries.restype = ctypes.c_int
+    lib.gp_update_summaries.argtypes = [vp, ctypes.c_int, i32, i32, i32, vp, vp, vp, i32, f32, f32, vp]
+    lib.gp_decode_attention.restype = ctypes.c_int
+    lib.gp_decode_attention.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, i32,
+                                        f32, vp, vp, sz, vp]
+    lib.gp_boundary_score.restype = ctypes.c_int
+    lib.gp_boundary_score.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, vp, i32,
+                                      vp, vp, vp, i32, i32, ctypes.POINTER(_Params), vp, vp, i32, vp,
+                                      sz, vp]
+    lib.gp_boundary_apply.restype = ctypes.c_int
+    lib.gp_boundary_apply.argtypes = [ctypes.POINTER(_KVLayer), i32, ctypes.POINTER(_PageState), vp, i32,
+                                      vp, vp, i32, ctypes.POINTER(_Params), vp, vp, vp, vp, sz, vp]
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().gp_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        raise GrowPageError(status, where)
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the library must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return GP_F32
+    if t.dtype == torch.bfloat16:
+        return GP_BF16
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+@dataclass
+class KVLayer:
+    """K and V pools [pool_pages, num_kv_heads, 16, head_dim] (float32 or bfloat16)."""
+    k: torch.Tensor
+    v: torch.Tensor
+
+    def c(self) -> _KVLayer:
+        pool, hkv, b, d = self.k.shape
+        return _KVLayer(_ptr(self.k), _ptr(self.v), pool, hkv, b, d, _dtype_code(self.k))
+
+
+@dataclass
+class PageState:
+    """Device page state (int32 tensors).  free_count is a one-element tensor."""
+    page_table: torch.Tensor   # [R, max_pages]
+    num_pages: torch.Tensor    # [R]
+    seq_lens: torch.Tensor     # [R]
+    refcount: torch.Tensor     # [pool_pages]
+    free_list: torch.Tensor    # [pool_pages]
+    free_count: torch.Tensor   # [1]
+
+    def c(self) -> _PageState:
+        R, maxp = self.page_table.shape
+        return _PageState(_ptr(self.page_table), _ptr(self.num_pages), _ptr(self.seq_lens),
+                          _ptr(self.refcount), _ptr(self.free_list), _ptr(self.free_count),
+                          R, maxp, self.refcount.shape[0])
+
+
+@dataclass
+class Params:
+    beta_s: float = 0.9
+    beta_l: float = 0.999
+    p: float = 0.99
+    tau: float = 0.0
+    scale: float = 1.0 / 128 ** 0.5
+    rope_theta: float = 1.0e6
+    k_loc: int = 4
+    reserve_pages: int = 0
+
+    def c(self) -> _Params:
+        return _Params(self.beta_s, self.beta_l, self.p, self.tau, self.scale, self.rope_theta,
+                       self.k_loc, self.reserve_pages)
+
+
+def gp_workspace_bytes(op: int, num_reqs: int, num_bnd: int, num_q_heads: int, num_kv_heads: int,
+                       head_dim: int, max_pages: int, dtype: torch.dtype, n_layers: int = 1) -> int:
+    code = GP_F32 if dtype == torch.float32 else GP_BF16
+    n = load().gp_workspace_bytes(op, num_reqs, num_bnd, num_q_heads, num_kv_heads, head_dim,
+                                  max_pages, PAGE_SIZE, code, n_layers)
+    if n == 0:
+        raise GrowPageError(2, "gp_workspace_bytes")
+    return int(n)
+
+
+def workspace(op: int, num_reqs: int, num_bnd: int, num_q_heads: int, num_kv_heads: int,
+              head_dim: int, max_pages: int, dtype: torch.dtype, n_layers: int = 1,
+              device="cuda") -> torch.Tensor:
+    """A zero-filled workspace of the size the library asks for."""
+    n = gp_workspace_bytes(op, num_reqs, num_bnd, num_q_heads, num_kv_heads, head_dim, max_pages,
+                           dtype, n_layers)
+    return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def gp_update_summaries(q_pre: torch.Tensor, slot_ids: torch.Tensor, init: torch.Tensor,
+                        qstate: torch.Tensor, beta_s: float, beta_l: float, stream=None) -> None:
+    R, Hq, d = q_pre.shape
+    st = load().gp_update_summaries(_ptr(q_pre), _dtype_code(q_pre), R, Hq, d, _ptr(slot_ids),
+                                    _ptr(init), _ptr(qstate), qstate.shape[0], beta_s, beta_l,
+                                    _stream(stream))
+    _check(st, "gp_update_summaries")
+
+
+def gp_decode_attention(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale: float,
+                        out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
+    c_kv, c_ps = kv.c(), ps.c()
+    st = load().gp_decode_attention(ctypes.byref(c_kv), ctypes.byref(c_ps), _ptr(q_post),
+                                    q_post.shape[1], scale, _ptr(out), _ptr(ws), ws.numel(),
+                                    _stream(stream))
+    _check(st, "gp_decode_attention")
+
+
+def gp_boundary_score(kv: KVLayer, ps: PageState, q_pre: torch.Tensor, qstate: torch.Tensor,
+                      slot_ids: torch.Tensor, positions: torch.Tensor, bnd: torch.Tensor,
+                      params: Params, k_counts: torch.Tensor, scores: torch.Tensor,
+                      ws: torch.Tensor, stream=None) -> None:
+    c_kv, c_ps, c_p = kv.c(), ps.c(), params.c()
+    st = load().gp_boundary_score(ctypes.byref(c_kv), ctypes.byref(c_ps), _ptr(q_pre), _ptr(qstate),
+                                  qstate.shape[0], _ptr(slot_ids), _ptr(positions), _ptr(bnd),
+                                  bnd.shape[0], q_pre.shape[1], ctypes.byref(c_p), _ptr(k_counts),
+                                  _ptr(scores), scores.shape[-1], _ptr(ws), ws.numel(),
+                                  _stream(stream))
+    _check(st, "gp_boundary_score")
+
+
+def gp_boundary_apply(layers: list[KVLayer], ps: PageState, bnd: torch.Tensor,
+                      k_counts: torch.Tensor, scores: torch.Tensor, params: Params,
+                      decisions: torch.Tensor, delta: torch.Tensor, counters: torch.Tensor,
+                      ws: torch.Tensor, stream=None) -> None:
+    arr = (_KVLayer * len(layers))(*[layer.c() for layer in layers])
+    c_ps, c_p = ps.c(), params.c()
+    st = load().gp_boundary_apply(arr, len(layers), ctypes.byref(c_ps), _ptr(bnd), bnd.shape[0],
+                                  _ptr(k_counts), _ptr(scores), scores.shape[-1], ctypes.byref(c_p),
+                                  _ptr(decisions), _ptr(delta), _ptr(counters), _ptr(ws),
+                                  ws.numel(), _stream(stream))
+    _check(st, "gp_boundary_apply")

@@ -1,0 +1,242 @@
+// Host side of the C ABI: argument validation, workspace carving and launch.
+// Every entry point checks what the host can see (pointers, shapes, sizes),
+// then enqueues its kernels on the caller's stream and returns.
+#include <math.h>
+
+#include "gp_internal.h"
+
+using namespace gp;
+
+namespace {
+
+bool dims_ok(int Hq, int Hkv, int D) {
+    if (Hkv <= 0 || Hq <= 0 || Hq % Hkv) return false;
+    const int G = Hq / Hkv;
+    return (D == 64 || D == 128) && (G == 1 || G == 2 || G == 4 || G == 8);
+}
+
+gp_status_t check_layer(const gp_kv_layer_t *kv) {
+    if (!kv || !kv->k || !kv->v) return GP_ERR_INVALID;
+    if (kv->pool_pages <= 0 || kv->num_kv_heads <= 0) return GP_ERR_INVALID;
+    if (kv->dtype != GP_F32 && kv->dtype != GP_BF16) return GP_ERR_INVALID;
+    if (kv->page_size != kPage) return GP_ERR_UNSUPPORTED;
+    if (kv->head_dim != 64 && kv->head_dim != 128) return GP_ERR_UNSUPPORTED;
+    return GP_OK;
+}
+
+gp_status_t check_state(const gp_page_state_t *ps, const gp_kv_layer_t *kv) {
+    if (!ps || !ps->page_table || !ps->num_pages || !ps->seq_lens) return GP_ERR_INVALID;
+    if (ps->num_reqs < 0 || ps->max_pages <= 0) return GP_ERR_INVALID;
+    if (kv && ps->pool_pages != kv->pool_pages) return GP_ERR_INVALID;
+    return GP_OK;
+}
+
+gp_status_t from_hip(hipError_t e) { return e == hipSuccess ? GP_OK : GP_ERR_HIP; }
+
+int elem_bytes(gp_dtype_t dt) { return dt == GP_F32 ? 4 : 2; }
+
+}  // namespace
+
+extern "C" {
+
+const char *gp_status_string(gp_status_t s) {
+    switch (s) {
+        case GP_OK: return "ok";
+        case GP_ERR_INVALID: return "invalid argument";
+        case GP_ERR_UNSUPPORTED: return "unsupported shape (page size 16, head_dim 64/128, GQA ratio 1/2/4/8)";
+        case GP_ERR_WORKSPACE: return "workspace too small";
+        case GP_ERR_HIP: return "HIP launch failed";
+    }
+    return "unknown status";
+}
+
+size_t gp_workspace_bytes(int32_t op, int32_t num_reqs, int32_t num_bnd, int32_t num_q_heads,
+                          int32_t num_kv_heads, int32_t head_dim, int32_t max_pages,
+                          int32_t page_size, gp_dtype_t dtype, int32_t n_layers) {
+    if (page_size != kPage || !dims_ok(num_q_heads, num_kv_heads, head_dim) || max_pages <= 0 ||
+        num_reqs < 0 || num_bnd < 0 || n_layers <= 0)
+        return 0;
+    switch (op) {
+        case GP_OP_DECODE:
+            return decode_ws(num_reqs, num_q_heads, num_kv_heads, head_dim, max_pages).total;
+        case GP_OP_SCORE: return score_ws(num_bnd, num_q_heads, num_kv_heads, max_pages).total;
+        case GP_OP_APPLY:
+            return apply_ws(num_bnd, num_kv_heads, head_dim, elem_bytes(dtype), max_pages, n_layers).total;
+    }
+    return 0;
+}
+
+gp_status_t gp_update_summaries(const void *q_pre, gp_dtype_t dtype, int32_t num_reqs,
+                                int32_t num_q_heads, int32_t head_dim, const int32_t *slot_ids,
+                                const uint8_t *init, float *qstate, int32_t num_slots, float beta_s,
+                                float beta_l, hipStream_t stream) {
+    if (num_reqs < 0 || num_q_heads <= 0 || head_dim <= 0 || num_slots <= 0) return GP_ERR_INVALID;
+    if (dtype != GP_F32 && dtype != GP_BF16) return GP_ERR_INVALID;
+    if (num_reqs == 0) return GP_OK;
+    if (!q_pre || !slot_ids || !init || !qstate) return GP_ERR_INVALID;
+    if (!(beta_s >= 0.0f && beta_s <= 1.0f && beta_l >= 0.0f && beta_l <= 1.0f)) return GP_ERR_INVALID;
+    SummaryArgs a;
+    a.q = q_pre;
+    a.slot_ids = slot_ids;
+    a.init = init;
+    a.qstate = qstate;
+    a.R = num_reqs;
+    a.HqD = num_q_heads * head_dim;
+    a.M = num_slots;
+    a.beta_s = beta_s;
+    a.beta_l = beta_l;
+    return from_hip(launch_summaries(dtype, a, stream));
+}
+
+gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
+                                int32_t num_q_heads, float scale, void *out, void *ws, size_t ws_bytes,
+                                hipStream_t stream) {
+    gp_status_t st = check_layer(kv);
+    if (st != GP_OK) return st;
+    if ((st = check_state(ps, kv)) != GP_OK) return st;
+    if (!dims_ok(num_q_heads, kv->num_kv_heads, kv->head_dim)) return GP_ERR_UNSUPPORTED;
+    if (!(scale > 0.0f) || !isfinite(scale)) return GP_ERR_INVALID;
+    if (ps->num_reqs == 0) return GP_OK;
+    if (!q_post || !out || !ws) return GP_ERR_INVALID;
+    const DecodeWs w = decode_ws(ps->num_reqs, num_q_heads, kv->num_kv_heads, kv->head_dim, ps->max_pages);
+    if (ws_bytes < w.total) return GP_ERR_WORKSPACE;
+    if (ps->num_reqs > 65535) return GP_ERR_UNSUPPORTED;
+    DecodeArgs a;
+    a.k = kv->k;
+    a.v = kv->v;
+    a.page_table = ps->page_table;
+    a.num_pages = ps->num_pages;
+    a.seq_lens = ps->seq_lens;
+    a.q = q_post;
+    a.out = out;
+    a.partial = reinterpret_cast<float *>(static_cast<unsigned char *>(ws) + w.partial);
+    a.counters = reinterpret_cast<uint32_t *>(static_cast<unsigned char *>(ws) + w.counters);
+    a.R = ps->num_reqs;
+    a.Hkv = kv->num_kv_heads;
+    a.max_pages = ps->max_pages;
+    a.pool_pages = kv->pool_pages;
+    a.max_chunks = w.max_chunks;
+    a.qscale = scale * 1.4426950408889634f;
+    return from_hip(launch_decode(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stream));
+}
+
+gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_pre,
+                              const float *qstate, int32_t num_slots, const int32_t *slot_ids,
+                              const int32_t *positions, const int32_t *bnd, int32_t num_bnd,
+                              int32_t num_q_heads, const gp_params_t *params, int32_t *k_counts,
+                              float *scores, int32_t max_cand, void *ws, size_t ws_bytes,
+                              hipStream_t stream) {
+    gp_status_t st = check_layer(kv);
+    if (st != GP_OK) return st;
+    if ((st = check_state(ps, kv)) != GP_OK) return st;
+    if (!dims_ok(num_q_heads, kv->num_kv_heads, kv->head_dim)) return GP_ERR_UNSUPPORTED;
+    if (!params || num_bnd < 0 || num_slots <= 0) return GP_ERR_INVALID;
+    if (num_bnd == 0) return GP_OK;
+    if (!q_pre || !qstate || !slot_ids || !positions || !bnd || !k_counts || !scores || !ws)
+        return GP_ERR_INVALID;
+    if (max_cand < (ps->max_pages - 1) * kPage) return GP_ERR_INVALID;
+    if (!(params->p > 0.0f && params->p <= 1.0f) || !(params->scale > 0.0f) ||
+        !(params->rope_theta > 0.0f))
+        return GP_ERR_INVALID;
+    if (num_bnd > 65535) return GP_ERR_UNSUPPORTED;
+    const ScoreWs w = score_ws(num_bnd, num_q_heads, kv->num_kv_heads, ps->max_pages);
+    if (ws_bytes < w.total) return GP_ERR_WORKSPACE;
+    ScoreArgs a;
+    unsigned char *base = static_cast<unsigned char *>(ws);
+    a.k = kv->k;
+    a.page_table = ps->page_table;
+    a.num_pages = ps->num_pages;
+    a.seq_lens = ps->seq_lens;
+    a.q_pre = q_pre;
+    a.qstate = qstate;
+    a.slot_ids = slot_ids;
+    a.positions = positions;
+    a.bnd = bnd;
+    a.k_counts = k_counts;
+    a.scores = scores;
+    a.logits = reinterpret_cast<double *>(base + w.logits);
+    a.part = reinterpret_cast<double *>(base + w.part);
+    a.weights = reinterpret_cast<float *>(base + w.weights);
+    a.Rb = num_bnd;
+    a.Hq = num_q_heads;
+    a.Hkv = kv->num_kv_heads;
+    a.M = num_slots;
+    a.max_pages = ps->max_pages;
+    a.pool_pages = kv->pool_pages;
+    a.max_cand = max_cand;
+    a.cmax = w.cmax;
+    a.nch = w.nch;
+    a.R = ps->num_reqs;
+    a.scale = params->scale;
+    a.theta = params->rope_theta;
+    a.p = params->p;
+    return from_hip(launch_score(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stream));
+}
+
+gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers, const gp_page_state_t *ps,
+                              const int32_t *bnd, int32_t num_bnd, const int32_t *k_counts,
+                              const float *scores, int32_t max_cand, const gp_params_t *params,
+                              int32_t *decisions, float *delta, int64_t *counters, void *ws,
+                              size_t ws_bytes, hipStream_t stream) {
+    if (!layers || n_layers <= 0 || !params || num_bnd < 0) return GP_ERR_INVALID;
+    if (n_layers > kMaxLayers) return GP_ERR_UNSUPPORTED;
+    gp_status_t st;
+    for (int l = 0; l < n_layers; ++l) {
+        if ((st = check_layer(&layers[l])) != GP_OK) return st;
+        if (layers[l].pool_pages != layers[0].pool_pages || layers[l].num_kv_heads != layers[0].num_kv_heads ||
+            layers[l].head_dim != layers[0].head_dim || layers[l].dtype != layers[0].dtype)
+            return GP_ERR_INVALID;
+    }
+    if ((st = check_state(ps, &layers[0])) != GP_OK) return st;
+    if (num_bnd == 0) return GP_OK;
+    if (!ps->refcount || !ps->free_list || !ps->free_count) return GP_ERR_INVALID;
+    if (!bnd || !k_counts || !scores || !decisions || !delta || !counters || !ws) return GP_ERR_INVALID;
+    if (max_cand < (ps->max_pages - 1) * kPage) return GP_ERR_INVALID;
+    if (params->k_loc < 0 || params->reserve_pages < 0) return GP_ERR_INVALID;
+    if (num_bnd > 2048) return GP_ERR_UNSUPPORTED;
+    const gp_kv_layer_t &L0 = layers[0];
+    const int E = elem_bytes(L0.dtype);
+    const ApplyWs w = apply_ws(num_bnd, L0.num_kv_heads, L0.head_dim, E, ps->max_pages, n_layers);
+    if (ws_bytes < w.total) return GP_ERR_WORKSPACE;
+    unsigned char *base = static_cast<unsigned char *>(ws);
+    ApplyArgs a;
+    a.page_table = ps->page_table;
+    a.num_pages = ps->num_pages;
+    a.seq_lens = ps->seq_lens;
+    a.refcount = ps->refcount;
+    a.free_list = ps->free_list;
+    a.free_count = ps->free_count;
+    a.bnd = bnd;
+    a.k_counts = k_counts;
+    a.scores = scores;
+    a.decisions = decisions;
+    a.delta = delta;
+    a.counters = reinterpret_cast<long long *>(counters);
+    a.req = reinterpret_cast<int32_t *>(base + w.req);
+    a.hdr = reinterpret_cast<int32_t *>(base + w.hdr);
+    a.nshc = reinterpret_cast<int32_t *>(base + w.nshc);
+    a.old_table = reinterpret_cast<int32_t *>(base + w.old_table);
+    a.released = reinterpret_cast<int32_t *>(base + w.released);
+    a.evict = reinterpret_cast<int32_t *>(base + w.evict);
+    a.border = base + w.border;
+    a.R = ps->num_reqs;
+    a.Rb = num_bnd;
+    a.Hkv = L0.num_kv_heads;
+    a.max_pages = ps->max_pages;
+    a.pool_pages = ps->pool_pages;
+    a.max_cand = max_cand;
+    a.n_layers = n_layers;
+    a.ncc = w.ncc;
+    a.npc = w.npc;
+    a.k_loc = params->k_loc;
+    a.reserve = params->reserve_pages;
+    a.tau = params->tau;
+    LayerPtrs lp[kMaxLayers];
+    for (int l = 0; l < n_layers; ++l) {
+        lp[l].k = layers[l].k;
+        lp[l].v = layers[l].v;
+    }
+    return from_hip(launch_apply(L0.dtype, L0.head_dim, a, lp, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,303 @@
+// Paged GQA decode attention (Sec. 3.1, attention-output equation), split over
+// the sequence.
+//
+// Work item = (request r, KV head h, chunk of kDecodeChunkPages pages).  One
+// workgroup of four wave64s serves the whole GQA group of h (G query heads),
+// so every K/V byte is read from HBM exactly once per step.  Inside a wave a
+// page (16 tokens x d) is read with fully coalesced 16-byte loads: lane l
+// holds dims [c*EPL, c*EPL+EPL) of token j*TPL + l/LPT for each of the LPP
+// loads, c = l % LPT.  Dot products are finished with cross-lane sums over
+// the LPT lanes of a token; the online-softmax running max is made
+// wave-uniform per page so that each lane can keep partial sums over its own
+// tokens.  Waves take pages round-robin and two pages are in flight per wave.
+// The four waves merge through LDS; a request that spans several chunks
+// writes (max, sum, o) partials and the last workgroup of (r, h) to finish,
+// found with an atomic counter, merges them and resets the counter to zero.
+//
+// Bound: HBM.  Algorithmic bytes per resident token and KV head:
+// 2 * d * sizeof(elem) (K and V), plus the page-table entries, q and out.
+#include "gp_internal.h"
+
+namespace gp {
+
+namespace {
+
+template <typename T>
+struct Traits;
+
+template <>
+struct Traits<uint16_t> {
+    static constexpr int EPL = 8;  // bf16 elements per 16-byte load
+    __device__ static inline void unpack(const uint4 &u, float *f) {
+        f[0] = bf16_lo(u.x); f[1] = bf16_hi(u.x);
+        f[2] = bf16_lo(u.y); f[3] = bf16_hi(u.y);
+        f[4] = bf16_lo(u.z); f[5] = bf16_hi(u.z);
+        f[6] = bf16_lo(u.w); f[7] = bf16_hi(u.w);
+    }
+    __device__ static inline void store(uint16_t *p, float x) { *p = f32_to_bf16(x); }
+    __device__ static inline float load(const uint16_t *p) { return bf16_to_f32(*p); }
+};
+
+template <>
+struct Traits<float> {
+    static constexpr int EPL = 4;
+    __device__ static inline void unpack(const uint4 &u, float *f) {
+        f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y);
+        f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
+    }
+    __device__ static inline void store(float *p, float x) { *p = x; }
+    __device__ static inline float load(const float *p) { return *p; }
+};
+
+constexpr float kNegInf = -__builtin_huge_valf();
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
+    using Tr = Traits<T>;
+    constexpr int EPL = Tr::EPL;
+    constexpr int LPT = D / EPL;          // lanes per token
+    constexpr int TPL = 64 / LPT;         // tokens per wave load
+    constexpr int LPP = kPage / TPL;      // loads per page
+    constexpr int NW = 4;                 // waves per workgroup
+    constexpr int CHUNK = kDecodeChunkPages * kPage;
+    static_assert(LPT >= 1 && LPT <= 64 && TPL * LPP == kPage, "layout");
+
+    __shared__ float s_m[NW][G], s_l[NW][G];
+    __shared__ float s_o[NW][G][D];
+    __shared__ int s_last;
+
+    const int chunk = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int Hkv = a.Hkv;
+    const int Hq = Hkv * G;
+
+    int P = a.num_pages[r];
+    P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
+    int m = a.seq_lens[r];
+    m = m < 0 ? 0 : (m > P * kPage ? P * kPage : m);
+    const int nchunks = cdiv(m, CHUNK);
+    T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
+    if (m == 0) {
+        if (chunk == 0)
+            for (int i = threadIdx.x; i < G * D; i += blockDim.x) Tr::store(out + i, 0.0f);
+        return;
+    }
+    if (chunk >= nchunks) return;
+
+    const int tok_begin = chunk * CHUNK;
+    const int tok_end = min(m, tok_begin + CHUNK);
+    const int page_begin = tok_begin / kPage, page_end = cdiv(tok_end, kPage);
+
+    const int c = lane % LPT, row = lane / LPT;
+    const T *qp = reinterpret_cast<const T *>(a.q) + ((size_t)r * Hq + (size_t)h * G) * D + c * EPL;
+    float q[G][EPL];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) q[g][e] = Tr::load(qp + (size_t)g * D + e) * a.qscale;
+
+    float mrun[G], l[G], o[G][EPL];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        mrun[g] = kNegInf;
+        l[g] = 0.0f;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) o[g][e] = 0.0f;
+    }
+
+    const int32_t *table = a.page_table + (size_t)r * a.max_pages;
+    const T *kpool = reinterpret_cast<const T *>(a.k);
+    const T *vpool = reinterpret_cast<const T *>(a.v);
+    const size_t head_off = (size_t)h * kPage * D;
+    const size_t page_elems = (size_t)Hkv * kPage * D;
+    const int lane_off = row * D + c * EPL;
+
+    for (int p0 = page_begin + wave; p0 < page_end; p0 += 2 * NW) {
+        uint4 kr[2][LPP], vr[2][LPP];
+        int ntok[2];
+        bool ok[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int p = p0 + u * NW;
+            int phys = p < page_end ? table[p] : -1;
+            ok[u] = phys >= 0 && phys < a.pool_pages;
+            ntok[u] = ok[u] ? min(kPage, m - p * kPage) : 0;
+            const size_t base = (size_t)(ok[u] ? phys : 0) * page_elems + head_off + lane_off;
+            if (ok[u]) {
+#pragma unroll
+                for (int j = 0; j < LPP; ++j) {
+                    kr[u][j] = *reinterpret_cast<const uint4 *>(kpool + base + (size_t)j * TPL * D);
+                    vr[u][j] = *reinterpret_cast<const uint4 *>(vpool + base + (size_t)j * TPL * D);
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            if (!ok[u]) continue;   // wave-uniform
+            float s[LPP][G];
+#pragma unroll
+            for (int j = 0; j < LPP; ++j) {
+                float kf[EPL];
+                Tr::unpack(kr[u][j], kf);
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    float acc = 0.0f;
+#pragma unroll
+                    for (int e = 0; e < EPL; ++e) acc = fmaf(q[g][e], kf[e], acc);
+                    s[j][g] = acc;
+                }
+            }
+#pragma unroll
+            for (int off = LPT / 2; off >= 1; off >>= 1)
+#pragma unroll
+                for (int j = 0; j < LPP; ++j)
+#pragma unroll
+                    for (int g = 0; g < G; ++g) s[j][g] += __shfl_xor(s[j][g], off, 64);
+            const bool full = ntok[u] == kPage;
+            float pmax[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g) pmax[g] = kNegInf;
+#pragma unroll
+            for (int j = 0; j < LPP; ++j) {
+                const bool valid = full || (j * TPL + row) < ntok[u];
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    s[j][g] = valid ? s[j][g] : kNegInf;
+                    pmax[g] = fmaxf(pmax[g], s[j][g]);
+                }
+            }
+#pragma unroll
+            for (int off = LPT; off < 64; off <<= 1)
+#pragma unroll
+                for (int g = 0; g < G; ++g) pmax[g] = fmaxf(pmax[g], __shfl_xor(pmax[g], off, 64));
+            float alpha[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const float mn = fmaxf(mrun[g], pmax[g]);
+                alpha[g] = exp2f(mrun[g] - mn);
+                mrun[g] = mn;
+                l[g] *= alpha[g];
+#pragma unroll
+                for (int e = 0; e < EPL; ++e) o[g][e] *= alpha[g];
+            }
+#pragma unroll
+            for (int j = 0; j < LPP; ++j) {
+                const bool valid = full || (j * TPL + row) < ntok[u];
+                float vf[EPL];
+                Tr::unpack(vr[u][j], vf);
+#pragma unroll
+                for (int e = 0; e < EPL; ++e) vf[e] = valid ? vf[e] : 0.0f;
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    const float pw = exp2f(s[j][g] - mrun[g]);
+                    l[g] += pw;
+#pragma unroll
+                    for (int e = 0; e < EPL; ++e) o[g][e] = fmaf(pw, vf[e], o[g][e]);
+                }
+            }
+        }
+    }
+
+    // sum over the token rows of the wave (all rows share the running max)
+#pragma unroll
+    for (int off = LPT; off < 64; off <<= 1)
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            l[g] += __shfl_xor(l[g], off, 64);
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) o[g][e] += __shfl_xor(o[g][e], off, 64);
+        }
+    if (row == 0) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) s_o[wave][g][c * EPL + e] = o[g][e];
+            if (c == 0) {
+                s_m[wave][g] = mrun[g];
+                s_l[wave][g] = l[g];
+            }
+        }
+    }
+    __syncthreads();
+
+    // merge the waves: thread -> (g, dim) pairs
+    const bool single = nchunks == 1;
+    float *part = a.partial + (((size_t)r * Hkv + h) * a.max_chunks + chunk) * G * (D + 2);
+    for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
+        const int g = i / D, dd = i % D;
+        float M = kNegInf;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][g]);
+        float Ls = 0.0f, Os = 0.0f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            const float f = s_m[w][g] == kNegInf ? 0.0f : exp2f(s_m[w][g] - M);
+            Ls += s_l[w][g] * f;
+            Os += s_o[w][g][dd] * f;
+        }
+        if (single) {
+            Tr::store(out + (size_t)g * D + dd, Os / Ls);
+        } else {
+            part[(size_t)g * (D + 2) + dd] = Os;
+            if (dd == 0) {
+                part[(size_t)g * (D + 2) + D] = M;
+                part[(size_t)g * (D + 2) + D + 1] = Ls;
+            }
+        }
+    }
+    if (single) return;
+
+    // last workgroup of (r, h) merges every chunk's partial
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t prev = __hip_atomic_fetch_add(a.counters + (size_t)r * Hkv + h, 1u,
+                                                     __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = (prev == (uint32_t)(nchunks - 1)) ? 1 : 0;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    const float *base = a.partial + ((size_t)r * Hkv + h) * a.max_chunks * G * (D + 2);
+    for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
+        const int g = i / D, dd = i % D;
+        float M = kNegInf;
+        for (int k = 0; k < nchunks; ++k) {
+            const float *pk = base + ((size_t)k * G + g) * (D + 2);
+            M = fmaxf(M, __builtin_nontemporal_load(pk + D));
+        }
+        float Ls = 0.0f, Os = 0.0f;
+        for (int k = 0; k < nchunks; ++k) {
+            const float *pk = base + ((size_t)k * G + g) * (D + 2);
+            const float mk = __builtin_nontemporal_load(pk + D);
+            const float f = mk == kNegInf ? 0.0f : exp2f(mk - M);
+            Ls += __builtin_nontemporal_load(pk + D + 1) * f;
+            Os += __builtin_nontemporal_load(pk + dd) * f;
+        }
+        Tr::store(out + (size_t)g * D + dd, Os / Ls);
+    }
+    if (threadIdx.x == 0) a.counters[(size_t)r * Hkv + h] = 0u;
+}
+
+template <typename T, int D>
+hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, hipStream_t s) {
+    switch (G) {
+        case 1: decode_kernel<T, D, 1><<<grid, 256, 0, s>>>(a); break;
+        case 2: decode_kernel<T, D, 2><<<grid, 256, 0, s>>>(a); break;
+        case 4: decode_kernel<T, D, 4><<<grid, 256, 0, s>>>(a); break;
+        case 8: decode_kernel<T, D, 8><<<grid, 256, 0, s>>>(a); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_decode(gp_dtype_t dt, int D, int G, const DecodeArgs &a, hipStream_t s) {
+    dim3 grid(a.max_chunks, a.Hkv, a.R);
+    if (dt == GP_BF16)
+        return D == 128 ? launch_g<uint16_t, 128>(G, a, grid, s) : launch_g<uint16_t, 64>(G, a, grid, s);
+    return D == 128 ? launch_g<float, 128>(G, a, grid, s) : launch_g<float, 64>(G, a, grid, s);
+}
+
+}  // namespace gp

@@ -1,0 +1,177 @@
+// Internal definitions shared by the library's translation units: workspace
+// layouts, launch descriptors and small device helpers.  Nothing here is part
+// of the public ABI (include/growpage.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "growpage.h"
+
+namespace gp {
+
+constexpr int kPage = 16;                 // tokens per page
+constexpr int kDecodeChunkPages = 16;     // pages per decode work item (split-K)
+constexpr int kScoreChunk = 256;          // candidate tokens per scoring work item
+constexpr int kProbChunk = 1024;          // tokens per weight/score work item
+constexpr int kCompactChunk = 256;        // slots per compaction work item
+constexpr int kMaxLayers = 64;            // layers one gp_boundary_apply call can take
+constexpr size_t kAlign = 256;
+
+__host__ __device__ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+__host__ __device__ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+// ---------------------------------------------------------------- layouts --
+
+struct DecodeWs {
+    size_t counters, partial, total;
+    int max_chunks;
+};
+
+__host__ __device__ inline DecodeWs decode_ws(int R, int Hq, int Hkv, int D, int max_pages) {
+    DecodeWs w;
+    const int G = Hq / Hkv;
+    w.max_chunks = cdiv(max_pages, kDecodeChunkPages);
+    size_t off = 0;
+    w.counters = off;
+    off = align_up(off + (size_t)R * Hkv * sizeof(uint32_t));
+    w.partial = off;
+    off = align_up(off + (size_t)R * Hkv * w.max_chunks * G * (D + 2) * sizeof(float));
+    w.total = off;
+    return w;
+}
+
+struct ScoreWs {
+    size_t logits, part, weights, total;
+    int cmax, nch;
+};
+
+// cmax = (max_pages - 1) * page: the most candidates any request can have.
+__host__ __device__ inline ScoreWs score_ws(int Rb, int Hq, int Hkv, int max_pages) {
+    ScoreWs w;
+    const int G = Hq / Hkv;
+    w.cmax = max_pages > 1 ? (max_pages - 1) * kPage : 0;
+    w.nch = cdiv(w.cmax > 0 ? w.cmax : 1, kScoreChunk);
+    size_t off = 0;
+    w.logits = off;   // [Rb][Hkv][2G][cmax] double
+    off = align_up(off + (size_t)Rb * Hkv * 2 * G * w.cmax * sizeof(double));
+    w.part = off;     // [Rb][Hkv][nch][2G][2] double (running max, sum of exp)
+    off = align_up(off + (size_t)Rb * Hkv * w.nch * 2 * G * 2 * sizeof(double));
+    w.weights = off;  // [Rb][Hkv][2][cmax] float
+    off = align_up(off + (size_t)Rb * Hkv * 2 * w.cmax * sizeof(float));
+    w.total = off;
+    return w;
+}
+
+struct ApplyWs {
+    size_t req, hdr, nshc, old_table, released, evict, border, total;
+    int ncc, npc;
+};
+
+// Per boundary request scratch (int32 fields).
+enum { RQ_R = 0, RQ_P, RQ_FLAGS, RQ_NSH, RQ_POP, RQ_DEC, RQ_STRIDE = 8 };
+// Call header (int32): free count before pops, after pops, released pages.
+enum { HDR_FC0 = 0, HDR_FC1, HDR_NREL, HDR_SIZE = 4 };
+constexpr int kPageBlock = 256;   // pages per work item when walking a page-table row
+
+__host__ __device__ inline ApplyWs apply_ws(int Rb, int Hkv, int D, int elem, int max_pages,
+                                            int n_layers) {
+    ApplyWs w;
+    w.ncc = cdiv(max_pages * kPage, kCompactChunk);
+    w.npc = cdiv(max_pages, kPageBlock);
+    size_t off = 0;
+    w.req = off;        // [Rb][RQ_STRIDE]
+    off = align_up(off + (size_t)Rb * RQ_STRIDE * sizeof(int32_t));
+    w.hdr = off;        // [HDR_SIZE]
+    off = align_up(off + HDR_SIZE * sizeof(int32_t));
+    w.nshc = off;       // [Rb][npc] shared pages per block of the table row
+    off = align_up(off + (size_t)Rb * w.npc * sizeof(int32_t));
+    w.old_table = off;  // [Rb][max_pages]
+    off = align_up(off + (size_t)Rb * max_pages * sizeof(int32_t));
+    w.released = off;   // [Rb * max_pages]
+    off = align_up(off + (size_t)Rb * max_pages * sizeof(int32_t));
+    w.evict = off;      // [L][Rb][Hkv][16]
+    off = align_up(off + (size_t)n_layers * Rb * Hkv * kPage * sizeof(int32_t));
+    w.border = off;     // [L][Rb][Hkv][ncc][2][16][D] elements
+    off = align_up(off + (size_t)n_layers * Rb * Hkv * w.ncc * 2 * kPage * D * elem);
+    w.total = off;
+    return w;
+}
+
+// ------------------------------------------------------------ launch args --
+
+struct DecodeArgs {
+    const void *k, *v;
+    const int32_t *page_table, *num_pages, *seq_lens;
+    const void *q;
+    void *out;
+    float *partial;
+    uint32_t *counters;
+    int R, Hkv, max_pages, pool_pages, max_chunks;
+    float qscale;   // scale * log2(e)
+};
+
+struct SummaryArgs {
+    const void *q;
+    const int32_t *slot_ids;
+    const uint8_t *init;
+    float *qstate;
+    int R, HqD, M;
+    double beta_s, beta_l;
+};
+
+struct ScoreArgs {
+    const void *k;
+    const int32_t *page_table, *num_pages, *seq_lens;
+    const void *q_pre;
+    const float *qstate;
+    const int32_t *slot_ids, *positions, *bnd;
+    int32_t *k_counts;
+    float *scores;
+    double *logits, *part;
+    float *weights;
+    int Rb, Hq, Hkv, M, max_pages, pool_pages, max_cand, cmax, nch, R;
+    double scale, theta, p;
+};
+
+struct ApplyArgs {
+    int32_t *page_table, *num_pages, *seq_lens, *refcount, *free_list, *free_count;
+    const int32_t *bnd, *k_counts;
+    const float *scores;
+    int32_t *decisions;
+    float *delta;
+    long long *counters;
+    int32_t *req, *hdr, *nshc, *old_table, *released, *evict;
+    unsigned char *border;
+    int R, Rb, Hkv, max_pages, pool_pages, max_cand, n_layers, ncc, npc, k_loc, reserve;
+    double tau;
+};
+
+struct LayerPtrs {
+    void *k, *v;
+};
+
+// ---------------------------------------------------------------- launchers --
+
+hipError_t launch_summaries(gp_dtype_t dt, const SummaryArgs &a, hipStream_t s);
+hipError_t launch_decode(gp_dtype_t dt, int D, int G, const DecodeArgs &a, hipStream_t s);
+hipError_t launch_score(gp_dtype_t dt, int D, int G, const ScoreArgs &a, hipStream_t s);
+hipError_t launch_apply(gp_dtype_t dt, int D, const ApplyArgs &a, const LayerPtrs *layers,
+                        hipStream_t s);
+
+// ---------------------------------------------------------- device helpers --
+
+__device__ inline float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ inline float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+__device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// float -> bfloat16, round to nearest even; NaN stays NaN.
+__device__ inline uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)0x7fc0;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+}  // namespace gp

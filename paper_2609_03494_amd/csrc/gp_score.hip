@@ -1,0 +1,380 @@
+// Boundary scoring (Sec. 3.2 "attention-demand trend", Sec. 3.3 token score,
+// App. E.1 "demand estimation at capacity boundaries").
+//
+// Three kernels per layer:
+//  1. logits: per (boundary request, KV head, chunk of kScoreChunk candidate
+//     tokens).  The workgroup first builds the 2G aligned summaries of its GQA
+//     group in LDS (RMS calibration to the current query, then rotation at the
+//     current position; fp64, angles computed on the device in fp64), then
+//     each thread takes one candidate token, reads its key once and forms its
+//     2G logits in fp64.  The chunk's running max and sum of exponentials per
+//     view go to the workspace next to the logits.
+//  2. weights: merge the chunk statistics per view, turn logits into the
+//     softmax weights, average the G query heads of each view (fp64), round to
+//     float32 and write a^S, a^L (workspace) and s = max(a^S, a^L) (output).
+//  3. top-p: per (request, KV head, view) a three-pass radix select on the
+//     float32 bit patterns finds the smallest k whose k largest weights reach
+//     p.  Per-bucket masses are accumulated as 2^-60 fixed-point integers, so
+//     sums are exact and independent of thread order.
+//
+// Bound: the key read (|C| * d * sizeof(elem) per KV head) plus 2G fp64
+// logits written and read back; kernel 1 does 2G fp64 FMAs per key element.
+#include "gp_internal.h"
+
+namespace gp {
+
+namespace {
+
+template <typename T>
+__device__ inline double ld(const T *p);
+template <>
+__device__ inline double ld<float>(const float *p) { return (double)*p; }
+template <>
+__device__ inline double ld<uint16_t>(const uint16_t *p) { return (double)bf16_to_f32(*p); }
+
+template <typename T>
+struct KRow;
+template <>
+struct KRow<uint16_t> {
+    static constexpr int EPV = 8;
+    __device__ static inline void get(const uint16_t *p, double *f) {
+        const uint4 u = *reinterpret_cast<const uint4 *>(p);
+        f[0] = bf16_lo(u.x); f[1] = bf16_hi(u.x); f[2] = bf16_lo(u.y); f[3] = bf16_hi(u.y);
+        f[4] = bf16_lo(u.z); f[5] = bf16_hi(u.z); f[6] = bf16_lo(u.w); f[7] = bf16_hi(u.w);
+    }
+};
+template <>
+struct KRow<float> {
+    static constexpr int EPV = 4;
+    __device__ static inline void get(const float *p, double *f) {
+        const float4 u = *reinterpret_cast<const float4 *>(p);
+        f[0] = u.x; f[1] = u.y; f[2] = u.z; f[3] = u.w;
+    }
+};
+
+__device__ inline bool boundary_of(const ScoreArgs &a, int i, int &r, int &P) {
+    r = a.bnd[i];
+    if (r < 0 || r >= a.R) return false;
+    P = a.num_pages[r];
+    if (P < 2 || P > a.max_pages) return false;
+    return a.seq_lens[r] == P * kPage;
+}
+
+// Products and sums are rounded one at a time, as in a plain fp64 evaluation.
+#pragma clang fp contract(off)
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256) void logits_kernel(ScoreArgs a) {
+    constexpr int V = 2 * G;
+    constexpr int H = D / 2;
+    __shared__ double s_q[V][D];
+    __shared__ double s_qt[G][D];
+    __shared__ double s_cos[H], s_sin[H];
+    __shared__ double s_ss[3 * G];
+    __shared__ double s_red[256 / 64][V];
+    __shared__ double s_max[V];
+
+    const int chunk = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    int r, P;
+    if (!boundary_of(a, i, r, P)) return;
+    const int C = (P - 1) * kPage;
+    const int t0 = chunk * kScoreChunk;
+    if (t0 >= C) return;
+    const int tid = threadIdx.x;
+    const int Hq = a.Hkv * G;
+    const int slot = a.slot_ids[r];
+    if (slot < 0 || slot >= a.M) return;
+
+    // summaries and current query of the GQA group
+    const float *qs = a.qstate + (size_t)slot * 2 * Hq * D;
+    const T *qp = reinterpret_cast<const T *>(a.q_pre) + (size_t)r * Hq * D;
+    for (int e = tid; e < V * D; e += blockDim.x) {
+        const int v = e / D, d = e % D, x = v / G, g = v % G;
+        s_q[v][d] = (double)qs[((size_t)x * Hq + h * G + g) * D + d];
+    }
+    for (int e = tid; e < G * D; e += blockDim.x) {
+        const int g = e / D, d = e % D;
+        s_qt[g][d] = ld<T>(qp + (size_t)(h * G + g) * D + d);
+    }
+    const double pos = (double)a.positions[r];
+    for (int k = tid; k < H; k += blockDim.x) {
+        const double ang = pos * pow(a.theta, (-2.0 * k) / D);
+        s_cos[k] = cos(ang);
+        s_sin[k] = sin(ang);
+    }
+    __syncthreads();
+    if (tid < 3 * G) {
+        const double *src = tid < V ? s_q[tid] : s_qt[tid - V];
+        double acc = 0.0;
+        for (int d = 0; d < D; ++d) acc += src[d] * src[d];
+        s_ss[tid] = acc;
+    }
+    __syncthreads();
+    // gamma = RMS(q_t) / RMS(qbar); a summary with zero RMS stays zero
+    for (int e = tid; e < V * H; e += blockDim.x) {
+        const int v = e / H, k = e % H, g = v % G;
+        const double den = s_ss[v];
+        const double gam = den == 0.0 ? 0.0 : sqrt(s_ss[V + g] / D) / sqrt(den / D);
+        const double x1 = gam * s_q[v][k], x2 = gam * s_q[v][k + H];
+        s_q[v][k] = x1 * s_cos[k] - x2 * s_sin[k];
+        s_q[v][k + H] = x2 * s_cos[k] + x1 * s_sin[k];
+    }
+    __syncthreads();
+
+    // one candidate token per thread
+    const int t = t0 + tid;
+    const bool live = t < C && tid < kScoreChunk;
+    double z[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) z[v] = 0.0;
+    if (live) {
+        const int phys = a.page_table[(size_t)r * a.max_pages + t / kPage];
+        if (phys >= 0 && phys < a.pool_pages) {
+            const T *kp = reinterpret_cast<const T *>(a.k) +
+                          (((size_t)phys * a.Hkv + h) * kPage + (t % kPage)) * D;
+            constexpr int EPV = KRow<T>::EPV;
+#pragma unroll 2
+            for (int d0 = 0; d0 < D; d0 += EPV) {
+                double kf[EPV];
+                KRow<T>::get(kp + d0, kf);
+#pragma unroll
+                for (int v = 0; v < V; ++v)
+#pragma unroll
+                    for (int e = 0; e < EPV; ++e) z[v] += s_q[v][d0 + e] * kf[e];
+            }
+        }
+#pragma unroll
+        for (int v = 0; v < V; ++v) z[v] *= a.scale;
+        double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax + t;
+#pragma unroll
+        for (int v = 0; v < V; ++v) lg[(size_t)v * a.cmax] = z[v];
+    }
+
+    // chunk statistics: max and sum of exp(z - max) per view
+    const int lane = tid & 63, wave = tid >> 6;
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        double mv = live ? z[v] : -__builtin_huge_val();
+        for (int off = 32; off >= 1; off >>= 1) mv = fmax(mv, __shfl_xor(mv, off, 64));
+        if (lane == 0) s_red[wave][v] = mv;
+    }
+    __syncthreads();
+    if (tid < V) {
+        double mv = s_red[0][tid];
+        for (int w = 1; w < 4; ++w) mv = fmax(mv, s_red[w][tid]);
+        s_max[tid] = mv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        double ev = live ? exp(z[v] - s_max[v]) : 0.0;
+        for (int off = 32; off >= 1; off >>= 1) ev += __shfl_xor(ev, off, 64);
+        if (lane == 0) s_red[wave][v] = ev;
+    }
+    __syncthreads();
+    if (tid < V) {
+        double sv = 0.0;
+        for (int w = 0; w < 4; ++w) sv += s_red[w][tid];
+        double *pt = a.part + ((((size_t)i * a.Hkv + h) * a.nch + chunk) * V + tid) * 2;
+        pt[0] = s_max[tid];
+        pt[1] = sv;
+    }
+}
+
+template <int G>
+__global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
+    constexpr int V = 2 * G;
+    __shared__ double s_M[V], s_L[V];
+    const int chunk = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    int r, P;
+    if (!boundary_of(a, i, r, P)) return;
+    const int C = (P - 1) * kPage;
+    const int t0 = chunk * kProbChunk;
+    if (t0 >= C) return;
+    const int tid = threadIdx.x;
+    const int used = cdiv(C, kScoreChunk);
+    if (tid < V) {
+        const double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch) * V * 2;
+        double M = -__builtin_huge_val();
+        for (int c = 0; c < used; ++c) M = fmax(M, pt[((size_t)c * V + tid) * 2]);
+        double L = 0.0;
+        for (int c = 0; c < used; ++c)
+            L += pt[((size_t)c * V + tid) * 2 + 1] * exp(pt[((size_t)c * V + tid) * 2] - M);
+        s_M[tid] = M;
+        s_L[tid] = L;
+    }
+    __syncthreads();
+    const double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax;
+    float *w = a.weights + ((size_t)i * a.Hkv + h) * 2 * a.cmax;
+    float *sc = a.scores + ((size_t)i * a.Hkv + h) * a.max_cand;
+    const int t_end = min(C, t0 + kProbChunk);
+    for (int t = t0 + tid; t < t_end; t += blockDim.x) {
+        float ax[2];
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+            double acc = 0.0;
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const int v = x * G + g;
+                acc += exp(lg[(size_t)v * a.cmax + t] - s_M[v]) / s_L[v];
+            }
+            ax[x] = (float)(acc / G);
+            w[(size_t)x * a.cmax + t] = ax[x];
+        }
+        sc[t] = fmaxf(ax[0], ax[1]);
+    }
+}
+
+__device__ inline unsigned long long fixed60(uint32_t bits) {
+    return (unsigned long long)ldexp((double)__uint_as_float(bits), 60);
+}
+
+// Inclusive scan of 256 per-thread values in thread order (Hillis-Steele in LDS).
+__device__ inline unsigned long long block_scan_u64(unsigned long long x, unsigned long long *buf) {
+    const int tid = threadIdx.x;
+    buf[tid] = x;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+        const unsigned long long y = tid >= off ? buf[tid - off] : 0ull;
+        __syncthreads();
+        buf[tid] += y;
+        __syncthreads();
+    }
+    const unsigned long long out = buf[tid];
+    __syncthreads();
+    return out;
+}
+
+__global__ __launch_bounds__(256) void top_p_kernel(ScoreArgs a) {
+    constexpr int NB = 2048;
+    __shared__ unsigned int s_cnt[NB];
+    __shared__ unsigned long long s_mass[NB];
+    __shared__ unsigned long long s_scan[256];
+    __shared__ int s_bucket;
+    __shared__ unsigned long long s_above_mass;
+    __shared__ unsigned int s_above_cnt;
+
+    const int x = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    const int tid = threadIdx.x;
+    int32_t *out = a.k_counts + ((size_t)i * a.Hkv + h) * 2 + x;
+    int r, P;
+    if (!boundary_of(a, i, r, P)) {
+        if (tid == 0) *out = 0;
+        return;
+    }
+    const int C = (P - 1) * kPage;
+    const float *wv = a.weights + (((size_t)i * a.Hkv + h) * 2 + x) * a.cmax;
+    const unsigned long long target = (unsigned long long)ldexp(a.p, 60);
+
+    uint32_t prefix = 0;
+    unsigned long long above_mass = 0;
+    unsigned int above_cnt = 0;
+    const int shifts[3] = {20, 9, 0};
+    const int nbits[3] = {11, 11, 9};
+    for (int pass = 0; pass < 3; ++pass) {
+        const int sh = shifts[pass], nb = 1 << nbits[pass];
+        for (int b = tid; b < nb; b += 256) {
+            s_cnt[b] = 0;
+            s_mass[b] = 0;
+        }
+        __syncthreads();
+        for (int t = tid; t < C; t += 256) {
+            const uint32_t u = __float_as_uint(wv[t]);
+            if ((u >> (sh + nbits[pass])) == prefix) {
+                const int b = (u >> sh) & (nb - 1);
+                atomicAdd(&s_cnt[b], 1u);
+                atomicAdd(&s_mass[b], fixed60(u));
+            }
+        }
+        __syncthreads();
+        // buckets in descending order: thread tid owns per consecutive buckets
+        const int per = nb / 256;
+        const int hi = nb - 1 - tid * per;
+        unsigned long long my_mass = 0;
+        unsigned int my_cnt = 0;
+        for (int k = 0; k < per; ++k) {
+            my_mass += s_mass[hi - k];
+            my_cnt += s_cnt[hi - k];
+        }
+        const unsigned long long incl = block_scan_u64(my_mass, s_scan);
+        const unsigned long long excl = incl - my_mass;
+        const unsigned long long need = target > above_mass ? target - above_mass : 0ull;
+        if (tid == 0) s_bucket = -1;
+        __syncthreads();
+        if (excl < need && incl >= need) {
+            unsigned long long cum = excl;
+            for (int k = 0; k < per; ++k) {
+                cum += s_mass[hi - k];
+                if (cum >= need) {
+                    s_bucket = hi - k;
+                    break;
+                }
+            }
+        }
+        __syncthreads();
+        const int B = s_bucket;
+        if (B < 0) {
+            // the weights sum to less than p: every candidate is needed
+            if (tid == 0) *out = C;
+            return;
+        }
+        // everything strictly above bucket B
+        unsigned long long am = 0;
+        unsigned int ac = 0;
+        for (int b = B + 1 + tid; b < nb; b += 256) {
+            am += s_mass[b];
+            ac += s_cnt[b];
+        }
+        const unsigned long long am_all = block_scan_u64(am, s_scan);
+        if (tid == 255) s_above_mass = am_all;
+        __syncthreads();
+        const unsigned long long ac_all = block_scan_u64((unsigned long long)ac, s_scan);
+        if (tid == 255) s_above_cnt = (unsigned int)ac_all;
+        __syncthreads();
+        above_mass += s_above_mass;
+        above_cnt += s_above_cnt;
+        prefix = (prefix << nbits[pass]) | (uint32_t)B;
+        __syncthreads();
+    }
+    if (tid == 0) {
+        // prefix is now the float32 bit pattern of the K-th largest weight T
+        const unsigned long long tf = fixed60(prefix);
+        const unsigned long long need = target - above_mass;   // > 0
+        unsigned long long j = tf == 0 ? 0ull : (need + tf - 1) / tf;
+        long long K = (long long)above_cnt + (long long)j;
+        if (tf == 0 || K > C) K = C;
+        *out = (int32_t)K;
+    }
+}
+
+template <typename T, int D>
+hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
+    dim3 g1(a.nch, a.Hkv, a.Rb), g2(cdiv(a.cmax, kProbChunk), a.Hkv, a.Rb), g3(2, a.Hkv, a.Rb);
+    if (a.cmax == 0) {
+        // no request can have candidates: the counts are written as zero
+        top_p_kernel<<<g3, 256, 0, s>>>(a);
+        return hipGetLastError();
+    }
+    switch (G) {
+#define GP_CASE(GG)                                                   \
+    case GG:                                                          \
+        logits_kernel<T, D, GG><<<g1, 256, 0, s>>>(a);                \
+        weights_kernel<GG><<<g2, 256, 0, s>>>(a);                     \
+        break;
+        GP_CASE(1) GP_CASE(2) GP_CASE(4) GP_CASE(8)
+#undef GP_CASE
+        default: return hipErrorInvalidValue;
+    }
+    top_p_kernel<<<g3, 256, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_score(gp_dtype_t dt, int D, int G, const ScoreArgs &a, hipStream_t s) {
+    if (a.Rb == 0) return hipSuccess;
+    if (dt == GP_BF16) return D == 128 ? launch_gd<uint16_t, 128>(G, a, s) : launch_gd<uint16_t, 64>(G, a, s);
+    return D == 128 ? launch_gd<float, 128>(G, a, s) : launch_gd<float, 64>(G, a, s);
+}
+
+}  // namespace gp

@@ -1,0 +1,58 @@
+// Dual-timescale query summaries (Sec. 3.2, EMA equation; App. E.1).
+//
+// One thread per four consecutive elements of a request's [Hq][d] query; the
+// pool row of the request's slot is updated in place.  Arithmetic is fp64 and
+// rounded once to float32, so that the stored summary is the correctly
+// rounded value of beta * qbar + (1 - beta) * q.  The kernel moves
+// 2 x 4 B (read + write) x 2 views per element plus the query: it is a few
+// microseconds of HBM traffic per step and is bound by launch latency.
+#include "gp_internal.h"
+
+namespace gp {
+
+template <typename T>
+__device__ inline float load_q(const T *p, size_t i);
+
+template <>
+__device__ inline float load_q<float>(const float *p, size_t i) { return p[i]; }
+
+template <>
+__device__ inline float load_q<uint16_t>(const uint16_t *p, size_t i) { return bf16_to_f32(p[i]); }
+
+// Products and the sum are rounded separately (no fused multiply-add), the
+// plain fp64 evaluation of the update.
+#pragma clang fp contract(off)
+template <typename T>
+__global__ __launch_bounds__(256) void summaries_kernel(SummaryArgs a) {
+    const int r = blockIdx.y;
+    const int slot = a.slot_ids[r];
+    if (slot < 0 || slot >= a.M) return;
+    const bool init = a.init[r] != 0;
+    const T *q = reinterpret_cast<const T *>(a.q) + (size_t)r * a.HqD;
+    float *S = a.qstate + (size_t)slot * 2 * a.HqD;
+    float *L = S + a.HqD;
+    const double cs = 1.0 - a.beta_s, cl = 1.0 - a.beta_l;
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < a.HqD; i += gridDim.x * blockDim.x) {
+        const float x = load_q<T>(q, i);
+        if (init) {
+            S[i] = x;
+            L[i] = x;
+        } else {
+            const double xd = (double)x;
+            S[i] = (float)(a.beta_s * (double)S[i] + cs * xd);
+            L[i] = (float)(a.beta_l * (double)L[i] + cl * xd);
+        }
+    }
+}
+
+hipError_t launch_summaries(gp_dtype_t dt, const SummaryArgs &a, hipStream_t s) {
+    const int threads = 256;
+    dim3 grid(cdiv(a.HqD, threads), a.R);
+    if (dt == GP_F32)
+        summaries_kernel<float><<<grid, threads, 0, s>>>(a);
+    else
+        summaries_kernel<uint16_t><<<grid, threads, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace gp

@@ -1,0 +1,87 @@
+"""The C-ABI library loads on the host and exports every entry point the header
+declares; host-side validation answers without touching a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_03494_amd as gp
+from paper_2609_03494_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2609_03494_amd import build
+        build.build()
+    return gp.load()
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "growpage.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]+?\b(gp_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_four_path_calls():
+    names = _declared()
+    for n in ("gp_update_summaries", "gp_decode_attention", "gp_boundary_score", "gp_boundary_apply"):
+        assert n in names
+    assert set(names) == set(_lib.EXPORTS)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code in range(5):
+        assert gp.status_string(code)
+
+
+def test_workspace_sizes(lib):
+    import torch
+    n = gp.gp_workspace_bytes(gp.GP_OP_DECODE, 64, 0, 32, 8, 128, 260, torch.bfloat16)
+    assert n > 64 * 8 * 4
+    assert gp.gp_workspace_bytes(gp.GP_OP_SCORE, 64, 4, 32, 8, 128, 260, torch.bfloat16) > 0
+    assert gp.gp_workspace_bytes(gp.GP_OP_APPLY, 64, 4, 32, 8, 128, 260, torch.bfloat16) > 0
+    assert lib.gp_workspace_bytes(0, 4, 0, 32, 8, 96, 10, 16, 1, 1) == 0      # head_dim 96
+    assert lib.gp_workspace_bytes(0, 4, 0, 24, 8, 128, 10, 16, 1, 1) == 0     # G = 3
+    assert lib.gp_workspace_bytes(0, 4, 0, 32, 8, 128, 10, 32, 1, 1) == 0     # page size 32
+
+
+def test_host_validation_without_launch(lib):
+    fake = 0x1000
+    kv = _lib._KVLayer(fake, fake, 100, 8, 16, 128, 1)
+    ps = _lib._PageState(fake, fake, fake, fake, fake, fake, 4, 10, 100)
+    # null layer -> invalid
+    assert lib.gp_decode_attention(None, ctypes.byref(ps), fake, 32, 0.1, fake, fake, 1 << 30, None) == 1
+    # head_dim 96 -> unsupported
+    bad = _lib._KVLayer(fake, fake, 100, 8, 16, 96, 1)
+    assert lib.gp_decode_attention(ctypes.byref(bad), ctypes.byref(ps), fake, 32, 0.1, fake, fake,
+                                   1 << 30, None) == 2
+    # workspace too small
+    assert lib.gp_decode_attention(ctypes.byref(kv), ctypes.byref(ps), fake, 32, 0.1, fake, fake, 16,
+                                   None) == 3
+    # pool sizes disagree
+    ps2 = _lib._PageState(fake, fake, fake, fake, fake, fake, 4, 10, 99)
+    assert lib.gp_decode_attention(ctypes.byref(kv), ctypes.byref(ps2), fake, 32, 0.1, fake, fake,
+                                   1 << 30, None) == 1
+    # summaries: beta outside [0, 1]
+    assert lib.gp_update_summaries(fake, 1, 4, 32, 128, fake, fake, fake, 512, 1.5, 0.9, None) == 1
+    # score: max_cand too small for the table width
+    p = _lib._Params(0.9, 0.999, 0.99, 0.0, 0.088, 1e6, 4, 0)
+    assert lib.gp_boundary_score(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 512, fake, fake, fake,
+                                 2, 32, ctypes.byref(p), fake, fake, 16, fake, 1 << 30, None) == 1
+    # apply: too many layers
+    arr = (_lib._KVLayer * 1)(kv)
+    assert lib.gp_boundary_apply(arr, 65, ctypes.byref(ps), fake, 2, fake, fake, 144, ctypes.byref(p),
+                                 fake, fake, fake, fake, 1 << 30, None) == 2
+    # zero requests is a no-op that succeeds
+    ps0 = _lib._PageState(fake, fake, fake, fake, fake, fake, 0, 10, 100)
+    assert lib.gp_decode_attention(ctypes.byref(kv), ctypes.byref(ps0), fake, 32, 0.1, fake, fake, 0,
+                                   None) == 0

@@ -1,0 +1,354 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle on
+the same seeded inputs.
+
+Bars (written per check below):
+  * decode attention: fp32 within 1e-5 of the row's largest |value|; bf16
+    within 2e-2 of it, and within half a bf16 step of each exact value;
+  * summaries: bit-identical float32;
+  * scores: within 1e-5 relative; working-set sizes identical unless the
+    oracle's running sum passes p within 1e-6 (then off by at most one);
+  * decisions, page tables, counts, free stack: identical;
+  * compacted K/V rows: bit-identical; a swap between tokens whose scores lie
+    within 1e-5 of the selection threshold is excused."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from _harness import (DeviceCase, PoolView, assert_rows_close, bf16_rounding_ok, oracle_state,
+                      row_index, threshold_band)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_03494_amd as gp
+    gp.load()          # the HIP library must be there: no fallback
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+# ----------------------------------------------------------------- helpers --
+
+def _tiny_prepared():
+    """Tiny case with its summaries built from the 8 seeded priors (init, then
+    EMA), then this step's query, on both sides."""
+    w = W.tiny()
+    dc = DeviceCase(w)
+    st = w.qstate
+    for j in range(w.q_priors.shape[0]):
+        init = np.full(w.num_reqs, j == 0, np.uint8)
+        st = O.update_summaries(w.q_priors[j], "f32", w.slot_ids, init, st, *_betas())
+        dc.update_summaries(w.q_priors[j], init, *_betas())
+    st = O.update_summaries(w.q_pre, "f32", w.slot_ids, np.zeros(w.num_reqs, np.uint8), st, *_betas())
+    dc.update_summaries(w.q_pre, np.zeros(w.num_reqs, np.uint8), *_betas())
+    return w, dc, st
+
+
+def _betas():
+    p = O.Params().as_f32(64)
+    return p.beta_s, p.beta_l
+
+
+def _decode_check(w, dc, requests=None):
+    scale = float(np.float32(1.0 / math.sqrt(w.head_dim)))
+    got = dc.decode(scale)
+    pool_k, pool_v = PoolView(w, "k"), PoolView(w, "v")
+    reqs = list(range(w.num_reqs)) if requests is None else list(requests)
+    ref = O.decode_attention(pool_k, pool_v, w.dtype, w.page_table, w.seq_lens, w.q_post,
+                             w.num_q_heads, scale, requests=reqs)
+    got, ref = got[reqs], ref[reqs]
+    if w.dtype == "f32":
+        return assert_rows_close(got, ref, 1e-5, "decode fp32")
+    worst = assert_rows_close(got, ref, 2e-2, "decode bf16")
+    assert bf16_rounding_ok(got, ref), "decode bf16: beyond bf16 rounding of the exact value"
+    return worst
+
+
+def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=None):
+    """Run one boundary event on both sides and compare everything."""
+    bnd = w.boundary if bnd is None else np.asarray(bnd, np.int32)
+    p32 = params.as_f32(w.head_dim)
+    qs = w.qstate if qstate_host is None else qstate_host
+    dc = DeviceCase(w) if dc is None else dc
+    st = oracle_state(w)
+    if free_count is not None:
+        st.free_count = free_count
+        dc.ps.free_count.fill_(free_count)
+    kp, vp = w.dense_pool("k"), w.dense_pool("v")
+    kp0, vp0 = kp.copy(), vp.copy()
+    before_state = st.copy()
+    ref = O.boundary_step([(kp, vp)], w.dtype, st, w.q_pre, qs, w.slot_ids, w.positions, bnd, p32)
+    got = dc.boundary(params, bnd=bnd)
+    b = w.page_size
+    # working-set sizes and scores
+    fragile = set()
+    for i, r in enumerate(bnd):
+        P = int(before_state.num_pages[r])
+        for h in range(w.num_kv_heads):
+            for x in range(2):
+                g, o = int(got["k_counts"][0, i, h, x]), int(ref["counts"][i][0, h, x])
+                a32 = ref["weights"][i][0][x, h]
+                if a32.size and O.top_p_fragile(a32, p32.p, 1e-6):
+                    fragile.add(i)
+                    assert abs(g - o) <= 1, (i, h, x, g, o)
+                else:
+                    assert g == o, f"K^{'SL'[x]} of boundary {i} head {h}: gpu {g} oracle {o}"
+            C = (P - 1) * b if int(before_state.seq_lens[r]) == P * b and P >= 2 else 0
+            if C:
+                s_g = got["scores"][0, i, h, :C]
+                s_o = ref["scores"][i][0][h]
+                np.testing.assert_allclose(s_g, s_o, rtol=1e-5, atol=0,
+                                           err_msg=f"scores boundary {i} head {h}")
+    # decisions
+    dec_g, dec_o = got["decisions"], ref["decisions"]
+    for i in range(len(bnd)):
+        if dec_g[i] != dec_o[i]:
+            assert i in fragile, f"decision {i}: gpu {dec_g[i]} oracle {dec_o[i]}"
+    if (dec_g != dec_o).any():
+        pytest.skip("a decision flipped on a fragile top-p count (excused); state not comparable")
+    np.testing.assert_array_equal(got["delta"], ref["delta"])
+    np.testing.assert_array_equal(got["counters"], ref["counters"])
+    # page state, bit-exact
+    gs = dc.host_state()
+    np.testing.assert_array_equal(gs.page_table, st.page_table)
+    np.testing.assert_array_equal(gs.num_pages, st.num_pages)
+    np.testing.assert_array_equal(gs.seq_lens, st.seq_lens)
+    np.testing.assert_array_equal(gs.refcount, st.refcount)
+    assert gs.free_count == st.free_count
+    np.testing.assert_array_equal(gs.free_list[: gs.free_count], st.free_list[: st.free_count])
+    # compacted K/V
+    excused = 0
+    for i, r in enumerate(bnd):
+        if dec_o[i] not in (O.COMPRESS, O.FALLBACK):
+            continue
+        P = int(before_state.num_pages[r])
+        n = (P - 1) * b
+        for which, pool, pool0 in (("k", kp, kp0), ("v", vp, vp0)):
+            want = O.gather_tokens(pool, st.page_table[r], n, b)
+            have = dc.gather(gs.page_table[r], n, which)
+            if np.array_equal(want, have):
+                continue
+            before = O.gather_tokens(pool0, before_state.page_table[r], P * b, b)
+            for h in range(w.num_kv_heads):
+                if np.array_equal(want[:, h], have[:, h]):
+                    continue
+                idx = row_index(before[:, h], have[:, h])
+                assert (idx >= 0).all(), f"compaction wrote rows that were never there (req {r})"
+                K_t = (P - 2) * b
+                assert (np.diff(idx[:K_t]) > 0).all() and (idx[K_t:] == np.arange((P - 1) * b, P * b)).all()
+                kept_o = ref["kept"][(i, 0, h)]
+                band = threshold_band(ref["scores"][i][0][h], kept_o, P, b, p32.k_loc)
+                diff = set(idx[:K_t].tolist()) ^ set(kept_o.tolist())
+                assert diff <= band, f"retained sets differ outside the threshold band (req {r}, head {h})"
+                excused += 1
+    return dict(ref=ref, got=got, excused=excused, decisions=dec_o)
+
+
+# ------------------------------------------------------------------- tests --
+
+def test_summaries_tiny_bit_exact():
+    _say("summaries: tiny case, 8 priors + current step")
+    w, dc, st = _tiny_prepared()
+    got = dc.qstate.cpu().numpy()
+    np.testing.assert_array_equal(got[w.slot_ids], st[w.slot_ids])
+    others = np.setdiff1d(np.arange(W.SLOTS), w.slot_ids)
+    assert np.isnan(got[others]).all()
+
+
+def test_summaries_bf16_and_poisoned_init():
+    _say("summaries: bf16 queries, one NaN-poisoned slot re-initialised")
+    w = W.qwen3_8b(num_reqs=6, len_lo=40, len_hi=300, budget_choices=(4, 8), free_pages=20)
+    dc = DeviceCase(w)
+    init = np.zeros(w.num_reqs, np.uint8)
+    init[2] = 1
+    qs = w.qstate.copy()
+    qs[w.slot_ids[2]] = np.nan
+    dc.qstate.copy_(torch.from_numpy(qs))
+    ref = O.update_summaries(w.q_pre, "bf16", w.slot_ids, init, qs, *_betas())
+    dc.update_summaries(w.q_pre, init, *_betas())
+    got = dc.qstate.cpu().numpy()
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_decode_tiny_fp32():
+    _say("decode: tiny fp32")
+    w = W.tiny()
+    _decode_check(w, DeviceCase(w))
+
+
+@pytest.mark.parametrize("seed", [2, 12])
+def test_decode_bf16_many_chunks_ragged(seed):
+    _say(f"decode: Qwen3-8B heads, 10 requests, 37..5000 tokens, seed {seed}")
+    w = W.qwen3_8b(seed=seed, num_reqs=10, len_lo=37, len_hi=5000, budget_choices=(3, 40, 400),
+                   free_pages=64)
+    _decode_check(w, DeviceCase(w))
+
+
+def test_decode_fp32_d128_and_bf16_d64():
+    _say("decode: fp32 d128 G4 and bf16 d64 G2 variants")
+    w = W._build(name="f32_d128", seed=21, dtype="f32", Hq=8, Hkv=2, d=128,
+                 n=np.array([1, 15, 16, 17, 255, 256, 257, 700]), budgets=None, free_pages=8,
+                 heavy_mode="scaled", heavy_frac=0.02, summary_mode="random")
+    _decode_check(w, DeviceCase(w))
+    w = W._build(name="bf16_d64", seed=22, dtype="bf16", Hq=4, Hkv=2, d=64,
+                 n=np.array([3, 64, 300, 1025]), budgets=None, free_pages=8,
+                 heavy_mode="scaled", heavy_frac=0.02, summary_mode="random")
+    _decode_check(w, DeviceCase(w))
+
+
+def test_decode_g8_prefix_shared():
+    _say("decode: Qwen3-32B heads (G = 8), shared prefix")
+    w = W.prefix_shared(num_reqs=6, prefix_len=256, tail_lo=20, tail_hi=900, free_pages=50)
+    _decode_check(w, DeviceCase(w))
+
+
+def test_decode_empty_request_gives_zero():
+    _say("decode: a request with no resident token")
+    w = W.qwen3_8b(num_reqs=3, len_lo=40, len_hi=90, budget_choices=(8,), free_pages=4)
+    dc = DeviceCase(w)
+    dc.ps.seq_lens[1] = 0
+    scale = float(np.float32(1 / math.sqrt(128)))
+    got = dc.decode(scale)
+    assert (got[1] == 0).all()
+    sl = w.seq_lens.copy()
+    sl[1] = 0
+    ref = O.decode_attention(PoolView(w, "k"), PoolView(w, "v"), w.dtype, w.page_table, sl,
+                             w.q_post, w.num_q_heads, scale, requests=[0, 2])
+    assert_rows_close(got[[0, 2]], ref[[0, 2]], 2e-2, "decode bf16")
+
+
+def test_boundary_tiny_all_branches():
+    params = {"tau=0": O.Params(), "grow": O.Params(tau=-math.inf), "compress": O.Params(tau=math.inf)}
+    for name, p in params.items():
+        _say(f"boundary: tiny fp32, {name}")
+        w, dc, st = _tiny_prepared()
+        _boundary_check(w, p, qstate_host=st, dc=dc)
+    for fc in (0, 1):
+        _say(f"boundary: tiny fp32, forced grow with {fc} free pages")
+        w, dc, st = _tiny_prepared()
+        res = _boundary_check(w, O.Params(tau=-math.inf), qstate_host=st, dc=dc, free_count=fc)
+        assert (res["decisions"] == ([O.FALLBACK, O.FALLBACK] if fc == 0 else [O.GROW, O.FALLBACK])).all()
+
+
+@pytest.mark.parametrize("tau", [0.0, math.inf])
+def test_boundary_qwen3_8b_reduced(tau):
+    _say(f"boundary: Qwen3-8B heads, 12 requests, tau {tau}")
+    w = W.qwen3_8b(seed=7, num_reqs=12, len_lo=300, len_hi=4000, budget_choices=(8, 60, 200),
+                   boundary_frac=0.5, free_pages=30)
+    assert len(w.boundary) == 6
+    _boundary_check(w, O.Params(tau=tau))
+
+
+def test_boundary_long_reasoning_reduced_split():
+    _say("boundary: long-reasoning shape reduced, every request at a boundary")
+    w = W.long_reasoning(num_reqs=8, len_lo=1500, len_hi=4200, free_pages=40)
+    res = _boundary_check(w, O.Params())
+    _say("decisions", res["decisions"].tolist())
+
+
+@pytest.mark.parametrize("free", [None, 0, 3])
+def test_boundary_high_concurrency_pressure(free):
+    _say(f"boundary: high-concurrency shape reduced, free pages {free}")
+    w = W.high_concurrency(num_reqs=40, median=400, lo=60, hi=3000, boundary_frac=0.25)
+    res = _boundary_check(w, O.Params(tau=-math.inf), free_count=free)
+    if free == 0:
+        assert (res["decisions"] == O.FALLBACK).all()
+
+
+def test_boundary_prefix_shared_replacement_and_preempt():
+    _say("boundary: prefix-shared, compress replaces shared pages")
+    w = W.prefix_shared(num_reqs=8, prefix_len=320, tail_lo=40, tail_hi=1200, boundary_frac=0.5,
+                        free_pages=200)
+    res = _boundary_check(w, O.Params(tau=math.inf))
+    assert (res["decisions"] == O.COMPRESS).all()
+    _say("boundary: prefix-shared with too few free pages -> preempt")
+    _boundary_check(w, O.Params(tau=math.inf), free_count=5)
+
+
+def test_boundary_releases_pages_no_one_else_holds():
+    _say("boundary: two requests sharing a prefix both compress; its pages are released")
+    w = W.prefix_shared(num_reqs=2, prefix_len=64, tail_lo=100, tail_hi=400, boundary_frac=1.0,
+                        free_pages=40)
+    assert len(w.boundary) == 2
+    _boundary_check(w, O.Params(tau=math.inf))
+
+
+def test_boundary_not_at_boundary_and_small_P():
+    _say("boundary: request not at a boundary, and P = 2 (whole first page evicted)")
+    w = W._build(name="edge", seed=31, dtype="bf16", Hq=8, Hkv=2, d=128,
+                 n=np.array([32, 45, 48, 16]), budgets=None, free_pages=6,
+                 heavy_mode="scaled", heavy_frac=0.05, summary_mode="random")
+    bnd = np.array([0, 1, 2, 3], np.int32)
+    res = _boundary_check(w, O.Params(tau=math.inf), bnd=bnd)
+    assert res["decisions"].tolist() == [O.COMPRESS, O.NOT_BOUNDARY, O.COMPRESS, O.GROW]
+    res = _boundary_check(w, O.Params(tau=-math.inf), bnd=bnd)
+    assert res["decisions"].tolist() == [O.GROW, O.NOT_BOUNDARY, O.GROW, O.GROW]
+
+
+def test_determinism_run_twice():
+    _say("determinism: the same boundary event twice gives identical bytes")
+    w = W.qwen3_8b(seed=9, num_reqs=8, len_lo=200, len_hi=3000, budget_choices=(20, 100),
+                   boundary_frac=0.5, free_pages=20)
+    outs = []
+    for _ in range(2):
+        dc = DeviceCase(w)
+        o = dc.decode(float(np.float32(1 / math.sqrt(128))))
+        res = dc.boundary(O.Params())
+        gs = dc.host_state()
+        kv = [dc.gather(gs.page_table[r], int(gs.seq_lens[r]), "k") for r in w.boundary]
+        outs.append((o, res, gs, kv))
+    a, b = outs
+    assert np.array_equal(a[0], b[0])
+    for key in ("k_counts", "scores", "decisions", "delta"):
+        assert np.array_equal(a[1][key], b[1][key])
+    assert np.array_equal(a[2].page_table, b[2].page_table)
+    assert all(np.array_equal(x, y) for x, y in zip(a[3], b[3]))
+
+
+# --------------------------------------------------- full benchmark shape --
+
+def test_full_qwen3_8b_sampled():
+    """The benchmark's workload at full size (64 requests, 32/8 heads, 200k free
+    pages), in the launch configuration the benchmark times: decode attention
+    checked on 8 sampled requests (all heads), the boundary event checked in
+    full on its 4 boundary requests."""
+    _say("full Qwen3-8B layer: generating inputs")
+    w = W.qwen3_8b()
+    dc = DeviceCase(w, poison_free_pages=False)
+    rng = np.random.default_rng(0)
+    sample = sorted(set(rng.choice(w.num_reqs, 6, replace=False).tolist()) | set(w.boundary[:2].tolist()))
+    _say("full Qwen3-8B layer: decode attention, sampled requests", sample)
+    _decode_check(w, dc, requests=sample)
+    _say("full Qwen3-8B layer: boundary event on", w.boundary.tolist())
+    # the oracle works on the boundary requests' pages only
+    res_g = dc.boundary(O.Params())
+    p32 = O.Params().as_f32(128)
+    st = oracle_state(w)
+    counts = []
+    for i, r in enumerate(w.boundary):
+        P = int(w.num_pages[r])
+        toks = O.gather_tokens(PoolView(w, "k"), w.page_table[r], P * 16, 16)
+        c, s, a32 = O.score_request(toks, "bf16", P, 16, w.q_pre[r], w.qstate[w.slot_ids[r]],
+                                    int(w.positions[r]), p32, p32.scale)
+        for h in range(8):
+            for x in range(2):
+                if not O.top_p_fragile(a32[x, h], p32.p):
+                    assert res_g["k_counts"][0, i, h, x] == c[h, x]
+            np.testing.assert_allclose(res_g["scores"][0, i, h, : (P - 1) * 16], s[h], rtol=1e-5, atol=0)
+        counts.append(c[None])
+    dec, delta = O.decide_and_allocate(st, w.boundary, counts, 16, p32)
+    assert np.array_equal(res_g["decisions"], dec)
+    gs = dc.host_state()
+    np.testing.assert_array_equal(gs.page_table, st.page_table)
+    np.testing.assert_array_equal(gs.seq_lens, st.seq_lens)
+    assert gs.free_count == st.free_count
+    _say("decisions", dec.tolist())
