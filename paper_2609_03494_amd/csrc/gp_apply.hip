@@ -107,7 +107,10 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
         s_flags[i] = flags;
         s_nsh[i] = nsh;
     }
-    if (tid == 0) s_fc0 = *a.free_count;
+    if (tid == 0) {
+        const int fc = *a.free_count;
+        s_fc0 = fc < 0 ? 0 : (fc > a.pool_pages ? a.pool_pages : fc);
+    }
     __syncthreads();
 
     if (tid == 0) {
@@ -159,7 +162,7 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
         if (dec == GP_GROW) {
             const int pid = a.free_list[fc0 - 1 - s_pop[i]];
             a.page_table[(size_t)r * a.max_pages + P] = pid;
-            a.refcount[pid] = 1;
+            if (pid >= 0 && pid < a.pool_pages) a.refcount[pid] = 1;
             a.num_pages[r] = P + 1;
         } else if (compressing(dec)) {
             a.seq_lens[r] = (P - 1) * kPage;
@@ -204,7 +207,7 @@ __global__ __launch_bounds__(256) void replace_kernel(ApplyArgs a) {
         const int k = base + s_scan[threadIdx.x] - 1;
         const int pid = a.free_list[a.hdr[HDR_FC0] - 1 - rq[RQ_POP] - k];
         row[j] = pid;
-        a.refcount[pid] = 1;
+        if (pid >= 0 && pid < a.pool_pages) a.refcount[pid] = 1;
     }
 }
 
@@ -322,6 +325,7 @@ __global__ __launch_bounds__(256) void select_kernel(ApplyArgs a, LayerTable lt)
         const int w = u % UPP;
         const int lp = b * kCompactChunk / kPage - 1;
         const int phys = src_row[lp];
+        if (phys < 0 || phys >= a.pool_pages) continue;
         const unsigned char *src = (kv ? vp : kp) + (size_t)phys * page_bytes + head_bytes + (size_t)w * 16;
         *reinterpret_cast<uint4 *>(bd + ((size_t)b * 2 + kv) * kPage * D * E + (size_t)w * 16) =
             *reinterpret_cast<const uint4 *>(src);
@@ -353,7 +357,7 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
                 const int id = s_rel[k];
                 int rank = 0;
                 for (int u = 0; u < n; ++u) rank += a.released[u] < id ? 1 : 0;
-                a.free_list[fc1 + rank] = id;
+                if (fc1 + rank < a.pool_pages) a.free_list[fc1 + rank] = id;
             }
             __syncthreads();
         }
@@ -391,9 +395,10 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
             if (!gone) {
                 const int d = s - before;
                 const int sp = src_row[s / kPage], dp = row[d / kPage];
+                const bool ok = sp >= 0 && sp < a.pool_pages && dp >= 0 && dp < a.pool_pages;
                 const long long so = (long long)sp * page_bytes + head_bytes + (long long)(s % kPage) * D * E;
                 const long long dof = (long long)dp * page_bytes + head_bytes + (long long)(d % kPage) * D * E;
-                if (so != dof) {
+                if (ok && so != dof) {
                     dst = d;
                     s_src_off[tid] = so;
                     s_dst_off[tid] = dof;
