@@ -11,8 +11,7 @@
 // wave-uniform per page so that each lane can keep partial sums over its own
 // tokens.  Waves take pages round-robin and two pages are in flight per wave.
 // The four waves merge through LDS; a request that spans several chunks
-// writes (max, sum, o) partials and the last workgroup of (r, h) to finish,
-// found with an atomic counter, merges them and resets the counter to zero.
+// writes (max, sum, o) partials that a second, small kernel merges.
 //
 // Bound: HBM.  Algorithmic bytes per resident token and KV head:
 // 2 * d * sizeof(elem) (K and V), plus the page-table entries, q and out.
@@ -64,7 +63,6 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 
     __shared__ float s_m[NW][G], s_l[NW][G];
     __shared__ float s_o[NW][G][D];
-    __shared__ int s_last;
 
     const int chunk = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -245,47 +243,53 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
             }
         }
     }
-    if (single) return;
+}
 
-    // last workgroup of (r, h) merges every chunk's partial
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const uint32_t prev = __hip_atomic_fetch_add(a.counters + (size_t)r * Hkv + h, 1u,
-                                                     __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = (prev == (uint32_t)(nchunks - 1)) ? 1 : 0;
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    const float *base = a.partial + ((size_t)r * Hkv + h) * a.max_chunks * G * (D + 2);
+// Second pass for requests that span several chunks: one workgroup per
+// (KV head, request) merges the chunks' (max, sum, o) partials.  Running it
+// as its own launch lets the kernel boundary publish the partials; a
+// device-scope fence per workgroup would write back and invalidate the L2 of
+// every XCD thousands of times per step.
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
+    using Tr = Traits<T>;
+    constexpr int CHUNK = kDecodeChunkPages * kPage;
+    const int h = blockIdx.x, r = blockIdx.y;
+    int P = a.num_pages[r];
+    P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
+    int m = a.seq_lens[r];
+    m = m < 0 ? 0 : (m > P * kPage ? P * kPage : m);
+    const int nchunks = cdiv(m, CHUNK);
+    if (nchunks <= 1) return;
+    const int Hq = a.Hkv * G;
+    T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
+    const float *base = a.partial + ((size_t)r * a.Hkv + h) * a.max_chunks * G * (D + 2);
     for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
         const int g = i / D, dd = i % D;
         float M = kNegInf;
-        for (int k = 0; k < nchunks; ++k) {
-            const float *pk = base + ((size_t)k * G + g) * (D + 2);
-            M = fmaxf(M, __builtin_nontemporal_load(pk + D));
-        }
+        for (int k = 0; k < nchunks; ++k) M = fmaxf(M, base[((size_t)k * G + g) * (D + 2) + D]);
         float Ls = 0.0f, Os = 0.0f;
         for (int k = 0; k < nchunks; ++k) {
             const float *pk = base + ((size_t)k * G + g) * (D + 2);
-            const float mk = __builtin_nontemporal_load(pk + D);
-            const float f = mk == kNegInf ? 0.0f : exp2f(mk - M);
-            Ls += __builtin_nontemporal_load(pk + D + 1) * f;
-            Os += __builtin_nontemporal_load(pk + dd) * f;
+            const float f = pk[D] == kNegInf ? 0.0f : exp2f(pk[D] - M);
+            Ls += pk[D + 1] * f;
+            Os += pk[dd] * f;
         }
         Tr::store(out + (size_t)g * D + dd, Os / Ls);
     }
-    if (threadIdx.x == 0) a.counters[(size_t)r * Hkv + h] = 0u;
 }
 
 template <typename T, int D>
 hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, hipStream_t s) {
+    dim3 mgrid(a.Hkv, a.R);
     switch (G) {
-        case 1: decode_kernel<T, D, 1><<<grid, 256, 0, s>>>(a); break;
-        case 2: decode_kernel<T, D, 2><<<grid, 256, 0, s>>>(a); break;
-        case 4: decode_kernel<T, D, 4><<<grid, 256, 0, s>>>(a); break;
-        case 8: decode_kernel<T, D, 8><<<grid, 256, 0, s>>>(a); break;
+#define GP_CASE(GG)                                                  \
+    case GG:                                                         \
+        decode_kernel<T, D, GG><<<grid, 256, 0, s>>>(a);             \
+        if (a.max_chunks > 1) merge_kernel<T, D, GG><<<mgrid, 256, 0, s>>>(a); \
+        break;
+        GP_CASE(1) GP_CASE(2) GP_CASE(4) GP_CASE(8)
+#undef GP_CASE
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
