@@ -264,6 +264,24 @@ template <int N>
 __device__ inline float dpp_ror(float x) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x120 + N, 0xf, 0xf, false));
 }
+#ifndef GP_DECODE_PREFETCH
+#define GP_DECODE_PREFETCH 0
+#endif
+#ifndef GP_DECODE_NT
+#define GP_DECODE_NT 0
+#endif
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// 16-byte load of streamed K/V data.
+__device__ inline uint4 ld16(const uint16_t *p) {
+#if GP_DECODE_NT
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+#else
+    return *reinterpret_cast<const uint4 *>(p);
+#endif
+}
+
 // LDS traffic between lanes of one wave: wait for the wave's LDS operations
 // and keep the compiler from moving memory accesses across this point.
 __device__ inline void wave_lds_sync() { __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
@@ -291,7 +309,7 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     constexpr int HR = (G + 3) / 4;       // lane rows that carry real heads
     constexpr int GI = G < 4 ? G : 4;     // heads per lane row
     constexpr int NW = 4;
-    constexpr int NP = 2;                 // pages per iteration and wave
+    constexpr int NP = kDecodeInFlight;   // pages per iteration and wave
     constexpr int CHUNK = kDecodeChunkPages * kPage;
 
     __shared__ float s_m[NW][G], s_l[NW][G];
@@ -353,25 +371,52 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     const int k_off = n * D + kg * KSPAN;
     const int v_off = vrow * D + vc * 8;
 
-    for (int p0 = page_begin + wave; p0 < page_end; p0 += NP * NW) {
-        uint4 kb[NP][KK], vb[NP][LPP];
-        int ntok[NP];
+    // page ids of the chunk: one per lane, read once; a wave picks its page
+    // with a uniform lane read
+    constexpr int IDS = (kDecodeChunkPages + 63) / 64;
+    int ids[IDS];
+#pragma unroll
+    for (int w8 = 0; w8 < IDS; ++w8) {
+        const int pi = page_begin + w8 * 64 + lane;
+        ids[w8] = pi < page_end ? table[pi] : -1;
+    }
+    auto load_pages = [&](int pstart, uint4 (&kb)[NP][KK], uint4 (&vb)[NP][LPP], int (&ntok)[NP]) {
 #pragma unroll
         for (int u = 0; u < NP; ++u) {
-            const int p = p0 + u * NW;
-            const int phys = p < page_end ? table[p] : -1;
+            const int p = pstart + u * NW;
+            int phys = -1;
+            if (p < page_end) {
+                const int rel = p - page_begin;
+#pragma unroll
+                for (int w8 = 0; w8 < IDS; ++w8)
+                    if (rel >= w8 * 64 && rel < w8 * 64 + 64) phys = __builtin_amdgcn_readlane(ids[w8], rel - w8 * 64);
+            }
             const bool ok = phys >= 0 && phys < a.pool_pages;
             ntok[u] = ok ? min(kPage, m - p * kPage) : 0;
             const size_t base = (size_t)(ok ? phys : 0) * page_elems + head_off;
             if (ok) {
 #pragma unroll
-                for (int kk = 0; kk < KK; ++kk)
-                    kb[u][kk] = *reinterpret_cast<const uint4 *>(kpool + base + k_off + kk * 8);
+                for (int kk = 0; kk < KK; ++kk) kb[u][kk] = ld16(kpool + base + k_off + kk * 8);
 #pragma unroll
-                for (int j = 0; j < LPP; ++j)
-                    vb[u][j] = *reinterpret_cast<const uint4 *>(vpool + base + v_off + (size_t)j * TPL * D);
+                for (int j = 0; j < LPP; ++j) vb[u][j] = ld16(vpool + base + v_off + (size_t)j * TPL * D);
             }
         }
+    };
+
+    uint4 kb[NP][KK], vb[NP][LPP];
+    int ntok[NP];
+    int p0 = page_begin + wave;
+#pragma unroll
+    for (int u = 0; u < NP; ++u) ntok[u] = 0;
+    if (p0 < page_end) load_pages(p0, kb, vb, ntok);
+    for (; p0 < page_end; p0 += NP * NW) {
+#if GP_DECODE_PREFETCH
+        uint4 kn[NP][KK], vn[NP][LPP];
+        int ntn[NP];
+#pragma unroll
+        for (int u = 0; u < NP; ++u) ntn[u] = 0;
+        if (p0 + NP * NW < page_end) load_pages(p0 + NP * NW, kn, vn, ntn);
+#endif
         // scores of NP pages; token n of page u, head 4*kg + i in s[u][i]
         float s[NP][GI];
 #pragma unroll
@@ -445,6 +490,20 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
             }
         }
         wave_lds_sync();
+#if GP_DECODE_PREFETCH
+#pragma unroll
+        for (int u = 0; u < NP; ++u) {
+            ntok[u] = ntn[u];
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) kb[u][kk] = kn[u][kk];
+#pragma unroll
+            for (int j = 0; j < LPP; ++j) vb[u][j] = vn[u][j];
+        }
+#else
+#pragma unroll
+        for (int u = 0; u < NP; ++u) ntok[u] = 0;
+        if (p0 + NP * NW < page_end) load_pages(p0 + NP * NW, kb, vb, ntok);
+#endif
     }
 
     // finish the wave: sums over the token rows of both layouts
@@ -506,6 +565,9 @@ template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     using Tr = Traits<T>;
     constexpr int CHUNK = kDecodeChunkPages * kPage;
+    constexpr int MAXC = kMaxDecodeChunks;
+    __shared__ float s_f[MAXC][G];                 // exp2(m_k - M) / L per chunk and head
+    __shared__ float s_ml[MAXC][G][2];
     const int h = blockIdx.x, r = blockIdx.y;
     int P = a.num_pages[r];
     P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
@@ -516,18 +578,34 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     const int Hq = a.Hkv * G;
     T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     const float *base = a.partial + ((size_t)r * a.Hkv + h) * a.max_chunks * G * (D + 2);
-    for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
-        const int g = i / D, dd = i % D;
+    const int tid = threadIdx.x;
+    // all (max, sum) pairs at once, then one thread per head folds them
+    for (int t = tid; t < nchunks * G && t < MAXC * G; t += blockDim.x) {
+        const int k = t / G, g = t % G;
+        s_ml[k][g][0] = base[((size_t)k * G + g) * (D + 2) + D];
+        s_ml[k][g][1] = base[((size_t)k * G + g) * (D + 2) + D + 1];
+    }
+    __syncthreads();
+    const int nc = nchunks < MAXC ? nchunks : MAXC;
+    if (tid < G) {
         float M = kNegInf;
-        for (int k = 0; k < nchunks; ++k) M = fmaxf(M, base[((size_t)k * G + g) * (D + 2) + D]);
-        float Ls = 0.0f, Os = 0.0f;
-        for (int k = 0; k < nchunks; ++k) {
-            const float *pk = base + ((size_t)k * G + g) * (D + 2);
-            const float f = pk[D] == kNegInf ? 0.0f : exp2f(pk[D] - M);
-            Ls += pk[D + 1] * f;
-            Os += pk[dd] * f;
+        for (int k = 0; k < nc; ++k) M = fmaxf(M, s_ml[k][tid][0]);
+        float L = 0.0f;
+        for (int k = 0; k < nc; ++k) {
+            const float f = s_ml[k][tid][0] == kNegInf ? 0.0f : exp2f(s_ml[k][tid][0] - M);
+            s_f[k][tid] = f;
+            L += s_ml[k][tid][1] * f;
         }
-        Tr::store(out + (size_t)g * D + dd, Os / Ls);
+        const float inv = 1.0f / L;
+        for (int k = 0; k < nc; ++k) s_f[k][tid] *= inv;
+    }
+    __syncthreads();
+    for (int i = tid; i < G * D; i += blockDim.x) {
+        const int g = i / D, dd = i % D;
+        float Os = 0.0f;
+#pragma unroll 8
+        for (int k = 0; k < nc; ++k) Os += base[((size_t)k * G + g) * (D + 2) + dd] * s_f[k][g];
+        Tr::store(out + (size_t)g * D + dd, Os);
     }
 }
 

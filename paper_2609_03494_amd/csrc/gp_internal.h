@@ -12,7 +12,15 @@
 namespace gp {
 
 constexpr int kPage = 16;                 // tokens per page
-constexpr int kDecodeChunkPages = 16;     // pages per decode work item (split-K)
+#ifndef GP_DECODE_CHUNK_PAGES
+#define GP_DECODE_CHUNK_PAGES 64
+#endif
+#ifndef GP_DECODE_PAGES_IN_FLIGHT
+#define GP_DECODE_PAGES_IN_FLIGHT 2
+#endif
+constexpr int kDecodeChunkPages = GP_DECODE_CHUNK_PAGES;   // pages per decode work item (split-K)
+constexpr int kDecodeInFlight = GP_DECODE_PAGES_IN_FLIGHT; // pages per wave per iteration
+constexpr int kMaxDecodeChunks = 128;                      // chunks one request may span
 constexpr int kScoreChunk = 256;          // candidate tokens per scoring work item
 constexpr int kProbChunk = 1024;          // tokens per weight/score work item
 constexpr int kCompactChunk = 256;        // slots per compaction work item
