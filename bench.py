@@ -77,9 +77,18 @@ def main():
     k.index_copy_(0, idx, bf(w.k_data[w.page_row[ids]]))
     v.index_copy_(0, idx, bf(w.v_data[w.page_row[ids]]))
     kv = gp.KVLayer(k, v)
-    pristine = dict(page_table=i32(w.page_table), num_pages=i32(w.num_pages), seq_lens=i32(w.seq_lens),
-                    refcount=i32(w.refcount), free_list=i32(w.free_list), free_count=i32([w.free_count]))
-    ps = gp.PageState(**{n: t.clone() for n, t in pristine.items()})
+    # all page metadata in one int32 buffer, so that the per-step restore is one copy
+    parts = dict(page_table=w.page_table, num_pages=w.num_pages, seq_lens=w.seq_lens,
+                 refcount=w.refcount, free_list=w.free_list, free_count=np.array([w.free_count]))
+    flat = np.concatenate([np.asarray(v, np.int32).ravel() for v in parts.values()])
+    meta0 = i32(flat)
+    meta = meta0.clone()
+    views, off = {}, 0
+    for name, arr in parts.items():
+        n = int(np.asarray(arr).size)
+        views[name] = meta[off: off + n].view(np.asarray(arr).shape)
+        off += n
+    ps = gp.PageState(**views)
     qstate0 = torch.from_numpy(w.qstate).to(dev)
     qstate = qstate0.clone()
     slots, positions = i32(w.slot_ids), i32(w.positions)
@@ -101,8 +110,7 @@ def main():
     stream = torch.cuda.current_stream()
 
     def restore():
-        for n, t in pristine.items():
-            getattr(ps, n).copy_(t, non_blocking=True)
+        meta.copy_(meta0, non_blocking=True)
         qstate.copy_(qstate0, non_blocking=True)
 
     ev = {}

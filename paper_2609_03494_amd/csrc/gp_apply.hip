@@ -224,6 +224,25 @@ __device__ inline void insert16(unsigned long long (&best)[kPage], unsigned long
     }
 }
 
+// A <- the 16 smallest of two ascending 16-lists, ascending.  A[k] vs B[15-k]
+// keeps the lower half of the bitonic sequence A ++ reverse(B); four
+// half-cleaner stages (distances 8, 4, 2, 1) sort it.  All indices are static,
+// so the lists stay in registers.
+__device__ inline void merge16(unsigned long long (&A)[kPage], const unsigned long long (&B)[kPage]) {
+#pragma unroll
+    for (int k = 0; k < kPage; ++k) A[k] = A[k] < B[kPage - 1 - k] ? A[k] : B[kPage - 1 - k];
+#pragma unroll
+    for (int s = kPage / 2; s >= 1; s >>= 1)
+#pragma unroll
+        for (int k = 0; k < kPage; ++k)
+            if ((k & s) == 0) {
+                const unsigned long long lo = A[k] < A[k + s] ? A[k] : A[k + s];
+                const unsigned long long hi = A[k] < A[k + s] ? A[k + s] : A[k];
+                A[k] = lo;
+                A[k + s] = hi;
+            }
+}
+
 template <int D, int E>
 __global__ __launch_bounds__(256) void select_kernel(ApplyArgs a, LayerTable lt) {
     __shared__ unsigned long long s_keys[256][kPage];
@@ -273,20 +292,15 @@ __global__ __launch_bounds__(256) void select_kernel(ApplyArgs a, LayerTable lt)
     __syncthreads();
     for (int stride = 128; stride >= 1; stride >>= 1) {
         if (tid < stride) {
-            // keep the 16 smallest of two ascending lists; at most 15 are taken
-            // from either list before the 16th pick, so no index runs past 15
-            unsigned long long M[kPage];
-            int ia = 0, ib = 0;
+            unsigned long long A[kPage], B[kPage];
 #pragma unroll
             for (int k = 0; k < kPage; ++k) {
-                const unsigned long long x = s_keys[tid][ia], y = s_keys[tid + stride][ib];
-                const bool ta = x <= y;
-                M[k] = ta ? x : y;
-                ia += ta ? 1 : 0;
-                ib += ta ? 0 : 1;
+                A[k] = s_keys[tid][k];
+                B[k] = s_keys[tid + stride][k];
             }
+            merge16(A, B);
 #pragma unroll
-            for (int k = 0; k < kPage; ++k) s_keys[tid][k] = M[k];
+            for (int k = 0; k < kPage; ++k) s_keys[tid][k] = A[k];
         }
         __syncthreads();
     }
@@ -319,16 +333,32 @@ __global__ __launch_bounds__(256) void select_kernel(ApplyArgs a, LayerTable lt)
     const size_t page_bytes = (size_t)a.Hkv * kPage * D * E;
     const size_t head_bytes = (size_t)h * kPage * D * E;
     unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc) * 2 * kPage * D * E;
-    for (int u = tid; u < (nb - 1) * 2 * UPP; u += blockDim.x) {
-        const int b = 1 + u / (2 * UPP);
-        const int kv = (u / UPP) & 1;
-        const int w = u % UPP;
-        const int lp = b * kCompactChunk / kPage - 1;
-        const int phys = src_row[lp];
-        if (phys < 0 || phys >= a.pool_pages) continue;
-        const unsigned char *src = (kv ? vp : kp) + (size_t)phys * page_bytes + head_bytes + (size_t)w * 16;
-        *reinterpret_cast<uint4 *>(bd + ((size_t)b * 2 + kv) * kPage * D * E + (size_t)w * 16) =
-            *reinterpret_cast<const uint4 *>(src);
+    const int units = (nb - 1) * 2 * UPP;
+    for (int base = 0; base < units; base += 256 * 8) {
+        uint4 val[8];
+        size_t dst[8];
+        bool ok[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int u = base + k * 256 + tid;
+            ok[k] = false;
+            if (u < units) {
+                const int b = 1 + u / (2 * UPP);
+                const int kv = (u / UPP) & 1;
+                const int w = u % UPP;
+                const int lp = b * kCompactChunk / kPage - 1;
+                const int phys = src_row[lp];
+                if (phys >= 0 && phys < a.pool_pages) {
+                    ok[k] = true;
+                    val[k] = *reinterpret_cast<const uint4 *>((kv ? vp : kp) + (size_t)phys * page_bytes +
+                                                              head_bytes + (size_t)w * 16);
+                    dst[k] = ((size_t)b * 2 + kv) * kPage * D * E + (size_t)w * 16;
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+            if (ok[k]) *reinterpret_cast<uint4 *>(bd + dst[k]) = val[k];
     }
 }
 

@@ -51,7 +51,7 @@ __host__ __device__ inline DecodeWs decode_ws(int R, int Hq, int Hkv, int D, int
 }
 
 struct ScoreWs {
-    size_t logits, part, weights, total;
+    size_t qt, logits, part, weights, total;
     int cmax, nch;
 };
 
@@ -62,6 +62,8 @@ __host__ __device__ inline ScoreWs score_ws(int Rb, int Hq, int Hkv, int max_pag
     w.cmax = max_pages > 1 ? (max_pages - 1) * kPage : 0;
     w.nch = cdiv(w.cmax > 0 ? w.cmax : 1, kScoreChunk);
     size_t off = 0;
+    w.qt = off;       // [Rb][Hkv][2G][D] double: calibrated, rotated summaries
+    off = align_up(off + (size_t)Rb * Hkv * 2 * G * 128 * sizeof(double));
     w.logits = off;   // [Rb][Hkv][2G][cmax] double
     off = align_up(off + (size_t)Rb * Hkv * 2 * G * w.cmax * sizeof(double));
     w.part = off;     // [Rb][Hkv][nch][2G][2] double (running max, sum of exp)
@@ -137,7 +139,7 @@ struct ScoreArgs {
     const int32_t *slot_ids, *positions, *bnd;
     int32_t *k_counts;
     float *scores;
-    double *logits, *part;
+    double *qt, *logits, *part;
     float *weights;
     int Rb, Hq, Hkv, M, max_pages, pool_pages, max_cand, cmax, nch, R;
     double scale, theta, p;

@@ -63,29 +63,26 @@ __device__ inline bool boundary_of(const ScoreArgs &a, int i, int &r, int &P) {
 // Products and sums are rounded one at a time, as in a plain fp64 evaluation.
 #pragma clang fp contract(off)
 
+// --------------------------------------------------------------------- prep --
+// One workgroup per (boundary request, KV head): the 2G summaries of its GQA
+// group scaled to the RMS of the current query (RMS calibration) and rotated
+// at the current position; angles pos * theta^(-2k/D) and their sine and
+// cosine are computed in fp64 on the device.
 template <typename T, int D, int G>
-__global__ __launch_bounds__(256) void logits_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(256) void prep_kernel(ScoreArgs a) {
     constexpr int V = 2 * G;
     constexpr int H = D / 2;
     __shared__ double s_q[V][D];
     __shared__ double s_qt[G][D];
     __shared__ double s_cos[H], s_sin[H];
     __shared__ double s_ss[3 * G];
-    __shared__ double s_red[256 / 64][V];
-    __shared__ double s_max[V];
-
-    const int chunk = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    const int h = blockIdx.x, i = blockIdx.y;
     int r, P;
     if (!boundary_of(a, i, r, P)) return;
-    const int C = (P - 1) * kPage;
-    const int t0 = chunk * kScoreChunk;
-    if (t0 >= C) return;
-    const int tid = threadIdx.x;
-    const int Hq = a.Hkv * G;
     const int slot = a.slot_ids[r];
     if (slot < 0 || slot >= a.M) return;
-
-    // summaries and current query of the GQA group
+    const int tid = threadIdx.x;
+    const int Hq = a.Hkv * G;
     const float *qs = a.qstate + (size_t)slot * 2 * Hq * D;
     const T *qp = reinterpret_cast<const T *>(a.q_pre) + (size_t)r * Hq * D;
     for (int e = tid; e < V * D; e += blockDim.x) {
@@ -103,46 +100,84 @@ __global__ __launch_bounds__(256) void logits_kernel(ScoreArgs a) {
         s_sin[k] = sin(ang);
     }
     __syncthreads();
-    if (tid < 3 * G) {
-        const double *src = tid < V ? s_q[tid] : s_qt[tid - V];
+    // 3G sums of squares, 8 lanes each
+    if (tid < 3 * G * 8) {
+        const int which = tid / 8, part = tid % 8;
+        const double *src = which < V ? s_q[which] : s_qt[which - V];
         double acc = 0.0;
-        for (int d = 0; d < D; ++d) acc += src[d] * src[d];
-        s_ss[tid] = acc;
+#pragma unroll
+        for (int d = part * (D / 8); d < (part + 1) * (D / 8); ++d) acc += src[d] * src[d];
+        acc += __shfl_xor(acc, 1, 8);
+        acc += __shfl_xor(acc, 2, 8);
+        acc += __shfl_xor(acc, 4, 8);
+        if (part == 0) s_ss[which] = acc;
     }
     __syncthreads();
-    // gamma = RMS(q_t) / RMS(qbar); a summary with zero RMS stays zero
+    double *out = a.qt + ((size_t)i * a.Hkv + h) * V * D;
     for (int e = tid; e < V * H; e += blockDim.x) {
         const int v = e / H, k = e % H, g = v % G;
         const double den = s_ss[v];
         const double gam = den == 0.0 ? 0.0 : sqrt(s_ss[V + g] / D) / sqrt(den / D);
         const double x1 = gam * s_q[v][k], x2 = gam * s_q[v][k + H];
-        s_q[v][k] = x1 * s_cos[k] - x2 * s_sin[k];
-        s_q[v][k + H] = x2 * s_cos[k] + x1 * s_sin[k];
+        out[(size_t)v * D + k] = x1 * s_cos[k] - x2 * s_sin[k];
+        out[(size_t)v * D + k + H] = x2 * s_cos[k] + x1 * s_sin[k];
     }
-    __syncthreads();
+}
 
-    // one candidate token per thread
+// ------------------------------------------------------------------- logits --
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256) void logits_kernel(ScoreArgs a) {
+    constexpr int V = 2 * G;
+    constexpr int EPV = KRow<T>::EPV;
+    constexpr int NV = D / EPV;                      // 16-byte units per key row
+    __shared__ double s_q[V][D];
+    __shared__ double s_red[256 / 64][V];
+    __shared__ double s_max[V];
+
+    const int chunk = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    int r, P;
+    if (!boundary_of(a, i, r, P)) return;
+    const int C = (P - 1) * kPage;
+    const int t0 = chunk * kScoreChunk;
+    if (t0 >= C) return;
+    const int slot = a.slot_ids[r];
+    if (slot < 0 || slot >= a.M) return;
+    const int tid = threadIdx.x;
+
+    // the key row of this thread's candidate, read whole before any use
     const int t = t0 + tid;
     const bool live = t < C && tid < kScoreChunk;
     double z[V];
 #pragma unroll
     for (int v = 0; v < V; ++v) z[v] = 0.0;
+    bool have = false;
+    uint4 krow[NV];
     if (live) {
         const int phys = a.page_table[(size_t)r * a.max_pages + t / kPage];
         if (phys >= 0 && phys < a.pool_pages) {
-            const T *kp = reinterpret_cast<const T *>(a.k) +
-                          (((size_t)phys * a.Hkv + h) * kPage + (t % kPage)) * D;
-            constexpr int EPV = KRow<T>::EPV;
-#pragma unroll 2
-            for (int d0 = 0; d0 < D; d0 += EPV) {
-                double kf[EPV];
-                KRow<T>::get(kp + d0, kf);
+            have = true;
+            const uint4 *kp = reinterpret_cast<const uint4 *>(reinterpret_cast<const T *>(a.k) +
+                              (((size_t)phys * a.Hkv + h) * kPage + (t % kPage)) * D);
 #pragma unroll
-                for (int v = 0; v < V; ++v)
-#pragma unroll
-                    for (int e = 0; e < EPV; ++e) z[v] += s_q[v][d0 + e] * kf[e];
-            }
+            for (int u = 0; u < NV; ++u) krow[u] = kp[u];
         }
+    }
+    const double *qt = a.qt + ((size_t)i * a.Hkv + h) * V * D;
+    for (int e = tid; e < V * D; e += blockDim.x) s_q[e / D][e % D] = qt[e];
+    __syncthreads();
+
+    if (have) {
+#pragma unroll
+        for (int u = 0; u < NV; ++u) {
+            double kf[EPV];
+            KRow<T>::get(reinterpret_cast<const T *>(&krow[u]), kf);
+#pragma unroll
+            for (int v = 0; v < V; ++v)
+#pragma unroll
+                for (int e = 0; e < EPV; ++e) z[v] += s_q[v][u * EPV + e] * kf[e];
+        }
+    }
+    if (live) {
 #pragma unroll
         for (int v = 0; v < V; ++v) z[v] *= a.scale;
         double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax + t;
@@ -181,6 +216,7 @@ __global__ __launch_bounds__(256) void logits_kernel(ScoreArgs a) {
     }
 }
 
+// ------------------------------------------------------------------ weights --
 template <int G>
 __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
     constexpr int V = 2 * G;
@@ -193,15 +229,23 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
     if (t0 >= C) return;
     const int tid = threadIdx.x;
     const int used = cdiv(C, kScoreChunk);
-    if (tid < V) {
-        const double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch) * V * 2;
-        double M = -__builtin_huge_val();
-        for (int c = 0; c < used; ++c) M = fmax(M, pt[((size_t)c * V + tid) * 2]);
-        double L = 0.0;
-        for (int c = 0; c < used; ++c)
-            L += pt[((size_t)c * V + tid) * 2 + 1] * exp(pt[((size_t)c * V + tid) * 2] - M);
-        s_M[tid] = M;
-        s_L[tid] = L;
+    const double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch) * V * 2;
+    // merge the chunk statistics: 32 lanes per view, views 8 at a time
+    for (int vb = 0; vb < V; vb += 8) {
+        const int v = vb + tid / 32, c0 = tid % 32;
+        if (v < V) {
+            double M = -__builtin_huge_val();
+            for (int c = c0; c < used; c += 32) M = fmax(M, pt[((size_t)c * V + v) * 2]);
+            for (int off = 16; off >= 1; off >>= 1) M = fmax(M, __shfl_xor(M, off, 32));
+            double L = 0.0;
+            for (int c = c0; c < used; c += 32)
+                L += pt[((size_t)c * V + v) * 2 + 1] * exp(pt[((size_t)c * V + v) * 2] - M);
+            for (int off = 16; off >= 1; off >>= 1) L += __shfl_xor(L, off, 32);
+            if (c0 == 0) {
+                s_M[v] = M;
+                s_L[v] = L;
+            }
+        }
     }
     __syncthreads();
     const double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax;
@@ -229,33 +273,21 @@ __device__ inline unsigned long long fixed60(uint32_t bits) {
     return (unsigned long long)ldexp((double)__uint_as_float(bits), 60);
 }
 
-// Inclusive scan of 256 per-thread values in thread order (Hillis-Steele in LDS).
-__device__ inline unsigned long long block_scan_u64(unsigned long long x, unsigned long long *buf) {
-    const int tid = threadIdx.x;
-    buf[tid] = x;
-    __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {
-        const unsigned long long y = tid >= off ? buf[tid - off] : 0ull;
-        __syncthreads();
-        buf[tid] += y;
-        __syncthreads();
-    }
-    const unsigned long long out = buf[tid];
-    __syncthreads();
-    return out;
-}
-
-__global__ __launch_bounds__(256) void top_p_kernel(ScoreArgs a) {
+// -------------------------------------------------------------------- top-p --
+// One workgroup of 1024 threads per (boundary request, KV head, view).  Each of
+// the three radix passes histograms the weights that share the prefix found so
+// far (count and 2^-60 fixed-point mass per bucket), then wave 0 scans the
+// buckets from the top to find the one where the running mass reaches p.
+__global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
     constexpr int NB = 2048;
     __shared__ unsigned int s_cnt[NB];
     __shared__ unsigned long long s_mass[NB];
-    __shared__ unsigned long long s_scan[256];
     __shared__ int s_bucket;
     __shared__ unsigned long long s_above_mass;
     __shared__ unsigned int s_above_cnt;
 
     const int x = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
     int32_t *out = a.k_counts + ((size_t)i * a.Hkv + h) * 2 + x;
     int r, P;
     if (!boundary_of(a, i, r, P)) {
@@ -273,41 +305,66 @@ __global__ __launch_bounds__(256) void top_p_kernel(ScoreArgs a) {
     const int nbits[3] = {11, 11, 9};
     for (int pass = 0; pass < 3; ++pass) {
         const int sh = shifts[pass], nb = 1 << nbits[pass];
-        for (int b = tid; b < nb; b += 256) {
+        for (int b = tid; b < nb; b += blockDim.x) {
             s_cnt[b] = 0;
             s_mass[b] = 0;
         }
         __syncthreads();
-        for (int t = tid; t < C; t += 256) {
-            const uint32_t u = __float_as_uint(wv[t]);
-            if ((u >> (sh + nbits[pass])) == prefix) {
-                const int b = (u >> sh) & (nb - 1);
-                atomicAdd(&s_cnt[b], 1u);
-                atomicAdd(&s_mass[b], fixed60(u));
+        for (int base = 0; base < C; base += 1024 * 4) {
+            uint32_t u[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int t = base + k * 1024 + tid;
+                u[k] = t < C ? __float_as_uint(wv[t]) : 0xffffffffu;
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                if (u[k] != 0xffffffffu && (u[k] >> (sh + nbits[pass])) == prefix) {
+                    const int b = (u[k] >> sh) & (nb - 1);
+                    atomicAdd(&s_cnt[b], 1u);
+                    atomicAdd(&s_mass[b], fixed60(u[k]));
+                }
             }
         }
         __syncthreads();
-        // buckets in descending order: thread tid owns per consecutive buckets
-        const int per = nb / 256;
-        const int hi = nb - 1 - tid * per;
-        unsigned long long my_mass = 0;
-        unsigned int my_cnt = 0;
-        for (int k = 0; k < per; ++k) {
-            my_mass += s_mass[hi - k];
-            my_cnt += s_cnt[hi - k];
-        }
-        const unsigned long long incl = block_scan_u64(my_mass, s_scan);
-        const unsigned long long excl = incl - my_mass;
-        const unsigned long long need = target > above_mass ? target - above_mass : 0ull;
-        if (tid == 0) s_bucket = -1;
-        __syncthreads();
-        if (excl < need && incl >= need) {
-            unsigned long long cum = excl;
+        if (tid < 64) {
+            // lane owns nb/64 consecutive buckets, lane 0 the highest
+            const int per = nb / 64;
+            const int hi = nb - 1 - lane * per;
+            unsigned long long mm = 0;
+            unsigned int cc = 0;
             for (int k = 0; k < per; ++k) {
-                cum += s_mass[hi - k];
-                if (cum >= need) {
-                    s_bucket = hi - k;
-                    break;
+                mm += s_mass[hi - k];
+                cc += s_cnt[hi - k];
+            }
+            unsigned long long im = mm;
+            unsigned int ic = cc;
+            for (int off = 1; off < 64; off <<= 1) {
+                const unsigned long long ym = __shfl_up(im, off, 64);
+                const unsigned int yc = __shfl_up(ic, off, 64);
+                if (lane >= off) {
+                    im += ym;
+                    ic += yc;
+                }
+            }
+            const unsigned long long need = target > above_mass ? target - above_mass : 0ull;
+            const unsigned long long em = im - mm;
+            const unsigned int ec = ic - cc;
+            const unsigned long long total = __shfl(im, 63, 64);
+            if (lane == 0 && total < need) s_bucket = -1;
+            if (em < need && im >= need) {
+                unsigned long long cum = em;
+                unsigned int cnt = ec;
+                for (int k = 0; k < per; ++k) {
+                    const int b = hi - k;
+                    if (cum + s_mass[b] >= need) {
+                        s_bucket = b;
+                        s_above_mass = cum;
+                        s_above_cnt = cnt;
+                        break;
+                    }
+                    cum += s_mass[b];
+                    cnt += s_cnt[b];
                 }
             }
         }
@@ -318,19 +375,6 @@ __global__ __launch_bounds__(256) void top_p_kernel(ScoreArgs a) {
             if (tid == 0) *out = C;
             return;
         }
-        // everything strictly above bucket B
-        unsigned long long am = 0;
-        unsigned int ac = 0;
-        for (int b = B + 1 + tid; b < nb; b += 256) {
-            am += s_mass[b];
-            ac += s_cnt[b];
-        }
-        const unsigned long long am_all = block_scan_u64(am, s_scan);
-        if (tid == 255) s_above_mass = am_all;
-        __syncthreads();
-        const unsigned long long ac_all = block_scan_u64((unsigned long long)ac, s_scan);
-        if (tid == 255) s_above_cnt = (unsigned int)ac_all;
-        __syncthreads();
         above_mass += s_above_mass;
         above_cnt += s_above_cnt;
         prefix = (prefix << nbits[pass]) | (uint32_t)B;
@@ -340,7 +384,7 @@ __global__ __launch_bounds__(256) void top_p_kernel(ScoreArgs a) {
         // prefix is now the float32 bit pattern of the K-th largest weight T
         const unsigned long long tf = fixed60(prefix);
         const unsigned long long need = target - above_mass;   // > 0
-        unsigned long long j = tf == 0 ? 0ull : (need + tf - 1) / tf;
+        const unsigned long long j = tf == 0 ? 0ull : (need + tf - 1) / tf;
         long long K = (long long)above_cnt + (long long)j;
         if (tf == 0 || K > C) K = C;
         *out = (int32_t)K;
@@ -349,15 +393,16 @@ __global__ __launch_bounds__(256) void top_p_kernel(ScoreArgs a) {
 
 template <typename T, int D>
 hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
-    dim3 g1(a.nch, a.Hkv, a.Rb), g2(cdiv(a.cmax, kProbChunk), a.Hkv, a.Rb), g3(2, a.Hkv, a.Rb);
+    dim3 g0(a.Hkv, a.Rb), g1(a.nch, a.Hkv, a.Rb), g2(cdiv(a.cmax, kProbChunk), a.Hkv, a.Rb), g3(2, a.Hkv, a.Rb);
     if (a.cmax == 0) {
         // no request can have candidates: the counts are written as zero
-        top_p_kernel<<<g3, 256, 0, s>>>(a);
+        top_p_kernel<<<g3, 1024, 0, s>>>(a);
         return hipGetLastError();
     }
     switch (G) {
 #define GP_CASE(GG)                                                   \
     case GG:                                                          \
+        prep_kernel<T, D, GG><<<g0, 256, 0, s>>>(a);                  \
         logits_kernel<T, D, GG><<<g1, 256, 0, s>>>(a);                \
         weights_kernel<GG><<<g2, 256, 0, s>>>(a);                     \
         break;
@@ -365,7 +410,7 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
 #undef GP_CASE
         default: return hipErrorInvalidValue;
     }
-    top_p_kernel<<<g3, 256, 0, s>>>(a);
+    top_p_kernel<<<g3, 1024, 0, s>>>(a);
     return hipGetLastError();
 }
 
