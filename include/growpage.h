@@ -32,7 +32,9 @@
  *    zero on completion, so it can be reused without clearing.  Two calls
  *    that run concurrently must not share a workspace.
  *  - Page size b is 16 tokens; head_dim is 64 or 128; num_q_heads is 1, 2, 4
- *    or 8 times num_kv_heads.  Other shapes return GP_ERR_UNSUPPORTED.
+ *    or 8 times num_kv_heads.  Decode attention takes page tables up to 8192
+ *    pages wide (131072 tokens per request), the boundary calls up to 4096
+ *    pages.  Other shapes return GP_ERR_UNSUPPORTED.
  *
  * Layout
  *  K and V pools     [pool_pages][num_kv_heads][page_size][head_dim], float32

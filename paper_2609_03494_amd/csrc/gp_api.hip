@@ -116,6 +116,7 @@ gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *
     a.max_pages = ps->max_pages;
     a.pool_pages = kv->pool_pages;
     a.max_chunks = w.max_chunks;
+    a.chunk_pages = w.chunk_pages;
     a.qscale = scale * 1.4426950408889634f;
     return from_hip(launch_decode(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stream));
 }
@@ -138,7 +139,7 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
     if (!(params->p > 0.0f && params->p <= 1.0f) || !(params->scale > 0.0f) ||
         !(params->rope_theta > 0.0f))
         return GP_ERR_INVALID;
-    if (num_bnd > 65535) return GP_ERR_UNSUPPORTED;
+    if (num_bnd > 65535 || ps->max_pages > kMaxBoundaryPages) return GP_ERR_UNSUPPORTED;
     const ScoreWs w = score_ws(num_bnd, num_q_heads, kv->num_kv_heads, ps->max_pages);
     if (ws_bytes < w.total) return GP_ERR_WORKSPACE;
     ScoreArgs a;
@@ -194,7 +195,7 @@ gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers, con
     if (!bnd || !k_counts || !scores || !decisions || !delta || !counters || !ws) return GP_ERR_INVALID;
     if (max_cand < (ps->max_pages - 1) * kPage) return GP_ERR_INVALID;
     if (params->k_loc < 0 || params->reserve_pages < 0) return GP_ERR_INVALID;
-    if (num_bnd > 2048) return GP_ERR_UNSUPPORTED;
+    if (num_bnd > 2048 || ps->max_pages > kMaxBoundaryPages) return GP_ERR_UNSUPPORTED;
     const gp_kv_layer_t &L0 = layers[0];
     const int E = elem_bytes(L0.dtype);
     const ApplyWs w = apply_ws(num_bnd, L0.num_kv_heads, L0.head_dim, E, ps->max_pages, n_layers);

@@ -44,23 +44,53 @@ struct LayerTable {
 
 __device__ inline bool compressing(int dec) { return dec == GP_COMPRESS || dec == GP_FALLBACK; }
 
-// ------------------------------------------------------------------ count --
-__global__ __launch_bounds__(256) void count_kernel(ApplyArgs a) {
+// ---------------------------------------------------------------- prepare --
+// Grid (compaction chunk cc, KV head x layer, boundary request), run before the
+// page table changes.  Every workgroup saves the rows of the page just below
+// compaction-chunk boundary cc (K and V of its head and layer); a neighbouring
+// chunk's writes may land there before the chunk that owns them has read them.
+// Workgroups of head 0, layer 0 and cc < npc also count the shared pages in
+// block cc of the request's table row.
+template <int D, int E>
+__global__ __launch_bounds__(256) void prepare_kernel(ApplyArgs a, LayerTable lt) {
     __shared__ int s_n;
-    const int blk = blockIdx.x, i = blockIdx.y;
-    if (threadIdx.x == 0) s_n = 0;
-    __syncthreads();
+    const int cc = blockIdx.x, i = blockIdx.z;
+    const int h = blockIdx.y % a.Hkv, l = blockIdx.y / a.Hkv;
+    const int tid = threadIdx.x;
     const int r = a.bnd[i];
+    int P = 0;
+    bool at_boundary = false;
     if (r >= 0 && r < a.R) {
-        const int P = a.num_pages[r];
-        const int j = blk * kPageBlock + threadIdx.x;
-        if (P >= 2 && P <= a.max_pages && a.seq_lens[r] == P * kPage && j < P) {
-            const int pid = a.page_table[(size_t)r * a.max_pages + j];
+        P = a.num_pages[r];
+        at_boundary = P >= 2 && P <= a.max_pages && a.seq_lens[r] == P * kPage;
+    }
+    const int32_t *row = a.page_table + (size_t)(at_boundary ? r : 0) * a.max_pages;
+    if (blockIdx.y == 0 && cc < a.npc) {
+        if (tid == 0) s_n = 0;
+        __syncthreads();
+        const int j = cc * kPageBlock + tid;
+        if (at_boundary && j < P) {
+            const int pid = row[j];
             if (pid >= 0 && pid < a.pool_pages && a.refcount[pid] > 1) atomicAdd(&s_n, 1);
         }
+        __syncthreads();
+        if (tid == 0) a.nshc[(size_t)i * a.npc + cc] = s_n;
     }
-    __syncthreads();
-    if (threadIdx.x == 0) a.nshc[(size_t)i * a.npc + blk] = s_n;
+    if (!at_boundary || cc == 0 || cc >= cdiv(P * kPage, kCompactChunk)) return;
+    constexpr int UPP = D * E / 16 * kPage;          // 16-byte units per page slice
+    const int lp = cc * kCompactChunk / kPage - 1;
+    const int phys = row[lp];
+    if (phys < 0 || phys >= a.pool_pages) return;
+    const size_t src_off = (size_t)phys * a.Hkv * kPage * D * E + (size_t)h * kPage * D * E;
+    unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc + cc) * 2 * kPage * D * E;
+    const unsigned char *kp = reinterpret_cast<const unsigned char *>(lt.k[l]) + src_off;
+    const unsigned char *vp = reinterpret_cast<const unsigned char *>(lt.v[l]) + src_off;
+    for (int u = tid; u < UPP; u += 256) {
+        const uint4 kx = *reinterpret_cast<const uint4 *>(kp + (size_t)u * 16);
+        const uint4 vx = *reinterpret_cast<const uint4 *>(vp + (size_t)u * 16);
+        *reinterpret_cast<uint4 *>(bd + (size_t)u * 16) = kx;
+        *reinterpret_cast<uint4 *>(bd + (size_t)(UPP + u) * 16) = vx;
+    }
 }
 
 // ----------------------------------------------------------------- decide --
@@ -212,42 +242,27 @@ __global__ __launch_bounds__(256) void replace_kernel(ApplyArgs a) {
 }
 
 // ----------------------------------------------------------------- select --
-__device__ inline void insert16(unsigned long long (&best)[kPage], unsigned long long key) {
-    if (key >= best[kPage - 1]) return;
-    best[kPage - 1] = key;
-#pragma unroll
-    for (int k = kPage - 1; k > 0; --k) {
-        const unsigned long long lo = best[k] < best[k - 1] ? best[k] : best[k - 1];
-        const unsigned long long hi = best[k] < best[k - 1] ? best[k - 1] : best[k];
-        best[k - 1] = lo;
-        best[k] = hi;
-    }
-}
+// Per (boundary request, KV head, layer) of a compressing request: every
+// candidate page keeps its q best tokens (score descending, slot ascending);
+// the 16 remaining candidates that come last in that order are evicted.
+// Eviction order is the ascending order of the 47-bit key
+// (score bits << 16) | (0xffff - slot): scores are non-negative floats, so
+// their bit patterns sort like their values, and a later slot loses a tie.
+// The 16th smallest key is found by a radix select over the key (fields of
+// 11, 11, 9 score bits and 11, 5 slot bits), each pass a histogram of the
+// keys that share the prefix found so far; wave 0 scans it for the bucket
+// that holds the next needed key.  Each pass re-reads the scores (L2-resident).
+constexpr int kSelPagesPerThread = 4;
+constexpr int kSelThreads = 1024;
+constexpr int kSelMaxPages = kSelPagesPerThread * kSelThreads;
 
-// A <- the 16 smallest of two ascending 16-lists, ascending.  A[k] vs B[15-k]
-// keeps the lower half of the bitonic sequence A ++ reverse(B); four
-// half-cleaner stages (distances 8, 4, 2, 1) sort it.  All indices are static,
-// so the lists stay in registers.
-__device__ inline void merge16(unsigned long long (&A)[kPage], const unsigned long long (&B)[kPage]) {
-#pragma unroll
-    for (int k = 0; k < kPage; ++k) A[k] = A[k] < B[kPage - 1 - k] ? A[k] : B[kPage - 1 - k];
-#pragma unroll
-    for (int s = kPage / 2; s >= 1; s >>= 1)
-#pragma unroll
-        for (int k = 0; k < kPage; ++k)
-            if ((k & s) == 0) {
-                const unsigned long long lo = A[k] < A[k + s] ? A[k] : A[k + s];
-                const unsigned long long hi = A[k] < A[k + s] ? A[k + s] : A[k];
-                A[k] = lo;
-                A[k + s] = hi;
-            }
-}
-
-template <int D, int E>
-__global__ __launch_bounds__(256) void select_kernel(ApplyArgs a, LayerTable lt) {
-    __shared__ unsigned long long s_keys[256][kPage];
+__global__ __launch_bounds__(1024) void select_kernel(ApplyArgs a) {
+    constexpr int NB = 2048;
+    __shared__ unsigned int s_hist[NB];
+    __shared__ int s_bucket, s_below, s_nev;
+    __shared__ int s_ev[kPage];
     const int h = blockIdx.x, i = blockIdx.y, l = blockIdx.z;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
     const int32_t *rq = a.req + (size_t)i * RQ_STRIDE;
     const int dec = rq[RQ_DEC];
     if (!compressing(dec)) return;
@@ -266,99 +281,135 @@ __global__ __launch_bounds__(256) void select_kernel(ApplyArgs a, LayerTable lt)
         }
     }
 
+    const int npages = min(P - 1, kSelMaxPages);
     const int Kt = (P - 2) * kPage;
     const int q = P >= 3 ? min(a.k_loc, Kt / (P - 1)) : 0;
     const float *s = a.scores + (((size_t)l * a.Rb + i) * a.Hkv + h) * a.max_cand;
-    unsigned long long best[kPage];
+
+    // local-quota masks of this thread's pages
+    uint32_t keep[kSelPagesPerThread];
 #pragma unroll
-    for (int k = 0; k < kPage; ++k) best[k] = ~0ull;
-    for (int j = tid; j < P - 1; j += blockDim.x) {
-        float v[kPage];
+    for (int u = 0; u < kSelPagesPerThread; ++u) {
+        const int j = tid + u * kSelThreads;
+        uint32_t mask = 0;
+        if (j < npages) {
+            float v[kPage];
 #pragma unroll
-        for (int t = 0; t < kPage; ++t) v[t] = s[j * kPage + t];
+            for (int t = 0; t < kPage; ++t) v[t] = s[j * kPage + t];
 #pragma unroll
-        for (int t = 0; t < kPage; ++t) {
-            int rank = 0;
+            for (int t = 0; t < kPage; ++t) {
+                int rank = 0;
 #pragma unroll
-            for (int u = 0; u < kPage; ++u) rank += (v[u] > v[t] || (v[u] == v[t] && u < t)) ? 1 : 0;
-            if (rank >= q) {
-                const uint32_t slot = (uint32_t)(j * kPage + t);
-                insert16(best, ((unsigned long long)__float_as_uint(v[t]) << 32) | (uint32_t)(~slot));
+                for (int w = 0; w < kPage; ++w) rank += (v[w] > v[t] || (v[w] == v[t] && w < t)) ? 1 : 0;
+                mask |= (rank < q ? 1u : 0u) << t;
             }
         }
-    }
-#pragma unroll
-    for (int k = 0; k < kPage; ++k) s_keys[tid][k] = best[k];
-    __syncthreads();
-    for (int stride = 128; stride >= 1; stride >>= 1) {
-        if (tid < stride) {
-            unsigned long long A[kPage], B[kPage];
-#pragma unroll
-            for (int k = 0; k < kPage; ++k) {
-                A[k] = s_keys[tid][k];
-                B[k] = s_keys[tid + stride][k];
-            }
-            merge16(A, B);
-#pragma unroll
-            for (int k = 0; k < kPage; ++k) s_keys[tid][k] = A[k];
-        }
-        __syncthreads();
-    }
-    if (tid == 0) {
-        int ev[kPage];
-        for (int k = 0; k < kPage; ++k) {
-            const unsigned long long key = s_keys[0][k];
-            ev[k] = key == ~0ull ? -1 : (int)(~(uint32_t)key);
-        }
-        for (int k = 1; k < kPage; ++k) {   // ascending slot order
-            const int x = ev[k];
-            int m = k - 1;
-            while (m >= 0 && ev[m] > x) {
-                ev[m + 1] = ev[m];
-                --m;
-            }
-            ev[m + 1] = x;
-        }
-        int32_t *out = a.evict + (((size_t)l * a.Rb + i) * a.Hkv + h) * kPage;
-        for (int k = 0; k < kPage; ++k) out[k] = ev[k];
+        keep[u] = mask;
     }
 
-    // border rows: the page just below every compaction chunk boundary
-    const int total = P * kPage;
-    const int nb = cdiv(total, kCompactChunk);
-    constexpr int UPR = D * E / 16;                 // 16-byte units per row
-    constexpr int UPP = UPR * kPage;                // units per page slice
-    const unsigned char *kp = reinterpret_cast<const unsigned char *>(lt.k[l]);
-    const unsigned char *vp = reinterpret_cast<const unsigned char *>(lt.v[l]);
-    const size_t page_bytes = (size_t)a.Hkv * kPage * D * E;
-    const size_t head_bytes = (size_t)h * kPage * D * E;
-    unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc) * 2 * kPage * D * E;
-    const int units = (nb - 1) * 2 * UPP;
-    for (int base = 0; base < units; base += 256 * 8) {
-        uint4 val[8];
-        size_t dst[8];
-        bool ok[8];
+    const int fsh[5] = {36, 25, 16, 5, 0};      // field shifts in the 47-bit key
+    const int fbits[5] = {11, 11, 9, 11, 5};
+    unsigned long long prefix = 0;
+    int need = kPage;                            // keys still to place at or below the prefix
+    for (int pass = 0; pass < 5; ++pass) {
+        const int sh = fsh[pass], nb = 1 << fbits[pass];
+        for (int b = tid; b < nb; b += blockDim.x) s_hist[b] = 0;
+        __syncthreads();
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int u = base + k * 256 + tid;
-            ok[k] = false;
-            if (u < units) {
-                const int b = 1 + u / (2 * UPP);
-                const int kv = (u / UPP) & 1;
-                const int w = u % UPP;
-                const int lp = b * kCompactChunk / kPage - 1;
-                const int phys = src_row[lp];
-                if (phys >= 0 && phys < a.pool_pages) {
-                    ok[k] = true;
-                    val[k] = *reinterpret_cast<const uint4 *>((kv ? vp : kp) + (size_t)phys * page_bytes +
-                                                              head_bytes + (size_t)w * 16);
-                    dst[k] = ((size_t)b * 2 + kv) * kPage * D * E + (size_t)w * 16;
-                }
+        for (int u = 0; u < kSelPagesPerThread; ++u) {
+            const int j = tid + u * kSelThreads;
+            if (j >= npages) continue;
+            uint32_t sbits[kPage];
+#pragma unroll
+            for (int t = 0; t < kPage; ++t) sbits[t] = __float_as_uint(s[j * kPage + t]);
+#pragma unroll
+            for (int t = 0; t < kPage; ++t) {
+                if (keep[u] & (1u << t)) continue;
+                const unsigned long long key = ((unsigned long long)sbits[t] << 16) |
+                                               (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
+                if ((key >> (sh + fbits[pass])) == prefix) atomicAdd(&s_hist[(key >> sh) & (nb - 1)], 1u);
             }
         }
+        __syncthreads();
+        if (tid < 64) {
+            // lane owns nb/64 consecutive buckets, lane 0 the lowest
+            const int per = nb >= 64 ? nb / 64 : 1;
+            const int lo = lane * per;
+            unsigned int cc = 0;
+            for (int k = 0; k < per; ++k) cc += lo + k < nb ? s_hist[lo + k] : 0u;
+            unsigned int ic = cc;
+            for (int off = 1; off < 64; off <<= 1) {
+                const unsigned int y = __shfl_up(ic, off, 64);
+                if (lane >= off) ic += y;
+            }
+            const unsigned int ec = ic - cc;
+            if (ec < (unsigned)need && ic >= (unsigned)need) {
+                unsigned int cum = ec;
+                for (int k = 0; k < per && lo + k < nb; ++k) {
+                    if (cum + s_hist[lo + k] >= (unsigned)need) {
+                        s_bucket = lo + k;
+                        s_below = (int)cum;
+                        break;
+                    }
+                    cum += s_hist[lo + k];
+                }
+            }
+            if (lane == 63 && ic < (unsigned)need) {   // fewer candidates than page_size
+                s_bucket = nb - 1;
+                s_below = (int)ic;
+            }
+        }
+        __syncthreads();
+        need -= s_below;
+        prefix = (prefix << fbits[pass]) | (unsigned long long)s_bucket;
+        __syncthreads();
+    }
+    // evict every candidate whose key is at most the threshold key
+    if (tid == 0) s_nev = 0;
+    if (tid < kPage) s_ev[tid] = -1;
+    __syncthreads();
 #pragma unroll
-        for (int k = 0; k < 8; ++k)
-            if (ok[k]) *reinterpret_cast<uint4 *>(bd + dst[k]) = val[k];
+    for (int u = 0; u < kSelPagesPerThread; ++u) {
+        const int j = tid + u * kSelThreads;
+        if (j >= npages) continue;
+        uint32_t sbits[kPage];
+#pragma unroll
+        for (int t = 0; t < kPage; ++t) sbits[t] = __float_as_uint(s[j * kPage + t]);
+#pragma unroll
+        for (int t = 0; t < kPage; ++t) {
+            if (keep[u] & (1u << t)) continue;
+            const unsigned long long key = ((unsigned long long)sbits[t] << 16) |
+                                           (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
+            if (key <= prefix) {
+                const int at = atomicAdd(&s_nev, 1);
+                if (at < kPage) s_ev[at] = j * kPage + t;
+            }
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int ev[kPage];
+#pragma unroll
+        for (int k = 0; k < kPage; ++k) ev[k] = s_ev[k] < 0 ? 0x7fffffff : s_ev[k];
+        // ascending slot order (bitonic sorting network, static indices)
+#pragma unroll
+        for (int k = 2; k <= kPage; k <<= 1)
+#pragma unroll
+            for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+                for (int x = 0; x < kPage; ++x) {
+                    const int y = x ^ j;
+                    if (y > x) {
+                        const bool up = (x & k) == 0;
+                        const int lo = ev[x] < ev[y] ? ev[x] : ev[y];
+                        const int hi = ev[x] < ev[y] ? ev[y] : ev[x];
+                        ev[x] = up ? lo : hi;
+                        ev[y] = up ? hi : lo;
+                    }
+                }
+        int32_t *out = a.evict + (((size_t)l * a.Rb + i) * a.Hkv + h) * kPage;
+#pragma unroll
+        for (int k = 0; k < kPage; ++k) out[k] = ev[k] == 0x7fffffff ? -1 : ev[k];
     }
 }
 
@@ -474,11 +525,12 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
 
 template <int D, int E>
 hipError_t launch_de(const ApplyArgs &a, const LayerTable &lt, hipStream_t s) {
-    dim3 gc(a.npc, a.Rb), gsel(a.Hkv, a.Rb, a.n_layers), gcomp(a.ncc, a.Hkv * a.n_layers, a.Rb);
-    count_kernel<<<gc, 256, 0, s>>>(a);
+    dim3 gprep(a.ncc, a.Hkv * a.n_layers, a.Rb), grep_(a.npc, a.Rb), gsel(a.Hkv, a.Rb, a.n_layers),
+        gcomp(a.ncc, a.Hkv * a.n_layers, a.Rb);
+    prepare_kernel<D, E><<<gprep, 256, 0, s>>>(a, lt);
     decide_kernel<<<1, 1024, 0, s>>>(a);
-    replace_kernel<<<gc, 256, 0, s>>>(a);
-    select_kernel<D, E><<<gsel, 256, 0, s>>>(a, lt);
+    replace_kernel<<<grep_, 256, 0, s>>>(a);
+    select_kernel<<<gsel, kSelThreads, 0, s>>>(a);
     compact_kernel<D, E><<<gcomp, 256, 0, s>>>(a, lt);
     return hipGetLastError();
 }

@@ -2,7 +2,7 @@
 // the sequence.
 //
 // Work item = (request r, KV head h, chunk of kDecodeChunkPages pages).  One
-// workgroup of four wave64s serves the whole GQA group of h (G query heads),
+// workgroup of wave64s serves the whole GQA group of h (G query heads),
 // so every K/V byte is read from HBM exactly once per step.  Inside a wave a
 // page (16 tokens x d) is read with fully coalesced 16-byte loads: lane l
 // holds dims [c*EPL, c*EPL+EPL) of token j*TPL + l/LPT for each of the LPP
@@ -58,13 +58,13 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     constexpr int TPL = 64 / LPT;         // tokens per wave load
     constexpr int LPP = kPage / TPL;      // loads per page
     constexpr int NW = 4;                 // waves per workgroup
-    constexpr int CHUNK = kDecodeChunkPages * kPage;
+    const int CHUNK = a.chunk_pages * kPage;
     static_assert(LPT >= 1 && LPT <= 64 && TPL * LPP == kPage, "layout");
 
     __shared__ float s_m[NW][G], s_l[NW][G];
     __shared__ float s_o[NW][G][D];
 
-    const int chunk = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
+    const int h = blockIdx.x, chunk = blockIdx.y, r = blockIdx.z;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int Hkv = a.Hkv;
     const int Hq = Hkv * G;
@@ -300,7 +300,7 @@ __device__ inline float row_sum16(float x) {
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(64 * kDecodeWaves) void decode_mfma_kernel(DecodeArgs a) {
     constexpr int KK = D / 32;            // MFMA steps per page
     constexpr int KSPAN = D / 4;          // key elements per lane per page
     constexpr int LPT = D / 8;            // lanes per token, value layout
@@ -308,16 +308,17 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     constexpr int LPP = kPage / TPL;      // value loads per page
     constexpr int HR = (G + 3) / 4;       // lane rows that carry real heads
     constexpr int GI = G < 4 ? G : 4;     // heads per lane row
-    constexpr int NW = 4;
+    constexpr int NW = kDecodeWaves;
     constexpr int NP = kDecodeInFlight;   // pages per iteration and wave
-    constexpr int CHUNK = kDecodeChunkPages * kPage;
+    const int CHUNK = a.chunk_pages * kPage;
 
     __shared__ float s_m[NW][G], s_l[NW][G];
     __shared__ float s_o[NW][G][D];
     __shared__ float s_p[NW][NP][kPage][G];
     __shared__ float s_alpha[NW][G];
+    __shared__ int s_ids[kDecodeChunkPages];
 
-    const int chunk = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
+    const int h = blockIdx.x, chunk = blockIdx.y, r = blockIdx.z;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int Hkv = a.Hkv;
     const int Hq = Hkv * G;
@@ -371,26 +372,15 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     const int k_off = n * D + kg * KSPAN;
     const int v_off = vrow * D + vc * 8;
 
-    // page ids of the chunk: one per lane, read once; a wave picks its page
-    // with a uniform lane read
-    constexpr int IDS = (kDecodeChunkPages + 63) / 64;
-    int ids[IDS];
-#pragma unroll
-    for (int w8 = 0; w8 < IDS; ++w8) {
-        const int pi = page_begin + w8 * 64 + lane;
-        ids[w8] = pi < page_end ? table[pi] : -1;
-    }
+    // page ids of the chunk, read once into LDS; a wave reads its page's id
+    // with a uniform LDS load
+    for (int k = threadIdx.x; k < page_end - page_begin; k += blockDim.x) s_ids[k] = table[page_begin + k];
+    __syncthreads();
     auto load_pages = [&](int pstart, uint4 (&kb)[NP][KK], uint4 (&vb)[NP][LPP], int (&ntok)[NP]) {
 #pragma unroll
         for (int u = 0; u < NP; ++u) {
             const int p = pstart + u * NW;
-            int phys = -1;
-            if (p < page_end) {
-                const int rel = p - page_begin;
-#pragma unroll
-                for (int w8 = 0; w8 < IDS; ++w8)
-                    if (rel >= w8 * 64 && rel < w8 * 64 + 64) phys = __builtin_amdgcn_readlane(ids[w8], rel - w8 * 64);
-            }
+            const int phys = p < page_end ? s_ids[p - page_begin] : -1;
             const bool ok = phys >= 0 && phys < a.pool_pages;
             ntok[u] = ok ? min(kPage, m - p * kPage) : 0;
             const size_t base = (size_t)(ok ? phys : 0) * page_elems + head_off;
@@ -564,7 +554,7 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     using Tr = Traits<T>;
-    constexpr int CHUNK = kDecodeChunkPages * kPage;
+    const int CHUNK = a.chunk_pages * kPage;
     constexpr int MAXC = kMaxDecodeChunks;
     __shared__ float s_f[MAXC][G];                 // exp2(m_k - M) / L per chunk and head
     __shared__ float s_ml[MAXC][G][2];
@@ -617,7 +607,7 @@ hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, hipStream_t s) {
 #define GP_CASE(GG)                                                  \
     case GG:                                                         \
         if (bf16)                                                    \
-            decode_mfma_kernel<D, GG><<<grid, 256, 0, s>>>(a);       \
+            decode_mfma_kernel<D, GG><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
         else                                                         \
             decode_kernel<float, D, GG><<<grid, 256, 0, s>>>(a);     \
         if (a.max_chunks > 1) merge_kernel<T, D, GG><<<mgrid, 256, 0, s>>>(a); \
@@ -632,7 +622,9 @@ hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_decode(gp_dtype_t dt, int D, int G, const DecodeArgs &a, hipStream_t s) {
-    dim3 grid(a.max_chunks, a.Hkv, a.R);
+    // the KV heads of one chunk are neighbours in dispatch order: they read the
+    // head slices of the same pages at about the same time
+    dim3 grid(a.Hkv, a.max_chunks, a.R);
     if (dt == GP_BF16)
         return D == 128 ? launch_g<uint16_t, 128>(G, a, grid, s) : launch_g<uint16_t, 64>(G, a, grid, s);
     return D == 128 ? launch_g<float, 128>(G, a, grid, s) : launch_g<float, 64>(G, a, grid, s);

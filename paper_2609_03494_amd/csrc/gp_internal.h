@@ -20,7 +20,12 @@ constexpr int kPage = 16;                 // tokens per page
 #endif
 constexpr int kDecodeChunkPages = GP_DECODE_CHUNK_PAGES;   // pages per decode work item (split-K)
 constexpr int kDecodeInFlight = GP_DECODE_PAGES_IN_FLIGHT; // pages per wave per iteration
+#ifndef GP_DECODE_WAVES
+#define GP_DECODE_WAVES 4
+#endif
+constexpr int kDecodeWaves = GP_DECODE_WAVES;              // waves per decode workgroup (bf16 path)
 constexpr int kMaxDecodeChunks = 128;                      // chunks one request may span
+constexpr int kMaxBoundaryPages = 4096;                    // table width the boundary calls accept
 constexpr int kScoreChunk = 256;          // candidate tokens per scoring work item
 constexpr int kProbChunk = 1024;          // tokens per weight/score work item
 constexpr int kCompactChunk = 256;        // slots per compaction work item
@@ -34,13 +39,19 @@ __host__ __device__ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 struct DecodeWs {
     size_t counters, partial, total;
-    int max_chunks;
+    int max_chunks, chunk_pages;
 };
+
+// Work split of decode attention: every request is cut into chunks of
+// kDecodeChunkPages pages; when a request spans several chunks a second kernel
+// merges their partial results.
+__host__ __device__ inline int decode_chunk_pages(int /*max_pages*/) { return kDecodeChunkPages; }
 
 __host__ __device__ inline DecodeWs decode_ws(int R, int Hq, int Hkv, int D, int max_pages) {
     DecodeWs w;
     const int G = Hq / Hkv;
-    w.max_chunks = cdiv(max_pages, kDecodeChunkPages);
+    w.chunk_pages = decode_chunk_pages(max_pages);
+    w.max_chunks = cdiv(max_pages, w.chunk_pages);
     size_t off = 0;
     w.counters = off;
     off = align_up(off + (size_t)R * Hkv * sizeof(uint32_t));
@@ -118,7 +129,7 @@ struct DecodeArgs {
     void *out;
     float *partial;
     uint32_t *counters;
-    int R, Hkv, max_pages, pool_pages, max_chunks;
+    int R, Hkv, max_pages, pool_pages, max_chunks, chunk_pages;
     float qscale;   // scale * log2(e)
 };
 

@@ -352,3 +352,58 @@ def test_full_qwen3_8b_sampled():
     np.testing.assert_array_equal(gs.seq_lens, st.seq_lens)
     assert gs.free_count == st.free_count
     _say("decisions", dec.tolist())
+
+
+# ------------------------------------------- selection on given scores --
+
+@pytest.mark.parametrize("pattern", ["few_values", "all_equal", "zeros_and_one"])
+def test_apply_selection_with_ties(pattern):
+    """gp_boundary_apply fed hand-made scores (heavy ties) against the oracle's
+    selection and compaction on the same scores."""
+    _say(f"apply: selection on tied scores ({pattern})")
+    import paper_2609_03494_amd as gp
+    w = W._build(name="ties", seed=41, dtype="bf16", Hq=8, Hkv=2, d=128,
+                 n=np.array([48, 160, 352, 1024]), budgets=None, free_pages=8,
+                 heavy_mode="scaled", heavy_frac=0.0, summary_mode="random")
+    dc = DeviceCase(w)
+    bnd = w.boundary
+    Rb, Hkv, b = len(bnd), w.num_kv_heads, w.page_size
+    max_cand = (w.max_pages - 1) * b
+    rng = np.random.default_rng(5)
+    scores = np.zeros((1, Rb, Hkv, max_cand), np.float32)
+    for i, r in enumerate(bnd):
+        C = (int(w.num_pages[r]) - 1) * b
+        if pattern == "few_values":
+            scores[0, i, :, :C] = rng.choice(np.float32([0.0, 1e-5, 2e-5, 0.5]), size=(Hkv, C))
+        elif pattern == "all_equal":
+            scores[0, i, :, :C] = np.float32(0.25)
+        else:
+            scores[0, i, :, :C] = 0.0
+            scores[0, i, :, rng.integers(0, C, size=3)] = 1.0
+    counts = np.zeros((1, Rb, Hkv, 2), np.int32)
+    p = O.Params(tau=math.inf)
+    p32 = p.as_f32(w.head_dim)
+    gparams = gp.Params(p32.beta_s, p32.beta_l, p32.p, p32.tau, p32.scale, p32.rope_theta, p32.k_loc, 0)
+    t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dt).cuda()
+    decisions = torch.zeros(Rb, dtype=torch.int32, device="cuda")
+    delta = torch.zeros(Rb, device="cuda")
+    ctr = torch.zeros(4, dtype=torch.int64, device="cuda")
+    ws = gp.workspace(gp.GP_OP_APPLY, w.num_reqs, Rb, w.num_q_heads, Hkv, w.head_dim, w.max_pages,
+                      torch.bfloat16)
+    gp.gp_boundary_apply(dc.layers, dc.ps, t(bnd.astype(np.int32), torch.int32), t(counts, torch.int32),
+                         t(scores, torch.float32), gparams, decisions, delta, ctr, ws)
+    torch.cuda.synchronize()
+    st = oracle_state(w)
+    dec, _ = O.decide_and_allocate(st, bnd, [c for c in counts[0][:, None]], b, p32)
+    assert np.array_equal(decisions.cpu().numpy(), dec)
+    gs = dc.host_state()
+    kp, vp = w.dense_pool("k"), w.dense_pool("v")
+    for i, r in enumerate(bnd):
+        P = int(w.num_pages[r])
+        for which, pool in (("k", kp), ("v", vp)):
+            before = O.gather_tokens(pool, w.page_table[r], P * b, b)
+            have = dc.gather(gs.page_table[r], (P - 1) * b, which)
+            for h in range(Hkv):
+                kept = O.select_retained(scores[0, i, h, : (P - 1) * b], P, b, p32.k_loc)
+                want = O.compact_tokens(before[:, h], kept, P, b)[: (P - 1) * b]
+                assert np.array_equal(have[:, h], want), (pattern, i, h, which)
