@@ -482,3 +482,39 @@ def test_not_boundary_is_reported_and_untouched():
                           w.qstate, w.slot_ids, w.positions, nb, O.Params())
     assert res["decisions"].tolist() == [O.NOT_BOUNDARY]
     assert np.array_equal(st.seq_lens, w.seq_lens)
+
+
+# ------------------------------------------------ library-routine pins ----
+
+def test_decode_attention_matches_torch_sdpa():
+    """Paged decode attention equals torch's scaled_dot_product_attention on the
+    gathered keys/values (fp64, CPU), with grouped-query heads expanded."""
+    w = W.qwen3_8b(seed=3, num_reqs=3, len_lo=40, len_hi=200, budget_choices=(4, 16), free_pages=5)
+    scale = 1.0 / math.sqrt(w.head_dim)
+    kp, vp = w.dense_pool("k"), w.dense_pool("v")
+    out = O.decode_attention(kp, vp, "bf16", w.page_table, w.seq_lens, w.q_post, w.num_q_heads, scale)
+    G = w.num_q_heads // w.num_kv_heads
+    for r in range(w.num_reqs):
+        m = int(w.seq_lens[r])
+        K = torch.from_numpy(O.widen(O.gather_tokens(kp, w.page_table[r], m, 16), "bf16"))
+        V = torch.from_numpy(O.widen(O.gather_tokens(vp, w.page_table[r], m, 16), "bf16"))
+        q = torch.from_numpy(O.widen(w.q_post[r], "bf16"))               # [Hq, d]
+        Kx = K.permute(1, 0, 2).repeat_interleave(G, 0)                  # [Hq, m, d]
+        Vx = V.permute(1, 0, 2).repeat_interleave(G, 0)
+        ref = torch.nn.functional.scaled_dot_product_attention(q[:, None, :], Kx, Vx, scale=scale)[:, 0]
+        assert np.allclose(out[r], ref.numpy(), rtol=0, atol=1e-12)
+
+
+def test_view_distributions_special_case_is_softmax():
+    """At position 0 (no rotation) with both summaries equal to the current query
+    (unit calibration), each view is the mean over the G query heads of
+    torch.softmax of the scaled key products."""
+    rng = np.random.default_rng(14)
+    C, Hkv, G, d = 50, 2, 3, 16
+    K = rng.standard_normal((C, Hkv, d))
+    qt = rng.standard_normal((Hkv * G, d))
+    a = O.view_distributions(K, qt, qt, qt, 0, 1e6, 0.25)
+    for h in range(Hkv):
+        ref = torch.stack([torch.softmax(0.25 * torch.from_numpy(K[:, h]) @ torch.from_numpy(qt[h * G + g]), 0)
+                           for g in range(G)]).mean(0).numpy()
+        assert np.allclose(a[0, h], ref, rtol=0, atol=1e-15) and np.allclose(a[1, h], ref, rtol=0, atol=1e-15)
