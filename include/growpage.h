@@ -189,8 +189,10 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
  *  - Shared pages (refcount > 1) are never written: a compressing request
  *    first pops one private page per shared page (GP_PREEMPT if too few), its
  *    compacted tokens go there, and the shared page loses one reference
- *    (App. E.2).  Pages whose count reaches zero are pushed on the stack at
- *    the end of the call, in (boundary index, logical page) order.
+ *    (App. E.2).  Sharing is judged on the counts as the call starts.  Pages
+ *    whose count reaches zero are pushed on the stack at the end of the
+ *    call, lowest page id first (the last pushed is popped first).
+ *  - Entries of bnd must be distinct (one boundary step per request).
  *  - counters[4] (int64) += number of COMPRESS, GROW, FALLBACK, PREEMPT. */
 gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers,
                               const gp_page_state_t *ps, const int32_t *bnd, int32_t num_bnd,

@@ -217,6 +217,7 @@ gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers, con
     a.req = reinterpret_cast<int32_t *>(base + w.req);
     a.hdr = reinterpret_cast<int32_t *>(base + w.hdr);
     a.nshc = reinterpret_cast<int32_t *>(base + w.nshc);
+    a.shflag = base + w.shflag;
     a.old_table = reinterpret_cast<int32_t *>(base + w.old_table);
     a.released = reinterpret_cast<int32_t *>(base + w.released);
     a.evict = reinterpret_cast<int32_t *>(base + w.evict);

@@ -2,30 +2,26 @@
 // boundaries (Sec. 3.2 aggregation and threshold, Sec. 3.3 Compress & Hold /
 // Grow by One Page, Sec. 4.2 fallback, App. E.2 prefix-preserving compaction).
 //
-// Five kernels, in stream order:
-//  count    per (boundary request, block of 256 table entries): how many of the
-//           request's pages are shared (refcount > 1).
-//  decide   one workgroup.  Per request, in parallel: Delta from the integer
-//           working-set counts (exact sign for tau = 0), want-grow.  Then one
-//           thread walks the requests in list order over LDS-resident data to
-//           hand out pages from the free stack (grow: 1 page, compress with a
-//           shared prefix: one page per shared page), writes the decision and
-//           applies grows and the new resident length of compressing requests.
-//  replace  per (request, block of 256 entries): a compressing request with
-//           shared pages gets its private replacement pages (ranked by logical
-//           page) and keeps a copy of its old table row for the copy step.
-//  select   per (request, KV head, layer): every candidate page keeps its
-//           local quota; the page_size lowest-ranked remaining tokens
-//           (score ascending, slot descending) are found with per-thread
-//           register lists merged pairwise in LDS.  The same workgroup saves the
-//           first rows of every compaction chunk boundary ("border" rows) that a
-//           neighbouring chunk will overwrite, and (head 0, layer 0) drops the
-//           request's references to replaced shared pages.
+// Three kernels, in stream order:
+//  pre      grid (1 + compaction chunks, KV head x layer, boundary request).
+//           Column 0 selects, for every request at a boundary, the tokens a
+//           compression would evict (the selection needs only the scores, so it
+//           does not wait for the decision).  The other columns save the rows
+//           just below each compaction-chunk boundary ("border" rows), which a
+//           neighbouring chunk may overwrite before their owner reads them, and
+//           record which pages of the table row are shared (refcount > 1).
+//  decide   one workgroup.  Delta from the integer working-set counts per
+//           request in parallel; then one thread walks the requests in list
+//           order over LDS-resident data to hand out pages from the free stack
+//           (grow: one page; compress with a shared prefix: one page per shared
+//           page); then grows are applied, compressing requests get their new
+//           resident length, and shared pages are replaced by private ones, the
+//           old references dropped (pages reaching zero are listed).
 //  compact  per (chunk of 256 slots, KV head x layer, request): reads every row
 //           that moves (the border rows from the saved copy), then writes it to
 //           its new slot; rows move down by at most page_size slots, so the only
-//           cross-chunk hazard is covered by the border copy.  Workgroup 0 also
-//           pushes the pages whose count reached zero, in page-id order.
+//           cross-chunk hazard is the one the border copy covers.  Workgroup 0
+//           also pushes the released pages back on the stack, lowest id first.
 //
 // Bound: compaction is HBM-bound: 2 (K, V) x 2 (read + write) x d x elem bytes
 // per moved row and KV head; everything else is latency-bound bookkeeping.
@@ -44,17 +40,193 @@ struct LayerTable {
 
 __device__ inline bool compressing(int dec) { return dec == GP_COMPRESS || dec == GP_FALLBACK; }
 
-// ---------------------------------------------------------------- prepare --
-// Grid (compaction chunk cc, KV head x layer, boundary request), run before the
-// page table changes.  Every workgroup saves the rows of the page just below
-// compaction-chunk boundary cc (K and V of its head and layer); a neighbouring
-// chunk's writes may land there before the chunk that owns them has read them.
-// Workgroups of head 0, layer 0 and cc < npc also count the shared pages in
-// block cc of the request's table row.
+// ----------------------------------------------------------------- select --
+// Per (boundary request, KV head, layer) of a compressing request: every
+// candidate page keeps its q best tokens (score descending, slot ascending);
+// the 16 remaining candidates that come last in that order are evicted.
+// Eviction order is the ascending order of the 48-bit key
+// (score bits << 16) | (0xffff - slot): scores are non-negative floats, so
+// their bit patterns sort like their values, and a later slot loses a tie.
+// The 16th smallest key is found by a radix select over 8-bit digits, each
+// pass a histogram of the keys that share the prefix found so far, scanned by
+// wave 0.  The two slot digits are only resolved when candidates tie on the
+// threshold score and not all of them are evicted.  Each thread keeps the
+// scores of its first two pages in registers and re-reads the rest.
+constexpr int kSelThreads = 1024;
+constexpr int kSelCached = 2;                           // pages per thread held in registers
+constexpr int kSelMaxPages = 4 * kSelThreads;
+
+__device__ inline void load_page_scores(const float *s, int j, uint32_t (&v)[kPage]) {
+#pragma unroll
+    for (int t = 0; t < kPage; ++t) v[t] = __float_as_uint(s[j * kPage + t]);
+}
+
+__device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P) {
+    constexpr int NB = 256;
+    __shared__ unsigned int s_hist[NB];
+    __shared__ int s_bucket, s_below, s_in_bucket, s_nev;
+    __shared__ int s_ev[kPage];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int npages = min(P - 1, kSelMaxPages);
+    const int Kt = (P - 2) * kPage;
+    const int q = P >= 3 ? min(a.k_loc, Kt / (P - 1)) : 0;
+    const float *s = a.scores + (((size_t)l * a.Rb + i) * a.Hkv + h) * a.max_cand;
+
+    uint32_t cache[kSelCached][kPage];
+    uint32_t keep[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int j = tid + u * kSelThreads;
+        uint32_t v[kPage];
+        uint32_t mask = 0;
+        if (j < npages) {
+            load_page_scores(s, j, v);
+#pragma unroll
+            for (int t = 0; t < kPage; ++t) {
+                int rank = 0;
+#pragma unroll
+                for (int w = 0; w < kPage; ++w) {
+                    const float x = __uint_as_float(v[w]), y = __uint_as_float(v[t]);
+                    rank += (x > y || (x == y && w < t)) ? 1 : 0;
+                }
+                mask |= (rank < q ? 1u : 0u) << t;
+            }
+        }
+        keep[u] = mask;
+        if (u < kSelCached) {
+#pragma unroll
+            for (int t = 0; t < kPage; ++t) cache[u < kSelCached ? u : 0][t] = v[t];
+        }
+    }
+
+    // the 48-bit key has 6 digits: 4 of the score, 2 of the inverted slot
+    unsigned long long prefix = 0;
+    int need = kPage;
+    int digits = 0;
+    for (int pass = 0; pass < 6; ++pass) {
+        const int sh = 40 - 8 * pass;
+        for (int b = tid; b < NB; b += blockDim.x) s_hist[b] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int j = tid + u * kSelThreads;
+            if (j >= npages) continue;
+            uint32_t v[kPage];
+            if (u < kSelCached) {
+#pragma unroll
+                for (int t = 0; t < kPage; ++t) v[t] = cache[u < kSelCached ? u : 0][t];
+            } else {
+                load_page_scores(s, j, v);
+            }
+#pragma unroll
+            for (int t = 0; t < kPage; ++t) {
+                if (keep[u] & (1u << t)) continue;
+                const unsigned long long key = ((unsigned long long)v[t] << 16) |
+                                               (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
+                if ((key >> (sh + 8)) == prefix) atomicAdd(&s_hist[(key >> sh) & 0xff], 1u);
+            }
+        }
+        __syncthreads();
+        if (tid < 64) {
+            // lane owns 4 consecutive buckets, lane 0 the lowest
+            const unsigned int c0 = s_hist[4 * lane], c1 = s_hist[4 * lane + 1];
+            const unsigned int c2 = s_hist[4 * lane + 2], c3 = s_hist[4 * lane + 3];
+            const unsigned int cc = c0 + c1 + c2 + c3;
+            unsigned int ic = cc;
+            for (int off = 1; off < 64; off <<= 1) {
+                const unsigned int y = __shfl_up(ic, off, 64);
+                if (lane >= off) ic += y;
+            }
+            const unsigned int ec = ic - cc;
+            if (ec < (unsigned)need && ic >= (unsigned)need) {
+                const unsigned int cs[4] = {c0, c1, c2, c3};
+                unsigned int cum = ec;
+                for (int k = 0; k < 4; ++k) {
+                    if (cum + cs[k] >= (unsigned)need) {
+                        s_bucket = 4 * lane + k;
+                        s_below = (int)cum;
+                        s_in_bucket = (int)cs[k];
+                        break;
+                    }
+                    cum += cs[k];
+                }
+            }
+            if (lane == 63 && ic < (unsigned)need) {   // fewer candidates than page_size
+                s_bucket = NB - 1;
+                s_below = (int)ic;
+                s_in_bucket = 0;
+            }
+        }
+        __syncthreads();
+        need -= s_below;
+        prefix = (prefix << 8) | (unsigned long long)s_bucket;
+        const int in_bucket = s_in_bucket;
+        digits = pass + 1;
+        __syncthreads();
+        // every key in the bucket is evicted: no later digit is needed
+        if (in_bucket == need) break;
+    }
+    const int rest = 48 - 8 * digits;      // key bits not fixed by the prefix
+    const unsigned long long hi = ((prefix + 1ull) << rest) - 1ull;   // largest key in the bucket
+
+    // evict every candidate whose key is at most the threshold
+    if (tid == 0) s_nev = 0;
+    if (tid < kPage) s_ev[tid] = -1;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int j = tid + u * kSelThreads;
+        if (j >= npages) continue;
+        uint32_t v[kPage];
+        if (u < kSelCached) {
+#pragma unroll
+            for (int t = 0; t < kPage; ++t) v[t] = cache[u < kSelCached ? u : 0][t];
+        } else {
+            load_page_scores(s, j, v);
+        }
+#pragma unroll
+        for (int t = 0; t < kPage; ++t) {
+            if (keep[u] & (1u << t)) continue;
+            const unsigned long long key = ((unsigned long long)v[t] << 16) |
+                                           (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
+            if (key <= hi) {
+                const int at = atomicAdd(&s_nev, 1);
+                if (at < kPage) s_ev[at] = j * kPage + t;
+            }
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int ev[kPage];
+#pragma unroll
+        for (int k = 0; k < kPage; ++k) ev[k] = s_ev[k] < 0 ? 0x7fffffff : s_ev[k];
+        // ascending slot order (bitonic sorting network, static indices)
+#pragma unroll
+        for (int k = 2; k <= kPage; k <<= 1)
+#pragma unroll
+            for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+                for (int x = 0; x < kPage; ++x) {
+                    const int y = x ^ j;
+                    if (y > x) {
+                        const bool up = (x & k) == 0;
+                        const int lo = ev[x] < ev[y] ? ev[x] : ev[y];
+                        const int hi2 = ev[x] < ev[y] ? ev[y] : ev[x];
+                        ev[x] = up ? lo : hi2;
+                        ev[y] = up ? hi2 : lo;
+                    }
+                }
+        int32_t *out = a.evict + (((size_t)l * a.Rb + i) * a.Hkv + h) * kPage;
+#pragma unroll
+        for (int k = 0; k < kPage; ++k) out[k] = ev[k] == 0x7fffffff ? -1 : ev[k];
+    }
+}
+
+// -------------------------------------------------------------------- pre --
 template <int D, int E>
-__global__ __launch_bounds__(256) void prepare_kernel(ApplyArgs a, LayerTable lt) {
+__global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
     __shared__ int s_n;
-    const int cc = blockIdx.x, i = blockIdx.z;
+    const int x = blockIdx.x, i = blockIdx.z;
     const int h = blockIdx.y % a.Hkv, l = blockIdx.y / a.Hkv;
     const int tid = threadIdx.x;
     const int r = a.bnd[i];
@@ -64,14 +236,25 @@ __global__ __launch_bounds__(256) void prepare_kernel(ApplyArgs a, LayerTable lt
         P = a.num_pages[r];
         at_boundary = P >= 2 && P <= a.max_pages && a.seq_lens[r] == P * kPage;
     }
+    if (x == 0) {
+        if (at_boundary) select_tokens(a, i, h, l, P);
+        return;
+    }
+    const int cc = x - 1;
     const int32_t *row = a.page_table + (size_t)(at_boundary ? r : 0) * a.max_pages;
     if (blockIdx.y == 0 && cc < a.npc) {
+        // shared pages of block cc of the table row, as the call starts
         if (tid == 0) s_n = 0;
         __syncthreads();
         const int j = cc * kPageBlock + tid;
-        if (at_boundary && j < P) {
-            const int pid = row[j];
-            if (pid >= 0 && pid < a.pool_pages && a.refcount[pid] > 1) atomicAdd(&s_n, 1);
+        if (j < a.max_pages) {
+            int shared = 0;
+            if (at_boundary && j < P) {
+                const int pid = row[j];
+                shared = pid >= 0 && pid < a.pool_pages && a.refcount[pid] > 1;
+            }
+            a.shflag[(size_t)i * a.max_pages + j] = (uint8_t)shared;
+            if (shared) atomicAdd(&s_n, 1);
         }
         __syncthreads();
         if (tid == 0) a.nshc[(size_t)i * a.npc + cc] = s_n;
@@ -85,11 +268,9 @@ __global__ __launch_bounds__(256) void prepare_kernel(ApplyArgs a, LayerTable lt
     unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc + cc) * 2 * kPage * D * E;
     const unsigned char *kp = reinterpret_cast<const unsigned char *>(lt.k[l]) + src_off;
     const unsigned char *vp = reinterpret_cast<const unsigned char *>(lt.v[l]) + src_off;
-    for (int u = tid; u < UPP; u += 256) {
-        const uint4 kx = *reinterpret_cast<const uint4 *>(kp + (size_t)u * 16);
-        const uint4 vx = *reinterpret_cast<const uint4 *>(vp + (size_t)u * 16);
-        *reinterpret_cast<uint4 *>(bd + (size_t)u * 16) = kx;
-        *reinterpret_cast<uint4 *>(bd + (size_t)(UPP + u) * 16) = vx;
+    for (int u = tid; u < 2 * UPP; u += blockDim.x) {
+        const unsigned char *src = u < UPP ? kp + (size_t)u * 16 : vp + (size_t)(u - UPP) * 16;
+        *reinterpret_cast<uint4 *>(bd + (size_t)u * 16) = *reinterpret_cast<const uint4 *>(src);
     }
 }
 
@@ -204,212 +385,42 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
         *a.free_count = fc0 - s_popped;
         for (int k = 0; k < 4; ++k) a.counters[k] += s_cnt[k];
     }
-}
 
-// ---------------------------------------------------------------- replace --
-__global__ __launch_bounds__(256) void replace_kernel(ApplyArgs a) {
-    __shared__ int s_scan[256];
-    const int blk = blockIdx.x, i = blockIdx.y;
-    const int32_t *rq = a.req + (size_t)i * RQ_STRIDE;
-    if (!compressing(rq[RQ_DEC]) || rq[RQ_NSH] == 0) return;
-    const int r = rq[RQ_R], P = rq[RQ_P];
-    const int j = blk * kPageBlock + threadIdx.x;
-    if (blk * kPageBlock >= P) return;
-    int32_t *row = a.page_table + (size_t)r * a.max_pages;
-    int shared = 0, old = -1;
-    if (j < P) {
-        old = row[j];
-        shared = (old >= 0 && old < a.pool_pages && a.refcount[old] > 1) ? 1 : 0;
-        a.old_table[(size_t)i * a.max_pages + j] = old;
-    }
-    // rank of this page among the request's shared pages
-    int base = 0;
-    for (int c = 0; c < blk; ++c) base += a.nshc[(size_t)i * a.npc + c];
-    s_scan[threadIdx.x] = shared;
-    __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {
-        const int y = threadIdx.x >= off ? s_scan[threadIdx.x - off] : 0;
-        __syncthreads();
-        s_scan[threadIdx.x] += y;
-        __syncthreads();
-    }
-    if (shared) {
-        const int k = base + s_scan[threadIdx.x] - 1;
-        const int pid = a.free_list[a.hdr[HDR_FC0] - 1 - rq[RQ_POP] - k];
-        row[j] = pid;
-        if (pid >= 0 && pid < a.pool_pages) a.refcount[pid] = 1;
-    }
-}
-
-// ----------------------------------------------------------------- select --
-// Per (boundary request, KV head, layer) of a compressing request: every
-// candidate page keeps its q best tokens (score descending, slot ascending);
-// the 16 remaining candidates that come last in that order are evicted.
-// Eviction order is the ascending order of the 47-bit key
-// (score bits << 16) | (0xffff - slot): scores are non-negative floats, so
-// their bit patterns sort like their values, and a later slot loses a tie.
-// The 16th smallest key is found by a radix select over the key (fields of
-// 11, 11, 9 score bits and 11, 5 slot bits), each pass a histogram of the
-// keys that share the prefix found so far; wave 0 scans it for the bucket
-// that holds the next needed key.  Each pass re-reads the scores (L2-resident).
-constexpr int kSelPagesPerThread = 4;
-constexpr int kSelThreads = 1024;
-constexpr int kSelMaxPages = kSelPagesPerThread * kSelThreads;
-
-__global__ __launch_bounds__(1024) void select_kernel(ApplyArgs a) {
-    constexpr int NB = 2048;
-    __shared__ unsigned int s_hist[NB];
-    __shared__ int s_bucket, s_below, s_nev;
-    __shared__ int s_ev[kPage];
-    const int h = blockIdx.x, i = blockIdx.y, l = blockIdx.z;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int32_t *rq = a.req + (size_t)i * RQ_STRIDE;
-    const int dec = rq[RQ_DEC];
-    if (!compressing(dec)) return;
-    const int r = rq[RQ_R], P = rq[RQ_P], nsh = rq[RQ_NSH];
-    const int32_t *row = a.page_table + (size_t)r * a.max_pages;
-    const int32_t *src_row = nsh > 0 ? a.old_table + (size_t)i * a.max_pages : row;
-
-    // the request drops its references to the shared pages it replaced
-    if (h == 0 && l == 0 && nsh > 0) {
-        for (int j = tid; j < P; j += blockDim.x) {
-            const int old = src_row[j];
-            if (old != row[j]) {
-                const int prev = atomicSub(&a.refcount[old], 1);
-                if (prev == 1) a.released[atomicAdd(&a.hdr[HDR_NREL], 1)] = old;
+    // compressing requests with shared pages: a private page replaces each
+    // shared one (ranked by logical page), the old row is kept for the copy,
+    // and the old reference is dropped; pages reaching zero are listed
+    __shared__ int s_scan[1024];
+    for (int i = 0; i < Rb; ++i) {
+        if (!compressing(s_dec[i]) || s_nsh[i] == 0) continue;      // uniform
+        const int r = a.bnd[i], P = s_P[i];
+        int32_t *row = a.page_table + (size_t)r * a.max_pages;
+        int base = 0;
+        for (int j0 = 0; j0 < P; j0 += 1024) {
+            const int j = j0 + tid;
+            const int sh = j < P ? a.shflag[(size_t)i * a.max_pages + j] : 0;
+            s_scan[tid] = sh;
+            __syncthreads();
+            for (int off = 1; off < 1024; off <<= 1) {
+                const int y = tid >= off ? s_scan[tid - off] : 0;
+                __syncthreads();
+                s_scan[tid] += y;
+                __syncthreads();
             }
-        }
-    }
-
-    const int npages = min(P - 1, kSelMaxPages);
-    const int Kt = (P - 2) * kPage;
-    const int q = P >= 3 ? min(a.k_loc, Kt / (P - 1)) : 0;
-    const float *s = a.scores + (((size_t)l * a.Rb + i) * a.Hkv + h) * a.max_cand;
-
-    // local-quota masks of this thread's pages
-    uint32_t keep[kSelPagesPerThread];
-#pragma unroll
-    for (int u = 0; u < kSelPagesPerThread; ++u) {
-        const int j = tid + u * kSelThreads;
-        uint32_t mask = 0;
-        if (j < npages) {
-            float v[kPage];
-#pragma unroll
-            for (int t = 0; t < kPage; ++t) v[t] = s[j * kPage + t];
-#pragma unroll
-            for (int t = 0; t < kPage; ++t) {
-                int rank = 0;
-#pragma unroll
-                for (int w = 0; w < kPage; ++w) rank += (v[w] > v[t] || (v[w] == v[t] && w < t)) ? 1 : 0;
-                mask |= (rank < q ? 1u : 0u) << t;
-            }
-        }
-        keep[u] = mask;
-    }
-
-    const int fsh[5] = {36, 25, 16, 5, 0};      // field shifts in the 47-bit key
-    const int fbits[5] = {11, 11, 9, 11, 5};
-    unsigned long long prefix = 0;
-    int need = kPage;                            // keys still to place at or below the prefix
-    for (int pass = 0; pass < 5; ++pass) {
-        const int sh = fsh[pass], nb = 1 << fbits[pass];
-        for (int b = tid; b < nb; b += blockDim.x) s_hist[b] = 0;
-        __syncthreads();
-#pragma unroll
-        for (int u = 0; u < kSelPagesPerThread; ++u) {
-            const int j = tid + u * kSelThreads;
-            if (j >= npages) continue;
-            uint32_t sbits[kPage];
-#pragma unroll
-            for (int t = 0; t < kPage; ++t) sbits[t] = __float_as_uint(s[j * kPage + t]);
-#pragma unroll
-            for (int t = 0; t < kPage; ++t) {
-                if (keep[u] & (1u << t)) continue;
-                const unsigned long long key = ((unsigned long long)sbits[t] << 16) |
-                                               (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
-                if ((key >> (sh + fbits[pass])) == prefix) atomicAdd(&s_hist[(key >> sh) & (nb - 1)], 1u);
-            }
-        }
-        __syncthreads();
-        if (tid < 64) {
-            // lane owns nb/64 consecutive buckets, lane 0 the lowest
-            const int per = nb >= 64 ? nb / 64 : 1;
-            const int lo = lane * per;
-            unsigned int cc = 0;
-            for (int k = 0; k < per; ++k) cc += lo + k < nb ? s_hist[lo + k] : 0u;
-            unsigned int ic = cc;
-            for (int off = 1; off < 64; off <<= 1) {
-                const unsigned int y = __shfl_up(ic, off, 64);
-                if (lane >= off) ic += y;
-            }
-            const unsigned int ec = ic - cc;
-            if (ec < (unsigned)need && ic >= (unsigned)need) {
-                unsigned int cum = ec;
-                for (int k = 0; k < per && lo + k < nb; ++k) {
-                    if (cum + s_hist[lo + k] >= (unsigned)need) {
-                        s_bucket = lo + k;
-                        s_below = (int)cum;
-                        break;
-                    }
-                    cum += s_hist[lo + k];
+            if (j < P) {
+                const int old = row[j];
+                a.old_table[(size_t)i * a.max_pages + j] = old;
+                if (sh) {
+                    const int k = base + s_scan[tid] - 1;
+                    const int pid = a.free_list[fc0 - 1 - s_pop[i] - k];
+                    row[j] = pid;
+                    if (pid >= 0 && pid < a.pool_pages) a.refcount[pid] = 1;
+                    const int prev = atomicSub(&a.refcount[old], 1);
+                    if (prev == 1) a.released[atomicAdd(&a.hdr[HDR_NREL], 1)] = old;
                 }
             }
-            if (lane == 63 && ic < (unsigned)need) {   // fewer candidates than page_size
-                s_bucket = nb - 1;
-                s_below = (int)ic;
-            }
+            base += s_scan[1023];
+            __syncthreads();
         }
-        __syncthreads();
-        need -= s_below;
-        prefix = (prefix << fbits[pass]) | (unsigned long long)s_bucket;
-        __syncthreads();
-    }
-    // evict every candidate whose key is at most the threshold key
-    if (tid == 0) s_nev = 0;
-    if (tid < kPage) s_ev[tid] = -1;
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < kSelPagesPerThread; ++u) {
-        const int j = tid + u * kSelThreads;
-        if (j >= npages) continue;
-        uint32_t sbits[kPage];
-#pragma unroll
-        for (int t = 0; t < kPage; ++t) sbits[t] = __float_as_uint(s[j * kPage + t]);
-#pragma unroll
-        for (int t = 0; t < kPage; ++t) {
-            if (keep[u] & (1u << t)) continue;
-            const unsigned long long key = ((unsigned long long)sbits[t] << 16) |
-                                           (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
-            if (key <= prefix) {
-                const int at = atomicAdd(&s_nev, 1);
-                if (at < kPage) s_ev[at] = j * kPage + t;
-            }
-        }
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int ev[kPage];
-#pragma unroll
-        for (int k = 0; k < kPage; ++k) ev[k] = s_ev[k] < 0 ? 0x7fffffff : s_ev[k];
-        // ascending slot order (bitonic sorting network, static indices)
-#pragma unroll
-        for (int k = 2; k <= kPage; k <<= 1)
-#pragma unroll
-            for (int j = k >> 1; j > 0; j >>= 1)
-#pragma unroll
-                for (int x = 0; x < kPage; ++x) {
-                    const int y = x ^ j;
-                    if (y > x) {
-                        const bool up = (x & k) == 0;
-                        const int lo = ev[x] < ev[y] ? ev[x] : ev[y];
-                        const int hi = ev[x] < ev[y] ? ev[y] : ev[x];
-                        ev[x] = up ? lo : hi;
-                        ev[y] = up ? hi : lo;
-                    }
-                }
-        int32_t *out = a.evict + (((size_t)l * a.Rb + i) * a.Hkv + h) * kPage;
-#pragma unroll
-        for (int k = 0; k < kPage; ++k) out[k] = ev[k] == 0x7fffffff ? -1 : ev[k];
     }
 }
 
@@ -525,12 +536,9 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
 
 template <int D, int E>
 hipError_t launch_de(const ApplyArgs &a, const LayerTable &lt, hipStream_t s) {
-    dim3 gprep(a.ncc, a.Hkv * a.n_layers, a.Rb), grep_(a.npc, a.Rb), gsel(a.Hkv, a.Rb, a.n_layers),
-        gcomp(a.ncc, a.Hkv * a.n_layers, a.Rb);
-    prepare_kernel<D, E><<<gprep, 256, 0, s>>>(a, lt);
+    dim3 gpre(1 + a.ncc, a.Hkv * a.n_layers, a.Rb), gcomp(a.ncc, a.Hkv * a.n_layers, a.Rb);
+    pre_kernel<D, E><<<gpre, 1024, 0, s>>>(a, lt);
     decide_kernel<<<1, 1024, 0, s>>>(a);
-    replace_kernel<<<grep_, 256, 0, s>>>(a);
-    select_kernel<<<gsel, kSelThreads, 0, s>>>(a);
     compact_kernel<D, E><<<gcomp, 256, 0, s>>>(a, lt);
     return hipGetLastError();
 }

@@ -86,7 +86,7 @@ __host__ __device__ inline ScoreWs score_ws(int Rb, int Hq, int Hkv, int max_pag
 }
 
 struct ApplyWs {
-    size_t req, hdr, nshc, old_table, released, evict, border, total;
+    size_t req, hdr, nshc, shflag, old_table, released, evict, border, total;
     int ncc, npc;
 };
 
@@ -94,7 +94,7 @@ struct ApplyWs {
 enum { RQ_R = 0, RQ_P, RQ_FLAGS, RQ_NSH, RQ_POP, RQ_DEC, RQ_STRIDE = 8 };
 // Call header (int32): free count before pops, after pops, released pages.
 enum { HDR_FC0 = 0, HDR_FC1, HDR_NREL, HDR_SIZE = 4 };
-constexpr int kPageBlock = 256;   // pages per work item when walking a page-table row
+constexpr int kPageBlock = 1024;  // pages per work item when walking a page-table row
 
 __host__ __device__ inline ApplyWs apply_ws(int Rb, int Hkv, int D, int elem, int max_pages,
                                             int n_layers) {
@@ -108,6 +108,8 @@ __host__ __device__ inline ApplyWs apply_ws(int Rb, int Hkv, int D, int elem, in
     off = align_up(off + HDR_SIZE * sizeof(int32_t));
     w.nshc = off;       // [Rb][npc] shared pages per block of the table row
     off = align_up(off + (size_t)Rb * w.npc * sizeof(int32_t));
+    w.shflag = off;     // [Rb][max_pages] uint8: page shared when the call starts
+    off = align_up(off + (size_t)Rb * max_pages);
     w.old_table = off;  // [Rb][max_pages]
     off = align_up(off + (size_t)Rb * max_pages * sizeof(int32_t));
     w.released = off;   // [Rb * max_pages]
@@ -164,6 +166,7 @@ struct ApplyArgs {
     float *delta;
     long long *counters;
     int32_t *req, *hdr, *nshc, *old_table, *released, *evict;
+    uint8_t *shflag;
     unsigned char *border;
     int R, Rb, Hkv, max_pages, pool_pages, max_cand, n_layers, ncc, npc, k_loc, reserve;
     double tau;
