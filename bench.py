@@ -3,22 +3,23 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
 
 A step is one pass of the whole path over the batch: restore the page metadata
-and the summary pool to the step's starting state (two device-to-device
-copies), update both query summaries of every request, paged decode attention
+to the step's starting state (one device-to-device copy), update both query summaries of every request, paged decode attention
 for every request, then boundary scoring and decide/select/compact for the
 requests at a capacity boundary.  Inputs are seeded synthetic tensors resident
-in HBM before timing starts.  The three phases (restore + summaries, decode,
-scoring, decide/select/compact) are each captured once as a HIP graph and
-replayed.  Scoring reads keys only, so it runs on a second stream beside decode
-attention; decide/select/compact wait for both (``--serial`` runs everything
-on one stream).
+in HBM before timing starts.  The step is captured once as a HIP graph and
+replayed (``--eager`` launches every call directly).  Scoring reads keys only,
+so it runs on a second stream beside decode attention; decide/select/compact
+wait for both (``--serial`` runs everything on one stream).
 
 Prints one JSON line.  ``value`` is GB/s of the every-step traffic (summaries
-and decode attention, algorithmic bytes) over the whole step's time,
-boundary work included in the time but not in the bytes.  The ``roofline``
-object covers the dominant kernel (decode attention) timed with HIP events
-around each launch on its own stream; ``cpu_baseline`` times the CPU oracle
-on a bounded sample of the same workload.
+and decode attention, algorithmic bytes) over the whole step's time, boundary
+work included in the time but not in the bytes; the timed region holds the K
+steps and nothing else.  The ``roofline`` object covers the dominant kernel
+(decode attention: split kernel + merge), timed with HIP events around K
+back-to-back launches on its stream after the timed steps.  A last,
+instrumented pass of K eager steps with events between the phases gives the
+time the boundary work adds after decode attention.  ``cpu_baseline`` times
+the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -98,8 +99,7 @@ def main():
         views[name] = meta[off: off + n].view(np.asarray(arr).shape)
         off += n
     ps = gp.PageState(**views)
-    qstate0 = torch.from_numpy(w.qstate).to(dev)
-    qstate = qstate0.clone()
+    qstate = torch.from_numpy(w.qstate).to(dev)
     slots, positions = i32(w.slot_ids), i32(w.positions)
     q_pre, q_post = bf(w.q_pre), bf(w.q_post)
     init = torch.zeros(R, dtype=torch.uint8, device=dev)
@@ -119,8 +119,10 @@ def main():
     stream = torch.cuda.current_stream()
 
     def restore():
+        # the page metadata goes back to the step's starting state, so that every
+        # step meets the same boundary requests; the summaries simply keep
+        # evolving from step to step, as they would in serving
         meta.copy_(meta0, non_blocking=True)
-        qstate.copy_(qstate0, non_blocking=True)
 
     def phase_pre():
         restore()
@@ -136,83 +138,87 @@ def main():
         gp.gp_boundary_apply([kv], ps, bnd, counts, scores, params, decisions, delta, counters, ws_a)
 
     side = torch.cuda.Stream()          # default priority, like the main stream
-    phases = [phase_pre, phase_decode, phase_score, phase_apply]
-    if not args.eager:
-        # each phase becomes one HIP graph, so the host stays ahead of the GPU
-        # and the events between phases time GPU work only
-        warm = torch.cuda.Stream()
-        warm.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(warm):
-            for _ in range(2):
-                for ph in phases:
-                    ph()
-        torch.cuda.current_stream().wait_stream(warm)
-        torch.cuda.synchronize()
-        graphs = []
-        for ph in phases:
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                ph()
-            graphs.append(g)
-        phases = [g.replay for g in graphs]
-    run_pre, run_decode, run_score, run_apply = phases
+    phase = dict(pre=phase_pre, decode=phase_decode, score=phase_score, apply=phase_apply)
 
-    ev = {}
+    def step(marks=None):
+        """One step on the current stream.  Scoring only reads keys, so unless
+        --serial it runs beside decode attention on a second stream (fork and
+        join by stream waits, which graph capture records as dependencies);
+        compaction waits for both."""
+        cur = torch.cuda.current_stream()
 
-    def step(record: bool):
-        run_pre()
+        def mark(name):
+            if marks is not None:
+                e_ = torch.cuda.Event(enable_timing=True)
+                e_.record(cur)
+                marks[name].append(e_)
+
+        phase["pre"]()
         if args.serial:
-            if record:
-                ev["d0"].append(torch.cuda.Event(enable_timing=True))
-                ev["d0"][-1].record(stream)
-            run_decode()
-            if record:
-                ev["d1"].append(torch.cuda.Event(enable_timing=True))
-                ev["d1"][-1].record(stream)
-            run_score()
-            run_apply()
+            mark("d0")
+            phase["decode"]()
+            mark("d1")
+            phase["score"]()
         else:
-            # scoring only reads keys, so it runs beside decode attention on a
-            # second stream; compaction (apply) waits for both
-            ready = torch.cuda.Event()
-            ready.record(stream)
+            side.wait_stream(cur)
             with torch.cuda.stream(side):
-                side.wait_event(ready)
-                run_score()
-                scored = torch.cuda.Event()
-                scored.record(side)
-            if record:
-                ev["d0"].append(torch.cuda.Event(enable_timing=True))
-                ev["d0"][-1].record(stream)
-            run_decode()
-            if record:
-                ev["d1"].append(torch.cuda.Event(enable_timing=True))
-                ev["d1"][-1].record(stream)
-            stream.wait_event(scored)
-            run_apply()
-        if record:
-            ev["b1"].append(torch.cuda.Event(enable_timing=True))
-            ev["b1"][-1].record(stream)
+                phase["score"]()
+            mark("d0")
+            phase["decode"]()
+            mark("d1")
+            cur.wait_stream(side)
+        phase["apply"]()
+        mark("b1")
+
+    # warm up every call (and the library's lazy state) eagerly first
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    if args.eager:
+        run_step = step
+    else:
+        # the whole step is one HIP graph: no launch gaps between its kernels
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        run_step = graph.replay
 
     for _ in range(args.warmup):
-        step(False)
+        run_step()
     torch.cuda.synchronize()
     counters.zero_()
-    ev = {"d0": [], "d1": [], "b1": []}
+    # timed region: K whole steps, nothing else on the streams
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     t0.record(stream)
     for _ in range(args.steps):
-        step(True)
+        run_step()
     t1.record(stream)
     torch.cuda.synchronize()
     step_ms = t0.elapsed_time(t1) / args.steps
-    dec_ms = [a.elapsed_time(c) for a, c in zip(ev["d0"], ev["d1"])]
-    bnd_ms = [a.elapsed_time(c) for a, c in zip(ev["d1"], ev["b1"])]
-    decode_ms = float(np.mean(dec_ms))
-    boundary_ms = float(np.mean(bnd_ms))
     split = counters.cpu().numpy().tolist()
+
+    # decode attention alone: K back-to-back launches of the decode call on its
+    # stream, bracketed by HIP events (the roofline's kernel timing)
+    restore()
+    torch.cuda.synchronize()
+    k0 = torch.cuda.Event(enable_timing=True)
+    k1 = torch.cuda.Event(enable_timing=True)
+    k0.record(stream)
+    for _ in range(args.steps):
+        phase_decode()
+    k1.record(stream)
+    torch.cuda.synchronize()
+    decode_ms = k0.elapsed_time(k1) / args.steps
+
+    # instrumented pass (eager launches, events between phases): how much of a
+    # step the boundary work adds after decode attention has finished
+    marks = {"d0": [], "d1": [], "b1": []}
+    for _ in range(args.steps):
+        step(marks)
+    torch.cuda.synchronize()
+    boundary_ms = float(np.mean([a.elapsed_time(c) for a, c in zip(marks["d1"], marks["b1"])]))
+    inline_decode_ms = float(np.mean([a.elapsed_time(c) for a, c in zip(marks["d0"], marks["d1"])]))
 
     # algorithmic bytes
     m = w.seq_lens.astype(np.int64)
@@ -260,8 +266,10 @@ def main():
                                "200k free pages",
                    "resident_tokens": int(m.sum()), "boundary_requests": Rb},
         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "launch": "eager" if args.eager else "one HIP graph per step",
         "decode_attention": {"ms": round(decode_ms, 4), "GB/s": round(dec_gbs, 1),
-                             "hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4), "bytes": decode_bytes},
+                             "hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4), "bytes": decode_bytes,
+                             "ms_inside_step": round(inline_decode_ms, 4)},
         "boundary": {"ms_after_decode": round(boundary_ms, 4),
                      "events_per_s": round(Rb / (step_ms * 1e-3), 1),
                      "overlapped_with_decode": not args.serial,

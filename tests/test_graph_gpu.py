@@ -13,11 +13,12 @@ from _harness import DeviceCase
 pytestmark = pytest.mark.gpu
 
 
-def test_graph_replays_match_eager():
+@pytest.mark.parametrize("fork", [False, True], ids=["one_stream", "score_on_side_stream"])
+def test_graph_replays_match_eager(fork):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     import paper_2609_03494_amd as gp
-    print("graph: capture decode + boundary step of a reduced Qwen3-8B batch", flush=True)
+    print(f"graph: capture decode + boundary step of a reduced Qwen3-8B batch, fork={fork}", flush=True)
     w = W.qwen3_8b(seed=17, num_reqs=10, len_lo=200, len_hi=3000, budget_choices=(20, 100, 200),
                    boundary_frac=0.4, free_pages=40)
     dc = DeviceCase(w)
@@ -36,6 +37,7 @@ def test_graph_replays_match_eager():
     ws_a = gp.workspace(gp.GP_OP_APPLY, w.num_reqs, Rb, w.num_q_heads, w.num_kv_heads, w.head_dim, w.max_pages, dt)
     out = torch.empty_like(dc.q_post)
     init = torch.zeros(w.num_reqs, dtype=torch.uint8, device="cuda")
+    aux = torch.cuda.Stream()          # default priority
     state0 = [t.clone() for t in (dc.ps.page_table, dc.ps.num_pages, dc.ps.seq_lens, dc.ps.refcount,
                                   dc.ps.free_list, dc.ps.free_count)]
     k0, v0, qs0 = dc.layers[0].k.clone(), dc.layers[0].v.clone(), dc.qstate.clone()
@@ -48,9 +50,19 @@ def test_graph_replays_match_eager():
         dc.layers[0].v.copy_(v0)
         dc.qstate.copy_(qs0)
         gp.gp_update_summaries(dc.q_pre, dc.slot_ids, init, dc.qstate, p32.beta_s, p32.beta_l)
+        cur = torch.cuda.current_stream()
+        if fork:
+            # scoring reads keys only: it may run beside decode attention
+            aux.wait_stream(cur)
+            with torch.cuda.stream(aux):
+                gp.gp_boundary_score(dc.layers[0], dc.ps, dc.q_pre, dc.qstate, dc.slot_ids, dc.positions,
+                                     bnd, params, counts, scores, ws_s)
         gp.gp_decode_attention(dc.layers[0], dc.ps, dc.q_post, p32.scale, out, dc.ws_decode)
-        gp.gp_boundary_score(dc.layers[0], dc.ps, dc.q_pre, dc.qstate, dc.slot_ids, dc.positions, bnd,
-                             params, counts, scores, ws_s)
+        if fork:
+            cur.wait_stream(aux)
+        else:
+            gp.gp_boundary_score(dc.layers[0], dc.ps, dc.q_pre, dc.qstate, dc.slot_ids, dc.positions, bnd,
+                                 params, counts, scores, ws_s)
         gp.gp_boundary_apply(dc.layers, dc.ps, bnd, counts, scores, params, dec, delta, ctr, ws_a)
 
     def snapshot():
