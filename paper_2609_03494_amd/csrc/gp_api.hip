@@ -100,7 +100,8 @@ gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *
     if (!q_post || !out || !ws) return GP_ERR_INVALID;
     const DecodeWs w = decode_ws(ps->num_reqs, num_q_heads, kv->num_kv_heads, kv->head_dim, ps->max_pages);
     if (ws_bytes < w.total) return GP_ERR_WORKSPACE;
-    if (ps->num_reqs > 65535 || w.max_chunks > kMaxDecodeChunks) return GP_ERR_UNSUPPORTED;
+    if (ps->num_reqs > 65535 || w.max_chunks > kMaxDecodeChunks || w.chunk_pages > kMaxChunkPages)
+        return GP_ERR_UNSUPPORTED;
     DecodeArgs a;
     a.k = kv->k;
     a.v = kv->v;
@@ -110,7 +111,6 @@ gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *
     a.q = q_post;
     a.out = out;
     a.partial = reinterpret_cast<float *>(static_cast<unsigned char *>(ws) + w.partial);
-    a.counters = reinterpret_cast<uint32_t *>(static_cast<unsigned char *>(ws) + w.counters);
     a.R = ps->num_reqs;
     a.Hkv = kv->num_kv_heads;
     a.max_pages = ps->max_pages;

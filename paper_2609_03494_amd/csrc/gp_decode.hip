@@ -1,17 +1,22 @@
 // Paged GQA decode attention (Sec. 3.1, attention-output equation), split over
 // the sequence.
 //
-// Work item = (request r, KV head h, chunk of kDecodeChunkPages pages).  One
-// workgroup of wave64s serves the whole GQA group of h (G query heads),
-// so every K/V byte is read from HBM exactly once per step.  Inside a wave a
-// page (16 tokens x d) is read with fully coalesced 16-byte loads: lane l
-// holds dims [c*EPL, c*EPL+EPL) of token j*TPL + l/LPT for each of the LPP
-// loads, c = l % LPT.  Dot products are finished with cross-lane sums over
-// the LPT lanes of a token; the online-softmax running max is made
-// wave-uniform per page so that each lane can keep partial sums over its own
-// tokens.  Waves take pages round-robin and two pages are in flight per wave.
-// The four waves merge through LDS; a request that spans several chunks
-// writes (max, sum, o) partials that a second, small kernel merges.
+// Work item = (KV head h, chunk of the request's pages, request r): one
+// workgroup serves the whole GQA group of h (G query heads), so every K/V byte
+// is read from HBM once per step.  Chunks are about kDecodeChunkPages pages,
+// sized so that a request of max_pages pages splits evenly.  A request that
+// spans several chunks leaves one (o, max, sum) partial per chunk, which a
+// second, small kernel merges; a request of a single chunk gets its output
+// from the first kernel.  Consecutive workgroups are the KV heads of one
+// chunk, so the head slices of the same pages are read at about the same
+// time.
+//
+// fp32 (vector ALUs): lane l holds dims [c*EPL, c*EPL+EPL) of token
+// j*TPL + l/LPT for each of the LPP loads of a page, c = l % LPT; dot products
+// finish with cross-lane sums over the LPT lanes of a token.  Four waves take
+// pages round-robin, two pages in flight per wave.
+//
+// bf16: see decode_split_kernel.
 //
 // Bound: HBM.  Algorithmic bytes per resident token and KV head:
 // 2 * d * sizeof(elem) (K and V), plus the page-table entries, q and out.
@@ -248,14 +253,13 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 // ---------------------------------------------------------------------------
 // bf16 path: Q.K^T on the matrix cores.  For one page, v_mfma_f32_16x16x32_bf16
 // computes S^T = Q (16 rows: the G query heads, rest zero) x K^T (16 tokens)
-// in D/32 steps.  Lane l supplies token l%16 and a 32-element slice of the
-// head dimension, so a lane reads D/4 consecutive elements of its token's
-// key row; the same permutation of the head dimension is applied to Q.  The
+// in D/32 steps.  In step kk, lane l supplies token l%16 and head dimensions
+// [32 kk + 8 (l/16), +8), so one load instruction reads 64 contiguous bytes of
+// each of the page's 16 key rows; Q is laid out with the same assignment.  The
 // result leaves head 4*(l/16)+i of token l%16 in register i of lane l, so the
 // per-page max and the row sums are 16-lane DPP reductions and every score is
-// exponentiated once.  P.V stays on the vector ALUs in fp32: V is read in the
-// coalesced layout of the fp32 path and the weights it needs are exchanged
-// through LDS.
+// exponentiated once.  P.V stays on the vector ALUs in fp32, with the weights
+// exchanged through LDS.
 // ---------------------------------------------------------------------------
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
@@ -264,23 +268,8 @@ template <int N>
 __device__ inline float dpp_ror(float x) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x120 + N, 0xf, 0xf, false));
 }
-#ifndef GP_DECODE_PREFETCH
-#define GP_DECODE_PREFETCH 0
-#endif
-#ifndef GP_DECODE_NT
-#define GP_DECODE_NT 0
-#endif
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-
-// 16-byte load of streamed K/V data.
-__device__ inline uint4 ld16(const uint16_t *p) {
-#if GP_DECODE_NT
-    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
-    return make_uint4(v.x, v.y, v.z, v.w);
-#else
-    return *reinterpret_cast<const uint4 *>(p);
-#endif
-}
+// 16-byte load of streamed K data.
+__device__ inline uint4 ld16(const uint16_t *p) { return *reinterpret_cast<const uint4 *>(p); }
 
 // LDS traffic between lanes of one wave: wait for the wave's LDS operations
 // and keep the compiler from moving memory accesses across this point.
@@ -299,29 +288,32 @@ __device__ inline float row_sum16(float x) {
     return x + dpp_ror<1>(x);
 }
 
+// Split decode (bf16): one workgroup of kDecodeWaves waves per (KV head,
+// chunk, request); the waves take the chunk's pages round-robin and keep one
+// page in flight each: the keys of a wave's next page are requested as soon
+// as the matrix cores have consumed the current ones, its values as soon as
+// P.V has.  In P.V each lane owns D/64 head dimensions for all 16 tokens of
+// the page, so a value load reads one whole 2D-byte row per instruction and
+// the accumulators take G * D / 64 registers; Q waits in LDS.  The waves
+// merge through LDS at the end.
 template <int D, int G>
-__global__ __launch_bounds__(64 * kDecodeWaves) void decode_mfma_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeArgs a) {
     constexpr int KK = D / 32;            // MFMA steps per page
-    constexpr int KSPAN = D / 4;          // key elements per lane per page
-    constexpr int LPT = D / 8;            // lanes per token, value layout
-    constexpr int TPL = 64 / LPT;         // tokens per value load
-    constexpr int LPP = kPage / TPL;      // value loads per page
+    constexpr int DPL = D / 64;           // head dims per lane in P.V (2 or 1)
     constexpr int HR = (G + 3) / 4;       // lane rows that carry real heads
     constexpr int GI = G < 4 ? G : 4;     // heads per lane row
     constexpr int NW = kDecodeWaves;
-    constexpr int NP = kDecodeInFlight;   // pages per iteration and wave
-    const int CHUNK = a.chunk_pages * kPage;
-
     __shared__ float s_m[NW][G], s_l[NW][G];
     __shared__ float s_o[NW][G][D];
-    __shared__ float s_p[NW][NP][kPage][G];
+    __shared__ float s_p[NW][kPage][G];
     __shared__ float s_alpha[NW][G];
-    __shared__ int s_ids[kDecodeChunkPages];
+    __shared__ bf16x8_t s_q[KK][4][G];
+    __shared__ int s_ids[kMaxChunkPages];
 
     const int h = blockIdx.x, chunk = blockIdx.y, r = blockIdx.z;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int Hkv = a.Hkv;
-    const int Hq = Hkv * G;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int Hkv = a.Hkv, Hq = Hkv * G;
+    const int CHUNK = a.chunk_pages * kPage;
 
     int P = a.num_pages[r];
     P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
@@ -331,7 +323,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_mfma_kernel(DecodeAr
     uint16_t *out = reinterpret_cast<uint16_t *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     if (m == 0) {
         if (chunk == 0)
-            for (int i = threadIdx.x; i < G * D; i += blockDim.x) out[i] = 0;
+            for (int i = tid; i < G * D; i += blockDim.x) out[i] = 0;
         return;
     }
     if (chunk >= nchunks) return;
@@ -339,21 +331,24 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_mfma_kernel(DecodeAr
     const int tok_end = min(m, tok_begin + CHUNK);
     const int page_begin = tok_begin / kPage, page_end = cdiv(tok_end, kPage);
 
-    // score layout: token n, key slice kg; value layout: token row vr, dims vc*8
-    const int n = lane & 15, kg = lane >> 4;
-    const int vrow = lane / LPT, vc = lane % LPT;
+    const int n = lane & 15, kg = lane >> 4;          // score layout: token n, key slice kg
+    const int v_off = lane * DPL;                     // P.V: lane owns dims [lane * DPL, +DPL)
+    const int k_off = n * D + kg * 8;
 
-    // Q as the MFMA A operand (rows >= G are zero)
-    const uint16_t *qg = reinterpret_cast<const uint16_t *>(a.q) + ((size_t)r * Hq + (size_t)h * G) * D;
-    bf16x8_t qa[KK];
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-        uint4 u = make_uint4(0u, 0u, 0u, 0u);
-        if (n < G) u = *reinterpret_cast<const uint4 *>(qg + (size_t)n * D + kg * KSPAN + kk * 8);
-        qa[kk] = __builtin_bit_cast(bf16x8_t, u);
+    // page ids and Q (MFMA A layout, rows < G) into LDS
+    const int32_t *table = a.page_table + (size_t)r * a.max_pages;
+    for (int k = tid; k < page_end - page_begin; k += blockDim.x) {
+        const int pid = table[page_begin + k];
+        s_ids[k] = pid >= 0 && pid < a.pool_pages ? pid : -1;
     }
+    const uint16_t *qg = reinterpret_cast<const uint16_t *>(a.q) + ((size_t)r * Hq + (size_t)h * G) * D;
+    if (tid < KK * 4 * G) {
+        const int kk = tid / (4 * G), rem = tid % (4 * G), q_kg = rem / G, q_n = rem % G;
+        s_q[kk][q_kg][q_n] = *reinterpret_cast<const bf16x8_t *>(qg + (size_t)q_n * D + kk * 32 + q_kg * 8);
+    }
+    __syncthreads();
 
-    float mrun[GI], lrun[GI], o[G][8];
+    float mrun[GI], lrun[GI], o[G][DPL];
 #pragma unroll
     for (int i = 0; i < GI; ++i) {
         mrun[i] = kNegInf;
@@ -362,90 +357,68 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_mfma_kernel(DecodeAr
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[g][e] = 0.0f;
+        for (int e = 0; e < DPL; ++e) o[g][e] = 0.0f;
 
-    const int32_t *table = a.page_table + (size_t)r * a.max_pages;
     const uint16_t *kpool = reinterpret_cast<const uint16_t *>(a.k);
     const uint16_t *vpool = reinterpret_cast<const uint16_t *>(a.v);
     const size_t head_off = (size_t)h * kPage * D;
     const size_t page_elems = (size_t)Hkv * kPage * D;
-    const int k_off = n * D + kg * KSPAN;
-    const int v_off = vrow * D + vc * 8;
-
-    // page ids of the chunk, read once into LDS; a wave reads its page's id
-    // with a uniform LDS load
-    for (int k = threadIdx.x; k < page_end - page_begin; k += blockDim.x) s_ids[k] = table[page_begin + k];
-    __syncthreads();
-    auto load_pages = [&](int pstart, uint4 (&kb)[NP][KK], uint4 (&vb)[NP][LPP], int (&ntok)[NP]) {
+    uint4 kb[KK];
+    uint32_t vw[kPage];
+    auto load_k = [&](int phys) {
+        const uint16_t *kp = kpool + (size_t)phys * page_elems + head_off + k_off;
 #pragma unroll
-        for (int u = 0; u < NP; ++u) {
-            const int p = pstart + u * NW;
-            const int phys = p < page_end ? s_ids[p - page_begin] : -1;
-            const bool ok = phys >= 0 && phys < a.pool_pages;
-            ntok[u] = ok ? min(kPage, m - p * kPage) : 0;
-            const size_t base = (size_t)(ok ? phys : 0) * page_elems + head_off;
-            if (ok) {
+        for (int kk = 0; kk < KK; ++kk) kb[kk] = ld16(kp + kk * 32);
+    };
+    auto load_v = [&](int phys) {
+        // one 2D-byte row per instruction: fully coalesced
+        const uint16_t *vp = vpool + (size_t)phys * page_elems + head_off + v_off;
 #pragma unroll
-                for (int kk = 0; kk < KK; ++kk) kb[u][kk] = ld16(kpool + base + k_off + kk * 8);
-#pragma unroll
-                for (int j = 0; j < LPP; ++j) vb[u][j] = ld16(vpool + base + v_off + (size_t)j * TPL * D);
-            }
+        for (int t = 0; t < kPage; ++t) {
+            if constexpr (DPL == 2)
+                vw[t] = *reinterpret_cast<const uint32_t *>(vp + t * D);
+            else
+                vw[t] = vp[t * D];
         }
     };
-
-    uint4 kb[NP][KK], vb[NP][LPP];
-    int ntok[NP];
-    int p0 = page_begin + wave;
+    int p = page_begin + wave;
+    int phys = p < page_end ? s_ids[p - page_begin] : -1;
+    if (phys >= 0) {
+        load_k(phys);
+        load_v(phys);
+    }
+    for (; p < page_end; p += NW) {
+        const int ntok = phys >= 0 ? min(kPage, m - p * kPage) : 0;
+        f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (ntok > 0) {
 #pragma unroll
-    for (int u = 0; u < NP; ++u) ntok[u] = 0;
-    if (p0 < page_end) load_pages(p0, kb, vb, ntok);
-    for (; p0 < page_end; p0 += NP * NW) {
-#if GP_DECODE_PREFETCH
-        uint4 kn[NP][KK], vn[NP][LPP];
-        int ntn[NP];
-#pragma unroll
-        for (int u = 0; u < NP; ++u) ntn[u] = 0;
-        if (p0 + NP * NW < page_end) load_pages(p0 + NP * NW, kn, vn, ntn);
-#endif
-        // scores of NP pages; token n of page u, head 4*kg + i in s[u][i]
-        float s[NP][GI];
-#pragma unroll
-        for (int u = 0; u < NP; ++u) {
-            f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
-            if (ntok[u] > 0) {
-#pragma unroll
-                for (int kk = 0; kk < KK; ++kk)
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], __builtin_bit_cast(bf16x8_t, kb[u][kk]),
-                                                                  acc, 0, 0, 0);
+            for (int kk = 0; kk < KK; ++kk) {
+                bf16x8_t qa = {};
+                if (n < G) qa = s_q[kk][kg][n];
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, __builtin_bit_cast(bf16x8_t, kb[kk]), acc, 0, 0, 0);
             }
-            const bool valid = n < ntok[u];
-#pragma unroll
-            for (int i = 0; i < GI; ++i) s[u][i] = valid ? acc[i] * a.qscale : kNegInf;
         }
-        float alpha[GI];
+        // the keys of the next page go out as soon as these are consumed
+        const int pn = p + NW;
+        const int phys_next = pn < page_end ? s_ids[pn - page_begin] : -1;
+        if (phys_next >= 0) load_k(phys_next);
+        const bool valid = n < ntok;
+        float sc[GI], alpha[GI];
 #pragma unroll
         for (int i = 0; i < GI; ++i) {
-            float pm = s[0][i];
-#pragma unroll
-            for (int u = 1; u < NP; ++u) pm = fmaxf(pm, s[u][i]);
-            pm = row_max16(pm);
+            sc[i] = valid ? acc[i] * a.qscale : kNegInf;
+            const float pm = row_max16(sc[i]);
             const float mn = fmaxf(mrun[i], pm);
             alpha[i] = mn == kNegInf ? 1.0f : exp2f(mrun[i] - mn);
             mrun[i] = mn;
-            float ps = 0.0f;
-#pragma unroll
-            for (int u = 0; u < NP; ++u) {
-                s[u][i] = mn == kNegInf ? 0.0f : exp2f(s[u][i] - mn);
-                ps += s[u][i];
-            }
-            lrun[i] = lrun[i] * alpha[i] + ps;
+            sc[i] = mn == kNegInf ? 0.0f : exp2f(sc[i] - mn);
+            lrun[i] = lrun[i] * alpha[i] + sc[i];
         }
-        // hand the weights and the rescale factors to the value layout
+        // hand the weights and the rescale factors to the P.V layout
         if (kg < HR) {
 #pragma unroll
             for (int i = 0; i < GI; ++i) {
-#pragma unroll
-                for (int u = 0; u < NP; ++u) s_p[wave][u][n][kg * 4 + i] = s[u][i];
+                s_p[wave][n][kg * 4 + i] = sc[i];
                 if (n == 0) s_alpha[wave][kg * 4 + i] = alpha[i];
             }
         }
@@ -454,57 +427,30 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_mfma_kernel(DecodeAr
         for (int g = 0; g < G; ++g) {
             const float al = s_alpha[wave][g];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) o[g][e] *= al;
+            for (int e = 0; e < DPL; ++e) o[g][e] *= al;
         }
 #pragma unroll
-        for (int u = 0; u < NP; ++u) {
-            if (ntok[u] == 0) continue;   // wave-uniform
-            const bool full = ntok[u] == kPage;
-#pragma unroll
-            for (int j = 0; j < LPP; ++j) {
-                const int t = j * TPL + vrow;
-                const bool valid = full || t < ntok[u];
-                float vf[8];
-                vf[0] = bf16_lo(vb[u][j].x); vf[1] = bf16_hi(vb[u][j].x);
-                vf[2] = bf16_lo(vb[u][j].y); vf[3] = bf16_hi(vb[u][j].y);
-                vf[4] = bf16_lo(vb[u][j].z); vf[5] = bf16_hi(vb[u][j].z);
-                vf[6] = bf16_lo(vb[u][j].w); vf[7] = bf16_hi(vb[u][j].w);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) vf[e] = valid ? vf[e] : 0.0f;
+        for (int t = 0; t < kPage; ++t) {
+            if (t < ntok) {      // wave-uniform; slots past the last token may hold anything
+                const float v0 = bf16_lo(vw[t]);
+                const float v1 = DPL == 2 ? bf16_hi(vw[t]) : 0.0f;
 #pragma unroll
                 for (int g = 0; g < G; ++g) {
-                    const float pw = s_p[wave][u][t][g];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) o[g][e] = fmaf(pw, vf[e], o[g][e]);
+                    const float pw = s_p[wave][t][g];
+                    o[g][0] = fmaf(pw, v0, o[g][0]);
+                    if constexpr (DPL == 2) o[g][DPL - 1] = fmaf(pw, v1, o[g][DPL - 1]);
                 }
             }
         }
         wave_lds_sync();
-#if GP_DECODE_PREFETCH
-#pragma unroll
-        for (int u = 0; u < NP; ++u) {
-            ntok[u] = ntn[u];
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk) kb[u][kk] = kn[u][kk];
-#pragma unroll
-            for (int j = 0; j < LPP; ++j) vb[u][j] = vn[u][j];
-        }
-#else
-#pragma unroll
-        for (int u = 0; u < NP; ++u) ntok[u] = 0;
-        if (p0 + NP * NW < page_end) load_pages(p0 + NP * NW, kb, vb, ntok);
-#endif
+        // ... and its values once these are
+        if (phys_next >= 0) load_v(phys_next);
+        phys = phys_next;
     }
 
-    // finish the wave: sums over the token rows of both layouts
+    // merge the waves: per-wave (max, sum) of each head, o of every dim
 #pragma unroll
     for (int i = 0; i < GI; ++i) lrun[i] = row_sum16(lrun[i]);
-#pragma unroll
-    for (int off = LPT; off < 64; off <<= 1)
-#pragma unroll
-        for (int g = 0; g < G; ++g)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) o[g][e] += __shfl_xor(o[g][e], off, 64);
     if (kg < HR && n == 0) {
 #pragma unroll
         for (int i = 0; i < GI; ++i) {
@@ -512,17 +458,15 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_mfma_kernel(DecodeAr
             s_l[wave][kg * 4 + i] = lrun[i];
         }
     }
-    if (vrow == 0) {
 #pragma unroll
-        for (int g = 0; g < G; ++g)
+    for (int g = 0; g < G; ++g)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) s_o[wave][g][vc * 8 + e] = o[g][e];
-    }
+        for (int e = 0; e < DPL; ++e) s_o[wave][g][v_off + e] = o[g][e];
     __syncthreads();
 
     const bool single = nchunks == 1;
     float *part = a.partial + (((size_t)r * Hkv + h) * a.max_chunks + chunk) * G * (D + 2);
-    for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
+    for (int i = tid; i < G * D; i += blockDim.x) {
         const int g = i / D, dd = i % D;
         float M = kNegInf;
 #pragma unroll
@@ -535,7 +479,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_mfma_kernel(DecodeAr
             Os += s_o[w][g][dd] * f;
         }
         if (single) {
-            out[(size_t)g * D + dd] = f32_to_bf16(Os / Ls);
+            out[(size_t)g * D + dd] = f32_to_bf16(Ls > 0.0f ? Os / Ls : 0.0f);
         } else {
             part[(size_t)g * (D + 2) + dd] = Os;
             if (dd == 0) {
@@ -607,7 +551,7 @@ hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, hipStream_t s) {
 #define GP_CASE(GG)                                                  \
     case GG:                                                         \
         if (bf16)                                                    \
-            decode_mfma_kernel<D, GG><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
+            decode_split_kernel<D, GG><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
         else                                                         \
             decode_kernel<float, D, GG><<<grid, 256, 0, s>>>(a);     \
         if (a.max_chunks > 1) merge_kernel<T, D, GG><<<mgrid, 256, 0, s>>>(a); \

@@ -15,13 +15,10 @@ constexpr int kPage = 16;                 // tokens per page
 #ifndef GP_DECODE_CHUNK_PAGES
 #define GP_DECODE_CHUNK_PAGES 64
 #endif
-#ifndef GP_DECODE_PAGES_IN_FLIGHT
-#define GP_DECODE_PAGES_IN_FLIGHT 2
-#endif
-constexpr int kDecodeChunkPages = GP_DECODE_CHUNK_PAGES;   // pages per decode work item (split-K)
-constexpr int kDecodeInFlight = GP_DECODE_PAGES_IN_FLIGHT; // pages per wave per iteration
+constexpr int kDecodeChunkPages = GP_DECODE_CHUNK_PAGES;   // pages per decode work item, about (split-K)
+constexpr int kMaxChunkPages = 64;                         // pages per decode chunk at most (LDS id table)
 #ifndef GP_DECODE_WAVES
-#define GP_DECODE_WAVES 4
+#define GP_DECODE_WAVES 8
 #endif
 constexpr int kDecodeWaves = GP_DECODE_WAVES;              // waves per decode workgroup (bf16 path)
 constexpr int kMaxDecodeChunks = 128;                      // chunks one request may span
@@ -38,14 +35,18 @@ __host__ __device__ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 // ---------------------------------------------------------------- layouts --
 
 struct DecodeWs {
-    size_t counters, partial, total;
+    size_t partial, total;
     int max_chunks, chunk_pages;
 };
 
-// Work split of decode attention: every request is cut into chunks of
-// kDecodeChunkPages pages; when a request spans several chunks a second kernel
-// merges their partial results.
-__host__ __device__ inline int decode_chunk_pages(int /*max_pages*/) { return kDecodeChunkPages; }
+// Work split of decode attention: every request is cut into chunks of about
+// kDecodeChunkPages pages (sized so that max_pages splits evenly); when a
+// request spans several chunks a second kernel merges their partial results.
+__host__ __device__ inline int decode_chunk_pages(int max_pages) {
+    int chunks = cdiv(max_pages, kDecodeChunkPages);
+    if (chunks > kMaxDecodeChunks) chunks = kMaxDecodeChunks;
+    return cdiv(max_pages, chunks);
+}
 
 __host__ __device__ inline DecodeWs decode_ws(int R, int Hq, int Hkv, int D, int max_pages) {
     DecodeWs w;
@@ -53,9 +54,7 @@ __host__ __device__ inline DecodeWs decode_ws(int R, int Hq, int Hkv, int D, int
     w.chunk_pages = decode_chunk_pages(max_pages);
     w.max_chunks = cdiv(max_pages, w.chunk_pages);
     size_t off = 0;
-    w.counters = off;
-    off = align_up(off + (size_t)R * Hkv * sizeof(uint32_t));
-    w.partial = off;
+    w.partial = off;    // float: [R][Hkv][max_chunks][G][D + 2] (o, max, sum)
     off = align_up(off + (size_t)R * Hkv * w.max_chunks * G * (D + 2) * sizeof(float));
     w.total = off;
     return w;
@@ -130,7 +129,6 @@ struct DecodeArgs {
     const void *q;
     void *out;
     float *partial;
-    uint32_t *counters;
     int R, Hkv, max_pages, pool_pages, max_chunks, chunk_pages;
     float qscale;   // scale * log2(e)
 };
