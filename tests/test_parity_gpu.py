@@ -205,6 +205,17 @@ def test_decode_fp32_d128_and_bf16_d64():
     _decode_check(w, DeviceCase(w))
 
 
+@pytest.mark.parametrize("num_reqs", [2048, 2100])
+def test_decode_bf16_large_batches(num_reqs):
+    # thousands of short requests: a grid with many workgroups, one chunk each
+    _say(f"decode: bf16 d64 G2, {num_reqs} short requests")
+    rng = np.random.default_rng(num_reqs)
+    n = rng.integers(1, 120, size=num_reqs)
+    w = W._build(name="bf16_many", seed=23, dtype="bf16", Hq=4, Hkv=2, d=64, n=n, budgets=None,
+                 free_pages=8, heavy_mode="scaled", heavy_frac=0.02, summary_mode="random")
+    _decode_check(w, DeviceCase(w))
+
+
 def test_decode_g8_prefix_shared():
     _say("decode: Qwen3-32B heads (G = 8), shared prefix")
     w = W.prefix_shared(num_reqs=6, prefix_len=256, tail_lo=20, tail_hi=900, free_pages=50)

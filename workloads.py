@@ -35,7 +35,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 PAGE = 16
-SLOTS = 512                      # query-summary slots (max_num_seqs)
+SLOTS = 512                      # query-summary slots (max_num_seqs); more when a batch is larger
 BF16_NAN = np.uint16(0x7FC0)
 
 
@@ -291,8 +291,9 @@ def _build(*, name, seed, dtype, Hq, Hkv, d, n, budgets, free_pages, heavy_mode,
         list(ex.map(one_request, range(R)))
 
     # query-summary pool: slots owned by no request stay NaN
-    slot_ids = rs.permutation(SLOTS)[:R].astype(np.int32)
-    qstate = np.full((SLOTS, 2, Hq, d), np.nan, dtype=np.float32)
+    nslots = max(SLOTS, R)
+    slot_ids = rs.permutation(nslots)[:R].astype(np.int32)
+    qstate = np.full((nslots, 2, Hq, d), np.nan, dtype=np.float32)
     if summary_mode == "random":
         qstate[slot_ids] = rs.standard_normal((R, 2, Hq, d), dtype=np.float32)
     elif summary_mode == "coin":
