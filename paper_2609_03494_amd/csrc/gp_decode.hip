@@ -495,6 +495,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
 // as its own launch lets the kernel boundary publish the partials; a
 // device-scope fence per workgroup would write back and invalidate the L2 of
 // every XCD thousands of times per step.
+constexpr int kFastMerge = 8;   // chunks a merge folds without staging
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     using Tr = Traits<T>;
@@ -513,6 +514,39 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     const float *base = a.partial + ((size_t)r * a.Hkv + h) * a.max_chunks * G * (D + 2);
     const int tid = threadIdx.x;
+    if (nchunks <= kFastMerge) {
+        // few chunks: every thread loads all it needs at once (one round trip,
+        // the (max, sum) of a head are the same address for a whole wave) and
+        // folds them itself
+        for (int i = tid; i < G * D; i += blockDim.x) {
+            const int g = i / D, dd = i % D;
+            float mk[kFastMerge], lk[kFastMerge], ok[kFastMerge];
+#pragma unroll
+            for (int k = 0; k < kFastMerge; ++k) {
+                mk[k] = kNegInf;
+                lk[k] = 0.0f;
+                ok[k] = 0.0f;
+                if (k < nchunks) {
+                    const float *pp = base + ((size_t)k * G + g) * (D + 2);
+                    mk[k] = pp[D];
+                    lk[k] = pp[D + 1];
+                    ok[k] = pp[dd];
+                }
+            }
+            float M = kNegInf;
+#pragma unroll
+            for (int k = 0; k < kFastMerge; ++k) M = fmaxf(M, mk[k]);
+            float L = 0.0f, Os = 0.0f;
+#pragma unroll
+            for (int k = 0; k < kFastMerge; ++k) {
+                const float f = mk[k] == kNegInf ? 0.0f : exp2f(mk[k] - M);
+                L += lk[k] * f;
+                Os += ok[k] * f;
+            }
+            Tr::store(out + (size_t)g * D + dd, L > 0.0f ? Os / L : 0.0f);
+        }
+        return;
+    }
     // all (max, sum) pairs at once, then one thread per head folds them
     for (int t = tid; t < nchunks * G && t < MAXC * G; t += blockDim.x) {
         const int k = t / G, g = t % G;
