@@ -211,6 +211,29 @@ def main():
     torch.cuda.synchronize()
     decode_ms = k0.elapsed_time(k1) / args.steps
 
+    # the summary update folded into decode attention (one launch) against the
+    # two calls, K back-to-back launches each
+    def timed_loop(fn):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    def fused_step():
+        gp.gp_decode_step(kv, ps, q_post, q_pre, params.scale, out, slots, init, qstate,
+                          params.beta_s, params.beta_l, ws_d)
+
+    def separate_step():
+        gp.gp_update_summaries(q_pre, slots, init, qstate, params.beta_s, params.beta_l)
+        gp.gp_decode_attention(kv, ps, q_post, params.scale, out, ws_d)
+
+    fused_ms = timed_loop(fused_step)
+    separate_ms = timed_loop(separate_step)
+
     # instrumented pass (eager launches, events between phases): how much of a
     # step the boundary work adds after decode attention has finished
     marks = {"d0": [], "d1": [], "b1": []}
@@ -269,7 +292,9 @@ def main():
         "launch": "eager" if args.eager else "one HIP graph per step",
         "decode_attention": {"ms": round(decode_ms, 4), "GB/s": round(dec_gbs, 1),
                              "hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4), "bytes": decode_bytes,
-                             "ms_inside_step": round(inline_decode_ms, 4)},
+                             "ms_inside_step": round(inline_decode_ms, 4),
+                             "with_summaries_one_launch_ms": round(fused_ms, 4),
+                             "with_summaries_two_launches_ms": round(separate_ms, 4)},
         "boundary": {"ms_after_decode": round(boundary_ms, 4),
                      "events_per_s": round(Rb / (step_ms * 1e-3), 1),
                      "overlapped_with_decode": not args.serial,

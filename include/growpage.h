@@ -149,6 +149,18 @@ gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *
                                 const void *q_post, int32_t num_q_heads, float scale,
                                 void *out, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* The summary update and decode attention of one step in a single launch
+ * (Sec. 4.1 folds the update into the attention kernel): the results are
+ * those of gp_update_summaries(q_pre, kv->dtype, ps->num_reqs, num_q_heads,
+ * kv->head_dim, slot_ids, init, qstate, num_slots, beta_s, beta_l) followed by
+ * gp_decode_attention(kv, ps, q_post, num_q_heads, scale, out, ws), bit for
+ * bit.  q_pre has the layout and dtype of q_post.  Takes the decode
+ * workspace. */
+gp_status_t gp_decode_step(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
+                           const void *q_pre, int32_t num_q_heads, float scale, void *out,
+                           const int32_t *slot_ids, const uint8_t *init, float *qstate, int32_t num_slots,
+                           float beta_s, float beta_l, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Boundary scoring of one layer (Sec. 3.2 and 3.3; App. E.1).
  * For boundary request i (r = bnd[i], at a boundary, P = num_pages[r]):
  * candidates are slots [0, (P-1) * page_size) (the most recent page is left

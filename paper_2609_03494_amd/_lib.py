@@ -22,7 +22,7 @@ GP_OP_DECODE, GP_OP_SCORE, GP_OP_APPLY = 0, 1, 2
 GP_COMPRESS, GP_GROW, GP_FALLBACK, GP_PREEMPT, GP_NOT_BOUNDARY = 0, 1, 2, 3, 4
 PAGE_SIZE = 16
 
-EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_boundary_score",
+EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_step", "gp_boundary_score",
            "gp_boundary_apply", "gp_workspace_bytes", "gp_status_string")
 
 
@@ -73,6 +73,9 @@ def load() -> ctypes.CDLL:
     lib.gp_decode_attention.restype = ctypes.c_int
     lib.gp_decode_attention.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, i32,
                                         f32, vp, vp, sz, vp]
+    lib.gp_decode_step.restype = ctypes.c_int
+    lib.gp_decode_step.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, vp, i32, f32,
+                                   vp, vp, vp, vp, i32, f32, f32, vp, sz, vp]
     lib.gp_boundary_score.restype = ctypes.c_int
     lib.gp_boundary_score.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, vp, i32,
                                       vp, vp, vp, i32, i32, ctypes.POINTER(_Params), vp, vp, i32, vp,
@@ -193,6 +196,18 @@ def gp_decode_attention(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale:
                                     q_post.shape[1], scale, _ptr(out), _ptr(ws), ws.numel(),
                                     _stream(stream))
     _check(st, "gp_decode_attention")
+
+
+def gp_decode_step(kv: KVLayer, ps: PageState, q_post: torch.Tensor, q_pre: torch.Tensor, scale: float,
+                   out: torch.Tensor, slot_ids: torch.Tensor, init: torch.Tensor, qstate: torch.Tensor,
+                   beta_s: float, beta_l: float, ws: torch.Tensor, stream=None) -> None:
+    """Summary update and decode attention of one step in one launch."""
+    c_kv, c_ps = kv.c(), ps.c()
+    st = load().gp_decode_step(ctypes.byref(c_kv), ctypes.byref(c_ps), _ptr(q_post), _ptr(q_pre),
+                               q_post.shape[1], scale, _ptr(out), _ptr(slot_ids), _ptr(init),
+                               _ptr(qstate), qstate.shape[0], beta_s, beta_l, _ptr(ws), ws.numel(),
+                               _stream(stream))
+    _check(st, "gp_decode_step")
 
 
 def gp_boundary_score(kv: KVLayer, ps: PageState, q_pre: torch.Tensor, qstate: torch.Tensor,

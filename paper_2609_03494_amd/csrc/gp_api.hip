@@ -88,16 +88,35 @@ gp_status_t gp_update_summaries(const void *q_pre, gp_dtype_t dtype, int32_t num
     return from_hip(launch_summaries(dtype, a, stream));
 }
 
-gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
-                                int32_t num_q_heads, float scale, void *out, void *ws, size_t ws_bytes,
-                                hipStream_t stream) {
+namespace {
+
+// Shared by gp_decode_attention and gp_decode_step; `sum` is the folded
+// summary update (q_pre == nullptr: none).
+struct FoldedSummaries {
+    const void *q_pre;
+    const int32_t *slot_ids;
+    const uint8_t *init;
+    float *qstate;
+    int32_t num_slots;
+    float beta_s, beta_l;
+};
+
+gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
+                        int32_t num_q_heads, float scale, void *out, void *ws, size_t ws_bytes,
+                        const FoldedSummaries *sum, hipStream_t stream) {
     gp_status_t st = check_layer(kv);
     if (st != GP_OK) return st;
     if ((st = check_state(ps, kv)) != GP_OK) return st;
     if (!dims_ok(num_q_heads, kv->num_kv_heads, kv->head_dim)) return GP_ERR_UNSUPPORTED;
     if (!(scale > 0.0f) || !isfinite(scale)) return GP_ERR_INVALID;
+    if (sum) {
+        if (sum->num_slots <= 0) return GP_ERR_INVALID;
+        if (!(sum->beta_s >= 0.0f && sum->beta_s <= 1.0f && sum->beta_l >= 0.0f && sum->beta_l <= 1.0f))
+            return GP_ERR_INVALID;
+    }
     if (ps->num_reqs == 0) return GP_OK;
     if (!q_post || !out || !ws) return GP_ERR_INVALID;
+    if (sum && (!sum->q_pre || !sum->slot_ids || !sum->init || !sum->qstate)) return GP_ERR_INVALID;
     const DecodeWs w = decode_ws(ps->num_reqs, num_q_heads, kv->num_kv_heads, kv->head_dim, ps->max_pages);
     if (ws_bytes < w.total) return GP_ERR_WORKSPACE;
     if (ps->num_reqs > 65535 || w.max_chunks > kMaxDecodeChunks || w.chunk_pages > kMaxChunkPages)
@@ -110,6 +129,13 @@ gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *
     a.seq_lens = ps->seq_lens;
     a.q = q_post;
     a.out = out;
+    a.q_pre = sum ? sum->q_pre : nullptr;
+    a.slot_ids = sum ? sum->slot_ids : nullptr;
+    a.init = sum ? sum->init : nullptr;
+    a.qstate = sum ? sum->qstate : nullptr;
+    a.M = sum ? sum->num_slots : 0;
+    a.beta_s = sum ? sum->beta_s : 0.0;
+    a.beta_l = sum ? sum->beta_l : 0.0;
     a.partial = reinterpret_cast<float *>(static_cast<unsigned char *>(ws) + w.partial);
     a.R = ps->num_reqs;
     a.Hkv = kv->num_kv_heads;
@@ -119,6 +145,22 @@ gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *
     a.chunk_pages = w.chunk_pages;
     a.qscale = scale * 1.4426950408889634f;
     return from_hip(launch_decode(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stream));
+}
+
+}  // namespace
+
+gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
+                                int32_t num_q_heads, float scale, void *out, void *ws, size_t ws_bytes,
+                                hipStream_t stream) {
+    return decode_call(kv, ps, q_post, num_q_heads, scale, out, ws, ws_bytes, nullptr, stream);
+}
+
+gp_status_t gp_decode_step(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
+                           const void *q_pre, int32_t num_q_heads, float scale, void *out,
+                           const int32_t *slot_ids, const uint8_t *init, float *qstate, int32_t num_slots,
+                           float beta_s, float beta_l, void *ws, size_t ws_bytes, hipStream_t stream) {
+    const FoldedSummaries sum{q_pre, slot_ids, init, qstate, num_slots, beta_s, beta_l};
+    return decode_call(kv, ps, q_post, num_q_heads, scale, out, ws, ws_bytes, &sum, stream);
 }
 
 gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_pre,

@@ -55,6 +55,32 @@ struct Traits<float> {
 
 constexpr float kNegInf = -__builtin_huge_valf();
 
+// gp_decode_step: the summary update of query heads [h G, h G + G) of request
+// r, done by the workgroup of the pair's first chunk (Sec. 4.1 folds the
+// update into the attention kernel).  Same arithmetic as the update kernel.
+template <typename T, int D, int G>
+__device__ inline void fold_summaries(const DecodeArgs &a, int r, int h) {
+    if (!a.qstate) return;
+    const int slot = a.slot_ids[r];
+    if (slot < 0 || slot >= a.M) return;
+    const int Hq = a.Hkv * G;
+    const bool ini = a.init[r] != 0;
+    const T *q = reinterpret_cast<const T *>(a.q_pre) + ((size_t)r * Hq + (size_t)h * G) * D;
+    float *S = a.qstate + (size_t)slot * 2 * Hq * D + (size_t)h * G * D;
+    float *L = S + (size_t)Hq * D;
+    const double cs = 1.0 - a.beta_s, cl = 1.0 - a.beta_l;
+    for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
+        const float x = Traits<T>::load(q + i);
+        if (ini) {
+            S[i] = x;
+            L[i] = x;
+        } else {
+            S[i] = ema_step(S[i], x, a.beta_s, cs);
+            L[i] = ema_step(L[i], x, a.beta_l, cl);
+        }
+    }
+}
+
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     using Tr = Traits<T>;
@@ -73,6 +99,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int Hkv = a.Hkv;
     const int Hq = Hkv * G;
+    if (chunk == 0) fold_summaries<T, D, G>(a, r, h);
 
     int P = a.num_pages[r];
     P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
@@ -313,6 +340,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     const int h = blockIdx.x, chunk = blockIdx.y, r = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int Hkv = a.Hkv, Hq = Hkv * G;
+    if (chunk == 0) fold_summaries<uint16_t, D, G>(a, r, h);
     const int CHUNK = a.chunk_pages * kPage;
 
     int P = a.num_pages[r];

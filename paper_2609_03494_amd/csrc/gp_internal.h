@@ -34,6 +34,17 @@ __host__ __device__ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 // ---------------------------------------------------------------- layouts --
 
+// One step of the dual-timescale EMA (Sec. 3.2) for one element: the fp64
+// value beta * prev + (1 - beta) * x with products and the sum rounded one at
+// a time (no fused multiply-add), then rounded once to float32.  Every kernel
+// that updates summaries goes through this, so they agree bit for bit.
+__device__ inline float ema_step(float prev, float x, double beta, double one_minus_beta) {
+#pragma clang fp contract(off)
+    const double a = beta * (double)prev;
+    const double b = one_minus_beta * (double)x;
+    return (float)(a + b);
+}
+
 struct DecodeWs {
     size_t partial, total;
     int max_chunks, chunk_pages;
@@ -128,6 +139,13 @@ struct DecodeArgs {
     const int32_t *page_table, *num_pages, *seq_lens;
     const void *q;
     void *out;
+    // summary update folded into the launch (gp_decode_step); qstate == nullptr: none
+    const void *q_pre;
+    const int32_t *slot_ids;
+    const uint8_t *init;
+    float *qstate;
+    int M;
+    double beta_s, beta_l;
     float *partial;
     int R, Hkv, max_pages, pool_pages, max_chunks, chunk_pages;
     float qscale;   // scale * log2(e)

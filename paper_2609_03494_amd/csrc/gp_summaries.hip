@@ -2,8 +2,8 @@
 //
 // One thread per four consecutive elements of a request's [Hq][d] query; the
 // pool row of the request's slot is updated in place.  Arithmetic is fp64 and
-// rounded once to float32, so that the stored summary is the correctly
-// rounded value of beta * qbar + (1 - beta) * q.  The kernel moves
+// rounded once to float32 (ema_step), the plain fp64 evaluation of
+// beta * qbar + (1 - beta) * q.  The kernel moves
 // 2 x 4 B (read + write) x 2 views per element plus the query: it is a few
 // microseconds of HBM traffic per step and is bound by launch latency.
 #include "gp_internal.h"
@@ -19,9 +19,6 @@ __device__ inline float load_q<float>(const float *p, size_t i) { return p[i]; }
 template <>
 __device__ inline float load_q<uint16_t>(const uint16_t *p, size_t i) { return bf16_to_f32(p[i]); }
 
-// Products and the sum are rounded separately (no fused multiply-add), the
-// plain fp64 evaluation of the update.
-#pragma clang fp contract(off)
 template <typename T>
 __global__ __launch_bounds__(256) void summaries_kernel(SummaryArgs a) {
     const int r = blockIdx.y;
@@ -38,9 +35,8 @@ __global__ __launch_bounds__(256) void summaries_kernel(SummaryArgs a) {
             S[i] = x;
             L[i] = x;
         } else {
-            const double xd = (double)x;
-            S[i] = (float)(a.beta_s * (double)S[i] + cs * xd);
-            L[i] = (float)(a.beta_l * (double)L[i] + cl * xd);
+            S[i] = ema_step(S[i], x, a.beta_s, cs);
+            L[i] = ema_step(L[i], x, a.beta_l, cl);
         }
     }
 }

@@ -81,6 +81,13 @@ def test_host_validation_without_launch(lib):
     arr = (_lib._KVLayer * 1)(kv)
     assert lib.gp_boundary_apply(arr, 65, ctypes.byref(ps), fake, 2, fake, fake, 144, ctypes.byref(p),
                                  fake, fake, fake, fake, 1 << 30, None) == 2
+    # fused step: beta outside [0, 1], null summary pool, then a small workspace
+    assert lib.gp_decode_step(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 32, 0.1, fake, fake, fake,
+                              fake, 512, 0.9, -0.5, fake, 1 << 30, None) == 1
+    assert lib.gp_decode_step(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 32, 0.1, fake, fake, fake,
+                              None, 512, 0.9, 0.999, fake, 1 << 30, None) == 1
+    assert lib.gp_decode_step(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 32, 0.1, fake, fake, fake,
+                              fake, 512, 0.9, 0.999, fake, 16, None) == 3
     # zero requests is a no-op that succeeds
     ps0 = _lib._PageState(fake, fake, fake, fake, fake, fake, 0, 10, 100)
     assert lib.gp_decode_attention(ctypes.byref(kv), ctypes.byref(ps0), fake, 32, 0.1, fake, fake, 0,

@@ -17,9 +17,10 @@ import pytest
 import torch
 
 import oracle as O
+import paper_2609_03494_amd as gp
 import workloads as W
 from _harness import (DeviceCase, PoolView, assert_rows_close, bf16_rounding_ok, oracle_state,
-                      row_index, threshold_band)
+                      row_index, threshold_band, to_numpy)
 
 pytestmark = pytest.mark.gpu
 
@@ -235,6 +236,49 @@ def test_decode_empty_request_gives_zero():
     ref = O.decode_attention(PoolView(w, "k"), PoolView(w, "v"), w.dtype, w.page_table, sl,
                              w.q_post, w.num_q_heads, scale, requests=[0, 2])
     assert_rows_close(got[[0, 2]], ref[[0, 2]], 2e-2, "decode bf16")
+
+
+@pytest.mark.parametrize("case", ["tiny_fp32", "qwen3_bf16", "g8_prefix_bf16"])
+def test_decode_step_fused_equals_separate(case):
+    # gp_decode_step folds the summary update into decode attention: summaries
+    # bit-identical to the oracle and to gp_update_summaries, outputs
+    # bit-identical to gp_decode_attention (a request with nothing resident
+    # still gets its summaries updated)
+    _say(f"decode step (fused summaries): {case}")
+    if case == "tiny_fp32":
+        w = W.tiny()
+    elif case == "qwen3_bf16":
+        w = W.qwen3_8b(seed=31, num_reqs=9, len_lo=30, len_hi=3000, budget_choices=(4, 40, 200),
+                       free_pages=32)
+    else:
+        w = W.prefix_shared(num_reqs=5, prefix_len=256, tail_lo=20, tail_hi=700, free_pages=40)
+    scale = float(np.float32(1.0 / math.sqrt(w.head_dim)))
+    bs, bl = _betas()
+    init = np.zeros(w.num_reqs, np.uint8)
+    init[::3] = 1
+    empty = 1 if w.num_reqs > 2 else None
+    cases = []
+    for fused in (False, True):
+        dc = DeviceCase(w)
+        if empty is not None:
+            dc.ps.seq_lens[empty] = 0
+        out = torch.empty_like(dc.q_post)
+        ini = torch.from_numpy(init).to("cuda")
+        if fused:
+            gp.gp_decode_step(dc.layers[0], dc.ps, dc.q_post, dc.q_pre, scale, out, dc.slot_ids, ini,
+                              dc.qstate, bs, bl, dc.ws_decode)
+        else:
+            gp.gp_update_summaries(dc.q_pre, dc.slot_ids, ini, dc.qstate, bs, bl)
+            gp.gp_decode_attention(dc.layers[0], dc.ps, dc.q_post, scale, out, dc.ws_decode)
+        torch.cuda.synchronize()
+        cases.append((to_numpy(out), dc.qstate.cpu().numpy()))
+    (out_s, qs_s), (out_f, qs_f) = cases
+    ref_qs = O.update_summaries(w.q_pre, w.dtype, w.slot_ids, init, w.qstate, bs, bl)
+    np.testing.assert_array_equal(qs_f.view(np.int32), ref_qs.view(np.int32))
+    np.testing.assert_array_equal(qs_f.view(np.int32), qs_s.view(np.int32))
+    np.testing.assert_array_equal(out_f, out_s)
+    if empty is not None:
+        assert (O.widen(out_f[empty], w.dtype) == 0).all()
 
 
 def test_boundary_tiny_all_branches():
