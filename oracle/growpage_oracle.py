@@ -28,12 +28,14 @@ from fractions import Fraction
 import numpy as np
 
 __all__ = [
-    "COMPRESS", "GROW", "FALLBACK", "PREEMPT", "NOT_BOUNDARY",
+    "COMPRESS", "GROW", "FALLBACK", "PREEMPT", "NOT_BOUNDARY", "SHRINK",
+    "POLICIES", "METRICS",
     "Params", "widen", "narrow",
     "ema_update", "update_summaries",
     "softmax", "attention", "renormalised_subset_output", "worst_case_error",
     "gather_tokens", "decode_attention",
     "rms", "calibrate", "rope", "view_distributions", "top_p_count", "top_p_fragile",
+    "entropy_count", "entropy_fragile",
     "token_scores", "score_request",
     "demand_trend", "decide_and_allocate",
     "local_quota", "select_retained", "compact_tokens",
@@ -41,7 +43,12 @@ __all__ = [
 ]
 
 # decision codes
-COMPRESS, GROW, FALLBACK, PREEMPT, NOT_BOUNDARY = 0, 1, 2, 3, 4
+COMPRESS, GROW, FALLBACK, PREEMPT, NOT_BOUNDARY, SHRINK = 0, 1, 2, 3, 4, 5
+
+# capacity-control policies (App. "alternative capacity-control policies") and
+# demand metrics (Sec. 3.2; the signal ablation replaces top-p by entropy)
+POLICIES = ("growpage", "fixed", "random", "inverse", "shrink")
+METRICS = ("top_p", "entropy")
 
 
 @dataclass
@@ -50,7 +57,17 @@ class Params:
     p = 0.99 (Sec. 3.2, working-set equation), tau = 0 (Sec. 3.2),
     k_loc = b/4 = 4 at b = 16 (reading: the paper's k_loc = 64 at b = 256,
     App. D.2, keeps a quarter of each block).  scale = 1/sqrt(head_dim)
-    (reading: the paper does not restate the attention scale)."""
+    (reading: the paper does not restate the attention scale).
+
+    Policy variants (App., alternative capacity-control policies):
+    ``fixed`` grows only while the capacity is below ``fixed_pages`` pages
+    (4096 tokens at b = 16) and compresses at every boundary after that;
+    ``random`` compresses with probability ``compress_prob`` = 0.7 (a draw per
+    boundary request, passed in) and grows otherwise; ``inverse`` grows iff
+    Delta <= tau; ``shrink`` shrinks iff Delta < ``shrink_threshold`` = -0.005
+    and the capacity after shrinking stays at least ``min_capacity_pages``
+    pages (1024 tokens), grows iff Delta > tau, and compresses otherwise.
+    ``metric``: ``top_p`` (default) or ``entropy`` (signal ablation)."""
     beta_s: float = 0.9
     beta_l: float = 0.999
     p: float = 0.99
@@ -59,6 +76,12 @@ class Params:
     rope_theta: float = 1.0e6
     reserve_pages: int = 0
     scale: float | None = None
+    policy: str = "growpage"
+    fixed_pages: int = 256
+    compress_prob: float = 0.7
+    shrink_threshold: float = -0.005
+    min_capacity_pages: int = 64
+    metric: str = "top_p"
 
     def as_f32(self, head_dim: int) -> "Params":
         """The same constants rounded to float32, the precision in which the
@@ -66,7 +89,9 @@ class Params:
         f = lambda v: float(np.float32(v))
         sc = self.scale if self.scale is not None else 1.0 / np.sqrt(head_dim)
         return Params(f(self.beta_s), f(self.beta_l), f(self.p), f(self.tau), int(self.k_loc),
-                      f(self.rope_theta), int(self.reserve_pages), f(sc))
+                      f(self.rope_theta), int(self.reserve_pages), f(sc), self.policy,
+                      int(self.fixed_pages), f(self.compress_prob), f(self.shrink_threshold),
+                      int(self.min_capacity_pages), self.metric)
 
 
 # ----------------------------------------------------------------------------
@@ -275,6 +300,33 @@ def top_p_fragile(a32: np.ndarray, p: float, eps: float = 1e-6) -> bool:
     return bool(near)
 
 
+def entropy_count(a32: np.ndarray) -> int:
+    """Working-set size from the attention entropy (the signal ablation's
+    alternative to top-p): H = -sum a ln a over the float32 weights (fp64,
+    zero weights contribute nothing), K = exp(H) rounded to the nearest
+    integer, at least 1 and at most len(a).
+    reading: the paper names the metric without defining the size; exp(H) is
+    the number of equally weighted tokens with the same entropy."""
+    v = np.asarray(a32, dtype=np.float32).astype(np.float64)
+    v = v[v > 0]
+    if v.size == 0:
+        return 1
+    H = -float(np.sum(v * np.log(v)))
+    k = int(np.floor(np.exp(H) + 0.5))
+    return max(1, min(k, int(np.asarray(a32).size)))
+
+
+def entropy_fragile(a32: np.ndarray, eps: float = 1e-6) -> bool:
+    """True when exp(H) lies within eps (relative) of a rounding midpoint."""
+    v = np.asarray(a32, dtype=np.float32).astype(np.float64)
+    v = v[v > 0]
+    if v.size == 0:
+        return False
+    e = float(np.exp(-np.sum(v * np.log(v))))
+    frac = e - np.floor(e)
+    return bool(abs(frac - 0.5) <= eps * max(1.0, e))
+
+
 def token_scores(a_s32: np.ndarray, a_l32: np.ndarray) -> np.ndarray:
     """s_i = max(a^S_i, a^L_i) per KV head (Sec. 3.3, eq. token_score)."""
     return np.maximum(np.asarray(a_s32, np.float32), np.asarray(a_l32, np.float32))
@@ -297,8 +349,11 @@ def score_request(tokens, dtype, P, b, q_t, qbar, pos, params: Params, scale):
     a = view_distributions(K, widen(q_t, dtype), np.asarray(qbar[0], np.float64),
                            np.asarray(qbar[1], np.float64), pos, params.rope_theta, scale)
     a32 = a.astype(np.float32)
-    counts = np.array([[top_p_count(a32[x, h], params.p) for x in range(2)]
-                       for h in range(Hkv)], dtype=np.int64)
+    if params.metric == "entropy":
+        count = lambda w: entropy_count(w)
+    else:
+        count = lambda w: top_p_count(w, params.p)
+    counts = np.array([[count(a32[x, h]) for x in range(2)] for h in range(Hkv)], dtype=np.int64)
     return counts, token_scores(a32[0], a32[1]), a32
 
 
@@ -331,7 +386,29 @@ class PageState:
                          self.refcount.copy(), self.free_list.copy(), int(self.free_count))
 
 
-def decide_and_allocate(state: PageState, bnd, counts, b: int, params: Params):
+def _wants(policy_params: Params, dl, P: int, draw):
+    """(want_grow, want_shrink) of one boundary request at P >= 2 pages with
+    demand trend dl (an exact rational, or None when the threshold is
+    infinite)."""
+    pp = policy_params
+    tau = Fraction(float(pp.tau)) if np.isfinite(pp.tau) else None
+    above = (pp.tau < 0) if tau is None else dl > tau          # Delta > tau
+    if pp.policy == "growpage":
+        return above, False
+    if pp.policy == "inverse":
+        return not above, False
+    if pp.policy == "fixed":
+        return P < pp.fixed_pages, False
+    if pp.policy == "random":
+        # reading: the draw is uniform in [0, 1); compress iff draw < prob
+        return not (float(np.float32(draw)) < float(np.float32(pp.compress_prob))), False
+    if pp.policy == "shrink":
+        shrink = (dl < Fraction(float(pp.shrink_threshold))) and (P - 1 >= pp.min_capacity_pages)
+        return above, shrink
+    raise ValueError(f"unknown policy {pp.policy!r}")
+
+
+def decide_and_allocate(state: PageState, bnd, counts, b: int, params: Params, draws=None):
     """Decision and allocation for the boundary requests, in list order.
 
     counts[i]: [layers, Hkv, 2] working-set sizes of boundary request i.
@@ -342,14 +419,19 @@ def decide_and_allocate(state: PageState, bnd, counts, b: int, params: Params):
     with other requests are never written, so a compressing request first takes
     one new private page per shared page and drops its reference to the shared
     one (App. E.2); if those pages cannot be had the request is preempted and
-    left untouched.
+    left untouched.  The policy variants (``params.policy``; App., alternative
+    capacity-control policies) change only which action is wanted; ``draws``
+    [Rb] are the uniform draws of the random policy.  Shrink keeps P - 1 pages:
+    the last page leaves the table and loses the request's reference, and
+    (P - 2) b tokens stay resident (two pages' worth evicted, one page of free
+    slots).
     readings: requests earlier in the list win scarce pages; "safely" granted
     means more than ``reserve_pages`` pages are free and the block table has
     room; a request with P <= 1 cannot compress, so it grows if it can and is
-    preempted otherwise; a page counts as shared if its reference count exceeds
-    one when the call starts; references are dropped after every pop of the
-    call and pages whose count reaches zero are pushed back onto the stack in
-    ascending page-id order.
+    preempted otherwise (the fixed policy grows below its budget only); a page
+    counts as shared if its reference count exceeds one when the call starts;
+    references are dropped after every pop of the call and pages whose count
+    reaches zero are pushed back onto the stack in ascending page-id order.
 
     Mutates ``state``; returns (decisions [Rb] int, delta [Rb] float32)."""
     Rb = len(bnd)
@@ -358,24 +440,22 @@ def decide_and_allocate(state: PageState, bnd, counts, b: int, params: Params):
     ref_at_start = state.refcount.copy()
     dropped = []
     max_pages = state.page_table.shape[1]
-    tau = Fraction(float(params.tau)) if np.isfinite(params.tau) else None
     for i in range(Rb):
         r = int(bnd[i])
         P = int(state.num_pages[r])
         if int(state.seq_lens[r]) != P * b:
             dec[i] = NOT_BOUNDARY
             continue
+        draw = None if draws is None else draws[i]
         if P <= 1:
-            want_grow = True
+            want_grow = P < params.fixed_pages if params.policy == "fixed" else True
+            want_shrink = False
         else:
             C = (P - 1) * b
             cs = np.asarray(counts[i])
             dl = demand_trend(cs[..., 0], cs[..., 1], C)
             delta[i] = np.float32(float(dl))
-            if tau is None:
-                want_grow = params.tau < 0          # -inf: always grow, +inf: never
-            else:
-                want_grow = dl > tau
+            want_grow, want_shrink = _wants(params, dl, P, draw)
         can_grow = state.free_count > params.reserve_pages and P < max_pages
         if want_grow and can_grow:
             pid = int(state.free_list[state.free_count - 1])
@@ -388,7 +468,8 @@ def decide_and_allocate(state: PageState, bnd, counts, b: int, params: Params):
         if P <= 1:
             dec[i] = PREEMPT
             continue
-        shared = [j for j in range(P) if ref_at_start[state.page_table[r, j]] > 1]
+        keep = P - 1 if want_shrink else P          # pages left in the table
+        shared = [j for j in range(keep) if ref_at_start[state.page_table[r, j]] > 1]
         if len(shared) > state.free_count:
             dec[i] = PREEMPT
             continue
@@ -398,8 +479,15 @@ def decide_and_allocate(state: PageState, bnd, counts, b: int, params: Params):
             dropped.append(int(state.page_table[r, j]))
             state.page_table[r, j] = pid
             state.refcount[pid] = 1
-        state.seq_lens[r] = (P - 1) * b
-        dec[i] = FALLBACK if want_grow else COMPRESS
+        if want_shrink:
+            dropped.append(int(state.page_table[r, P - 1]))
+            state.page_table[r, P - 1] = -1
+            state.num_pages[r] = P - 1
+            state.seq_lens[r] = (P - 2) * b
+            dec[i] = SHRINK
+        else:
+            state.seq_lens[r] = (P - 1) * b
+            dec[i] = FALLBACK if want_grow else COMPRESS
     for old in dropped:
         state.refcount[old] -= 1
     for pid in sorted({old for old in dropped if state.refcount[old] == 0}):
@@ -412,12 +500,13 @@ def decide_and_allocate(state: PageState, bnd, counts, b: int, params: Params):
 # A8: selection (Sec. 3.3, eq. local_global_selection)
 # ----------------------------------------------------------------------------
 
-def local_quota(P: int, b: int, k_loc: int) -> int:
-    """Per-block quota: k_loc, capped so the local picks fit in K_t = (P-2) b.
+def local_quota(P: int, b: int, k_loc: int, drop: int = 1) -> int:
+    """Per-block quota: k_loc, capped so the local picks fit in K_t.
     reading: compressing frees exactly one page, so (P-1) b slots stay
     occupied and the b protected recent tokens take one page of them
-    (Sec. 3.3; App. E.2); K_t = (P-2) b historical tokens are kept."""
-    K_t = (P - 2) * b
+    (Sec. 3.3; App. E.2); K_t = (P-2) b historical tokens are kept.  A shrink
+    evicts ``drop`` = 2 pages' worth, K_t = (P-3) b."""
+    K_t = (P - 1 - drop) * b
     return max(0, min(k_loc, K_t // (P - 1)))
 
 
@@ -427,15 +516,16 @@ def _order(s32: np.ndarray, idx: np.ndarray) -> np.ndarray:
     return idx[np.lexsort((idx, -s32[idx].astype(np.float64)))]
 
 
-def select_retained(s32: np.ndarray, P: int, b: int, k_loc: int) -> np.ndarray:
+def select_retained(s32: np.ndarray, P: int, b: int, k_loc: int, drop: int = 1) -> np.ndarray:
     """S = S_loc U TopK_{K_t - |S_loc|}(C minus S_loc), S_loc = union over
     historical blocks B_j of TopK_{k_loc}(B_j) (Sec. 3.3).  Blocks are the
-    pages of the candidate set.  Returns the kept slots in ascending order."""
+    pages of the candidate set; K_t = (P - 1 - drop) b (drop = 1 for Compress
+    & Hold, 2 for a shrink).  Returns the kept slots in ascending order."""
     s32 = np.asarray(s32, dtype=np.float32)
     C = (P - 1) * b
     assert s32.shape[0] == C
-    K_t = (P - 2) * b
-    q = local_quota(P, b, k_loc)
+    K_t = (P - 1 - drop) * b
+    q = local_quota(P, b, k_loc, drop)
     local = []
     for j in range(P - 1):
         blk = np.arange(j * b, (j + 1) * b)
@@ -450,15 +540,16 @@ def select_retained(s32: np.ndarray, P: int, b: int, k_loc: int) -> np.ndarray:
 # A9: compaction (Sec. 3.3; Sec. 4.2; App. E.2)
 # ----------------------------------------------------------------------------
 
-def compact_tokens(tokens: np.ndarray, kept: np.ndarray, P: int, b: int) -> np.ndarray:
-    """New logical contents of one KV head after Compress & Hold: the kept
-    historical tokens in their original order, then the b protected tokens of
-    the last page, filling slots [0, (P-1) b).  Slots from (P-1) b on keep
-    their old contents (they are free).  reading: the order is stable."""
+def compact_tokens(tokens: np.ndarray, kept: np.ndarray, P: int, b: int, drop: int = 1) -> np.ndarray:
+    """New logical contents of one KV head after Compress & Hold (drop = 1) or
+    a shrink (drop = 2): the kept historical tokens in their original order,
+    then the b protected tokens of the last page, filling slots
+    [0, (P - drop) b).  Later slots keep their old contents (they are free).
+    reading: the order is stable."""
     out = tokens.copy()
-    K_t = (P - 2) * b
+    K_t = (P - 1 - drop) * b
     out[:K_t] = tokens[kept]
-    out[K_t:(P - 1) * b] = tokens[(P - 1) * b: P * b]
+    out[K_t:K_t + b] = tokens[(P - 1) * b: P * b]
     return out
 
 
@@ -467,7 +558,7 @@ def compact_tokens(tokens: np.ndarray, kept: np.ndarray, P: int, b: int) -> np.n
 # ----------------------------------------------------------------------------
 
 def boundary_step(layers, dtype, state: PageState, q_pre, qstate, slot_ids, positions, bnd,
-                  params: Params, b: int = 16):
+                  params: Params, b: int = 16, draws=None):
     """Score, decide, select and compact, for every boundary request, over one or
     more layers.  ``layers`` is a list of (k_pool, v_pool) dense arrays
     [pool_pages, Hkv, b, d] (storage type) that are modified in place, and
@@ -503,28 +594,32 @@ def boundary_step(layers, dtype, state: PageState, q_pre, qstate, slot_ids, posi
         scores_all.append(per_layer_s)
         weights_all.append(per_layer_w)
     old_tables = {int(r): state.page_table[int(r)].copy() for r in bnd}
-    dec, delta = decide_and_allocate(state, bnd, counts_all, b, params)
+    old_pages = {int(r): int(state.num_pages[int(r)]) for r in bnd}
+    dec, delta = decide_and_allocate(state, bnd, counts_all, b, params, draws)
     kept_all = {}
     for i, r in enumerate(bnd):
         r = int(r)
-        if dec[i] not in (COMPRESS, FALLBACK):
+        if dec[i] not in (COMPRESS, FALLBACK, SHRINK):
             continue
-        P = int(state.num_pages[r])
+        drop = 2 if dec[i] == SHRINK else 1
+        P = old_pages[r]
         for ell, (kp, vp) in enumerate(layers):
             old = old_tables[r]
             new = state.page_table[r]
             for pool in (kp, vp):
                 toks = gather_tokens(pool, old, P * b, b).copy()      # [P b, Hkv, d]
                 for h in range(toks.shape[1]):
-                    kept = select_retained(scores_all[i][ell][h], P, b, params.k_loc)
+                    kept = select_retained(scores_all[i][ell][h], P, b, params.k_loc, drop)
                     kept_all[(i, ell, h)] = kept
-                    toks[:, h] = compact_tokens(toks[:, h], kept, P, b)
-                # write the first (P-1) b slots back through the new table
-                for j in range(P - 1):
+                    toks[:, h] = compact_tokens(toks[:, h], kept, P, b, drop)
+                # write the resident pages back through the new table
+                for j in range(P - drop):
                     pool[int(new[j])] = toks[j * b:(j + 1) * b].transpose(1, 0, 2)
     counters = np.zeros(4, dtype=np.int64)
     for code in dec:
-        if code < 4:
+        if code == SHRINK:
+            counters[COMPRESS] += 1          # reading: a shrink counts as a compression
+        elif code < 4:
             counters[code] += 1
     return dict(decisions=dec, delta=delta, counts=counts_all, scores=scores_all,
                 weights=weights_all, kept=kept_all, counters=counters)
