@@ -82,7 +82,27 @@ enum {
     GP_GROW = 1,          /* Grow by One Page: a free page appended to the table   */
     GP_FALLBACK = 2,      /* wanted to grow, no page could be granted: compressed  */
     GP_PREEMPT = 3,       /* neither possible; state untouched (scheduler decides) */
-    GP_NOT_BOUNDARY = 4   /* m_r != P_r * page_size; state untouched               */
+    GP_NOT_BOUNDARY = 4,  /* m_r != P_r * page_size; state untouched               */
+    GP_SHRINK = 5         /* GP_POLICY_SHRINK only: two pages of tokens evicted,   */
+                          /* the last page returned, P_r - 1 pages kept            */
+};
+
+/* Capacity-control policies (the paper's appendix on alternative
+ * capacity-control policies).  GP_POLICY_GROWPAGE is the method itself. */
+enum {
+    GP_POLICY_GROWPAGE = 0,  /* grow iff Delta > tau, else Compress & Hold         */
+    GP_POLICY_FIXED = 1,     /* grow while P_r < fixed_pages, compress after that  */
+    GP_POLICY_RANDOM = 2,    /* compress iff draws[i] < compress_prob, else grow   */
+    GP_POLICY_INVERSE = 3,   /* grow iff Delta <= tau, else compress               */
+    GP_POLICY_SHRINK = 4     /* Delta < shrink_threshold: shrink (if P_r - 1 >=     */
+                             /* max(min_capacity_pages, 2)); Delta > tau: grow;    */
+                             /* otherwise compress                                 */
+};
+
+/* Demand metric behind K^x (Sec. 3.2; the signal ablation). */
+enum {
+    GP_METRIC_TOP_P = 0,     /* min k whose k largest weights reach p              */
+    GP_METRIC_ENTROPY = 1    /* exp(-sum a ln a) rounded to the nearest integer    */
 };
 
 /* Which workspace gp_workspace_bytes() sizes. */
@@ -114,7 +134,12 @@ typedef struct {
  * p 0.99 (Sec. 3.2), tau 0 (Sec. 3.2), k_loc a quarter of a block (App. D.2
  * uses 64 of 256; 4 of 16 here), scale 1/sqrt(head_dim), rope_theta 1e6
  * (half-split rotary pairs, as in Qwen3).  reserve_pages: a grow is granted
- * only while more than this many pages are free (Sec. 4.2, "safely"). */
+ * only while more than this many pages are free (Sec. 4.2, "safely").
+ * The remaining fields select a policy variant and the demand metric; all
+ * zero is the method itself.  Appendix values: fixed_pages 256 (4096
+ * tokens), compress_prob 0.7, shrink_threshold -0.005, min_capacity_pages 64
+ * (1024 tokens).  draws: DEVICE [num_bnd] float32 uniform in [0, 1), one per
+ * boundary request, read by GP_POLICY_RANDOM only (may be NULL otherwise). */
 typedef struct {
     float beta_s, beta_l;
     float p;
@@ -123,6 +148,13 @@ typedef struct {
     float rope_theta;
     int32_t k_loc;
     int32_t reserve_pages;
+    int32_t policy;              /* GP_POLICY_*                                 */
+    int32_t metric;              /* GP_METRIC_*                                 */
+    int32_t fixed_pages;
+    int32_t min_capacity_pages;
+    float compress_prob;
+    float shrink_threshold;
+    const float *draws;
 } gp_params_t;
 
 /* Dual-timescale summaries (Sec. 3.2, EMA equation; App. E.1).
@@ -168,8 +200,10 @@ gp_status_t gp_decode_step(const gp_kv_layer_t *kv, const gp_page_state_t *ps, c
  * (RMS calibration), rotated at positions[r], and its softmax over the
  * candidates' keys is taken; the G query heads of a KV head are averaged.
  * Outputs, per KV head h:
- *   k_counts[i][h][x]  top-p working-set size K^x (min k whose k largest
- *                      weights reach p), x = 0 (S), 1 (L);
+ *   k_counts[i][h][x]  working-set size K^x, x = 0 (S), 1 (L): with
+ *                      GP_METRIC_TOP_P the min k whose k largest weights
+ *                      reach p; with GP_METRIC_ENTROPY exp(H) of the weights
+ *                      rounded to the nearest integer, clamped to [1, |C|];
  *   scores[i][h][c]    s_c = max(a^S_c, a^L_c) for c < (P-1) * page_size.
  * Weights are computed in fp64 and rounded to float32; K^x is decided on the
  * float32 weights.  Requests not at a boundary get k_counts 0.  Requires
@@ -187,7 +221,15 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
  * scores[l][num_bnd][Hkv][max_cand] from gp_boundary_score).
  *  - Delta = r^S - r^L, the mean over (layer, KV head) of K^x / |C|
  *    (Sec. 3.2, aggregation equation), evaluated from the integer counts;
- *    Grow iff Delta > tau.  delta[i] receives Delta as float32.
+ *    Grow iff Delta > tau.  delta[i] receives Delta as float32.  Threshold
+ *    tests are exact: the integer sum D = sum (K^S - K^L) is compared with
+ *    t * |C| * Hkv * n_layers in fp64.
+ *  - params->policy replaces the grow test (App., alternative
+ *    capacity-control policies): FIXED grows iff P < fixed_pages; RANDOM
+ *    grows iff !(draws[i] < compress_prob); INVERSE grows iff Delta <= tau;
+ *    SHRINK grows iff Delta > tau, shrinks iff Delta < shrink_threshold and
+ *    P - 1 >= max(min_capacity_pages, 2), else compresses.  With P <= 1
+ *    FIXED grows iff P < fixed_pages, the others always want to grow.
  *  - Requests are served in list order.  A grow pops the free-page stack
  *    (refcount 1, appended at index P); if no page can be granted (stack at or
  *    below reserve_pages, or the table row full) the request compresses
@@ -198,6 +240,10 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
  *    rest of K_t goes to the best remaining candidates (order: score
  *    descending, slot ascending).  Kept tokens stay in order, followed by the
  *    protected last page (Sec. 3.3, selection equation).
+ *  - Shrink (GP_SHRINK) evicts two pages of candidates by the same rule with
+ *    K_t = (P-3) * page_size, moves the last page right after the kept
+ *    tokens, sets m = (P-2) * page_size and P = P - 1, and drops the table's
+ *    reference to the old last page (released if its count reaches zero).
  *  - Shared pages (refcount > 1) are never written: a compressing request
  *    first pops one private page per shared page (GP_PREEMPT if too few), its
  *    compacted tokens go there, and the shared page loses one reference
@@ -205,7 +251,8 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
  *    whose count reaches zero are pushed on the stack at the end of the
  *    call, lowest page id first (the last pushed is popped first).
  *  - Entries of bnd must be distinct (one boundary step per request).
- *  - counters[4] (int64) += number of COMPRESS, GROW, FALLBACK, PREEMPT. */
+ *  - counters[4] (int64) += number of COMPRESS, GROW, FALLBACK, PREEMPT
+ *    (a shrink counts as a compression). */
 gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers,
                               const gp_page_state_t *ps, const int32_t *bnd, int32_t num_bnd,
                               const int32_t *k_counts, const float *scores, int32_t max_cand,

@@ -403,7 +403,9 @@ def _wants(policy_params: Params, dl, P: int, draw):
         # reading: the draw is uniform in [0, 1); compress iff draw < prob
         return not (float(np.float32(draw)) < float(np.float32(pp.compress_prob))), False
     if pp.policy == "shrink":
-        shrink = (dl < Fraction(float(pp.shrink_threshold))) and (P - 1 >= pp.min_capacity_pages)
+        # reading: a shrink keeps at least two pages (one page of survivors
+        # plus one of free slots), whatever the floor says
+        shrink = (dl < Fraction(float(pp.shrink_threshold))) and (P - 1 >= max(pp.min_capacity_pages, 2))
         return above, shrink
     raise ValueError(f"unknown policy {pp.policy!r}")
 

@@ -20,6 +20,9 @@ LIB_PATH = os.path.join(_HERE, "libgrowpage.so")
 GP_F32, GP_BF16 = 0, 1
 GP_OP_DECODE, GP_OP_SCORE, GP_OP_APPLY = 0, 1, 2
 GP_COMPRESS, GP_GROW, GP_FALLBACK, GP_PREEMPT, GP_NOT_BOUNDARY = 0, 1, 2, 3, 4
+GP_SHRINK = 5
+GP_POLICY_GROWPAGE, GP_POLICY_FIXED, GP_POLICY_RANDOM, GP_POLICY_INVERSE, GP_POLICY_SHRINK = 0, 1, 2, 3, 4
+GP_METRIC_TOP_P, GP_METRIC_ENTROPY = 0, 1
 PAGE_SIZE = 16
 
 EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_step", "gp_boundary_score",
@@ -49,7 +52,10 @@ class _PageState(ctypes.Structure):
 class _Params(ctypes.Structure):
     _fields_ = [("beta_s", ctypes.c_float), ("beta_l", ctypes.c_float), ("p", ctypes.c_float),
                 ("tau", ctypes.c_float), ("scale", ctypes.c_float), ("rope_theta", ctypes.c_float),
-                ("k_loc", ctypes.c_int32), ("reserve_pages", ctypes.c_int32)]
+                ("k_loc", ctypes.c_int32), ("reserve_pages", ctypes.c_int32),
+                ("policy", ctypes.c_int32), ("metric", ctypes.c_int32), ("fixed_pages", ctypes.c_int32),
+                ("min_capacity_pages", ctypes.c_int32), ("compress_prob", ctypes.c_float),
+                ("shrink_threshold", ctypes.c_float), ("draws", ctypes.c_void_p)]
 
 
 _lib = None
@@ -155,10 +161,21 @@ class Params:
     rope_theta: float = 1.0e6
     k_loc: int = 4
     reserve_pages: int = 0
+    policy: int = 0                 # GP_POLICY_*
+    metric: int = 0                 # GP_METRIC_*
+    fixed_pages: int = 256
+    min_capacity_pages: int = 64
+    compress_prob: float = 0.7
+    shrink_threshold: float = -0.005
+    draws: torch.Tensor | None = None   # [num_bnd] float32 on the device (RANDOM only)
 
     def c(self) -> _Params:
+        if self.draws is not None and (self.draws.dtype != torch.float32 or not self.draws.is_contiguous()):
+            raise ValueError("draws must be a contiguous float32 tensor")
         return _Params(self.beta_s, self.beta_l, self.p, self.tau, self.scale, self.rope_theta,
-                       self.k_loc, self.reserve_pages)
+                       self.k_loc, self.reserve_pages, self.policy, self.metric, self.fixed_pages,
+                       self.min_capacity_pages, self.compress_prob, self.shrink_threshold,
+                       _ptr(self.draws))
 
 
 def gp_workspace_bytes(op: int, num_reqs: int, num_bnd: int, num_q_heads: int, num_kv_heads: int,

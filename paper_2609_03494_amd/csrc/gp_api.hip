@@ -181,6 +181,7 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
     if (!(params->p > 0.0f && params->p <= 1.0f) || !(params->scale > 0.0f) ||
         !(params->rope_theta > 0.0f))
         return GP_ERR_INVALID;
+    if (params->metric != GP_METRIC_TOP_P && params->metric != GP_METRIC_ENTROPY) return GP_ERR_INVALID;
     if (num_bnd > 65535 || ps->max_pages > kMaxBoundaryPages) return GP_ERR_UNSUPPORTED;
     const ScoreWs w = score_ws(num_bnd, num_q_heads, kv->num_kv_heads, ps->max_pages);
     if (ws_bytes < w.total) return GP_ERR_WORKSPACE;
@@ -214,6 +215,7 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
     a.scale = params->scale;
     a.theta = params->rope_theta;
     a.p = params->p;
+    a.metric = params->metric;
     return from_hip(launch_score(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stream));
 }
 
@@ -237,6 +239,11 @@ gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers, con
     if (!bnd || !k_counts || !scores || !decisions || !delta || !counters || !ws) return GP_ERR_INVALID;
     if (max_cand < (ps->max_pages - 1) * kPage) return GP_ERR_INVALID;
     if (params->k_loc < 0 || params->reserve_pages < 0) return GP_ERR_INVALID;
+    if (params->policy < GP_POLICY_GROWPAGE || params->policy > GP_POLICY_SHRINK) return GP_ERR_INVALID;
+    if (params->policy == GP_POLICY_RANDOM &&
+        (!params->draws || !(params->compress_prob >= 0.0f && params->compress_prob <= 1.0f)))
+        return GP_ERR_INVALID;
+    if (params->policy == GP_POLICY_SHRINK && !isfinite(params->shrink_threshold)) return GP_ERR_INVALID;
     if (num_bnd > 2048 || ps->max_pages > kMaxBoundaryPages) return GP_ERR_UNSUPPORTED;
     const gp_kv_layer_t &L0 = layers[0];
     const int E = elem_bytes(L0.dtype);
@@ -276,6 +283,12 @@ gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers, con
     a.k_loc = params->k_loc;
     a.reserve = params->reserve_pages;
     a.tau = params->tau;
+    a.policy = params->policy;
+    a.fixed_pages = params->fixed_pages;
+    a.min_cap = params->min_capacity_pages;
+    a.compress_prob = params->compress_prob;
+    a.shrink_threshold = params->shrink_threshold;
+    a.draws = params->draws;
     LayerPtrs lp[kMaxLayers];
     for (int l = 0; l < n_layers; ++l) {
         lp[l].k = layers[l].k;

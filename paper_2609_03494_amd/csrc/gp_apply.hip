@@ -41,13 +41,14 @@ struct LayerTable {
 __device__ inline bool compressing(int dec) { return dec == GP_COMPRESS || dec == GP_FALLBACK; }
 
 // ----------------------------------------------------------------- select --
-// Per (boundary request, KV head, layer) of a compressing request: every
-// candidate page keeps its q best tokens (score descending, slot ascending);
-// the 16 remaining candidates that come last in that order are evicted.
+// Per (boundary request, KV head, layer): every candidate page keeps its q
+// best tokens (score descending, slot ascending); the nev remaining candidates
+// that come last in that order are evicted (nev = 16 for Compress & Hold, 32
+// for a shrink, which keeps K_t = (P - 1 - drop) * 16 tokens).
 // Eviction order is the ascending order of the 48-bit key
 // (score bits << 16) | (0xffff - slot): scores are non-negative floats, so
 // their bit patterns sort like their values, and a later slot loses a tie.
-// The 16th smallest key is found by a radix select over 8-bit digits, each
+// The nev-th smallest key is found by a radix select over 8-bit digits, each
 // pass a histogram of the keys that share the prefix found so far, scanned by
 // wave 0.  The two slot digits are only resolved when candidates tie on the
 // threshold score and not all of them are evicted.  Each thread keeps the
@@ -61,15 +62,16 @@ __device__ inline void load_page_scores(const float *s, int j, uint32_t (&v)[kPa
     for (int t = 0; t < kPage; ++t) v[t] = __float_as_uint(s[j * kPage + t]);
 }
 
-__device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P) {
+__device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, int nev, int drop,
+                              int out_offset) {
     constexpr int NB = 256;
     __shared__ unsigned int s_hist[NB];
     __shared__ int s_bucket, s_below, s_in_bucket, s_nev;
-    __shared__ int s_ev[kPage];
+    __shared__ int s_ev[kShrinkEvict];
     const int tid = threadIdx.x, lane = tid & 63;
     const int npages = min(P - 1, kSelMaxPages);
-    const int Kt = (P - 2) * kPage;
-    const int q = P >= 3 ? min(a.k_loc, Kt / (P - 1)) : 0;
+    const int Kt = (P - 1 - drop) * kPage;
+    const int q = Kt > 0 ? min(a.k_loc, Kt / (P - 1)) : 0;
     const float *s = a.scores + (((size_t)l * a.Rb + i) * a.Hkv + h) * a.max_cand;
 
     uint32_t cache[kSelCached][kPage];
@@ -101,7 +103,7 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P) {
 
     // the 48-bit key has 6 digits: 4 of the score, 2 of the inverted slot
     unsigned long long prefix = 0;
-    int need = kPage;
+    int need = nev;
     int digits = 0;
     for (int pass = 0; pass < 6; ++pass) {
         const int sh = 40 - 8 * pass;
@@ -151,7 +153,7 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P) {
                     cum += cs[k];
                 }
             }
-            if (lane == 63 && ic < (unsigned)need) {   // fewer candidates than page_size
+            if (lane == 63 && ic < (unsigned)need) {   // fewer candidates than nev
                 s_bucket = NB - 1;
                 s_below = (int)ic;
                 s_in_bucket = 0;
@@ -171,7 +173,7 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P) {
 
     // evict every candidate whose key is at most the threshold
     if (tid == 0) s_nev = 0;
-    if (tid < kPage) s_ev[tid] = -1;
+    if (tid < kShrinkEvict) s_ev[tid] = -1;
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -191,22 +193,22 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P) {
                                            (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
             if (key <= hi) {
                 const int at = atomicAdd(&s_nev, 1);
-                if (at < kPage) s_ev[at] = j * kPage + t;
+                if (at < nev) s_ev[at] = j * kPage + t;
             }
         }
     }
     __syncthreads();
     if (tid == 0) {
-        int ev[kPage];
+        int ev[kShrinkEvict];
 #pragma unroll
-        for (int k = 0; k < kPage; ++k) ev[k] = s_ev[k] < 0 ? 0x7fffffff : s_ev[k];
+        for (int k = 0; k < kShrinkEvict; ++k) ev[k] = s_ev[k] < 0 ? 0x7fffffff : s_ev[k];
         // ascending slot order (bitonic sorting network, static indices)
 #pragma unroll
-        for (int k = 2; k <= kPage; k <<= 1)
+        for (int k = 2; k <= kShrinkEvict; k <<= 1)
 #pragma unroll
             for (int j = k >> 1; j > 0; j >>= 1)
 #pragma unroll
-                for (int x = 0; x < kPage; ++x) {
+                for (int x = 0; x < kShrinkEvict; ++x) {
                     const int y = x ^ j;
                     if (y > x) {
                         const bool up = (x & k) == 0;
@@ -216,10 +218,10 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P) {
                         ev[y] = up ? hi2 : lo;
                     }
                 }
-        int32_t *out = a.evict + (((size_t)l * a.Rb + i) * a.Hkv + h) * kPage;
-#pragma unroll
-        for (int k = 0; k < kPage; ++k) out[k] = ev[k] == 0x7fffffff ? -1 : ev[k];
+        int32_t *out = a.evict + (((size_t)l * a.Rb + i) * a.Hkv + h) * kEvictSlots + out_offset;
+        for (int k = 0; k < nev; ++k) out[k] = ev[k] == 0x7fffffff ? -1 : ev[k];
     }
+    __syncthreads();
 }
 
 // -------------------------------------------------------------------- pre --
@@ -237,7 +239,11 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
         at_boundary = P >= 2 && P <= a.max_pages && a.seq_lens[r] == P * kPage;
     }
     if (x == 0) {
-        if (at_boundary) select_tokens(a, i, h, l, P);
+        if (at_boundary) {
+            select_tokens(a, i, h, l, P, kPage, 1, 0);
+            if (a.policy == GP_POLICY_SHRINK && P - 1 >= max(a.min_cap, 2))
+                select_tokens(a, i, h, l, P, kShrinkEvict, 2, kPage);
+        }
         return;
     }
     const int cc = x - 1;
@@ -260,25 +266,31 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
         if (tid == 0) a.nshc[(size_t)i * a.npc + cc] = s_n;
     }
     if (!at_boundary || cc == 0 || cc >= cdiv(P * kPage, kCompactChunk)) return;
+    // the kBorderRows rows below slot cc * kCompactChunk: the two pages before it
     constexpr int UPP = D * E / 16 * kPage;          // 16-byte units per page slice
-    const int lp = cc * kCompactChunk / kPage - 1;
-    const int phys = row[lp];
-    if (phys < 0 || phys >= a.pool_pages) return;
-    const size_t src_off = (size_t)phys * a.Hkv * kPage * D * E + (size_t)h * kPage * D * E;
-    unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc + cc) * 2 * kPage * D * E;
-    const unsigned char *kp = reinterpret_cast<const unsigned char *>(lt.k[l]) + src_off;
-    const unsigned char *vp = reinterpret_cast<const unsigned char *>(lt.v[l]) + src_off;
-    for (int u = tid; u < 2 * UPP; u += blockDim.x) {
-        const unsigned char *src = u < UPP ? kp + (size_t)u * 16 : vp + (size_t)(u - UPP) * 16;
-        *reinterpret_cast<uint4 *>(bd + (size_t)u * 16) = *reinterpret_cast<const uint4 *>(src);
+    constexpr int NBP = kBorderRows / kPage;         // pages saved per boundary
+    unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc + cc) * 2 * kBorderRows * D * E;
+    for (int u = tid; u < 2 * NBP * UPP; u += blockDim.x) {
+        const int kv = u / (NBP * UPP), rem = u % (NBP * UPP), pg = rem / UPP, w = rem % UPP;
+        const int lp = cc * kCompactChunk / kPage - NBP + pg;
+        const int phys = row[lp];
+        if (phys < 0 || phys >= a.pool_pages) continue;
+        const size_t src_off = (size_t)phys * a.Hkv * kPage * D * E + (size_t)h * kPage * D * E;
+        const unsigned char *src = reinterpret_cast<const unsigned char *>(kv == 0 ? lt.k[l] : lt.v[l]) + src_off;
+        *reinterpret_cast<uint4 *>(bd + (size_t)u * 16) = *reinterpret_cast<const uint4 *>(src + (size_t)w * 16);
     }
 }
 
 // ----------------------------------------------------------------- decide --
+// Flags per boundary request: bit 0 at a boundary, bit 1 wants to grow, bit 2
+// wants to shrink.
+enum { F_BOUNDARY = 1, F_GROW = 2, F_SHRINK = 4 };
+
 __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
     __shared__ int s_P[kMaxBnd];
-    __shared__ int s_flags[kMaxBnd];   // bit 0: at a boundary, bit 1: wants to grow
-    __shared__ int s_nsh[kMaxBnd];
+    __shared__ int s_flags[kMaxBnd];
+    __shared__ int s_nsh[kMaxBnd];     // shared pages to replace (after the decision)
+    __shared__ int s_nsh_last[kMaxBnd];  // whether the last page is one of them
     __shared__ int s_dec[kMaxBnd];
     __shared__ int s_pop[kMaxBnd];
     __shared__ long long s_cnt[4];
@@ -288,13 +300,13 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
 
     for (int i = tid; i < Rb; i += blockDim.x) {
         const int r = a.bnd[i];
-        int P = 0, flags = 0, nsh = 0;
+        int P = 0, flags = 0, nsh = 0, last_shared = 0;
         float dl = 0.0f;
         if (r >= 0 && r < a.R) {
             P = a.num_pages[r];
             if (P >= 0 && P <= a.max_pages && a.seq_lens[r] == P * kPage) {
-                flags = 1;
-                bool want = true;
+                flags = F_BOUNDARY;
+                bool grow, shrink = false;
                 if (P >= 2) {
                     long long D = 0;
                     for (int l = 0; l < a.n_layers; ++l)
@@ -302,21 +314,37 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
                             const int32_t *kc = a.k_counts + (((size_t)l * Rb + i) * a.Hkv + h) * 2;
                             D += (long long)kc[0] - (long long)kc[1];
                         }
-                    // Delta = (sum K^S - sum K^L) / (|C| * Hkv * layers); the
-                    // quotient is correctly rounded, so its sign is exact.
-                    const double denom = (double)(P - 1) * kPage * a.Hkv * a.n_layers;
-                    const double dd = (double)D / denom;
-                    dl = (float)dd;
-                    want = dd > a.tau;
+                    // Delta = D / denom, denom = |C| * Hkv * layers.  Thresholds
+                    // compare exactly as D against t * denom: t is a float and
+                    // denom < 2^29, so the product is exact in fp64.
+                    const long long denom = (long long)(P - 1) * kPage * a.Hkv * a.n_layers;
+                    dl = (float)((double)D / (double)denom);
+                    const bool above = (double)D > a.tau * (double)denom;      // Delta > tau
+                    switch (a.policy) {
+                        case GP_POLICY_INVERSE: grow = !above; break;
+                        case GP_POLICY_FIXED: grow = P < a.fixed_pages; break;
+                        case GP_POLICY_RANDOM: grow = !(a.draws[i] < a.compress_prob); break;
+                        case GP_POLICY_SHRINK:
+                            grow = above;
+                            shrink = (double)D < a.shrink_threshold * (double)denom &&
+                                     P - 1 >= max(a.min_cap, 2);
+                            break;
+                        default: grow = above; break;
+                    }
                     for (int c = 0; c < a.npc; ++c) nsh += a.nshc[(size_t)i * a.npc + c];
+                    last_shared = a.shflag[(size_t)i * a.max_pages + P - 1];
+                } else {
+                    grow = a.policy == GP_POLICY_FIXED ? P < a.fixed_pages : true;
                 }
-                if (want) flags |= 2;
+                if (grow) flags |= F_GROW;
+                if (shrink) flags |= F_SHRINK;
             }
         }
         a.delta[i] = dl;
         s_P[i] = P;
         s_flags[i] = flags;
         s_nsh[i] = nsh;
+        s_nsh_last[i] = last_shared;
     }
     if (tid == 0) {
         const int fc = *a.free_count;
@@ -331,24 +359,25 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
         for (int i = 0; i < Rb; ++i) {
             const int P = s_P[i], fl = s_flags[i];
             int dec = GP_NOT_BOUNDARY, pop = 0;
-            if (fl & 1) {
-                const bool want = (fl & 2) != 0;
+            if (fl & F_BOUNDARY) {
+                const bool want = (fl & F_GROW) != 0, shrink = (fl & F_SHRINK) != 0;
                 const int avail = fc0 - popped;
                 const bool can_grow = avail > a.reserve && P < a.max_pages;
+                // a shrink keeps pages [0, P - 1) only: the last page needs no copy
+                const int nsh = shrink ? s_nsh[i] - s_nsh_last[i] : s_nsh[i];
                 if (want && can_grow) {
                     dec = GP_GROW;
                     pop = popped;
                     popped += 1;
-                } else if (P <= 1) {
-                    dec = GP_PREEMPT;
-                } else if (s_nsh[i] > avail) {
+                } else if (P <= 1 || nsh > avail) {
                     dec = GP_PREEMPT;
                 } else {
-                    dec = want ? GP_FALLBACK : GP_COMPRESS;
+                    dec = shrink ? GP_SHRINK : (want ? GP_FALLBACK : GP_COMPRESS);
                     pop = popped;
-                    popped += s_nsh[i];
+                    popped += nsh;
+                    s_nsh[i] = nsh;
                 }
-                cnt[dec] += 1;
+                cnt[dec == GP_SHRINK ? GP_COMPRESS : dec] += 1;   // a shrink counts as a compression
             }
             s_dec[i] = dec;
             s_pop[i] = pop;
@@ -362,12 +391,13 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
     for (int i = tid; i < Rb; i += blockDim.x) {
         const int dec = s_dec[i], P = s_P[i];
         const int r = a.bnd[i];
+        const bool moves = compressing(dec) || dec == GP_SHRINK;
         a.decisions[i] = dec;
         int32_t *rq = a.req + (size_t)i * RQ_STRIDE;
         rq[RQ_R] = r;
         rq[RQ_P] = P;
         rq[RQ_FLAGS] = s_flags[i];
-        rq[RQ_NSH] = compressing(dec) ? s_nsh[i] : 0;
+        rq[RQ_NSH] = moves ? s_nsh[i] : 0;
         rq[RQ_POP] = s_pop[i];
         rq[RQ_DEC] = dec;
         if (dec == GP_GROW) {
@@ -377,6 +407,9 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
             a.num_pages[r] = P + 1;
         } else if (compressing(dec)) {
             a.seq_lens[r] = (P - 1) * kPage;
+        } else if (dec == GP_SHRINK) {
+            a.seq_lens[r] = (P - 2) * kPage;
+            a.num_pages[r] = P - 1;
         }
     }
     if (tid == 0) {
@@ -386,18 +419,22 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
         for (int k = 0; k < 4; ++k) a.counters[k] += s_cnt[k];
     }
 
-    // compressing requests with shared pages: a private page replaces each
-    // shared one (ranked by logical page), the old row is kept for the copy,
-    // and the old reference is dropped; pages reaching zero are listed
+    // Requests whose table row changes: the old row is kept for the copy; a
+    // private page replaces each shared page that stays (ranked by logical
+    // page) and the old reference is dropped; a shrink also drops the last
+    // page.  Pages whose count reaches zero are listed.
     __shared__ int s_scan[1024];
     for (int i = 0; i < Rb; ++i) {
-        if (!compressing(s_dec[i]) || s_nsh[i] == 0) continue;      // uniform
+        const int dec = s_dec[i];
+        const bool shrink = dec == GP_SHRINK;
+        if (!(compressing(dec) && s_nsh[i] > 0) && !shrink) continue;      // uniform
         const int r = a.bnd[i], P = s_P[i];
+        const int keep = shrink ? P - 1 : P;
         int32_t *row = a.page_table + (size_t)r * a.max_pages;
         int base = 0;
         for (int j0 = 0; j0 < P; j0 += 1024) {
             const int j = j0 + tid;
-            const int sh = j < P ? a.shflag[(size_t)i * a.max_pages + j] : 0;
+            const int sh = j < keep ? a.shflag[(size_t)i * a.max_pages + j] : 0;
             s_scan[tid] = sh;
             __syncthreads();
             for (int off = 1; off < 1024; off <<= 1) {
@@ -414,8 +451,13 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
                     const int pid = a.free_list[fc0 - 1 - s_pop[i] - k];
                     row[j] = pid;
                     if (pid >= 0 && pid < a.pool_pages) a.refcount[pid] = 1;
-                    const int prev = atomicSub(&a.refcount[old], 1);
-                    if (prev == 1) a.released[atomicAdd(&a.hdr[HDR_NREL], 1)] = old;
+                }
+                if (sh || (shrink && j == P - 1)) {
+                    if (shrink && j == P - 1) row[j] = -1;
+                    if (old >= 0 && old < a.pool_pages) {
+                        const int prev = atomicSub(&a.refcount[old], 1);
+                        if (prev == 1) a.released[atomicAdd(&a.hdr[HDR_NREL], 1)] = old;
+                    }
                 }
             }
             base += s_scan[1023];
@@ -430,7 +472,7 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
     constexpr int UPR = D * E / 16;
     constexpr int ROWS = kCompactChunk;
     constexpr int UNITS = ROWS * UPR / 256;         // 16-byte units per thread
-    __shared__ int s_ev[kPage];
+    __shared__ int s_ev[kShrinkEvict];
     __shared__ int s_dst[ROWS];
     __shared__ long long s_src_off[ROWS], s_dst_off[ROWS];
     __shared__ int s_rel[1024];
@@ -460,14 +502,19 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
     }
 
     const int32_t *rq = a.req + (size_t)i * RQ_STRIDE;
-    if (!compressing(rq[RQ_DEC])) return;
+    const int dec = rq[RQ_DEC];
+    const bool shrink = dec == GP_SHRINK;
+    if (!compressing(dec) && !shrink) return;
     const int r = rq[RQ_R], P = rq[RQ_P], nsh = rq[RQ_NSH];
+    const int nev = shrink ? kShrinkEvict : kPage;
     const int total = P * kPage;
     const int s0 = cc * ROWS;
     if (s0 >= total) return;
     const int32_t *row = a.page_table + (size_t)r * a.max_pages;
-    const int32_t *src_row = nsh > 0 ? a.old_table + (size_t)i * a.max_pages : row;
-    if (tid < kPage) s_ev[tid] = a.evict[(((size_t)l * a.Rb + i) * a.Hkv + h) * kPage + tid];
+    const int32_t *src_row = nsh > 0 || shrink ? a.old_table + (size_t)i * a.max_pages : row;
+    if (tid < kShrinkEvict)
+        s_ev[tid] = tid < nev ? a.evict[(((size_t)l * a.Rb + i) * a.Hkv + h) * kEvictSlots + (shrink ? kPage : 0) + tid]
+                              : -1;
     __syncthreads();
 
     const size_t page_bytes = (size_t)a.Hkv * kPage * D * E;
@@ -480,7 +527,7 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
             int before = 0;
             bool gone = false;
 #pragma unroll
-            for (int k = 0; k < kPage; ++k) {
+            for (int k = 0; k < kShrinkEvict; ++k) {
                 before += (s_ev[k] >= 0 && s_ev[k] < s) ? 1 : 0;
                 gone = gone || s_ev[k] == s;
             }
@@ -501,7 +548,7 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
     }
     __syncthreads();
 
-    const unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc) * 2 * kPage * D * E;
+    const unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc) * 2 * kBorderRows * D * E;
     unsigned char *pools[2] = {reinterpret_cast<unsigned char *>(lt.k[l]),
                                reinterpret_cast<unsigned char *>(lt.v[l])};
 #pragma unroll
@@ -514,9 +561,9 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
             const int rr = u / UPR, w = u % UPR;
             val[k] = make_uint4(0u, 0u, 0u, 0u);
             if (s_dst[rr] >= 0) {
-                if (has_border && rr >= ROWS - kPage) {
-                    const unsigned char *src = bd + ((size_t)(cc + 1) * 2 + kv) * kPage * D * E +
-                                               (size_t)(rr - (ROWS - kPage)) * D * E + (size_t)w * 16;
+                if (has_border && rr >= ROWS - kBorderRows) {
+                    const unsigned char *src = bd + ((size_t)(cc + 1) * 2 + kv) * kBorderRows * D * E +
+                                               (size_t)(rr - (ROWS - kBorderRows)) * D * E + (size_t)w * 16;
                     val[k] = *reinterpret_cast<const uint4 *>(src);
                 } else {
                     val[k] = *reinterpret_cast<const uint4 *>(pool + s_src_off[rr] + (size_t)w * 16);

@@ -105,6 +105,11 @@ enum { RQ_R = 0, RQ_P, RQ_FLAGS, RQ_NSH, RQ_POP, RQ_DEC, RQ_STRIDE = 8 };
 // Call header (int32): free count before pops, after pops, released pages.
 enum { HDR_FC0 = 0, HDR_FC1, HDR_NREL, HDR_SIZE = 4 };
 constexpr int kPageBlock = 1024;  // pages per work item when walking a page-table row
+// Eviction lists per (layer, boundary request, KV head): slots [0, 16) for a
+// Compress & Hold, [16, 48) for a shrink.  Rows move down by at most 32 slots.
+constexpr int kShrinkEvict = 2 * kPage;
+constexpr int kEvictSlots = kPage + kShrinkEvict;
+constexpr int kBorderRows = kShrinkEvict;
 
 __host__ __device__ inline ApplyWs apply_ws(int Rb, int Hkv, int D, int elem, int max_pages,
                                             int n_layers) {
@@ -124,10 +129,10 @@ __host__ __device__ inline ApplyWs apply_ws(int Rb, int Hkv, int D, int elem, in
     off = align_up(off + (size_t)Rb * max_pages * sizeof(int32_t));
     w.released = off;   // [Rb * max_pages]
     off = align_up(off + (size_t)Rb * max_pages * sizeof(int32_t));
-    w.evict = off;      // [L][Rb][Hkv][16]
-    off = align_up(off + (size_t)n_layers * Rb * Hkv * kPage * sizeof(int32_t));
-    w.border = off;     // [L][Rb][Hkv][ncc][2][16][D] elements
-    off = align_up(off + (size_t)n_layers * Rb * Hkv * w.ncc * 2 * kPage * D * elem);
+    w.evict = off;      // [L][Rb][Hkv][kEvictSlots]
+    off = align_up(off + (size_t)n_layers * Rb * Hkv * kEvictSlots * sizeof(int32_t));
+    w.border = off;     // [L][Rb][Hkv][ncc][2][kBorderRows][D] elements
+    off = align_up(off + (size_t)n_layers * Rb * Hkv * w.ncc * 2 * kBorderRows * D * elem);
     w.total = off;
     return w;
 }
@@ -172,6 +177,7 @@ struct ScoreArgs {
     float *weights;
     int Rb, Hq, Hkv, M, max_pages, pool_pages, max_cand, cmax, nch, R;
     double scale, theta, p;
+    int metric;       // GP_METRIC_*
 };
 
 struct ApplyArgs {
@@ -186,6 +192,11 @@ struct ApplyArgs {
     unsigned char *border;
     int R, Rb, Hkv, max_pages, pool_pages, max_cand, n_layers, ncc, npc, k_loc, reserve;
     double tau;
+    // policy variant (GP_POLICY_*) and its constants
+    int policy, fixed_pages, min_cap;
+    float compress_prob;
+    double shrink_threshold;
+    const float *draws;
 };
 
 struct LayerPtrs {

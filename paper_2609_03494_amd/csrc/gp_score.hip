@@ -391,6 +391,38 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
     }
 }
 
+// ------------------------------------------------------------------ entropy --
+// The signal ablation's alternative demand metric: per (request, KV head,
+// view) the entropy H = -sum a ln a of the float32 weights (fp64, zero weights
+// contribute nothing) and K = exp(H) rounded to the nearest integer, clamped
+// to [1, |C|].
+__global__ __launch_bounds__(256) void entropy_kernel(ScoreArgs a) {
+    __shared__ double s_red[4];
+    const int x = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int32_t *out = a.k_counts + ((size_t)i * a.Hkv + h) * 2 + x;
+    int r, P;
+    if (!boundary_of(a, i, r, P)) {
+        if (tid == 0) *out = 0;
+        return;
+    }
+    const int C = (P - 1) * kPage;
+    const float *wv = a.weights + (((size_t)i * a.Hkv + h) * 2 + x) * a.cmax;
+    double acc = 0.0;
+    for (int t = tid; t < C; t += blockDim.x) {
+        const double w = (double)wv[t];
+        if (w > 0.0) acc += w * log(w);
+    }
+    for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (lane == 0) s_red[wave] = acc;
+    __syncthreads();
+    if (tid == 0) {
+        const double H = -(s_red[0] + s_red[1] + s_red[2] + s_red[3]);
+        const double e = floor(exp(H) + 0.5);
+        *out = e < 1.0 ? 1 : (e > (double)C ? C : (int)e);
+    }
+}
+
 template <typename T, int D>
 hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
     dim3 g0(a.Hkv, a.Rb), g1(a.nch, a.Hkv, a.Rb), g2(cdiv(a.cmax, kProbChunk), a.Hkv, a.Rb), g3(2, a.Hkv, a.Rb);
@@ -410,7 +442,10 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
 #undef GP_CASE
         default: return hipErrorInvalidValue;
     }
-    top_p_kernel<<<g3, 1024, 0, s>>>(a);
+    if (a.metric == GP_METRIC_ENTROPY)
+        entropy_kernel<<<g3, 256, 0, s>>>(a);
+    else
+        top_p_kernel<<<g3, 1024, 0, s>>>(a);
     return hipGetLastError();
 }
 

@@ -50,6 +50,22 @@ def oracle_state(w: W.Workload) -> O.PageState:
                        w.refcount.copy(), w.free_list.copy(), int(w.free_count))
 
 
+POLICY_CODES = {"growpage": gp.GP_POLICY_GROWPAGE, "fixed": gp.GP_POLICY_FIXED,
+                "random": gp.GP_POLICY_RANDOM, "inverse": gp.GP_POLICY_INVERSE,
+                "shrink": gp.GP_POLICY_SHRINK}
+METRIC_CODES = {"top_p": gp.GP_METRIC_TOP_P, "entropy": gp.GP_METRIC_ENTROPY}
+
+
+def library_params(params: O.Params, head_dim: int, draws=None) -> "gp.Params":
+    """The oracle's constants, rounded to float32, as the library's struct;
+    draws (host float32 [num_bnd]) are copied to the device."""
+    p32 = params.as_f32(head_dim)
+    d = None if draws is None else torch.from_numpy(np.asarray(draws, np.float32)).to(DEV)
+    return gp.Params(p32.beta_s, p32.beta_l, p32.p, p32.tau, p32.scale, p32.rope_theta, p32.k_loc,
+                     p32.reserve_pages, POLICY_CODES[p32.policy], METRIC_CODES[p32.metric],
+                     p32.fixed_pages, p32.min_capacity_pages, p32.compress_prob, p32.shrink_threshold, d)
+
+
 class DeviceCase:
     """One workload resident on the GPU, with the library's workspaces."""
 
@@ -96,14 +112,12 @@ class DeviceCase:
         return O.widen(to_numpy(out), self.w.dtype)
 
     # ------------------------------------------------------------- A3..A9
-    def boundary(self, params: O.Params, bnd=None, q_pre_layers=None, qstate_layers=None):
+    def boundary(self, params: O.Params, bnd=None, q_pre_layers=None, qstate_layers=None, draws=None):
         w = self.w
         bnd = w.boundary if bnd is None else np.asarray(bnd, np.int32)
         Rb = int(bnd.shape[0])
         dt = torch_dtype(w)
-        p32 = params.as_f32(w.head_dim)
-        gparams = gp.Params(p32.beta_s, p32.beta_l, p32.p, p32.tau, p32.scale, p32.rope_theta,
-                            p32.k_loc, p32.reserve_pages)
+        gparams = library_params(params, w.head_dim, draws)
         max_cand = (w.max_pages - 1) * w.page_size
         L = self.n_layers
         bnd_t = torch.from_numpy(bnd.astype(np.int32)).to(DEV)

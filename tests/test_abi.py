@@ -81,6 +81,17 @@ def test_host_validation_without_launch(lib):
     arr = (_lib._KVLayer * 1)(kv)
     assert lib.gp_boundary_apply(arr, 65, ctypes.byref(ps), fake, 2, fake, fake, 144, ctypes.byref(p),
                                  fake, fake, fake, fake, 1 << 30, None) == 2
+    # score: unknown demand metric
+    pm = _lib._Params(0.9, 0.999, 0.99, 0.0, 0.088, 1e6, 4, 0, 0, 2)
+    assert lib.gp_boundary_score(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 512, fake, fake, fake,
+                                 2, 32, ctypes.byref(pm), fake, fake, 144, fake, 1 << 30, None) == 1
+    # apply: unknown policy, random policy without draws or with a probability
+    # outside [0, 1], shrink with a non-finite threshold
+    for fields in ((9, 0, 0, 0, 0.7, -0.005, None), (2, 0, 0, 0, 0.7, -0.005, None),
+                   (2, 0, 0, 0, 1.5, -0.005, fake), (4, 0, 0, 64, 0.7, float("nan"), None)):
+        pa = _lib._Params(0.9, 0.999, 0.99, 0.0, 0.088, 1e6, 4, 0, *fields)
+        assert lib.gp_boundary_apply(arr, 1, ctypes.byref(ps), fake, 2, fake, fake, 144, ctypes.byref(pa),
+                                     fake, fake, fake, fake, 1 << 30, None) == 1, fields
     # fused step: beta outside [0, 1], null summary pool, then a small workspace
     assert lib.gp_decode_step(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 32, 0.1, fake, fake, fake,
                               fake, 512, 0.9, -0.5, fake, 1 << 30, None) == 1

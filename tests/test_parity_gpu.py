@@ -74,7 +74,14 @@ def _decode_check(w, dc, requests=None):
     return worst
 
 
-def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=None):
+def _fragile(a32, p32):
+    """A working-set size another float evaluation order may move by one."""
+    if p32.metric == "entropy":
+        return O.entropy_fragile(a32, 1e-6)
+    return O.top_p_fragile(a32, p32.p, 1e-6)
+
+
+def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=None, draws=None):
     """Run one boundary event on both sides and compare everything."""
     bnd = w.boundary if bnd is None else np.asarray(bnd, np.int32)
     p32 = params.as_f32(w.head_dim)
@@ -87,8 +94,9 @@ def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=N
     kp, vp = w.dense_pool("k"), w.dense_pool("v")
     kp0, vp0 = kp.copy(), vp.copy()
     before_state = st.copy()
-    ref = O.boundary_step([(kp, vp)], w.dtype, st, w.q_pre, qs, w.slot_ids, w.positions, bnd, p32)
-    got = dc.boundary(params, bnd=bnd)
+    ref = O.boundary_step([(kp, vp)], w.dtype, st, w.q_pre, qs, w.slot_ids, w.positions, bnd, p32,
+                          draws=draws)
+    got = dc.boundary(params, bnd=bnd, draws=draws)
     b = w.page_size
     # working-set sizes and scores
     fragile = set()
@@ -98,7 +106,7 @@ def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=N
             for x in range(2):
                 g, o = int(got["k_counts"][0, i, h, x]), int(ref["counts"][i][0, h, x])
                 a32 = ref["weights"][i][0][x, h]
-                if a32.size and O.top_p_fragile(a32, p32.p, 1e-6):
+                if a32.size and _fragile(a32, p32):
                     fragile.add(i)
                     assert abs(g - o) <= 1, (i, h, x, g, o)
                 else:
@@ -129,10 +137,11 @@ def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=N
     # compacted K/V
     excused = 0
     for i, r in enumerate(bnd):
-        if dec_o[i] not in (O.COMPRESS, O.FALLBACK):
+        if dec_o[i] not in (O.COMPRESS, O.FALLBACK, O.SHRINK):
             continue
         P = int(before_state.num_pages[r])
-        n = (P - 1) * b
+        drop = 2 if dec_o[i] == O.SHRINK else 1
+        n = (P - drop) * b
         for which, pool, pool0 in (("k", kp, kp0), ("v", vp, vp0)):
             want = O.gather_tokens(pool, st.page_table[r], n, b)
             have = dc.gather(gs.page_table[r], n, which)
@@ -144,7 +153,7 @@ def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=N
                     continue
                 idx = row_index(before[:, h], have[:, h])
                 assert (idx >= 0).all(), f"compaction wrote rows that were never there (req {r})"
-                K_t = (P - 2) * b
+                K_t = (P - 1 - drop) * b
                 assert (np.diff(idx[:K_t]) > 0).all() and (idx[K_t:] == np.arange((P - 1) * b, P * b)).all()
                 kept_o = ref["kept"][(i, 0, h)]
                 band = threshold_band(ref["scores"][i][0][h], kept_o, P, b, p32.k_loc)
@@ -347,6 +356,74 @@ def test_boundary_not_at_boundary_and_small_P():
     assert res["decisions"].tolist() == [O.COMPRESS, O.NOT_BOUNDARY, O.COMPRESS, O.GROW]
     res = _boundary_check(w, O.Params(tau=-math.inf), bnd=bnd)
     assert res["decisions"].tolist() == [O.GROW, O.NOT_BOUNDARY, O.GROW, O.GROW]
+
+
+# ------------------------------------ capacity policies and demand metric --
+
+@pytest.mark.parametrize("policy", ["fixed", "random", "inverse", "shrink"])
+def test_boundary_policy_variants(policy):
+    """The appendix's alternative capacity-control policies against the oracle
+    on a reduced Qwen3-8B batch (12 requests, 6 at a boundary)."""
+    w = W.qwen3_8b(seed=7, num_reqs=12, len_lo=300, len_hi=4000, budget_choices=(8, 60, 200),
+                   boundary_frac=0.5, free_pages=30)
+    draws = W.policy_draws(3, len(w.boundary)) if policy == "random" else None
+    kw = dict(policy=policy, fixed_pages=40, min_capacity_pages=4)
+    _say(f"boundary: policy {policy}, Qwen3-8B heads, 12 requests")
+    res = _boundary_check(w, O.Params(**kw), draws=draws)
+    _say("decisions", res["decisions"].tolist())
+    if policy == "shrink":
+        _say("boundary: policy shrink, every boundary request shrinks")
+        res = _boundary_check(w, O.Params(tau=math.inf, shrink_threshold=10.0, **kw))
+        assert (res["decisions"] == O.SHRINK).all()
+
+
+def test_boundary_shrink_prefix_shared_and_floor():
+    """Shrink replaces the shared pages it keeps, drops its reference to the
+    last page, and is preempted when private pages run out; below the floor it
+    compresses."""
+    w = W.prefix_shared(num_reqs=8, prefix_len=320, tail_lo=40, tail_hi=1200, boundary_frac=0.5,
+                        free_pages=200)
+    p = O.Params(policy="shrink", tau=math.inf, shrink_threshold=10.0, min_capacity_pages=2)
+    _say("boundary: shrink on a shared prefix")
+    res = _boundary_check(w, p)
+    assert (res["decisions"] == O.SHRINK).all()
+    _say("boundary: shrink on a shared prefix, 5 free pages")
+    _boundary_check(w, p, free_count=5)
+    _say("boundary: shrink floor above every request -> compress")
+    res = _boundary_check(w, O.Params(policy="shrink", tau=math.inf, shrink_threshold=10.0,
+                                      min_capacity_pages=4096))
+    assert (res["decisions"] == O.COMPRESS).all()
+
+
+def test_boundary_shrink_tiny_and_small_P():
+    """P = 3 is the smallest request that can shrink (one page of survivors);
+    P = 2 compresses."""
+    w = W._build(name="edge", seed=31, dtype="f32", Hq=4, Hkv=2, d=64,
+                 n=np.array([48, 32, 64, 100]), budgets=None, free_pages=6,
+                 heavy_mode="scaled", heavy_frac=0.05, summary_mode="random")
+    bnd = np.array([0, 1, 2, 3], np.int32)
+    p = O.Params(policy="shrink", tau=math.inf, shrink_threshold=10.0, min_capacity_pages=0)
+    res = _boundary_check(w, p, bnd=bnd)
+    assert res["decisions"].tolist() == [O.SHRINK, O.COMPRESS, O.SHRINK, O.NOT_BOUNDARY]
+
+
+@pytest.mark.parametrize("case", ["tiny", "qwen3", "long"])
+def test_boundary_entropy_metric(case):
+    """The signal ablation's entropy working-set size in place of top-p."""
+    p = O.Params(metric="entropy")
+    if case == "tiny":
+        _say("boundary: entropy metric, tiny fp32")
+        w, dc, st = _tiny_prepared()
+        _boundary_check(w, p, qstate_host=st, dc=dc)
+        return
+    if case == "qwen3":
+        w = W.qwen3_8b(seed=7, num_reqs=12, len_lo=300, len_hi=4000, budget_choices=(8, 60, 200),
+                       boundary_frac=0.5, free_pages=30)
+    else:
+        w = W.long_reasoning(num_reqs=8, len_lo=1500, len_hi=4200, free_pages=40)
+    _say(f"boundary: entropy metric, {case}")
+    res = _boundary_check(w, p)
+    _say("decisions", res["decisions"].tolist())
 
 
 def test_determinism_run_twice():

@@ -414,3 +414,9 @@ CONFIGS = {
 
 def make(name: str, **kw) -> Workload:
     return CONFIGS[name](**kw)
+
+
+def policy_draws(seed: int, n: int) -> np.ndarray:
+    """Uniform float32 draws in [0, 1), one per boundary request, for the
+    random capacity policy (the draw is an input to both implementations)."""
+    return np.random.default_rng(seed).random(n, dtype=np.float32)
