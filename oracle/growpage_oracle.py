@@ -67,7 +67,9 @@ class Params:
     Delta <= tau; ``shrink`` shrinks iff Delta < ``shrink_threshold`` = -0.005
     and the capacity after shrinking stays at least ``min_capacity_pages``
     pages (1024 tokens), grows iff Delta > tau, and compresses otherwise.
-    ``metric``: ``top_p`` (default) or ``entropy`` (signal ablation)."""
+    ``metric``: ``top_p`` (default) or ``entropy`` (signal ablation).
+    ``layout``: ``shift`` (default, the stable compaction) or ``fill`` (the
+    hole-filling variant of ``compact_tokens``)."""
     beta_s: float = 0.9
     beta_l: float = 0.999
     p: float = 0.99
@@ -82,6 +84,7 @@ class Params:
     shrink_threshold: float = -0.005
     min_capacity_pages: int = 64
     metric: str = "top_p"
+    layout: str = "shift"
 
     def as_f32(self, head_dim: int) -> "Params":
         """The same constants rounded to float32, the precision in which the
@@ -91,7 +94,7 @@ class Params:
         return Params(f(self.beta_s), f(self.beta_l), f(self.p), f(self.tau), int(self.k_loc),
                       f(self.rope_theta), int(self.reserve_pages), f(sc), self.policy,
                       int(self.fixed_pages), f(self.compress_prob), f(self.shrink_threshold),
-                      int(self.min_capacity_pages), self.metric)
+                      int(self.min_capacity_pages), self.metric, self.layout)
 
 
 # ----------------------------------------------------------------------------
@@ -542,16 +545,36 @@ def select_retained(s32: np.ndarray, P: int, b: int, k_loc: int, drop: int = 1) 
 # A9: compaction (Sec. 3.3; Sec. 4.2; App. E.2)
 # ----------------------------------------------------------------------------
 
-def compact_tokens(tokens: np.ndarray, kept: np.ndarray, P: int, b: int, drop: int = 1) -> np.ndarray:
+def compact_tokens(tokens: np.ndarray, kept: np.ndarray, P: int, b: int, drop: int = 1,
+                   layout: str = "shift") -> np.ndarray:
     """New logical contents of one KV head after Compress & Hold (drop = 1) or
-    a shrink (drop = 2): the kept historical tokens in their original order,
-    then the b protected tokens of the last page, filling slots
-    [0, (P - drop) b).  Later slots keep their old contents (they are free).
-    reading: the order is stable."""
+    a shrink (drop = 2); the survivors (kept historical tokens and the b
+    protected tokens of the last page) end up in slots [0, (P - drop) b).
+    Later slots keep their old contents (they are free).
+
+    layout "shift": the kept tokens in their original order, then the
+    protected page (reading: the order is stable).
+    layout "fill": the hole-filling variant (every survivor below
+    T = (P - drop) b stays where it is; the survivors at or above T, in slot
+    order, fill the evicted slots below T, in slot order), which moves O(b)
+    tokens instead of shifting the whole cache.  Attention over the resident
+    tokens does not depend on their order; later events see pages that mix
+    old and recent tokens."""
     out = tokens.copy()
-    K_t = (P - 1 - drop) * b
-    out[:K_t] = tokens[kept]
-    out[K_t:K_t + b] = tokens[(P - 1) * b: P * b]
+    if layout == "shift":
+        K_t = (P - 1 - drop) * b
+        out[:K_t] = tokens[kept]
+        out[K_t:K_t + b] = tokens[(P - 1) * b: P * b]
+        return out
+    if layout != "fill":
+        raise ValueError(f"unknown layout {layout!r}")
+    T = (P - drop) * b
+    survivors = set(int(x) for x in kept) | set(range((P - 1) * b, P * b))
+    holes = [slot for slot in range(T) if slot not in survivors]
+    movers = [slot for slot in range(T, P * b) if slot in survivors]
+    assert len(holes) == len(movers)
+    for dst, src in zip(holes, movers):
+        out[dst] = tokens[src]
     return out
 
 
@@ -613,7 +636,7 @@ def boundary_step(layers, dtype, state: PageState, q_pre, qstate, slot_ids, posi
                 for h in range(toks.shape[1]):
                     kept = select_retained(scores_all[i][ell][h], P, b, params.k_loc, drop)
                     kept_all[(i, ell, h)] = kept
-                    toks[:, h] = compact_tokens(toks[:, h], kept, P, b, drop)
+                    toks[:, h] = compact_tokens(toks[:, h], kept, P, b, drop, params.layout)
                 # write the resident pages back through the new table
                 for j in range(P - drop):
                     pool[int(new[j])] = toks[j * b:(j + 1) * b].transpose(1, 0, 2)
