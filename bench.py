@@ -24,6 +24,7 @@ the CPU oracle on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import math
 import os
@@ -243,6 +244,25 @@ def main():
     boundary_ms = float(np.mean([a.elapsed_time(c) for a, c in zip(marks["d1"], marks["b1"])]))
     inline_decode_ms = float(np.mean([a.elapsed_time(c) for a, c in zip(marks["d0"], marks["d1"])]))
 
+    # gp_boundary_apply alone with every boundary request compressing, in each
+    # compaction layout: the method's stable shift and the hole-filling variant
+    def apply_ms(layout):
+        p = dataclasses.replace(params, tau=math.inf, layout=layout)
+        ev = []
+        for _ in range(args.steps):
+            restore()
+            phase_score()
+            a0 = torch.cuda.Event(enable_timing=True)
+            a1 = torch.cuda.Event(enable_timing=True)
+            a0.record(stream)
+            gp.gp_boundary_apply([kv], ps, bnd, counts, scores, p, decisions, delta, counters, ws_a)
+            a1.record(stream)
+            ev.append((a0, a1))
+        torch.cuda.synchronize()
+        return float(np.mean([x.elapsed_time(y) for x, y in ev]))
+
+    apply_layout_ms = {"shift": apply_ms(gp.GP_LAYOUT_SHIFT), "fill": apply_ms(gp.GP_LAYOUT_FILL)}
+
     # algorithmic bytes
     m = w.seq_lens.astype(np.int64)
     decode_bytes = int(m.sum()) * Hkv * d * e * 2 + int(w.num_pages.sum()) * 4 + 2 * R * Hq * d * e
@@ -298,7 +318,8 @@ def main():
         "boundary": {"ms_after_decode": round(boundary_ms, 4),
                      "events_per_s": round(Rb / (step_ms * 1e-3), 1),
                      "overlapped_with_decode": not args.serial,
-                     "compress_grow_fallback_preempt": split},
+                     "compress_grow_fallback_preempt": split,
+                     "apply_ms_all_compress": {k_: round(v_, 4) for k_, v_ in apply_layout_ms.items()}},
         "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
         "cpu_baseline": cpu,

@@ -105,6 +105,18 @@ enum {
     GP_METRIC_ENTROPY = 1    /* exp(-sum a ln a) rounded to the nearest integer    */
 };
 
+/* Where compaction puts the survivors (Sec. 3.3).  SHIFT is the paper's
+ * stable compaction: kept tokens in slot order, then the protected page.
+ * FILL leaves every survivor below T (the resident length after the event)
+ * in place and moves the survivors at or above T, in slot order, into the
+ * evicted slots below T, in slot order: O(b) rows per KV head instead of the
+ * whole cache.  Attention does not depend on token order; later boundary
+ * events see pages that mix old and recent tokens. */
+enum {
+    GP_LAYOUT_SHIFT = 0,
+    GP_LAYOUT_FILL = 1
+};
+
 /* Which workspace gp_workspace_bytes() sizes. */
 enum { GP_OP_DECODE = 0, GP_OP_SCORE = 1, GP_OP_APPLY = 2 };
 
@@ -139,7 +151,8 @@ typedef struct {
  * zero is the method itself.  Appendix values: fixed_pages 256 (4096
  * tokens), compress_prob 0.7, shrink_threshold -0.005, min_capacity_pages 64
  * (1024 tokens).  draws: DEVICE [num_bnd] float32 uniform in [0, 1), one per
- * boundary request, read by GP_POLICY_RANDOM only (may be NULL otherwise). */
+ * boundary request, read by GP_POLICY_RANDOM only (may be NULL otherwise).
+ * layout: GP_LAYOUT_SHIFT (0, the method) or GP_LAYOUT_FILL. */
 typedef struct {
     float beta_s, beta_l;
     float p;
@@ -155,6 +168,7 @@ typedef struct {
     float compress_prob;
     float shrink_threshold;
     const float *draws;
+    int32_t layout;              /* GP_LAYOUT_*                                 */
 } gp_params_t;
 
 /* Dual-timescale summaries (Sec. 3.2, EMA equation; App. E.1).

@@ -23,6 +23,7 @@ GP_COMPRESS, GP_GROW, GP_FALLBACK, GP_PREEMPT, GP_NOT_BOUNDARY = 0, 1, 2, 3, 4
 GP_SHRINK = 5
 GP_POLICY_GROWPAGE, GP_POLICY_FIXED, GP_POLICY_RANDOM, GP_POLICY_INVERSE, GP_POLICY_SHRINK = 0, 1, 2, 3, 4
 GP_METRIC_TOP_P, GP_METRIC_ENTROPY = 0, 1
+GP_LAYOUT_SHIFT, GP_LAYOUT_FILL = 0, 1
 PAGE_SIZE = 16
 
 EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_step", "gp_boundary_score",
@@ -55,7 +56,7 @@ class _Params(ctypes.Structure):
                 ("k_loc", ctypes.c_int32), ("reserve_pages", ctypes.c_int32),
                 ("policy", ctypes.c_int32), ("metric", ctypes.c_int32), ("fixed_pages", ctypes.c_int32),
                 ("min_capacity_pages", ctypes.c_int32), ("compress_prob", ctypes.c_float),
-                ("shrink_threshold", ctypes.c_float), ("draws", ctypes.c_void_p)]
+                ("shrink_threshold", ctypes.c_float), ("draws", ctypes.c_void_p), ("layout", ctypes.c_int32)]
 
 
 _lib = None
@@ -168,6 +169,7 @@ class Params:
     compress_prob: float = 0.7
     shrink_threshold: float = -0.005
     draws: torch.Tensor | None = None   # [num_bnd] float32 on the device (RANDOM only)
+    layout: int = 0                 # GP_LAYOUT_*
 
     def c(self) -> _Params:
         if self.draws is not None and (self.draws.dtype != torch.float32 or not self.draws.is_contiguous()):
@@ -175,7 +177,7 @@ class Params:
         return _Params(self.beta_s, self.beta_l, self.p, self.tau, self.scale, self.rope_theta,
                        self.k_loc, self.reserve_pages, self.policy, self.metric, self.fixed_pages,
                        self.min_capacity_pages, self.compress_prob, self.shrink_threshold,
-                       _ptr(self.draws))
+                       _ptr(self.draws), self.layout)
 
 
 def gp_workspace_bytes(op: int, num_reqs: int, num_bnd: int, num_q_heads: int, num_kv_heads: int,

@@ -244,6 +244,7 @@ gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers, con
         (!params->draws || !(params->compress_prob >= 0.0f && params->compress_prob <= 1.0f)))
         return GP_ERR_INVALID;
     if (params->policy == GP_POLICY_SHRINK && !isfinite(params->shrink_threshold)) return GP_ERR_INVALID;
+    if (params->layout != GP_LAYOUT_SHIFT && params->layout != GP_LAYOUT_FILL) return GP_ERR_INVALID;
     if (num_bnd > 2048 || ps->max_pages > kMaxBoundaryPages) return GP_ERR_UNSUPPORTED;
     const gp_kv_layer_t &L0 = layers[0];
     const int E = elem_bytes(L0.dtype);
@@ -289,6 +290,7 @@ gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers, con
     a.compress_prob = params->compress_prob;
     a.shrink_threshold = params->shrink_threshold;
     a.draws = params->draws;
+    a.layout = params->layout;
     LayerPtrs lp[kMaxLayers];
     for (int l = 0; l < n_layers; ++l) {
         lp[l].k = layers[l].k;

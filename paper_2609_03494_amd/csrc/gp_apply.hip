@@ -19,9 +19,13 @@
 //           old references dropped (pages reaching zero are listed).
 //  compact  per (chunk of 256 slots, KV head x layer, request): reads every row
 //           that moves (the border rows from the saved copy), then writes it to
-//           its new slot; rows move down by at most page_size slots, so the only
-//           cross-chunk hazard is the one the border copy covers.  Workgroup 0
-//           also pushes the released pages back on the stack, lowest id first.
+//           its new slot; in the shift layout rows move down by at most two
+//           pages (a shrink), so the only cross-chunk hazard is the one the
+//           32-row border copy covers.  In the fill layout only the survivors at
+//           or above the new resident length move, into evicted slots below it,
+//           so no row is written that another chunk reads and chunks with no
+//           moving row leave at once.  Workgroup 0 also pushes the released
+//           pages back on the stack, lowest id first.
 //
 // Bound: compaction is HBM-bound: 2 (K, V) x 2 (read + write) x d x elem bytes
 // per moved row and KV head; everything else is latency-bound bookkeeping.
@@ -265,7 +269,8 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
         __syncthreads();
         if (tid == 0) a.nshc[(size_t)i * a.npc + cc] = s_n;
     }
-    if (!at_boundary || cc == 0 || cc >= cdiv(P * kPage, kCompactChunk)) return;
+    // the fill layout never overwrites a row that another chunk still reads
+    if (!at_boundary || cc == 0 || cc >= cdiv(P * kPage, kCompactChunk) || a.layout == GP_LAYOUT_FILL) return;
     // the kBorderRows rows below slot cc * kCompactChunk: the two pages before it
     constexpr int UPP = D * E / 16 * kPage;          // 16-byte units per page slice
     constexpr int NBP = kBorderRows / kPage;         // pages saved per boundary
@@ -519,21 +524,28 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
 
     const size_t page_bytes = (size_t)a.Hkv * kPage * D * E;
     const size_t head_bytes = (size_t)h * kPage * D * E;
-    const bool has_border = s0 + ROWS < total;
+    const bool fill = a.layout == GP_LAYOUT_FILL;
+    const bool has_border = !fill && s0 + ROWS < total;
+    const int T = total - nev;              // resident length after the event
+    int dst = -1;
     {
         const int s = s0 + tid;
-        int dst = -1;
         if (s < total) {
-            int before = 0;
+            int before = 0, between = 0;    // evicted below s; evicted in [T, s)
             bool gone = false;
 #pragma unroll
             for (int k = 0; k < kShrinkEvict; ++k) {
                 before += (s_ev[k] >= 0 && s_ev[k] < s) ? 1 : 0;
+                between += (s_ev[k] >= T && s_ev[k] < s) ? 1 : 0;
                 gone = gone || s_ev[k] == s;
             }
             if (!gone) {
-                const int d = s - before;
-                const int sp = src_row[s / kPage], dp = row[d / kPage];
+                // shift: down past the evicted slots below.  fill: rows below T
+                // stay; the k-th survivor at or above T takes the k-th evicted
+                // slot (the list is sorted, so the slots below T come first).
+                const int rank = s - T - between;
+                const int d = !fill ? s - before : (s < T ? s : s_ev[min(max(rank, 0), kShrinkEvict - 1)]);
+                const int sp = src_row[s / kPage], dp = d >= 0 ? row[d / kPage] : -1;
                 const bool ok = sp >= 0 && sp < a.pool_pages && dp >= 0 && dp < a.pool_pages;
                 const long long so = (long long)sp * page_bytes + head_bytes + (long long)(s % kPage) * D * E;
                 const long long dof = (long long)dp * page_bytes + head_bytes + (long long)(d % kPage) * D * E;
@@ -546,7 +558,7 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
         }
         s_dst[tid] = dst;
     }
-    __syncthreads();
+    if (!__syncthreads_or(dst >= 0)) return;   // nothing moves in this chunk
 
     const unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc) * 2 * kBorderRows * D * E;
     unsigned char *pools[2] = {reinterpret_cast<unsigned char *>(lt.k[l]),

@@ -197,6 +197,7 @@ struct ApplyArgs {
     float compress_prob;
     double shrink_threshold;
     const float *draws;
+    int layout;       // GP_LAYOUT_*
 };
 
 struct LayerPtrs {

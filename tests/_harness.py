@@ -54,6 +54,7 @@ POLICY_CODES = {"growpage": gp.GP_POLICY_GROWPAGE, "fixed": gp.GP_POLICY_FIXED,
                 "random": gp.GP_POLICY_RANDOM, "inverse": gp.GP_POLICY_INVERSE,
                 "shrink": gp.GP_POLICY_SHRINK}
 METRIC_CODES = {"top_p": gp.GP_METRIC_TOP_P, "entropy": gp.GP_METRIC_ENTROPY}
+LAYOUT_CODES = {"shift": gp.GP_LAYOUT_SHIFT, "fill": gp.GP_LAYOUT_FILL}
 
 
 def library_params(params: O.Params, head_dim: int, draws=None) -> "gp.Params":
@@ -63,7 +64,8 @@ def library_params(params: O.Params, head_dim: int, draws=None) -> "gp.Params":
     d = None if draws is None else torch.from_numpy(np.asarray(draws, np.float32)).to(DEV)
     return gp.Params(p32.beta_s, p32.beta_l, p32.p, p32.tau, p32.scale, p32.rope_theta, p32.k_loc,
                      p32.reserve_pages, POLICY_CODES[p32.policy], METRIC_CODES[p32.metric],
-                     p32.fixed_pages, p32.min_capacity_pages, p32.compress_prob, p32.shrink_threshold, d)
+                     p32.fixed_pages, p32.min_capacity_pages, p32.compress_prob, p32.shrink_threshold, d,
+                     LAYOUT_CODES[p32.layout])
 
 
 class DeviceCase:

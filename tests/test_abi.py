@@ -86,9 +86,10 @@ def test_host_validation_without_launch(lib):
     assert lib.gp_boundary_score(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 512, fake, fake, fake,
                                  2, 32, ctypes.byref(pm), fake, fake, 144, fake, 1 << 30, None) == 1
     # apply: unknown policy, random policy without draws or with a probability
-    # outside [0, 1], shrink with a non-finite threshold
+    # outside [0, 1], shrink with a non-finite threshold, unknown layout
     for fields in ((9, 0, 0, 0, 0.7, -0.005, None), (2, 0, 0, 0, 0.7, -0.005, None),
-                   (2, 0, 0, 0, 1.5, -0.005, fake), (4, 0, 0, 64, 0.7, float("nan"), None)):
+                   (2, 0, 0, 0, 1.5, -0.005, fake), (4, 0, 0, 64, 0.7, float("nan"), None),
+                   (0, 0, 0, 0, 0.7, -0.005, None, 2)):
         pa = _lib._Params(0.9, 0.999, 0.99, 0.0, 0.088, 1e6, 4, 0, *fields)
         assert lib.gp_boundary_apply(arr, 1, ctypes.byref(ps), fake, 2, fake, fake, 144, ctypes.byref(pa),
                                      fake, fake, fake, fake, 1 << 30, None) == 1, fields

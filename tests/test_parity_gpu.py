@@ -154,10 +154,15 @@ def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=N
                 idx = row_index(before[:, h], have[:, h])
                 assert (idx >= 0).all(), f"compaction wrote rows that were never there (req {r})"
                 K_t = (P - 1 - drop) * b
-                assert (np.diff(idx[:K_t]) > 0).all() and (idx[K_t:] == np.arange((P - 1) * b, P * b)).all()
+                protected = np.arange((P - 1) * b, P * b)
+                kept_g = np.setdiff1d(idx, protected)
+                assert kept_g.size == K_t and np.isin(protected, idx).all()
+                # the rows are exactly the layout of the GPU's own kept set
+                lay = O.compact_tokens(np.arange(P * b), kept_g, P, b, drop, p32.layout)[:n]
+                assert np.array_equal(idx, lay), f"layout of the kept rows (req {r}, head {h})"
                 kept_o = ref["kept"][(i, 0, h)]
                 band = threshold_band(ref["scores"][i][0][h], kept_o, P, b, p32.k_loc)
-                diff = set(idx[:K_t].tolist()) ^ set(kept_o.tolist())
+                diff = set(kept_g.tolist()) ^ set(kept_o.tolist())
                 assert diff <= band, f"retained sets differ outside the threshold band (req {r}, head {h})"
                 excused += 1
     return dict(ref=ref, got=got, excused=excused, decisions=dec_o)
@@ -424,6 +429,32 @@ def test_boundary_entropy_metric(case):
     _say(f"boundary: entropy metric, {case}")
     res = _boundary_check(w, p)
     _say("decisions", res["decisions"].tolist())
+
+
+@pytest.mark.parametrize("case", ["qwen3_compress", "qwen3_shrink", "prefix_compress", "prefix_shrink",
+                                  "tiny", "long"])
+def test_boundary_fill_layout(case):
+    """The hole-filling compaction layout against the oracle's: compress and
+    shrink, with and without shared prefix pages."""
+    shrink = dict(policy="shrink", shrink_threshold=10.0, min_capacity_pages=2)
+    if case == "tiny":
+        _say("boundary: fill layout, tiny fp32")
+        w, dc, st = _tiny_prepared()
+        _boundary_check(w, O.Params(tau=math.inf, layout="fill"), qstate_host=st, dc=dc)
+        return
+    if case.startswith("qwen3"):
+        w = W.qwen3_8b(seed=7, num_reqs=12, len_lo=300, len_hi=4000, budget_choices=(8, 60, 200),
+                       boundary_frac=0.5, free_pages=30)
+    elif case == "long":
+        w = W.long_reasoning(num_reqs=8, len_lo=1500, len_hi=4200, free_pages=40)
+    else:
+        w = W.prefix_shared(num_reqs=8, prefix_len=320, tail_lo=40, tail_hi=1200, boundary_frac=0.5,
+                            free_pages=200)
+    kw = shrink if case.endswith("shrink") else {}
+    _say(f"boundary: fill layout, {case}")
+    res = _boundary_check(w, O.Params(tau=math.inf, layout="fill", **kw))
+    want = O.SHRINK if case.endswith("shrink") else O.COMPRESS
+    assert (res["decisions"] == want).all()
 
 
 def test_determinism_run_twice():
