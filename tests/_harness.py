@@ -71,12 +71,16 @@ def library_params(params: O.Params, head_dim: int, draws=None) -> "gp.Params":
 class DeviceCase:
     """One workload resident on the GPU, with the library's workspaces."""
 
-    def __init__(self, w: W.Workload, poison_free_pages: bool = True, n_layers: int = 1):
+    def __init__(self, w: W.Workload, poison_free_pages: bool = True, n_layers: int = 1,
+                 distinct_layers: bool = False):
+        """n_layers K/V pools; with distinct_layers layer l holds the contents of
+        W.layer_variant(w, l) (otherwise every layer a copy of w's)."""
         self.w = w
         dt = torch_dtype(w)
         shape = (w.pool_pages, w.num_kv_heads, w.page_size, w.head_dim)
         self.layers = []
-        for _ in range(n_layers):
+        self.layer_workloads = [W.layer_variant(w, l) if distinct_layers else w for l in range(n_layers)]
+        for wl in self.layer_workloads:
             k = torch.empty(shape, dtype=dt, device=DEV)
             v = torch.empty(shape, dtype=dt, device=DEV)
             if poison_free_pages:
@@ -85,8 +89,8 @@ class DeviceCase:
             ids = np.nonzero(w.page_row >= 0)[0]
             idx = torch.from_numpy(ids.astype(np.int64)).to(DEV)
             rows = w.page_row[ids]
-            k.index_copy_(0, idx, to_torch(w.k_data[rows], w.dtype))
-            v.index_copy_(0, idx, to_torch(w.v_data[rows], w.dtype))
+            k.index_copy_(0, idx, to_torch(wl.k_data[rows], w.dtype))
+            v.index_copy_(0, idx, to_torch(wl.v_data[rows], w.dtype))
             self.layers.append(gp.KVLayer(k, v))
         i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(DEV)
         self.ps = gp.PageState(i32(w.page_table), i32(w.num_pages), i32(w.seq_lens),
@@ -97,6 +101,10 @@ class DeviceCase:
         self.q_pre = to_torch(w.q_pre, w.dtype)
         self.q_post = to_torch(w.q_post, w.dtype)
         self.n_layers = n_layers
+        # per-layer queries and summary pools (layer 0: the ones above)
+        self.q_pre_layers = [self.q_pre] + [to_torch(wl.q_pre, w.dtype) for wl in self.layer_workloads[1:]]
+        self.qstate_layers = [self.qstate] + [torch.from_numpy(wl.qstate.copy()).to(DEV)
+                                              for wl in self.layer_workloads[1:]]
         R, Hq, Hkv, d, maxp = w.num_reqs, w.num_q_heads, w.num_kv_heads, w.head_dim, w.max_pages
         self.ws_decode = gp.workspace(gp.GP_OP_DECODE, R, 0, Hq, Hkv, d, maxp, dt)
 
@@ -130,8 +138,8 @@ class DeviceCase:
         ws_a = gp.workspace(gp.GP_OP_APPLY, w.num_reqs, Rb, w.num_q_heads, w.num_kv_heads,
                             w.head_dim, w.max_pages, dt, n_layers=L)
         for ell in range(L):
-            qp = self.q_pre if q_pre_layers is None else q_pre_layers[ell]
-            qs = self.qstate if qstate_layers is None else qstate_layers[ell]
+            qp = self.q_pre_layers[ell] if q_pre_layers is None else q_pre_layers[ell]
+            qs = self.qstate_layers[ell] if qstate_layers is None else qstate_layers[ell]
             gp.gp_boundary_score(self.layers[ell], self.ps, qp, qs, self.slot_ids, self.positions,
                                  bnd_t, gparams, k_counts[ell], scores[ell], ws_s)
         decisions = torch.full((Rb,), -1, dtype=torch.int32, device=DEV)

@@ -81,42 +81,50 @@ def _fragile(a32, p32):
     return O.top_p_fragile(a32, p32.p, 1e-6)
 
 
-def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=None, draws=None):
-    """Run one boundary event on both sides and compare everything."""
+def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=None, draws=None,
+                    n_layers=1):
+    """Run one boundary event on both sides and compare everything.  With
+    n_layers > 1 every layer holds its own contents (W.layer_variant) and the
+    decision aggregates over all of them."""
     bnd = w.boundary if bnd is None else np.asarray(bnd, np.int32)
     p32 = params.as_f32(w.head_dim)
-    qs = w.qstate if qstate_host is None else qstate_host
-    dc = DeviceCase(w) if dc is None else dc
+    dc = DeviceCase(w, n_layers=n_layers, distinct_layers=True) if dc is None else dc
+    L = dc.n_layers
+    wls = dc.layer_workloads
     st = oracle_state(w)
     if free_count is not None:
         st.free_count = free_count
         dc.ps.free_count.fill_(free_count)
-    kp, vp = w.dense_pool("k"), w.dense_pool("v")
-    kp0, vp0 = kp.copy(), vp.copy()
+    pools = [(wl.dense_pool("k"), wl.dense_pool("v")) for wl in wls]
+    pools0 = [(k.copy(), v.copy()) for k, v in pools]
     before_state = st.copy()
-    ref = O.boundary_step([(kp, vp)], w.dtype, st, w.q_pre, qs, w.slot_ids, w.positions, bnd, p32,
+    q_layers = [wl.q_pre for wl in wls]
+    s_layers = [wl.qstate for wl in wls]
+    if qstate_host is not None:
+        s_layers[0] = qstate_host
+    ref = O.boundary_step(pools, w.dtype, st, q_layers, s_layers, w.slot_ids, w.positions, bnd, p32,
                           draws=draws)
     got = dc.boundary(params, bnd=bnd, draws=draws)
     b = w.page_size
-    # working-set sizes and scores
+    # working-set sizes and scores, per layer
     fragile = set()
     for i, r in enumerate(bnd):
         P = int(before_state.num_pages[r])
-        for h in range(w.num_kv_heads):
-            for x in range(2):
-                g, o = int(got["k_counts"][0, i, h, x]), int(ref["counts"][i][0, h, x])
-                a32 = ref["weights"][i][0][x, h]
-                if a32.size and _fragile(a32, p32):
-                    fragile.add(i)
-                    assert abs(g - o) <= 1, (i, h, x, g, o)
-                else:
-                    assert g == o, f"K^{'SL'[x]} of boundary {i} head {h}: gpu {g} oracle {o}"
-            C = (P - 1) * b if int(before_state.seq_lens[r]) == P * b and P >= 2 else 0
-            if C:
-                s_g = got["scores"][0, i, h, :C]
-                s_o = ref["scores"][i][0][h]
-                np.testing.assert_allclose(s_g, s_o, rtol=1e-5, atol=0,
-                                           err_msg=f"scores boundary {i} head {h}")
+        C = (P - 1) * b if int(before_state.seq_lens[r]) == P * b and P >= 2 else 0
+        for ell in range(L):
+            for h in range(w.num_kv_heads):
+                for x in range(2):
+                    g, o = int(got["k_counts"][ell, i, h, x]), int(ref["counts"][i][ell, h, x])
+                    a32 = ref["weights"][i][ell][x, h]
+                    if a32.size and _fragile(a32, p32):
+                        fragile.add(i)
+                        assert abs(g - o) <= 1, (i, ell, h, x, g, o)
+                    else:
+                        assert g == o, f"K^{'SL'[x]} of boundary {i} layer {ell} head {h}: gpu {g} oracle {o}"
+                if C:
+                    np.testing.assert_allclose(got["scores"][ell, i, h, :C], ref["scores"][i][ell][h],
+                                               rtol=1e-5, atol=0,
+                                               err_msg=f"scores boundary {i} layer {ell} head {h}")
     # decisions
     dec_g, dec_o = got["decisions"], ref["decisions"]
     for i in range(len(bnd)):
@@ -134,7 +142,7 @@ def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=N
     np.testing.assert_array_equal(gs.refcount, st.refcount)
     assert gs.free_count == st.free_count
     np.testing.assert_array_equal(gs.free_list[: gs.free_count], st.free_list[: st.free_count])
-    # compacted K/V
+    # compacted K/V of every layer
     excused = 0
     for i, r in enumerate(bnd):
         if dec_o[i] not in (O.COMPRESS, O.FALLBACK, O.SHRINK):
@@ -142,29 +150,31 @@ def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=N
         P = int(before_state.num_pages[r])
         drop = 2 if dec_o[i] == O.SHRINK else 1
         n = (P - drop) * b
-        for which, pool, pool0 in (("k", kp, kp0), ("v", vp, vp0)):
-            want = O.gather_tokens(pool, st.page_table[r], n, b)
-            have = dc.gather(gs.page_table[r], n, which)
-            if np.array_equal(want, have):
-                continue
-            before = O.gather_tokens(pool0, before_state.page_table[r], P * b, b)
-            for h in range(w.num_kv_heads):
-                if np.array_equal(want[:, h], have[:, h]):
+        for ell in range(L):
+            for x, which in enumerate(("k", "v")):
+                pool, pool0 = pools[ell][x], pools0[ell][x]
+                want = O.gather_tokens(pool, st.page_table[r], n, b)
+                have = dc.gather(gs.page_table[r], n, which, layer=ell)
+                if np.array_equal(want, have):
                     continue
-                idx = row_index(before[:, h], have[:, h])
-                assert (idx >= 0).all(), f"compaction wrote rows that were never there (req {r})"
-                K_t = (P - 1 - drop) * b
-                protected = np.arange((P - 1) * b, P * b)
-                kept_g = np.setdiff1d(idx, protected)
-                assert kept_g.size == K_t and np.isin(protected, idx).all()
-                # the rows are exactly the layout of the GPU's own kept set
-                lay = O.compact_tokens(np.arange(P * b), kept_g, P, b, drop, p32.layout)[:n]
-                assert np.array_equal(idx, lay), f"layout of the kept rows (req {r}, head {h})"
-                kept_o = ref["kept"][(i, 0, h)]
-                band = threshold_band(ref["scores"][i][0][h], kept_o, P, b, p32.k_loc)
-                diff = set(kept_g.tolist()) ^ set(kept_o.tolist())
-                assert diff <= band, f"retained sets differ outside the threshold band (req {r}, head {h})"
-                excused += 1
+                before = O.gather_tokens(pool0, before_state.page_table[r], P * b, b)
+                for h in range(w.num_kv_heads):
+                    if np.array_equal(want[:, h], have[:, h]):
+                        continue
+                    idx = row_index(before[:, h], have[:, h])
+                    assert (idx >= 0).all(), f"compaction wrote rows that were never there (req {r})"
+                    K_t = (P - 1 - drop) * b
+                    protected = np.arange((P - 1) * b, P * b)
+                    kept_g = np.setdiff1d(idx, protected)
+                    assert kept_g.size == K_t and np.isin(protected, idx).all()
+                    # the rows are exactly the layout of the GPU's own kept set
+                    lay = O.compact_tokens(np.arange(P * b), kept_g, P, b, drop, p32.layout)[:n]
+                    assert np.array_equal(idx, lay), f"layout of the kept rows (req {r}, head {h})"
+                    kept_o = ref["kept"][(i, ell, h)]
+                    band = threshold_band(ref["scores"][i][ell][h], kept_o, P, b, p32.k_loc)
+                    diff = set(kept_g.tolist()) ^ set(kept_o.tolist())
+                    assert diff <= band, f"retained sets differ outside the threshold band (req {r}, head {h})"
+                    excused += 1
     return dict(ref=ref, got=got, excused=excused, decisions=dec_o)
 
 
@@ -455,6 +465,39 @@ def test_boundary_fill_layout(case):
     res = _boundary_check(w, O.Params(tau=math.inf, layout="fill", **kw))
     want = O.SHRINK if case.endswith("shrink") else O.COMPRESS
     assert (res["decisions"] == want).all()
+
+
+# --------------------------------------------- decisions over many layers --
+
+@pytest.mark.parametrize("case", ["tau0", "compress", "shrink", "fill"])
+def test_boundary_three_layers(case):
+    """One decision per request from the counts of three layers with their own
+    contents (Sec. 3.2, aggregation over layers and KV heads), then selection
+    and compaction of every layer in the same call."""
+    w = W.qwen3_8b(seed=7, num_reqs=12, len_lo=300, len_hi=4000, budget_choices=(8, 60, 200),
+                   boundary_frac=0.5, free_pages=30)
+    p = {"tau0": O.Params(), "compress": O.Params(tau=math.inf),
+         "shrink": O.Params(policy="shrink", min_capacity_pages=4, shrink_threshold=0.001),
+         "fill": O.Params(tau=math.inf, layout="fill")}[case]
+    _say(f"boundary: three layers, Qwen3-8B heads, 12 requests, {case}")
+    res = _boundary_check(w, p, n_layers=3)
+    _say("decisions", res["decisions"].tolist(), "delta", res["ref"]["delta"].tolist())
+
+
+def test_boundary_36_layers_small():
+    """Every layer of a Qwen3-8B-deep model (36) on a small fp32 batch."""
+    w = W._build(name="deep", seed=41, dtype="f32", Hq=4, Hkv=2, d=64,
+                 n=np.array([96, 160, 100, 48]), budgets=None, free_pages=6, heavy_mode="scaled",
+                 heavy_frac=0.05, summary_mode="random")
+    for tau in (0.0, math.inf):
+        _say(f"boundary: 36 layers, small fp32 batch, tau {tau}")
+        _boundary_check(w, O.Params(tau=tau), n_layers=36)
+
+
+def test_boundary_two_layers_long_reasoning():
+    w = W.long_reasoning(num_reqs=6, len_lo=1500, len_hi=3000, free_pages=40)
+    _say("boundary: two layers, long-reasoning shape reduced")
+    _boundary_check(w, O.Params(), n_layers=2)
 
 
 def test_determinism_run_twice():

@@ -28,6 +28,7 @@ shows up in the results.
 """
 from __future__ import annotations
 
+import dataclasses
 import os
 from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
@@ -420,3 +421,27 @@ def policy_draws(seed: int, n: int) -> np.ndarray:
     """Uniform float32 draws in [0, 1), one per boundary request, for the
     random capacity policy (the draw is an input to both implementations)."""
     return np.random.default_rng(seed).random(n, dtype=np.float32)
+
+
+def layer_variant(w: Workload, layer: int) -> Workload:
+    """The same batch seen at another attention layer: the page tables, lengths,
+    positions and summary slots are shared by every layer, the contents differ.
+    Layer 0 is ``w`` itself; layer l > 0 mixes each value of layer 0 with a
+    fresh seeded N(0, 1) draw, 0.6 x + 0.8 z (unit variance, heavy keys stay
+    somewhat heavy).  Empty slots and unowned summary slots stay NaN."""
+    if layer == 0:
+        return w
+    rng = np.random.default_rng([int(w.meta.get("seed", 0)), 7919, layer])
+
+    def mix(a, storage):
+        x = a.astype(np.float32) if storage == "f32" else \
+            (a.astype(np.uint32) << np.uint32(16)).view(np.float32)
+        z = rng.standard_normal(x.shape, dtype=np.float32)
+        y = (np.float32(0.6) * x + np.float32(0.8) * z).astype(np.float32)
+        return y if storage == "f32" else _to_bf16_bits(y)
+
+    st = w.dtype
+    return dataclasses.replace(
+        w, k_data=mix(w.k_data, st), v_data=mix(w.v_data, st), q_pre=mix(w.q_pre, st),
+        q_post=mix(w.q_post, st), qstate=mix(w.qstate, "f32"), q_priors=None,
+        meta=dict(w.meta, layer=layer))
