@@ -40,6 +40,7 @@ __all__ = [
     "demand_trend", "decide_and_allocate",
     "local_quota", "select_retained", "compact_tokens",
     "PageState", "boundary_step",
+    "append_token", "serve_step",
 ]
 
 # decision codes
@@ -648,3 +649,72 @@ def boundary_step(layers, dtype, state: PageState, q_pre, qstate, slot_ids, posi
             counters[code] += 1
     return dict(decisions=dec, delta=delta, counts=counts_all, scores=scores_all,
                 weights=weights_all, kept=kept_all, counters=counters)
+
+
+# ----------------------------------------------------------------------------
+# A decode loop: one token per request and step, boundary events as they come,
+# compaction asynchronous to the next step (App. E.3)
+# ----------------------------------------------------------------------------
+
+def append_token(pools, state: PageState, r: int, kv_new, b: int = 16) -> bool:
+    """Write the current token's K and V ([Hkv, d] each, per layer) of request
+    r at slot m_r of its paged cache and count it resident.  A request whose
+    pages are full (m_r = P_r b) cannot take a token: it is at a capacity
+    boundary and waits for a decision (Sec. 3.3).  Returns whether it
+    appended."""
+    m, P = int(state.seq_lens[r]), int(state.num_pages[r])
+    if m >= P * b:
+        return False
+    pid = int(state.page_table[r, m // b])
+    for (kp, vp), (k_new, v_new) in zip(pools, kv_new):
+        kp[pid, :, m % b] = k_new
+        vp[pid, :, m % b] = v_new
+    state.seq_lens[r] = m + 1
+    return True
+
+
+def serve_step(pools, dtype, state: PageState, held, qstate, slot_ids, positions, inputs,
+               params: Params, b: int = 16):
+    """One decode step of a batch with asynchronous compaction (App. E.3).
+
+    ``held``: requests whose compaction from the previous step is still
+    running; they sit this step out (no token, no summary update, no output)
+    and rejoin the next one.  Every other request appends its token if it has
+    room, updates its summaries (Sec. 3.2; only requests that took a token),
+    and decodes over its resident tokens (Sec. 3.1).  Requests whose pages are
+    now full take the boundary event (``boundary_step``, in request order);
+    those that compress or shrink are held for the next step.
+
+    ``inputs``: dict with k_new, v_new ([R, Hkv, d] per layer, lists) and
+    q_pre, q_post ([R, Hq, d]).  ``positions`` (logical index of each
+    request's current token) advances with every appended token.
+    reading: a request that could not take a token (preempted at its boundary)
+    still decodes over its full cache and meets its boundary again.
+    Returns (out [R, Hq, d] fp64 with NaN rows for held requests, new qstate,
+    new held set, boundary_step result, appended list)."""
+    R = state.page_table.shape[0]
+    held = set(int(r) for r in held)
+    active = [r for r in range(R) if r not in held]
+    appended = []
+    for r in active:
+        kv_r = [(k[r], v[r]) for k, v in zip(inputs["k_new"], inputs["v_new"])]
+        if append_token(pools, state, r, kv_r, b):
+            positions[r] += 1
+            appended.append(r)
+    qs = np.array(qstate, dtype=np.float32, copy=True)
+    if appended:
+        idx = np.array(appended)
+        upd = update_summaries(inputs["q_pre"][idx], dtype, slot_ids[idx],
+                               np.zeros(idx.size, np.uint8), qs, params.beta_s, params.beta_l)
+        qs = upd
+    d = pools[0][0].shape[-1]
+    scale = params.scale if params.scale is not None else 1.0 / np.sqrt(d)
+    Hq = inputs["q_post"].shape[1]
+    out = decode_attention(pools[0][0], pools[0][1], dtype, state.page_table, state.seq_lens,
+                           inputs["q_post"], Hq, scale, b, requests=active)
+    bnd = np.array([r for r in active if int(state.seq_lens[r]) == int(state.num_pages[r]) * b],
+                   dtype=np.int32)
+    res = boundary_step(pools, dtype, state, inputs["q_pre"], qs, slot_ids, positions, bnd, params, b)
+    new_held = {int(bnd[i]) for i, dec in enumerate(res["decisions"])
+                if dec in (COMPRESS, FALLBACK, SHRINK)}
+    return out, qs, new_held, res, appended

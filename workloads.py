@@ -445,3 +445,23 @@ def layer_variant(w: Workload, layer: int) -> Workload:
         w, k_data=mix(w.k_data, st), v_data=mix(w.v_data, st), q_pre=mix(w.q_pre, st),
         q_post=mix(w.q_post, st), qstate=mix(w.qstate, "f32"), q_priors=None,
         meta=dict(w.meta, layer=layer))
+
+
+def step_inputs(w: Workload, n_steps: int, seed: int = 0, n_layers: int = 1) -> list:
+    """Per decode step, the new token of every request: its keys and values
+    ([R, Hkv, d] per layer), pre- and post-RoPE queries ([R, Hq, d]), all
+    seeded N(0, 1) in the workload's storage type.  The loop's synthetic
+    continuation of the batch."""
+    rng = np.random.default_rng([int(w.meta.get("seed", 0)), 104729, seed])
+    R, Hq, Hkv, d = w.num_reqs, w.num_q_heads, w.num_kv_heads, w.head_dim
+
+    def draw(shape):
+        x = rng.standard_normal(shape, dtype=np.float32)
+        return x if w.dtype == "f32" else _to_bf16_bits(x)
+
+    out = []
+    for _ in range(n_steps):
+        out.append(dict(k_new=[draw((R, Hkv, d)) for _ in range(n_layers)],
+                        v_new=[draw((R, Hkv, d)) for _ in range(n_layers)],
+                        q_pre=draw((R, Hq, d)), q_post=draw((R, Hq, d))))
+    return out
