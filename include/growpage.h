@@ -44,6 +44,14 @@
  *  num_pages, seq_lens  [num_reqs] int32: pages held P_r and resident tokens
  *                    m_r (m_r <= P_r * page_size).  A request is at a capacity
  *                    boundary when m_r == P_r * page_size (Sec. 3.3).
+ *                    seq_lens[r] < 0 marks a HELD request (App. E.3: its
+ *                    compaction is still running): it stands for
+ *                    m_r = -seq_lens[r] - 1, and the request is out of the
+ *                    step's batch -- decode attention writes no output for
+ *                    it, the step prologue gives it no token, and the boundary
+ *                    calls treat it as not at a boundary.  Only
+ *                    gp_boundary_decide(hold = 1) creates held requests and
+ *                    gp_release_held() ends them.
  *  refcount          [pool_pages] int32 references from page tables (pages
  *                    shared by a common prefix have refcount > 1, App. E.2).
  *  free_list, free_count  stack of free page ids; the top is
@@ -189,7 +197,8 @@ gp_status_t gp_update_summaries(const void *q_pre, gp_dtype_t dtype, int32_t num
  * out[r][g] = sum_{i < m_r} softmax_i(scale * q_post[r][g] . k_i) v_i, with
  * k_i, v_i read from KV head g / (num_q_heads / num_kv_heads) through the page
  * table.  fp32 accumulation; output in the KV dtype.  A request with m_r == 0
- * gets a zero output.  Page slots at or beyond m_r are never used, whatever
+ * gets a zero output; a held request (seq_lens[r] < 0) gets none (its rows of
+ * out are not written, and gp_decode_step leaves its summaries alone).  Page slots at or beyond m_r are never used, whatever
  * they hold.  out: [num_reqs][num_q_heads][head_dim]. */
 gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
                                 const void *q_post, int32_t num_q_heads, float scale,
@@ -272,6 +281,66 @@ gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers,
                               const int32_t *k_counts, const float *scores, int32_t max_cand,
                               const gp_params_t *params, int32_t *decisions, float *delta,
                               int64_t *counters, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* gp_boundary_apply in three stream-ordered parts, for overlap with decoding
+ * (App. E.3, asynchronous decoding and compression).  Each takes exactly the
+ * arguments of gp_boundary_apply, and the three calls of one event must get
+ * the same arguments and the same workspace, in this order:
+ *  - select:  the eviction lists of every boundary request (selection needs
+ *             only the scores) and the rows compaction will read.  Reads the
+ *             page state, K/V and scores; writes only the workspace, so it may
+ *             run beside decode attention.
+ *  - decide:  decisions, delta, counters, page allocation and table updates.
+ *             With hold != 0 a request that compresses or shrinks is left HELD
+ *             (seq_lens[r] = -(new m) - 1) so that a decode step launched while
+ *             its compaction runs leaves it out; otherwise as in apply.
+ *  - compact: moves the rows and returns released pages to the stack.  Reads
+ *             and writes only the pages of requests that compress or shrink,
+ *             so it may run beside the next step's decode of the others.
+ * gp_boundary_apply == select, decide (hold 0), compact on one stream.  The
+ * workspace holds the event until compact has completed: an event that
+ * overlaps the previous one's compaction needs a second workspace. */
+gp_status_t gp_boundary_select(const gp_kv_layer_t *layers, int32_t n_layers,
+                               const gp_page_state_t *ps, const int32_t *bnd, int32_t num_bnd,
+                               const int32_t *k_counts, const float *scores, int32_t max_cand,
+                               const gp_params_t *params, int32_t *decisions, float *delta,
+                               int64_t *counters, void *ws, size_t ws_bytes, hipStream_t stream);
+gp_status_t gp_boundary_decide(const gp_kv_layer_t *layers, int32_t n_layers,
+                               const gp_page_state_t *ps, const int32_t *bnd, int32_t num_bnd,
+                               const int32_t *k_counts, const float *scores, int32_t max_cand,
+                               const gp_params_t *params, int32_t *decisions, float *delta,
+                               int64_t *counters, void *ws, size_t ws_bytes, hipStream_t stream,
+                               int32_t hold);
+gp_status_t gp_boundary_compact(const gp_kv_layer_t *layers, int32_t n_layers,
+                                const gp_page_state_t *ps, const int32_t *bnd, int32_t num_bnd,
+                                const int32_t *k_counts, const float *scores, int32_t max_cand,
+                                const gp_params_t *params, int32_t *decisions, float *delta,
+                                int64_t *counters, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Ends every hold: seq_lens[r] < 0 becomes -seq_lens[r] - 1 (App. E.3: a
+ * compressed request rejoins the batch once its compaction has completed;
+ * the caller orders this call after that compaction). */
+gp_status_t gp_release_held(const gp_page_state_t *ps, hipStream_t stream);
+
+/* Step prologue of the decode loop (Sec. 3.1 paged cache; Sec. 3.2 EMA;
+ * App. E.1 query-state pool): for every request r that is not held and has
+ * room (0 <= m_r < P_r * page_size), over all n_layers layers,
+ *  - the token's keys and values k_new[l][r], v_new[l][r] ([Hkv][head_dim],
+ *    post-RoPE, the KV dtype) are written at slot m_r of the paged cache;
+ *  - the summaries of slot slot_ids[r] in layer l's pool take one EMA step
+ *    with q_pre[l][r] (or are set to it if init[r] != 0), exactly as
+ *    gp_update_summaries does;
+ * then m_r and positions[r] advance by one.  Requests with full pages (at a
+ * boundary, awaiting a decision) and held requests are left untouched.
+ * k_new, v_new [n_layers][num_reqs][Hkv][head_dim]; q_pre
+ * [n_layers][num_reqs][num_q_heads][head_dim]; qstate
+ * [n_layers][num_slots][2][num_q_heads][head_dim] (the paper's per-layer
+ * pool); init may be NULL (no new slots).  Slots must be distinct. */
+gp_status_t gp_append_step(const gp_kv_layer_t *layers, int32_t n_layers, const gp_page_state_t *ps,
+                           int32_t *positions, const void *k_new, const void *v_new, const void *q_pre,
+                           int32_t num_q_heads, const int32_t *slot_ids, const uint8_t *init,
+                           float *qstate, int32_t num_slots, float beta_s, float beta_l,
+                           hipStream_t stream);
 
 /* Bytes of workspace an operation needs (op = GP_OP_DECODE / SCORE / APPLY). */
 size_t gp_workspace_bytes(int32_t op, int32_t num_reqs, int32_t num_bnd, int32_t num_q_heads,

@@ -27,7 +27,8 @@ GP_LAYOUT_SHIFT, GP_LAYOUT_FILL = 0, 1
 PAGE_SIZE = 16
 
 EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_step", "gp_boundary_score",
-           "gp_boundary_apply", "gp_workspace_bytes", "gp_status_string")
+           "gp_boundary_apply", "gp_boundary_select", "gp_boundary_decide", "gp_boundary_compact",
+           "gp_release_held", "gp_append_step", "gp_workspace_bytes", "gp_status_string")
 
 
 class GrowPageError(RuntimeError):
@@ -88,8 +89,18 @@ def load() -> ctypes.CDLL:
                                       vp, vp, vp, i32, i32, ctypes.POINTER(_Params), vp, vp, i32, vp,
                                       sz, vp]
     lib.gp_boundary_apply.restype = ctypes.c_int
-    lib.gp_boundary_apply.argtypes = [ctypes.POINTER(_KVLayer), i32, ctypes.POINTER(_PageState), vp, i32,
-                                      vp, vp, i32, ctypes.POINTER(_Params), vp, vp, vp, vp, sz, vp]
+    apply_args = [ctypes.POINTER(_KVLayer), i32, ctypes.POINTER(_PageState), vp, i32,
+                  vp, vp, i32, ctypes.POINTER(_Params), vp, vp, vp, vp, sz, vp]
+    for name in ("gp_boundary_apply", "gp_boundary_select", "gp_boundary_compact"):
+        getattr(lib, name).restype = ctypes.c_int
+        getattr(lib, name).argtypes = apply_args
+    lib.gp_boundary_decide.restype = ctypes.c_int
+    lib.gp_boundary_decide.argtypes = apply_args + [i32]
+    lib.gp_release_held.restype = ctypes.c_int
+    lib.gp_release_held.argtypes = [ctypes.POINTER(_PageState), vp]
+    lib.gp_append_step.restype = ctypes.c_int
+    lib.gp_append_step.argtypes = [ctypes.POINTER(_KVLayer), i32, ctypes.POINTER(_PageState), vp, vp, vp, vp,
+                                   i32, vp, vp, vp, i32, f32, f32, vp]
     _lib = lib
     return lib
 
@@ -242,14 +253,61 @@ def gp_boundary_score(kv: KVLayer, ps: PageState, q_pre: torch.Tensor, qstate: t
     _check(st, "gp_boundary_score")
 
 
+def _apply_like(name, layers, ps, bnd, k_counts, scores, params, decisions, delta, counters, ws, stream,
+                *extra) -> None:
+    arr = (_KVLayer * len(layers))(*[layer.c() for layer in layers])
+    c_ps, c_p = ps.c(), params.c()
+    st = getattr(load(), name)(arr, len(layers), ctypes.byref(c_ps), _ptr(bnd), bnd.shape[0],
+                               _ptr(k_counts), _ptr(scores), scores.shape[-1], ctypes.byref(c_p),
+                               _ptr(decisions), _ptr(delta), _ptr(counters), _ptr(ws),
+                               ws.numel(), _stream(stream), *extra)
+    _check(st, name)
+
+
 def gp_boundary_apply(layers: list[KVLayer], ps: PageState, bnd: torch.Tensor,
                       k_counts: torch.Tensor, scores: torch.Tensor, params: Params,
                       decisions: torch.Tensor, delta: torch.Tensor, counters: torch.Tensor,
                       ws: torch.Tensor, stream=None) -> None:
-    arr = (_KVLayer * len(layers))(*[layer.c() for layer in layers])
-    c_ps, c_p = ps.c(), params.c()
-    st = load().gp_boundary_apply(arr, len(layers), ctypes.byref(c_ps), _ptr(bnd), bnd.shape[0],
-                                  _ptr(k_counts), _ptr(scores), scores.shape[-1], ctypes.byref(c_p),
-                                  _ptr(decisions), _ptr(delta), _ptr(counters), _ptr(ws),
-                                  ws.numel(), _stream(stream))
-    _check(st, "gp_boundary_apply")
+    _apply_like("gp_boundary_apply", layers, ps, bnd, k_counts, scores, params, decisions, delta, counters,
+                ws, stream)
+
+
+def gp_boundary_select(layers, ps, bnd, k_counts, scores, params, decisions, delta, counters, ws,
+                       stream=None) -> None:
+    """First part of gp_boundary_apply: eviction lists and saved rows (workspace only)."""
+    _apply_like("gp_boundary_select", layers, ps, bnd, k_counts, scores, params, decisions, delta, counters,
+                ws, stream)
+
+
+def gp_boundary_decide(layers, ps, bnd, k_counts, scores, params, decisions, delta, counters, ws,
+                       hold: bool = False, stream=None) -> None:
+    """Second part: decisions and page metadata; hold=True leaves compressing requests held."""
+    _apply_like("gp_boundary_decide", layers, ps, bnd, k_counts, scores, params, decisions, delta, counters,
+                ws, stream, int(bool(hold)))
+
+
+def gp_boundary_compact(layers, ps, bnd, k_counts, scores, params, decisions, delta, counters, ws,
+                        stream=None) -> None:
+    """Third part: compaction and the release of freed pages."""
+    _apply_like("gp_boundary_compact", layers, ps, bnd, k_counts, scores, params, decisions, delta, counters,
+                ws, stream)
+
+
+def gp_release_held(ps: PageState, stream=None) -> None:
+    c_ps = ps.c()
+    _check(load().gp_release_held(ctypes.byref(c_ps), _stream(stream)), "gp_release_held")
+
+
+def gp_append_step(layers: list[KVLayer], ps: PageState, positions: torch.Tensor, k_new: torch.Tensor,
+                   v_new: torch.Tensor, q_pre: torch.Tensor, slot_ids: torch.Tensor, init: torch.Tensor | None,
+                   qstate: torch.Tensor, beta_s: float, beta_l: float, stream=None) -> None:
+    """k_new, v_new [L][R][Hkv][d]; q_pre [L][R][Hq][d]; qstate [L][M][2][Hq][d]."""
+    L = len(layers)
+    if k_new.dim() != 4 or k_new.shape[0] != L or q_pre.dim() != 4 or qstate.dim() != 5:
+        raise ValueError("gp_append_step: k_new/v_new [L,R,Hkv,d], q_pre [L,R,Hq,d], qstate [L,M,2,Hq,d]")
+    arr = (_KVLayer * L)(*[layer.c() for layer in layers])
+    c_ps = ps.c()
+    st = load().gp_append_step(arr, L, ctypes.byref(c_ps), _ptr(positions), _ptr(k_new), _ptr(v_new),
+                               _ptr(q_pre), q_pre.shape[2], _ptr(slot_ids), _ptr(init), _ptr(qstate),
+                               qstate.shape[1], float(beta_s), float(beta_l), _stream(stream))
+    _check(st, "gp_append_step")

@@ -20,7 +20,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libgrowpage.so")
-SOURCES = ["gp_api.hip", "gp_summaries.hip", "gp_decode.hip", "gp_score.hip", "gp_apply.hip"]
+SOURCES = ["gp_api.hip", "gp_summaries.hip", "gp_decode.hip", "gp_score.hip", "gp_apply.hip",
+           "gp_append.hip"]
 ARCH = os.environ.get("GP_OFFLOAD_ARCH", "gfx950")
 
 

@@ -219,11 +219,13 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
     return from_hip(launch_score(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stream));
 }
 
-gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers, const gp_page_state_t *ps,
-                              const int32_t *bnd, int32_t num_bnd, const int32_t *k_counts,
-                              const float *scores, int32_t max_cand, const gp_params_t *params,
-                              int32_t *decisions, float *delta, int64_t *counters, void *ws,
-                              size_t ws_bytes, hipStream_t stream) {
+namespace {
+
+gp_status_t apply_call(const gp_kv_layer_t *layers, int32_t n_layers, const gp_page_state_t *ps,
+                       const int32_t *bnd, int32_t num_bnd, const int32_t *k_counts, const float *scores,
+                       int32_t max_cand, const gp_params_t *params, int32_t *decisions, float *delta,
+                       int64_t *counters, void *ws, size_t ws_bytes, hipStream_t stream, int stages,
+                       int hold) {
     if (!layers || n_layers <= 0 || !params || num_bnd < 0) return GP_ERR_INVALID;
     if (n_layers > kMaxLayers) return GP_ERR_UNSUPPORTED;
     gp_status_t st;
@@ -291,12 +293,89 @@ gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers, con
     a.shrink_threshold = params->shrink_threshold;
     a.draws = params->draws;
     a.layout = params->layout;
+    a.hold = hold;
     LayerPtrs lp[kMaxLayers];
     for (int l = 0; l < n_layers; ++l) {
         lp[l].k = layers[l].k;
         lp[l].v = layers[l].v;
     }
-    return from_hip(launch_apply(L0.dtype, L0.head_dim, a, lp, stream));
+    return from_hip(launch_apply(L0.dtype, L0.head_dim, a, lp, stages, stream));
+}
+
+}  // namespace
+
+#define GP_APPLY_ARGS                                                                              \
+    const gp_kv_layer_t *layers, int32_t n_layers, const gp_page_state_t *ps, const int32_t *bnd, \
+        int32_t num_bnd, const int32_t *k_counts, const float *scores, int32_t max_cand,          \
+        const gp_params_t *params, int32_t *decisions, float *delta, int64_t *counters, void *ws,  \
+        size_t ws_bytes, hipStream_t stream
+#define GP_APPLY_PASS                                                                                \
+    layers, n_layers, ps, bnd, num_bnd, k_counts, scores, max_cand, params, decisions, delta, counters, \
+        ws, ws_bytes, stream
+
+gp_status_t gp_boundary_apply(GP_APPLY_ARGS) {
+    return apply_call(GP_APPLY_PASS, kStageSelect | kStageDecide | kStageCompact, 0);
+}
+
+gp_status_t gp_boundary_select(GP_APPLY_ARGS) { return apply_call(GP_APPLY_PASS, kStageSelect, 0); }
+
+gp_status_t gp_boundary_decide(GP_APPLY_ARGS, int32_t hold) {
+    return apply_call(GP_APPLY_PASS, kStageDecide, hold != 0);
+}
+
+gp_status_t gp_boundary_compact(GP_APPLY_ARGS) { return apply_call(GP_APPLY_PASS, kStageCompact, 0); }
+
+gp_status_t gp_append_step(const gp_kv_layer_t *layers, int32_t n_layers, const gp_page_state_t *ps,
+                           int32_t *positions, const void *k_new, const void *v_new, const void *q_pre,
+                           int32_t num_q_heads, const int32_t *slot_ids, const uint8_t *init,
+                           float *qstate, int32_t num_slots, float beta_s, float beta_l,
+                           hipStream_t stream) {
+    if (!layers || n_layers <= 0) return GP_ERR_INVALID;
+    if (n_layers > kMaxLayers) return GP_ERR_UNSUPPORTED;
+    gp_status_t st;
+    for (int l = 0; l < n_layers; ++l) {
+        if ((st = check_layer(&layers[l])) != GP_OK) return st;
+        if (layers[l].pool_pages != layers[0].pool_pages || layers[l].num_kv_heads != layers[0].num_kv_heads ||
+            layers[l].head_dim != layers[0].head_dim || layers[l].dtype != layers[0].dtype)
+            return GP_ERR_INVALID;
+    }
+    if ((st = check_state(ps, &layers[0])) != GP_OK) return st;
+    if (!dims_ok(num_q_heads, layers[0].num_kv_heads, layers[0].head_dim)) return GP_ERR_UNSUPPORTED;
+    if (!(beta_s >= 0.0f && beta_s <= 1.0f) || !(beta_l >= 0.0f && beta_l <= 1.0f) || num_slots <= 0)
+        return GP_ERR_INVALID;
+    if (ps->num_reqs == 0) return GP_OK;
+    if (!positions || !k_new || !v_new || !q_pre || !slot_ids || !qstate) return GP_ERR_INVALID;
+    AppendArgs a;
+    for (int l = 0; l < kMaxLayers; ++l) {
+        a.k[l] = l < n_layers ? layers[l].k : nullptr;
+        a.v[l] = l < n_layers ? layers[l].v : nullptr;
+    }
+    a.page_table = ps->page_table;
+    a.num_pages = ps->num_pages;
+    a.seq_lens = ps->seq_lens;
+    a.positions = positions;
+    a.k_new = k_new;
+    a.v_new = v_new;
+    a.q_pre = q_pre;
+    a.slot_ids = slot_ids;
+    a.init = init;
+    a.qstate = qstate;
+    a.R = ps->num_reqs;
+    a.Hq = num_q_heads;
+    a.Hkv = layers[0].num_kv_heads;
+    a.M = num_slots;
+    a.max_pages = ps->max_pages;
+    a.pool_pages = ps->pool_pages;
+    a.n_layers = n_layers;
+    a.beta_s = beta_s;
+    a.beta_l = beta_l;
+    return from_hip(launch_append(layers[0].dtype, layers[0].head_dim, a, stream));
+}
+
+gp_status_t gp_release_held(const gp_page_state_t *ps, hipStream_t stream) {
+    if (!ps || !ps->seq_lens || ps->num_reqs < 0) return GP_ERR_INVALID;
+    if (ps->num_reqs == 0) return GP_OK;
+    return from_hip(launch_release(ps->seq_lens, ps->num_reqs, stream));
 }
 
 }  // extern "C"

@@ -411,9 +411,12 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
             if (pid >= 0 && pid < a.pool_pages) a.refcount[pid] = 1;
             a.num_pages[r] = P + 1;
         } else if (compressing(dec)) {
-            a.seq_lens[r] = (P - 1) * kPage;
+            // a held request is left out of decoding until released: -(m + 1)
+            const int m = (P - 1) * kPage;
+            a.seq_lens[r] = a.hold ? -m - 1 : m;
         } else if (dec == GP_SHRINK) {
-            a.seq_lens[r] = (P - 2) * kPage;
+            const int m = (P - 2) * kPage;
+            a.seq_lens[r] = a.hold ? -m - 1 : m;
             a.num_pages[r] = P - 1;
         }
     }
@@ -593,18 +596,33 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
     }
 }
 
+// ---------------------------------------------------------------- release --
+// Held requests (seq_len = -(m + 1)) get their resident length back.
+__global__ __launch_bounds__(256) void release_kernel(int32_t *seq_lens, int R) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r < R) {
+        const int m = seq_lens[r];
+        if (m < 0) seq_lens[r] = -m - 1;
+    }
+}
+
 template <int D, int E>
-hipError_t launch_de(const ApplyArgs &a, const LayerTable &lt, hipStream_t s) {
+hipError_t launch_de(const ApplyArgs &a, const LayerTable &lt, int stages, hipStream_t s) {
     dim3 gpre(1 + a.ncc, a.Hkv * a.n_layers, a.Rb), gcomp(a.ncc, a.Hkv * a.n_layers, a.Rb);
-    pre_kernel<D, E><<<gpre, 1024, 0, s>>>(a, lt);
-    decide_kernel<<<1, 1024, 0, s>>>(a);
-    compact_kernel<D, E><<<gcomp, 256, 0, s>>>(a, lt);
+    if (stages & kStageSelect) pre_kernel<D, E><<<gpre, 1024, 0, s>>>(a, lt);
+    if (stages & kStageDecide) decide_kernel<<<1, 1024, 0, s>>>(a);
+    if (stages & kStageCompact) compact_kernel<D, E><<<gcomp, 256, 0, s>>>(a, lt);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_apply(gp_dtype_t dt, int D, const ApplyArgs &a, const LayerPtrs *layers,
+hipError_t launch_release(int32_t *seq_lens, int R, hipStream_t s) {
+    release_kernel<<<cdiv(R, 256), 256, 0, s>>>(seq_lens, R);
+    return hipGetLastError();
+}
+
+hipError_t launch_apply(gp_dtype_t dt, int D, const ApplyArgs &a, const LayerPtrs *layers, int stages,
                         hipStream_t s) {
     if (a.Rb == 0) return hipSuccess;
     LayerTable lt;
@@ -612,8 +630,8 @@ hipError_t launch_apply(gp_dtype_t dt, int D, const ApplyArgs &a, const LayerPtr
         lt.k[l] = l < a.n_layers ? layers[l].k : nullptr;
         lt.v[l] = l < a.n_layers ? layers[l].v : nullptr;
     }
-    if (dt == GP_BF16) return D == 128 ? launch_de<128, 2>(a, lt, s) : launch_de<64, 2>(a, lt, s);
-    return D == 128 ? launch_de<128, 4>(a, lt, s) : launch_de<64, 4>(a, lt, s);
+    if (dt == GP_BF16) return D == 128 ? launch_de<128, 2>(a, lt, stages, s) : launch_de<64, 2>(a, lt, stages, s);
+    return D == 128 ? launch_de<128, 4>(a, lt, stages, s) : launch_de<64, 4>(a, lt, stages, s);
 }
 
 }  // namespace gp

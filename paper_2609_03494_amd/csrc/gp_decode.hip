@@ -99,12 +99,13 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int Hkv = a.Hkv;
     const int Hq = Hkv * G;
+    int m = a.seq_lens[r];
+    if (m < 0) return;                        // held: not in this step's batch
     if (chunk == 0) fold_summaries<T, D, G>(a, r, h);
 
     int P = a.num_pages[r];
     P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
-    int m = a.seq_lens[r];
-    m = m < 0 ? 0 : (m > P * kPage ? P * kPage : m);
+    m = m > P * kPage ? P * kPage : m;
     const int nchunks = cdiv(m, CHUNK);
     T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     if (m == 0) {
@@ -340,13 +341,14 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     const int h = blockIdx.x, chunk = blockIdx.y, r = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int Hkv = a.Hkv, Hq = Hkv * G;
+    int m = a.seq_lens[r];
+    if (m < 0) return;                        // held: not in this step's batch
     if (chunk == 0) fold_summaries<uint16_t, D, G>(a, r, h);
     const int CHUNK = a.chunk_pages * kPage;
 
     int P = a.num_pages[r];
     P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
-    int m = a.seq_lens[r];
-    m = m < 0 ? 0 : (m > P * kPage ? P * kPage : m);
+    m = m > P * kPage ? P * kPage : m;
     const int nchunks = cdiv(m, CHUNK);
     uint16_t *out = reinterpret_cast<uint16_t *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     if (m == 0) {
@@ -535,7 +537,7 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     int P = a.num_pages[r];
     P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
     int m = a.seq_lens[r];
-    m = m < 0 ? 0 : (m > P * kPage ? P * kPage : m);
+    m = m < 0 ? 0 : (m > P * kPage ? P * kPage : m);     // held requests: nothing to merge
     const int nchunks = cdiv(m, CHUNK);
     if (nchunks <= 1) return;
     const int Hq = a.Hkv * G;

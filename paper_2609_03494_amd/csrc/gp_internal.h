@@ -165,6 +165,18 @@ struct SummaryArgs {
     double beta_s, beta_l;
 };
 
+struct AppendArgs {
+    void *k[kMaxLayers];
+    void *v[kMaxLayers];
+    int32_t *page_table, *num_pages, *seq_lens, *positions;
+    const void *k_new, *v_new, *q_pre;
+    const int32_t *slot_ids;
+    const uint8_t *init;
+    float *qstate;
+    int R, Hq, Hkv, M, max_pages, pool_pages, n_layers;
+    double beta_s, beta_l;
+};
+
 struct ScoreArgs {
     const void *k;
     const int32_t *page_table, *num_pages, *seq_lens;
@@ -198,6 +210,7 @@ struct ApplyArgs {
     double shrink_threshold;
     const float *draws;
     int layout;       // GP_LAYOUT_*
+    int hold;         // mark compressing requests held (negative seq_len)
 };
 
 struct LayerPtrs {
@@ -207,10 +220,15 @@ struct LayerPtrs {
 // ---------------------------------------------------------------- launchers --
 
 hipError_t launch_summaries(gp_dtype_t dt, const SummaryArgs &a, hipStream_t s);
+hipError_t launch_append(gp_dtype_t dt, int D, const AppendArgs &a, hipStream_t s);
 hipError_t launch_decode(gp_dtype_t dt, int D, int G, const DecodeArgs &a, hipStream_t s);
 hipError_t launch_score(gp_dtype_t dt, int D, int G, const ScoreArgs &a, hipStream_t s);
-hipError_t launch_apply(gp_dtype_t dt, int D, const ApplyArgs &a, const LayerPtrs *layers,
+// Stages of the boundary apply (selection, decision, compaction).
+constexpr int kStageSelect = 1, kStageDecide = 2, kStageCompact = 4;
+
+hipError_t launch_apply(gp_dtype_t dt, int D, const ApplyArgs &a, const LayerPtrs *layers, int stages,
                         hipStream_t s);
+hipError_t launch_release(int32_t *seq_lens, int R, hipStream_t s);
 
 // ---------------------------------------------------------- device helpers --
 

@@ -100,6 +100,20 @@ def test_host_validation_without_launch(lib):
                               None, 512, 0.9, 0.999, fake, 1 << 30, None) == 1
     assert lib.gp_decode_step(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 32, 0.1, fake, fake, fake,
                               fake, 512, 0.9, 0.999, fake, 16, None) == 3
+    # release: null state; append: beta outside [0, 1], too many layers, null summaries
+    assert lib.gp_release_held(None, None) == 1
+    assert lib.gp_append_step(arr, 1, ctypes.byref(ps), fake, fake, fake, fake, 32, fake, None, fake, 512,
+                              1.5, 0.999, None) == 1
+    assert lib.gp_append_step(arr, 65, ctypes.byref(ps), fake, fake, fake, fake, 32, fake, None, fake, 512,
+                              0.9, 0.999, None) == 2
+    assert lib.gp_append_step(arr, 1, ctypes.byref(ps), fake, fake, fake, fake, 32, fake, None, None, 512,
+                              0.9, 0.999, None) == 1
+    # split apply validates like apply; decide takes the hold flag last
+    for name in ("gp_boundary_select", "gp_boundary_compact"):
+        assert getattr(lib, name)(arr, 65, ctypes.byref(ps), fake, 2, fake, fake, 144, ctypes.byref(p),
+                                  fake, fake, fake, fake, 1 << 30, None) == 2
+    assert lib.gp_boundary_decide(arr, 65, ctypes.byref(ps), fake, 2, fake, fake, 144, ctypes.byref(p),
+                                  fake, fake, fake, fake, 1 << 30, None, 1) == 2
     # zero requests is a no-op that succeeds
     ps0 = _lib._PageState(fake, fake, fake, fake, fake, fake, 0, 10, 100)
     assert lib.gp_decode_attention(ctypes.byref(kv), ctypes.byref(ps0), fake, 32, 0.1, fake, fake, 0,
