@@ -4,12 +4,13 @@
 
 A step is one pass of the whole path over the batch: restore the page metadata
 to the step's starting state (one device-to-device copy), update both query summaries of every request, paged decode attention
-for every request, then boundary scoring and decide/select/compact for the
+for every request, then boundary scoring, selection, the decision and compaction for the
 requests at a capacity boundary.  Inputs are seeded synthetic tensors resident
 in HBM before timing starts.  The step is captured once as a HIP graph and
-replayed (``--eager`` launches every call directly).  Scoring reads keys only,
-so it runs on a second stream beside decode attention; decide/select/compact
-wait for both (``--serial`` runs everything on one stream).
+replayed (``--eager`` launches every call directly).  Scoring and selection
+read keys and scores only, so they run on a second stream beside decode
+attention; the decision and compaction wait for both (``--serial`` runs
+everything on one stream).
 
 Prints one JSON line.  ``value`` is GB/s of the every-step traffic (summaries
 and decode attention, algorithmic bytes) over the whole step's time, boundary
@@ -50,6 +51,8 @@ def parse():
     ap.add_argument("--eager", action="store_true", help="launch every call directly (no HIP graphs)")
     ap.add_argument("--serial", action="store_true",
                     help="run boundary scoring after decode attention on one stream")
+    ap.add_argument("--loop-steps", type=int, default=50,
+                    help="steps of the decode-loop measurement (0 skips it)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, run a plain device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -132,20 +135,26 @@ def main():
     def phase_decode():
         gp.gp_decode_attention(kv, ps, q_post, params.scale, out, ws_d)
 
+    bargs = ([kv], ps, bnd, counts, scores, params, decisions, delta, counters, ws_a)
+
     def phase_score():
+        # scoring, then the eviction lists every boundary request would use if
+        # it compressed: both read keys and scores only
         gp.gp_boundary_score(kv, ps, q_pre, qstate, slots, positions, bnd, params, counts, scores, ws_s)
+        gp.gp_boundary_select(*bargs)
 
     def phase_apply():
-        gp.gp_boundary_apply([kv], ps, bnd, counts, scores, params, decisions, delta, counters, ws_a)
+        gp.gp_boundary_decide(*bargs, hold=False)
+        gp.gp_boundary_compact(*bargs)
 
     side = torch.cuda.Stream()          # default priority, like the main stream
     phase = dict(pre=phase_pre, decode=phase_decode, score=phase_score, apply=phase_apply)
 
     def step(marks=None):
-        """One step on the current stream.  Scoring only reads keys, so unless
-        --serial it runs beside decode attention on a second stream (fork and
-        join by stream waits, which graph capture records as dependencies);
-        compaction waits for both."""
+        """One step on the current stream.  Scoring and selection only read,
+        so unless --serial they run beside decode attention on a second stream
+        (fork and join by stream waits, which graph capture records as
+        dependencies); the decision and compaction wait for both."""
         cur = torch.cuda.current_stream()
 
         def mark(name):
@@ -263,6 +272,17 @@ def main():
 
     apply_layout_ms = {"shift": apply_ms(gp.GP_LAYOUT_SHIFT), "fill": apply_ms(gp.GP_LAYOUT_FILL)}
 
+    # the decode loop itself (App. E.3): every step appends each running
+    # request's new token (K/V into its pages, one summary EMA step), decodes,
+    # and takes the boundary event of every request whose pages are full.
+    # "sync" decides and compacts before the next step; "async" leaves
+    # compressing requests held for one step and runs their compaction on a
+    # third stream beside the next step's append and decode.  Both start from
+    # the same state and see the same seeded tokens; the W + K steps are two
+    # HIP graphs (inputs picked by a device-side step counter).
+    loop = serving_loops(args, gp, W, w, kv, ps, meta, meta0, qstate, slots, positions, params, k, v) \
+        if args.loop_steps > 0 else None
+
     # algorithmic bytes
     m = w.seq_lens.astype(np.int64)
     decode_bytes = int(m.sum()) * Hkv * d * e * 2 + int(w.num_pages.sum()) * 4 + 2 * R * Hq * d * e
@@ -320,11 +340,139 @@ def main():
                      "overlapped_with_decode": not args.serial,
                      "compress_grow_fallback_preempt": split,
                      "apply_ms_all_compress": {k_: round(v_, 4) for k_, v_ in apply_layout_ms.items()}},
+        "serving_loop": loop,
         "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def serving_loops(args, gp, W, w, kv, ps, meta, meta0, qstate, slots, positions, params, k, v):
+    """Times the decode loop synchronously and with asynchronous compaction,
+    from the same starting state; returns the report object."""
+    import torch
+
+    dev = "cuda"
+    R, Hq, Hkv, d = w.num_reqs, w.num_q_heads, w.num_kv_heads, w.head_dim
+    n_warm, n_steps = max(args.warmup, 1), args.loop_steps
+    S = n_warm + n_steps
+    dt = torch.bfloat16
+    inp = W.step_inputs(w, S, seed=0)
+
+    def stack(key, layer0=False):
+        a = np.stack([x[key][0] if layer0 else x[key] for x in inp])
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(dt).to(dev)
+
+    k_all, v_all = stack("k_new", True), stack("v_new", True)          # [S][R][Hkv][d]
+    qpre_all, qpost_all = stack("q_pre"), stack("q_post")              # [S][R][Hq][d]
+    t_idx = torch.zeros(1, dtype=torch.int64, device=dev)
+    bnd = torch.arange(R, dtype=torch.int32, device=dev)               # every request; kernels filter
+    max_cand = (w.max_pages - 1) * w.page_size
+    counts = torch.zeros((1, R, Hkv, 2), dtype=torch.int32, device=dev)
+    scores = torch.zeros((1, R, Hkv, max_cand), device=dev)
+    dec = torch.zeros(R, dtype=torch.int32, device=dev)
+    delta = torch.zeros(R, device=dev)
+    ctr = torch.zeros(4, dtype=torch.int64, device=dev)
+    out = torch.empty((R, Hq, d), dtype=dt, device=dev)
+    ws_d = gp.workspace(gp.GP_OP_DECODE, R, 0, Hq, Hkv, d, w.max_pages, dt)
+    ws_s = gp.workspace(gp.GP_OP_SCORE, R, R, Hq, Hkv, d, w.max_pages, dt)
+    ws_a = [gp.workspace(gp.GP_OP_APPLY, R, R, Hq, Hkv, d, w.max_pages, dt) for _ in range(2)]
+    qstate5 = qstate.view(1, *qstate.shape)
+    side_a, side_b = torch.cuda.Stream(), torch.cuda.Stream()
+
+    # the starting state, restored before each variant
+    snap = dict(meta=meta0.clone(), qstate=qstate.clone(), positions=positions.clone(), k=k.clone(),
+                v=v.clone())
+
+    def restore_all():
+        meta.copy_(snap["meta"])
+        qstate.copy_(snap["qstate"])
+        positions.copy_(snap["positions"])
+        k.copy_(snap["k"])
+        v.copy_(snap["v"])
+        ctr.zero_()
+        t_idx.zero_()
+        for x in ws_a:
+            x.zero_()
+
+    def one_step(async_, parity):
+        cur = torch.cuda.current_stream()
+        k_new = torch.index_select(k_all, 0, t_idx)                    # [1][R][Hkv][d]
+        v_new = torch.index_select(v_all, 0, t_idx)
+        q_pre = torch.index_select(qpre_all, 0, t_idx)                 # [1][R][Hq][d]
+        q_post = torch.index_select(qpost_all, 0, t_idx)[0]
+        gp.gp_append_step([kv], ps, positions, k_new, v_new, q_pre, slots, None, qstate5,
+                          params.beta_s, params.beta_l)
+        ws = ws_a[parity] if async_ else ws_a[0]
+        bargs = ([kv], ps, bnd, counts, scores, params, dec, delta, ctr, ws)
+        side_b.wait_stream(cur)
+        with torch.cuda.stream(side_b):
+            gp.gp_boundary_score(kv, ps, q_pre[0], qstate, slots, positions, bnd, params, counts[0],
+                                 scores[0], ws_s)
+            gp.gp_boundary_select(*bargs)
+        gp.gp_decode_attention(kv, ps, q_post, params.scale, out, ws_d)
+        cur.wait_stream(side_b)
+        if async_:
+            cur.wait_stream(side_a)                                     # the previous compaction
+            gp.gp_release_held(ps)
+            gp.gp_boundary_decide(*bargs, hold=True)
+            side_a.wait_stream(cur)
+            with torch.cuda.stream(side_a):
+                gp.gp_boundary_compact(*bargs)
+        else:
+            gp.gp_boundary_decide(*bargs, hold=False)
+            gp.gp_boundary_compact(*bargs)
+        t_idx.add_(1)
+        return k_new, v_new, q_pre, q_post
+
+    def capture(n, async_):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            cur = torch.cuda.current_stream()
+            side_a.wait_stream(cur)
+            side_b.wait_stream(cur)
+            # each step's inputs stay allocated until the capture ends, so no
+            # later step reuses memory that a side-stream node still reads
+            keep = [one_step(async_, j % 2) for j in range(n)]
+            cur.wait_stream(side_a)
+            cur.wait_stream(side_b)
+        del keep
+        return g
+
+    res = {}
+    for name, async_ in (("sync", False), ("async", True)):
+        restore_all()
+        torch.cuda.synchronize()
+        g_warm, g_run = capture(n_warm, async_), capture(n_steps, async_)
+        restore_all()
+        torch.cuda.synchronize()
+        g_warm.replay()
+        torch.cuda.synchronize()
+        pos0 = int(positions.sum().item())
+        ctr0 = ctr.cpu().numpy().copy()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g_run.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        tokens = int(positions.sum().item()) - pos0
+        split = (ctr.cpu().numpy() - ctr0).tolist()
+        res[name] = {"ms_per_step": round(ms / n_steps, 4), "tokens_per_s": round(tokens / (ms * 1e-3), 1),
+                     "tokens": tokens, "boundary_events": int(sum(split)),
+                     "compress_grow_fallback_preempt": split}
+        del g_warm, g_run
+    restore_all()
+    torch.cuda.synchronize()
+    del snap
+    res["steps"] = n_steps
+    res["async_speedup"] = round(res["async"]["tokens_per_s"] / res["sync"]["tokens_per_s"], 4)
+    res["note"] = ("one layer of the Qwen3-8B layer workload run as a decode loop: per step, append "
+                   "(new K/V into the pages, summary EMA), decode attention, and the boundary event of "
+                   "every request whose pages are full; async holds compressing requests for one step "
+                   "and overlaps their compaction with the next step (App. E.3)")
+    return res
 
 
 def _kernel_hash() -> str:
