@@ -23,7 +23,7 @@ constexpr int kMaxChunkPages = 64;                         // pages per decode c
 constexpr int kDecodeWaves = GP_DECODE_WAVES;              // waves per decode workgroup (bf16 path)
 constexpr int kMaxDecodeChunks = 128;                      // chunks one request may span
 constexpr int kMaxBoundaryPages = 4096;                    // table width the boundary calls accept
-constexpr int kScoreChunk = 256;          // candidate tokens per scoring work item
+constexpr int kStatBlock = 64;            // candidate tokens per softmax-statistics block (one wave)
 constexpr int kProbChunk = 1024;          // tokens per weight/score work item
 constexpr int kCompactChunk = 256;        // slots per compaction work item
 constexpr int kMaxLayers = 64;            // layers one gp_boundary_apply call can take
@@ -81,13 +81,13 @@ __host__ __device__ inline ScoreWs score_ws(int Rb, int Hq, int Hkv, int max_pag
     ScoreWs w;
     const int G = Hq / Hkv;
     w.cmax = max_pages > 1 ? (max_pages - 1) * kPage : 0;
-    w.nch = cdiv(w.cmax > 0 ? w.cmax : 1, kScoreChunk);
+    w.nch = cdiv(w.cmax > 0 ? w.cmax : 1, kStatBlock);
     size_t off = 0;
     w.qt = off;       // [Rb][Hkv][2G][D] double: calibrated, rotated summaries
     off = align_up(off + (size_t)Rb * Hkv * 2 * G * 128 * sizeof(double));
-    w.logits = off;   // [Rb][Hkv][2G][cmax] double
+    w.logits = off;   // [Rb][Hkv][2G][cmax] double: exp(z - block max)
     off = align_up(off + (size_t)Rb * Hkv * 2 * G * w.cmax * sizeof(double));
-    w.part = off;     // [Rb][Hkv][nch][2G][2] double (running max, sum of exp)
+    w.part = off;     // [Rb][Hkv][nch][2G][2] double: block max, block sum of exp
     off = align_up(off + (size_t)Rb * Hkv * w.nch * 2 * G * 2 * sizeof(double));
     w.weights = off;  // [Rb][Hkv][2][cmax] float
     off = align_up(off + (size_t)Rb * Hkv * 2 * w.cmax * sizeof(float));

@@ -2,16 +2,17 @@
 // App. E.1 "demand estimation at capacity boundaries").
 //
 // Three kernels per layer:
-//  1. logits: per (boundary request, KV head, chunk of kScoreChunk candidate
-//     tokens).  The workgroup first builds the 2G aligned summaries of its GQA
-//     group in LDS (RMS calibration to the current query, then rotation at the
-//     current position; fp64, angles computed on the device in fp64), then
-//     each thread takes one candidate token, reads its key once and forms its
-//     2G logits in fp64.  The chunk's running max and sum of exponentials per
-//     view go to the workspace next to the logits.
-//  2. weights: merge the chunk statistics per view, turn logits into the
-//     softmax weights, average the G query heads of each view (fp64), round to
-//     float32 and write a^S, a^L (workspace) and s = max(a^S, a^L) (output).
+//  0. prep: per (boundary request, KV head) the 2G aligned summaries of its
+//     GQA group (RMS calibration to the current query, then rotation at the
+//     current position; fp64, angles computed on the device in fp64).
+//  1. logits: per (boundary request, KV head, block of kStatBlock candidate
+//     tokens), one wave: each lane reads its token's key once and forms its
+//     2G logits in fp64; the block's max and sum of exponentials per view go
+//     to the workspace, and exp(z - block max) replaces the logit.
+//  2. weights: merge the block statistics per view, scale each token's
+//     exponentials into softmax weights, average the G query heads of each
+//     view (fp64), round to float32 and write a^S, a^L (workspace) and
+//     s = max(a^S, a^L) (output).
 //  3. top-p: per (request, KV head, view) a three-pass radix select on the
 //     float32 bit patterns finds the smallest k whose k largest weights reach
 //     p.  Per-bucket masses are accumulated as 2^-60 fixed-point integers, so
@@ -34,21 +35,22 @@ __device__ inline double ld<uint16_t>(const uint16_t *p) { return (double)bf16_t
 
 template <typename T>
 struct KRow;
+// Elements g*4 .. g*4+3 of a key row held as 16-byte units (g uniform).
 template <>
 struct KRow<uint16_t> {
     static constexpr int EPV = 8;
-    __device__ static inline void get(const uint16_t *p, double *f) {
-        const uint4 u = *reinterpret_cast<const uint4 *>(p);
+    __device__ static inline void get_group(const uint4 *row, int g, double *f) {
+        const uint2 u = reinterpret_cast<const uint2 *>(row)[g];
         f[0] = bf16_lo(u.x); f[1] = bf16_hi(u.x); f[2] = bf16_lo(u.y); f[3] = bf16_hi(u.y);
-        f[4] = bf16_lo(u.z); f[5] = bf16_hi(u.z); f[6] = bf16_lo(u.w); f[7] = bf16_hi(u.w);
     }
 };
 template <>
 struct KRow<float> {
     static constexpr int EPV = 4;
-    __device__ static inline void get(const float *p, double *f) {
-        const float4 u = *reinterpret_cast<const float4 *>(p);
-        f[0] = u.x; f[1] = u.y; f[2] = u.z; f[3] = u.w;
+    __device__ static inline void get_group(const uint4 *row, int g, double *f) {
+        const uint4 u = row[g];
+        f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y);
+        f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
     }
 };
 
@@ -125,102 +127,102 @@ __global__ __launch_bounds__(256) void prep_kernel(ScoreArgs a) {
 }
 
 // ------------------------------------------------------------------- logits --
+// Grid (blocks of kStatBlock candidates, KV head, boundary request), one wave
+// per workgroup, one candidate token per lane.  The lane reads its token's key
+// row once (all of it in flight at once) and parks it in LDS (rows padded to
+// avoid bank conflicts; a lane only ever reads its own row).  A loop over
+// groups of four head dimensions then forms the 2G logits with fp64 fused
+// multiply-adds: the loop counter and the summary addresses are wave-uniform,
+// so the 2G * 4 summary values of a group are scalar loads used directly as
+// FMA operands, with no LDS or vector-register traffic for them.  The block's
+// max m and sum of exp(z - m) per view go to the statistics array; the logits
+// array receives exp(z - m), so that the weights need a product, not an
+// exponential, per token.  A lane whose page id is invalid contributes zero
+// logits.
 template <typename T, int D, int G>
-__global__ __launch_bounds__(256) void logits_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
     constexpr int V = 2 * G;
     constexpr int EPV = KRow<T>::EPV;
     constexpr int NV = D / EPV;                      // 16-byte units per key row
-    __shared__ double s_q[V][D];
-    __shared__ double s_red[256 / 64][V];
-    __shared__ double s_max[V];
+    constexpr int ROW = NV + 1;                      // staged row stride, 16-byte units
+    constexpr int DG = 4;                            // head dimensions per loop step
+    constexpr int NG = D / DG;
+    static_assert(kStatBlock == 64, "one wave per statistics block");
+    __shared__ uint4 s_k[kStatBlock * ROW];
 
-    const int chunk = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    const int blk = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    const int lane = threadIdx.x;
     int r, P;
     if (!boundary_of(a, i, r, P)) return;
     const int C = (P - 1) * kPage;
-    const int t0 = chunk * kScoreChunk;
+    const int t0 = blk * kStatBlock;
     if (t0 >= C) return;
     const int slot = a.slot_ids[r];
     if (slot < 0 || slot >= a.M) return;
-    const int tid = threadIdx.x;
 
-    // the key row of this thread's candidate, read whole before any use
-    const int t = t0 + tid;
-    const bool live = t < C && tid < kScoreChunk;
-    double z[V];
-#pragma unroll
-    for (int v = 0; v < V; ++v) z[v] = 0.0;
-    bool have = false;
+    const int t = t0 + lane;
+    const bool live = t < C;
     uint4 krow[NV];
+#pragma unroll
+    for (int u = 0; u < NV; ++u) krow[u] = make_uint4(0u, 0u, 0u, 0u);
     if (live) {
         const int phys = a.page_table[(size_t)r * a.max_pages + t / kPage];
         if (phys >= 0 && phys < a.pool_pages) {
-            have = true;
             const uint4 *kp = reinterpret_cast<const uint4 *>(reinterpret_cast<const T *>(a.k) +
                               (((size_t)phys * a.Hkv + h) * kPage + (t % kPage)) * D);
 #pragma unroll
             for (int u = 0; u < NV; ++u) krow[u] = kp[u];
         }
     }
-    const double *qt = a.qt + ((size_t)i * a.Hkv + h) * V * D;
-    for (int e = tid; e < V * D; e += blockDim.x) s_q[e / D][e % D] = qt[e];
-    __syncthreads();
+    uint4 *myrow = s_k + lane * ROW;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) myrow[u] = krow[u];
 
-    if (have) {
+    const double *__restrict__ qt = a.qt + ((size_t)i * a.Hkv + h) * V * D;
+    double z[V];
 #pragma unroll
-        for (int u = 0; u < NV; ++u) {
-            double kf[EPV];
-            KRow<T>::get(reinterpret_cast<const T *>(&krow[u]), kf);
+    for (int v = 0; v < V; ++v) z[v] = 0.0;
+#pragma unroll 1
+    for (int g = 0; g < NG; ++g) {
+        double kf[DG];
+        KRow<T>::get_group(myrow, g, kf);
+        const double *qg = qt + g * DG;
 #pragma unroll
-            for (int v = 0; v < V; ++v)
+        for (int e = 0; e < DG; ++e)
 #pragma unroll
-                for (int e = 0; e < EPV; ++e) z[v] += s_q[v][u * EPV + e] * kf[e];
-        }
-    }
-    if (live) {
-#pragma unroll
-        for (int v = 0; v < V; ++v) z[v] *= a.scale;
-        double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax + t;
-#pragma unroll
-        for (int v = 0; v < V; ++v) lg[(size_t)v * a.cmax] = z[v];
+            for (int v = 0; v < V; ++v) z[v] = fma(qg[v * D + e], kf[e], z[v]);
     }
 
-    // chunk statistics: max and sum of exp(z - max) per view
-    const int lane = tid & 63, wave = tid >> 6;
+    double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax + t;
+    double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch + blk) * V * 2;
 #pragma unroll
     for (int v = 0; v < V; ++v) {
-        double mv = live ? z[v] : -__builtin_huge_val();
+        const double zv = z[v] * a.scale;
+        double mv = live ? zv : -__builtin_huge_val();
         for (int off = 32; off >= 1; off >>= 1) mv = fmax(mv, __shfl_xor(mv, off, 64));
-        if (lane == 0) s_red[wave][v] = mv;
-    }
-    __syncthreads();
-    if (tid < V) {
-        double mv = s_red[0][tid];
-        for (int w = 1; w < 4; ++w) mv = fmax(mv, s_red[w][tid]);
-        s_max[tid] = mv;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int v = 0; v < V; ++v) {
-        double ev = live ? exp(z[v] - s_max[v]) : 0.0;
-        for (int off = 32; off >= 1; off >>= 1) ev += __shfl_xor(ev, off, 64);
-        if (lane == 0) s_red[wave][v] = ev;
-    }
-    __syncthreads();
-    if (tid < V) {
-        double sv = 0.0;
-        for (int w = 0; w < 4; ++w) sv += s_red[w][tid];
-        double *pt = a.part + ((((size_t)i * a.Hkv + h) * a.nch + chunk) * V + tid) * 2;
-        pt[0] = s_max[tid];
-        pt[1] = sv;
+        const double ev = live ? exp(zv - mv) : 0.0;
+        double sv = ev;
+        for (int off = 32; off >= 1; off >>= 1) sv += __shfl_xor(sv, off, 64);
+        if (live) lg[(size_t)v * a.cmax] = ev;
+        if (lane == 0) {
+            pt[v * 2] = mv;
+            pt[v * 2 + 1] = sv;
+        }
     }
 }
 
 // ------------------------------------------------------------------ weights --
+// Grid (chunks of kProbChunk candidates, KV head, boundary request).  The
+// statistics blocks are merged per view: M = max m_b, L = sum s_b exp(m_b - M);
+// then each block b of the chunk gets the factor f_b = exp(m_b - M) / L, and a
+// token's softmax weight in view (g, x) is its stored exp(z - m_b) times f_b.
+// The G query heads of a view are averaged in fp64 and rounded to float32.
 template <int G>
 __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
     constexpr int V = 2 * G;
+    constexpr int BPC = kProbChunk / kStatBlock;     // statistics blocks per chunk
     __shared__ double s_M[V], s_L[V];
+    __shared__ double s_f[BPC][V];
     const int chunk = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
     int r, P;
     if (!boundary_of(a, i, r, P)) return;
@@ -228,9 +230,9 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
     const int t0 = chunk * kProbChunk;
     if (t0 >= C) return;
     const int tid = threadIdx.x;
-    const int used = cdiv(C, kScoreChunk);
+    const int used = cdiv(C, kStatBlock);
     const double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch) * V * 2;
-    // merge the chunk statistics: 32 lanes per view, views 8 at a time
+    // merge the block statistics: 32 lanes per view, views 8 at a time
     for (int vb = 0; vb < V; vb += 8) {
         const int v = vb + tid / 32, c0 = tid % 32;
         if (v < V) {
@@ -248,11 +250,19 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
         }
     }
     __syncthreads();
+    const int b0 = t0 / kStatBlock;
+    for (int e = tid; e < BPC * V; e += blockDim.x) {
+        const int bb = e / V, v = e % V;
+        const int b = b0 + bb;
+        s_f[bb][v] = b < used ? exp(pt[((size_t)b * V + v) * 2] - s_M[v]) / s_L[v] : 0.0;
+    }
+    __syncthreads();
     const double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax;
     float *w = a.weights + ((size_t)i * a.Hkv + h) * 2 * a.cmax;
     float *sc = a.scores + ((size_t)i * a.Hkv + h) * a.max_cand;
     const int t_end = min(C, t0 + kProbChunk);
     for (int t = t0 + tid; t < t_end; t += blockDim.x) {
+        const int bb = (t - t0) / kStatBlock;
         float ax[2];
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
@@ -260,7 +270,7 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 const int v = x * G + g;
-                acc += exp(lg[(size_t)v * a.cmax + t] - s_M[v]) / s_L[v];
+                acc += lg[(size_t)v * a.cmax + t] * s_f[bb][v];
             }
             ax[x] = (float)(acc / G);
             w[(size_t)x * a.cmax + t] = ax[x];
@@ -425,7 +435,7 @@ __global__ __launch_bounds__(256) void entropy_kernel(ScoreArgs a) {
 
 template <typename T, int D>
 hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
-    dim3 g0(a.Hkv, a.Rb), g1(a.nch, a.Hkv, a.Rb), g2(cdiv(a.cmax, kProbChunk), a.Hkv, a.Rb), g3(2, a.Hkv, a.Rb);
+    dim3 g0(a.Hkv, a.Rb), g1(cdiv(a.cmax, kStatBlock), a.Hkv, a.Rb), g2(cdiv(a.cmax, kProbChunk), a.Hkv, a.Rb), g3(2, a.Hkv, a.Rb);
     if (a.cmax == 0) {
         // no request can have candidates: the counts are written as zero
         top_p_kernel<<<g3, 1024, 0, s>>>(a);
@@ -435,7 +445,7 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
 #define GP_CASE(GG)                                                   \
     case GG:                                                          \
         prep_kernel<T, D, GG><<<g0, 256, 0, s>>>(a);                  \
-        logits_kernel<T, D, GG><<<g1, 256, 0, s>>>(a);                \
+        logits_kernel<T, D, GG><<<g1, kStatBlock, 0, s>>>(a);                \
         weights_kernel<GG><<<g2, 256, 0, s>>>(a);                     \
         break;
         GP_CASE(1) GP_CASE(2) GP_CASE(4) GP_CASE(8)

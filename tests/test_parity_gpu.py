@@ -19,7 +19,7 @@ import torch
 import oracle as O
 import paper_2609_03494_amd as gp
 import workloads as W
-from _harness import (DeviceCase, PoolView, assert_rows_close, bf16_rounding_ok, oracle_state,
+from _harness import (DEV, DeviceCase, PoolView, assert_rows_close, bf16_rounding_ok, oracle_state,
                       row_index, threshold_band, to_numpy)
 
 pytestmark = pytest.mark.gpu
@@ -260,6 +260,36 @@ def test_decode_empty_request_gives_zero():
     ref = O.decode_attention(PoolView(w, "k"), PoolView(w, "v"), w.dtype, w.page_table, sl,
                              w.q_post, w.num_q_heads, scale, requests=[0, 2])
     assert_rows_close(got[[0, 2]], ref[[0, 2]], 2e-2, "decode bf16")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_decode_back_to_back_calls_see_their_own_partials(dtype):
+    """Requests of several chunks are merged by the workgroup that finishes
+    last, through partials that other workgroups wrote from other XCDs.  Two
+    calls with different queries alternate on one stream with no
+    synchronisation between them (same workspace, same partial slots); every
+    output must equal, bit for bit, that of the same call run alone."""
+    _say(f"decode: 64 alternating back-to-back calls, {dtype}, requests of 1..7 chunks")
+    w = W._build(name="b2b", seed=41, dtype=dtype, Hq=8 if dtype == "f32" else 32,
+                 Hkv=2 if dtype == "f32" else 8, d=128, n=np.array([5, 700, 1100, 2100, 3000, 4500, 5200, 6100]),
+                 budgets=None, free_pages=8, heavy_mode="scaled", heavy_frac=0.02, summary_mode="random")
+    dc = DeviceCase(w)
+    scale = float(np.float32(1 / math.sqrt(w.head_dim)))
+    gen = torch.Generator(device="cpu").manual_seed(5)
+    qs = [dc.q_post, (torch.randn(dc.q_post.shape, generator=gen) * 2).to(dc.q_post.dtype).to(DEV)]
+    alone = []
+    for q in qs:
+        out = torch.empty_like(q)
+        gp.gp_decode_attention(dc.layers[0], dc.ps, q, scale, out, dc.ws_decode)
+        torch.cuda.synchronize()
+        alone.append(out.clone())
+    assert not torch.equal(alone[0], alone[1])
+    outs = [torch.empty_like(qs[0]) for _ in range(64)]
+    for j, out in enumerate(outs):
+        gp.gp_decode_attention(dc.layers[0], dc.ps, qs[j % 2], scale, out, dc.ws_decode)
+    torch.cuda.synchronize()
+    for j, out in enumerate(outs):
+        assert torch.equal(out, alone[j % 2]), f"call {j}"
 
 
 @pytest.mark.parametrize("case", ["tiny_fp32", "qwen3_bf16", "g8_prefix_bf16"])
