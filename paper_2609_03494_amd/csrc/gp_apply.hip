@@ -3,7 +3,7 @@
 // Grow by One Page, Sec. 4.2 fallback, App. E.2 prefix-preserving compaction).
 //
 // Three kernels, in stream order:
-//  pre      grid (1 + compaction chunks, KV head x layer, boundary request).
+//  pre      grid (KV head x layer, 1 + compaction chunks, boundary request).
 //           Column 0 selects, for every request at a boundary, the tokens a
 //           compression would evict (the selection needs only the scores, so it
 //           does not wait for the decision).  The other columns save the rows
@@ -17,7 +17,7 @@
 //           page); then grows are applied, compressing requests get their new
 //           resident length, and shared pages are replaced by private ones, the
 //           old references dropped (pages reaching zero are listed).
-//  compact  per (chunk of 256 slots, KV head x layer, request): reads every row
+//  compact  per (KV head x layer, chunk of 256 slots, request): reads every row
 //           that moves (the border rows from the saved copy), then writes it to
 //           its new slot; in the shift layout rows move down by at most two
 //           pages (a shrink), so the only cross-chunk hazard is the one the
@@ -232,8 +232,8 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
 template <int D, int E>
 __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
     __shared__ int s_n;
-    const int x = blockIdx.x, i = blockIdx.z;
-    const int h = blockIdx.y % a.Hkv, l = blockIdx.y / a.Hkv;
+    const int x = blockIdx.y, i = blockIdx.z;
+    const int h = blockIdx.x % a.Hkv, l = blockIdx.x / a.Hkv;
     const int tid = threadIdx.x;
     const int r = a.bnd[i];
     int P = 0;
@@ -252,7 +252,7 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
     }
     const int cc = x - 1;
     const int32_t *row = a.page_table + (size_t)(at_boundary ? r : 0) * a.max_pages;
-    if (blockIdx.y == 0 && cc < a.npc) {
+    if (blockIdx.x == 0 && cc < a.npc) {
         // shared pages of block cc of the table row, as the call starts
         if (tid == 0) s_n = 0;
         __syncthreads();
@@ -484,11 +484,11 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
     __shared__ int s_dst[ROWS];
     __shared__ long long s_src_off[ROWS], s_dst_off[ROWS];
     __shared__ int s_rel[1024];
-    const int cc = blockIdx.x, i = blockIdx.z;
-    const int h = blockIdx.y % a.Hkv, l = blockIdx.y / a.Hkv;
+    const int cc = blockIdx.y, i = blockIdx.z;
+    const int h = blockIdx.x % a.Hkv, l = blockIdx.x / a.Hkv;
     const int tid = threadIdx.x;
 
-    if (cc == 0 && blockIdx.y == 0 && i == 0) {
+    if (cc == 0 && blockIdx.x == 0 && i == 0) {
         // pages released by this call go back on the stack, lowest id first
         const int n = a.hdr[HDR_NREL];
         const int fc1 = a.hdr[HDR_FC1];
@@ -608,7 +608,8 @@ __global__ __launch_bounds__(256) void release_kernel(int32_t *seq_lens, int R) 
 
 template <int D, int E>
 hipError_t launch_de(const ApplyArgs &a, const LayerTable &lt, int stages, hipStream_t s) {
-    dim3 gpre(1 + a.ncc, a.Hkv * a.n_layers, a.Rb), gcomp(a.ncc, a.Hkv * a.n_layers, a.Rb);
+    // (KV head, layer) is the fastest grid index: each head stays on one XCD
+    dim3 gpre(a.Hkv * a.n_layers, 1 + a.ncc, a.Rb), gcomp(a.Hkv * a.n_layers, a.ncc, a.Rb);
     if (stages & kStageSelect) pre_kernel<D, E><<<gpre, 1024, 0, s>>>(a, lt);
     if (stages & kStageDecide) decide_kernel<<<1, 1024, 0, s>>>(a);
     if (stages & kStageCompact) compact_kernel<D, E><<<gcomp, 256, 0, s>>>(a, lt);

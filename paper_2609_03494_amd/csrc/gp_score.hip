@@ -127,7 +127,7 @@ __global__ __launch_bounds__(256) void prep_kernel(ScoreArgs a) {
 }
 
 // ------------------------------------------------------------------- logits --
-// Grid (blocks of kStatBlock candidates, KV head, boundary request), one wave
+// Grid (KV head, blocks of kStatBlock candidates, boundary request), one wave
 // per workgroup, one candidate token per lane.  The lane reads its token's key
 // row once (all of it in flight at once) and parks it in LDS (rows padded to
 // avoid bank conflicts; a lane only ever reads its own row).  A loop over
@@ -150,7 +150,7 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
     static_assert(kStatBlock == 64, "one wave per statistics block");
     __shared__ uint4 s_k[kStatBlock * ROW];
 
-    const int blk = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    const int h = blockIdx.x, blk = blockIdx.y, i = blockIdx.z;
     const int lane = threadIdx.x;
     int r, P;
     if (!boundary_of(a, i, r, P)) return;
@@ -212,7 +212,7 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
 }
 
 // ------------------------------------------------------------------ weights --
-// Grid (chunks of kProbChunk candidates, KV head, boundary request).  The
+// Grid (KV head, chunks of kProbChunk candidates, boundary request).  The
 // statistics blocks are merged per view: M = max m_b, L = sum s_b exp(m_b - M);
 // then each block b of the chunk gets the factor f_b = exp(m_b - M) / L, and a
 // token's softmax weight in view (g, x) is its stored exp(z - m_b) times f_b.
@@ -223,7 +223,7 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
     constexpr int BPC = kProbChunk / kStatBlock;     // statistics blocks per chunk
     __shared__ double s_M[V], s_L[V];
     __shared__ double s_f[BPC][V];
-    const int chunk = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    const int h = blockIdx.x, chunk = blockIdx.y, i = blockIdx.z;
     int r, P;
     if (!boundary_of(a, i, r, P)) return;
     const int C = (P - 1) * kPage;
@@ -296,7 +296,7 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
     __shared__ unsigned long long s_above_mass;
     __shared__ unsigned int s_above_cnt;
 
-    const int x = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    const int h = blockIdx.x, x = blockIdx.y, i = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63;
     int32_t *out = a.k_counts + ((size_t)i * a.Hkv + h) * 2 + x;
     int r, P;
@@ -408,7 +408,7 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
 // to [1, |C|].
 __global__ __launch_bounds__(256) void entropy_kernel(ScoreArgs a) {
     __shared__ double s_red[4];
-    const int x = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+    const int h = blockIdx.x, x = blockIdx.y, i = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     int32_t *out = a.k_counts + ((size_t)i * a.Hkv + h) * 2 + x;
     int r, P;
@@ -435,7 +435,10 @@ __global__ __launch_bounds__(256) void entropy_kernel(ScoreArgs a) {
 
 template <typename T, int D>
 hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
-    dim3 g0(a.Hkv, a.Rb), g1(cdiv(a.cmax, kStatBlock), a.Hkv, a.Rb), g2(cdiv(a.cmax, kProbChunk), a.Hkv, a.Rb), g3(2, a.Hkv, a.Rb);
+    // the KV head is the fastest grid index everywhere: workgroups are handed to
+    // the XCDs round-robin, so head h's workgroups all run on one XCD and read
+    // back what the previous kernel left in that XCD's L2
+    dim3 g0(a.Hkv, a.Rb), g1(a.Hkv, cdiv(a.cmax, kStatBlock), a.Rb), g2(a.Hkv, cdiv(a.cmax, kProbChunk), a.Rb), g3(a.Hkv, 2, a.Rb);
     if (a.cmax == 0) {
         // no request can have candidates: the counts are written as zero
         top_p_kernel<<<g3, 1024, 0, s>>>(a);
