@@ -17,7 +17,7 @@
 //           page); then grows are applied, compressing requests get their new
 //           resident length, and shared pages are replaced by private ones, the
 //           old references dropped (pages reaching zero are listed).
-//  compact  per (KV head x layer, chunk of 256 slots, request): reads every row
+//  compact  per (K or V x KV head x layer, chunk of 256 slots, request): reads every row
 //           that moves (the border rows from the saved copy), then writes it to
 //           its new slot; in the shift layout rows move down by at most two
 //           pages (a shrink), so the only cross-chunk hazard is the one the
@@ -475,17 +475,31 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
 }
 
 // ---------------------------------------------------------------- compact --
+// Grid (2 x KV head x layer, chunk of kCompactChunk slots, boundary request):
+// the lowest bit of x picks K or V, so each workgroup moves one of them.  The
+// kernel sits on the step's critical path and its work is small, so it is
+// built around few memory round trips: (1) the decision, the request id and
+// both eviction lists, (2) every page-table entry the chunk can need (its
+// source pages in the old and the current table row, the destination range of
+// the shift layout, the pages of the evicted slots for the fill layout),
+// (3) the rows themselves, then the stores.
 template <int D, int E>
 __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt) {
-    constexpr int UPR = D * E / 16;
+    constexpr int UPR = D * E / 16;                 // 16-byte units per row
     constexpr int ROWS = kCompactChunk;
     constexpr int UNITS = ROWS * UPR / 256;         // 16-byte units per thread
+    constexpr int PPC = ROWS / kPage;               // pages per chunk
+    constexpr int NBP = kShrinkEvict / kPage;       // pages a row can move down by
     __shared__ int s_ev[kShrinkEvict];
     __shared__ int s_dst[ROWS];
     __shared__ long long s_src_off[ROWS], s_dst_off[ROWS];
     __shared__ int s_rel[1024];
+    __shared__ int s_src_pg[PPC];                   // source page of each chunk page
+    __shared__ int s_lo_pg[NBP + PPC];              // current row, pages [s0/16 - NBP, s0/16 + PPC)
+    __shared__ int s_ev_pg[kShrinkEvict];           // current row, page of each evicted slot
     const int cc = blockIdx.y, i = blockIdx.z;
-    const int h = blockIdx.x % a.Hkv, l = blockIdx.x / a.Hkv;
+    const int kv = blockIdx.x & 1;
+    const int h = (blockIdx.x >> 1) % a.Hkv, l = (blockIdx.x >> 1) / a.Hkv;
     const int tid = threadIdx.x;
 
     if (cc == 0 && blockIdx.x == 0 && i == 0) {
@@ -509,20 +523,41 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
         }
     }
 
+    // (1) decision, request, both eviction lists (the shrink list starts at kPage)
     const int32_t *rq = a.req + (size_t)i * RQ_STRIDE;
-    const int dec = rq[RQ_DEC];
+    const int dec = rq[RQ_DEC], P = rq[RQ_P], nsh = rq[RQ_NSH];
+    const int r = a.bnd[i];
+    const int32_t *evl = a.evict + (((size_t)l * a.Rb + i) * a.Hkv + h) * kEvictSlots;
+    int ev_c = -1, ev_s = -1;
+    if (tid < kShrinkEvict) {
+        ev_s = evl[kPage + tid];
+        if (tid < kPage) ev_c = evl[tid];
+    }
     const bool shrink = dec == GP_SHRINK;
     if (!compressing(dec) && !shrink) return;
-    const int r = rq[RQ_R], P = rq[RQ_P], nsh = rq[RQ_NSH];
+    if (r < 0 || r >= a.R) return;
     const int nev = shrink ? kShrinkEvict : kPage;
     const int total = P * kPage;
     const int s0 = cc * ROWS;
     if (s0 >= total) return;
+    const int ev_mine = shrink ? ev_s : ev_c;
+    if (tid < kShrinkEvict) s_ev[tid] = tid < nev ? ev_mine : -1;
+
+    // (2) page-table entries
     const int32_t *row = a.page_table + (size_t)r * a.max_pages;
     const int32_t *src_row = nsh > 0 || shrink ? a.old_table + (size_t)i * a.max_pages : row;
-    if (tid < kShrinkEvict)
-        s_ev[tid] = tid < nev ? a.evict[(((size_t)l * a.Rb + i) * a.Hkv + h) * kEvictSlots + (shrink ? kPage : 0) + tid]
-                              : -1;
+    const int pg0 = s0 / kPage;
+    if (tid < kShrinkEvict) {
+        // thread k holds evicted slot k
+        const int ev = tid < nev ? ev_mine : -1;
+        s_ev_pg[tid] = ev >= 0 && ev / kPage < P ? row[ev / kPage] : -1;
+    } else if (tid < kShrinkEvict + PPC) {
+        const int k = tid - kShrinkEvict, j = pg0 + k;
+        s_src_pg[k] = j < P ? src_row[j] : -1;
+    } else if (tid < kShrinkEvict + 2 * PPC + NBP) {
+        const int k = tid - kShrinkEvict - PPC, j = pg0 - NBP + k;
+        s_lo_pg[k] = j >= 0 && j < P ? row[j] : -1;
+    }
     __syncthreads();
 
     const size_t page_bytes = (size_t)a.Hkv * kPage * D * E;
@@ -546,9 +581,14 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
                 // shift: down past the evicted slots below.  fill: rows below T
                 // stay; the k-th survivor at or above T takes the k-th evicted
                 // slot (the list is sorted, so the slots below T come first).
-                const int rank = s - T - between;
-                const int d = !fill ? s - before : (s < T ? s : s_ev[min(max(rank, 0), kShrinkEvict - 1)]);
-                const int sp = src_row[s / kPage], dp = d >= 0 ? row[d / kPage] : -1;
+                const int rank = min(max(s - T - between, 0), kShrinkEvict - 1);
+                const int d = !fill ? s - before : (s < T ? s : s_ev[rank]);
+                const int sp = s_src_pg[tid / kPage];
+                int dp = -1;
+                if (d >= 0) {
+                    if (!fill || s < T) dp = s_lo_pg[d / kPage - (pg0 - NBP)];   // d in [s0 - 32, s0 + ROWS)
+                    else dp = s_ev_pg[rank];
+                }
                 const bool ok = sp >= 0 && sp < a.pool_pages && dp >= 0 && dp < a.pool_pages;
                 const long long so = (long long)sp * page_bytes + head_bytes + (long long)(s % kPage) * D * E;
                 const long long dof = (long long)dp * page_bytes + head_bytes + (long long)(d % kPage) * D * E;
@@ -563,36 +603,31 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
     }
     if (!__syncthreads_or(dst >= 0)) return;   // nothing moves in this chunk
 
+    // (3) the rows: all loads, then all stores (rows move down within the chunk)
     const unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc) * 2 * kBorderRows * D * E;
-    unsigned char *pools[2] = {reinterpret_cast<unsigned char *>(lt.k[l]),
-                               reinterpret_cast<unsigned char *>(lt.v[l])};
+    unsigned char *pool = reinterpret_cast<unsigned char *>(kv == 0 ? lt.k[l] : lt.v[l]);
+    uint4 val[UNITS];
 #pragma unroll
-    for (int kv = 0; kv < 2; ++kv) {
-        unsigned char *pool = pools[kv];
-        uint4 val[UNITS];
-#pragma unroll
-        for (int k = 0; k < UNITS; ++k) {
-            const int u = k * 256 + tid;
-            const int rr = u / UPR, w = u % UPR;
-            val[k] = make_uint4(0u, 0u, 0u, 0u);
-            if (s_dst[rr] >= 0) {
-                if (has_border && rr >= ROWS - kBorderRows) {
-                    const unsigned char *src = bd + ((size_t)(cc + 1) * 2 + kv) * kBorderRows * D * E +
-                                               (size_t)(rr - (ROWS - kBorderRows)) * D * E + (size_t)w * 16;
-                    val[k] = *reinterpret_cast<const uint4 *>(src);
-                } else {
-                    val[k] = *reinterpret_cast<const uint4 *>(pool + s_src_off[rr] + (size_t)w * 16);
-                }
+    for (int k = 0; k < UNITS; ++k) {
+        const int u = k * 256 + tid;
+        const int rr = u / UPR, w = u % UPR;
+        val[k] = make_uint4(0u, 0u, 0u, 0u);
+        if (s_dst[rr] >= 0) {
+            if (has_border && rr >= ROWS - kBorderRows) {
+                const unsigned char *src = bd + ((size_t)(cc + 1) * 2 + kv) * kBorderRows * D * E +
+                                           (size_t)(rr - (ROWS - kBorderRows)) * D * E + (size_t)w * 16;
+                val[k] = *reinterpret_cast<const uint4 *>(src);
+            } else {
+                val[k] = *reinterpret_cast<const uint4 *>(pool + s_src_off[rr] + (size_t)w * 16);
             }
         }
-        __syncthreads();
+    }
+    __syncthreads();
 #pragma unroll
-        for (int k = 0; k < UNITS; ++k) {
-            const int u = k * 256 + tid;
-            const int rr = u / UPR, w = u % UPR;
-            if (s_dst[rr] >= 0) *reinterpret_cast<uint4 *>(pool + s_dst_off[rr] + (size_t)w * 16) = val[k];
-        }
-        __syncthreads();
+    for (int k = 0; k < UNITS; ++k) {
+        const int u = k * 256 + tid;
+        const int rr = u / UPR, w = u % UPR;
+        if (s_dst[rr] >= 0) *reinterpret_cast<uint4 *>(pool + s_dst_off[rr] + (size_t)w * 16) = val[k];
     }
 }
 
@@ -609,7 +644,7 @@ __global__ __launch_bounds__(256) void release_kernel(int32_t *seq_lens, int R) 
 template <int D, int E>
 hipError_t launch_de(const ApplyArgs &a, const LayerTable &lt, int stages, hipStream_t s) {
     // (KV head, layer) is the fastest grid index: each head stays on one XCD
-    dim3 gpre(a.Hkv * a.n_layers, 1 + a.ncc, a.Rb), gcomp(a.Hkv * a.n_layers, a.ncc, a.Rb);
+    dim3 gpre(a.Hkv * a.n_layers, 1 + a.ncc, a.Rb), gcomp(2 * a.Hkv * a.n_layers, a.ncc, a.Rb);
     if (stages & kStageSelect) pre_kernel<D, E><<<gpre, 1024, 0, s>>>(a, lt);
     if (stages & kStageDecide) decide_kernel<<<1, 1024, 0, s>>>(a);
     if (stages & kStageCompact) compact_kernel<D, E><<<gcomp, 256, 0, s>>>(a, lt);

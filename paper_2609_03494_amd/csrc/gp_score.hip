@@ -221,6 +221,8 @@ template <int G>
 __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
     constexpr int V = 2 * G;
     constexpr int BPC = kProbChunk / kStatBlock;     // statistics blocks per chunk
+    constexpr int TPT = kProbChunk / 256;            // tokens per thread
+    constexpr int NPL = 4;                           // statistics blocks per lane kept in registers
     __shared__ double s_M[V], s_L[V];
     __shared__ double s_f[BPC][V];
     const int h = blockIdx.x, chunk = blockIdx.y, i = blockIdx.z;
@@ -231,37 +233,61 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
     if (t0 >= C) return;
     const int tid = threadIdx.x;
     const int used = cdiv(C, kStatBlock);
+    const int b0 = t0 / kStatBlock;
     const double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch) * V * 2;
-    // merge the block statistics: 32 lanes per view, views 8 at a time
+    const double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax;
+
+    // The kernel runs beside decode attention, where every memory round trip
+    // is slow: the exponentials of this thread's tokens and the statistics
+    // are all requested before any of them is used.
+    double e[TPT][V];
+#pragma unroll
+    for (int k = 0; k < TPT; ++k) {
+        const int t = t0 + k * 256 + tid;
+#pragma unroll
+        for (int v = 0; v < V; ++v) e[k][v] = t < C ? lg[(size_t)v * a.cmax + t] : 0.0;
+    }
+    // merge the block statistics: 32 lanes per view, views 8 at a time; lane
+    // c0 holds blocks c0, c0 + 32, ... (the first NPL of them in registers)
     for (int vb = 0; vb < V; vb += 8) {
         const int v = vb + tid / 32, c0 = tid % 32;
         if (v < V) {
+            double mk[NPL], sk[NPL];
+#pragma unroll
+            for (int k = 0; k < NPL; ++k) {
+                const int c = c0 + 32 * k;
+                mk[k] = c < used ? pt[((size_t)c * V + v) * 2] : -__builtin_huge_val();
+                sk[k] = c < used ? pt[((size_t)c * V + v) * 2 + 1] : 0.0;
+            }
             double M = -__builtin_huge_val();
-            for (int c = c0; c < used; c += 32) M = fmax(M, pt[((size_t)c * V + v) * 2]);
+#pragma unroll
+            for (int k = 0; k < NPL; ++k) M = fmax(M, mk[k]);
+            for (int c = c0 + 32 * NPL; c < used; c += 32) M = fmax(M, pt[((size_t)c * V + v) * 2]);
             for (int off = 16; off >= 1; off >>= 1) M = fmax(M, __shfl_xor(M, off, 32));
             double L = 0.0;
-            for (int c = c0; c < used; c += 32)
+#pragma unroll
+            for (int k = 0; k < NPL; ++k)
+                if (c0 + 32 * k < used) L += sk[k] * exp(mk[k] - M);
+            for (int c = c0 + 32 * NPL; c < used; c += 32)
                 L += pt[((size_t)c * V + v) * 2 + 1] * exp(pt[((size_t)c * V + v) * 2] - M);
             for (int off = 16; off >= 1; off >>= 1) L += __shfl_xor(L, off, 32);
-            if (c0 == 0) {
-                s_M[v] = M;
-                s_L[v] = L;
+            // factors of the chunk's blocks: f_b = exp(m_b - M) / L
+#pragma unroll
+            for (int k = 0; k < NPL; ++k) {
+                const int c = c0 + 32 * k;
+                if (c < used && c >= b0 && c < b0 + BPC) s_f[c - b0][v] = exp(mk[k] - M) / L;
             }
+            for (int c = c0 + 32 * NPL; c < used; c += 32)
+                if (c >= b0 && c < b0 + BPC) s_f[c - b0][v] = exp(pt[((size_t)c * V + v) * 2] - M) / L;
         }
     }
     __syncthreads();
-    const int b0 = t0 / kStatBlock;
-    for (int e = tid; e < BPC * V; e += blockDim.x) {
-        const int bb = e / V, v = e % V;
-        const int b = b0 + bb;
-        s_f[bb][v] = b < used ? exp(pt[((size_t)b * V + v) * 2] - s_M[v]) / s_L[v] : 0.0;
-    }
-    __syncthreads();
-    const double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax;
     float *w = a.weights + ((size_t)i * a.Hkv + h) * 2 * a.cmax;
     float *sc = a.scores + ((size_t)i * a.Hkv + h) * a.max_cand;
-    const int t_end = min(C, t0 + kProbChunk);
-    for (int t = t0 + tid; t < t_end; t += blockDim.x) {
+#pragma unroll
+    for (int k = 0; k < TPT; ++k) {
+        const int t = t0 + k * 256 + tid;
+        if (t >= C) continue;
         const int bb = (t - t0) / kStatBlock;
         float ax[2];
 #pragma unroll
@@ -270,7 +296,7 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 const int v = x * G + g;
-                acc += lg[(size_t)v * a.cmax + t] * s_f[bb][v];
+                acc += e[k][v] * s_f[bb][v];
             }
             ax[x] = (float)(acc / G);
             w[(size_t)x * a.cmax + t] = ax[x];
@@ -286,8 +312,8 @@ __device__ inline unsigned long long fixed60(uint32_t bits) {
 // -------------------------------------------------------------------- top-p --
 // One workgroup of 1024 threads per (boundary request, KV head, view).  Each of
 // the three radix passes histograms the weights that share the prefix found so
-// far (count and 2^-60 fixed-point mass per bucket), then wave 0 scans the
-// buckets from the top to find the one where the running mass reaches p.
+// far (count and 2^-60 fixed-point mass per bucket), then the workgroup scans
+// the buckets from the top to find the one where the running mass reaches p.
 __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
     constexpr int NB = 2048;
     __shared__ unsigned int s_cnt[NB];
@@ -295,6 +321,8 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
     __shared__ int s_bucket;
     __shared__ unsigned long long s_above_mass;
     __shared__ unsigned int s_above_cnt;
+    __shared__ unsigned long long s_wmass[16];
+    __shared__ unsigned int s_wcnt[16];
 
     const int h = blockIdx.x, x = blockIdx.y, i = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -308,6 +336,14 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
     const float *wv = a.weights + (((size_t)i * a.Hkv + h) * 2 + x) * a.cmax;
     const unsigned long long target = (unsigned long long)ldexp(a.p, 60);
 
+    // the first 4 * 1024 weights stay in registers across the passes (every
+    // candidate set up to 4096 tokens); longer ones re-read the rest
+    uint32_t cached[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int t = k * 1024 + tid;
+        cached[k] = t < C ? __float_as_uint(wv[t]) : 0xffffffffu;
+    }
     uint32_t prefix = 0;
     unsigned long long above_mass = 0;
     unsigned int above_cnt = 0;
@@ -325,7 +361,7 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int t = base + k * 1024 + tid;
-                u[k] = t < C ? __float_as_uint(wv[t]) : 0xffffffffu;
+                u[k] = base == 0 ? cached[k] : (t < C ? __float_as_uint(wv[t]) : 0xffffffffu);
             }
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -337,16 +373,22 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
             }
         }
         __syncthreads();
-        if (tid < 64) {
-            // lane owns nb/64 consecutive buckets, lane 0 the highest
-            const int per = nb / 64;
-            const int hi = nb - 1 - lane * per;
+        // Scan of the buckets from the highest down, over the whole workgroup:
+        // thread t owns descending positions [t * per, (t + 1) * per).  The
+        // thread whose range holds the position where the running mass first
+        // reaches the mass still needed names that bucket, with the count and
+        // mass strictly above it.
+        {
+            const int per = nb >= 1024 ? nb / 1024 : 1;
+            const bool owns = tid * per < nb;
             unsigned long long mm = 0;
             unsigned int cc = 0;
-            for (int k = 0; k < per; ++k) {
-                mm += s_mass[hi - k];
-                cc += s_cnt[hi - k];
-            }
+            if (owns)
+                for (int k = 0; k < per; ++k) {
+                    const int b = nb - 1 - (tid * per + k);
+                    mm += s_mass[b];
+                    cc += s_cnt[b];
+                }
             unsigned long long im = mm;
             unsigned int ic = cc;
             for (int off = 1; off < 64; off <<= 1) {
@@ -357,16 +399,24 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
                     ic += yc;
                 }
             }
+            if (lane == 63) {
+                s_wmass[tid >> 6] = im;
+                s_wcnt[tid >> 6] = ic;
+            }
+            __syncthreads();
+            for (int w = 0; w < (tid >> 6); ++w) {
+                im += s_wmass[w];
+                ic += s_wcnt[w];
+            }
             const unsigned long long need = target > above_mass ? target - above_mass : 0ull;
             const unsigned long long em = im - mm;
             const unsigned int ec = ic - cc;
-            const unsigned long long total = __shfl(im, 63, 64);
-            if (lane == 0 && total < need) s_bucket = -1;
-            if (em < need && im >= need) {
+            if (tid == 1023 && im < need) s_bucket = -1;    // the candidates fall short of p
+            if (owns && em < need && im >= need) {
                 unsigned long long cum = em;
                 unsigned int cnt = ec;
                 for (int k = 0; k < per; ++k) {
-                    const int b = hi - k;
+                    const int b = nb - 1 - (tid * per + k);
                     if (cum + s_mass[b] >= need) {
                         s_bucket = b;
                         s_above_mass = cum;
