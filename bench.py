@@ -39,10 +39,29 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 
+# workload name -> (metric suffix, description)
+WORKLOADS = {
+    "qwen3_8b": ("Qwen3-8B layer shape",
+                 "qwen3_8b_layer: 64 requests, 32 q / 8 kv heads, d 128, page 16, lengths U[1024,8192] "
+                 "under page budgets {64,128,256}, 4 at a boundary, 200k free pages"),
+    "long_reasoning": ("long-reasoning shape",
+                       "long_reasoning: 32 requests, 32 q / 8 kv heads, d 128, page 16, lengths "
+                       "U[16384,32768], all at a boundary, heavy fraction per request in {0.1%,1%,10%}, "
+                       "200k free pages"),
+    "high_concurrency": ("high-concurrency shape",
+                         "high_concurrency: 256 requests, 32 q / 8 kv heads, d 128, page 16, lognormal "
+                         "lengths (median 2048, sigma 0.8, [256,16384]), 1/8 at a boundary, pool 1.1x use"),
+    "prefix_shared": ("prefix-shared Qwen3-32B layer shape",
+                      "prefix_shared: 128 requests, 64 q / 8 kv heads, d 128, page 16, a 2048-token shared "
+                      "prefix then private tails U[512,8192], 1/16 at a boundary, 200k free pages"),
+}
+
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--workload", default="qwen3_8b", choices=sorted(WORKLOADS),
+                    help="qwen3_8b is the benchmark; the others report the same fields at their shapes")
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
@@ -72,7 +91,7 @@ def main():
 
     gp.load()
     dev = "cuda"
-    w = W.qwen3_8b()
+    w = W.make(args.workload)
     R, Hq, Hkv, d, b = w.num_reqs, w.num_q_heads, w.num_kv_heads, w.head_dim, w.page_size
     e = 2
     dt = torch.bfloat16
@@ -283,7 +302,7 @@ def main():
     # the same state and see the same seeded tokens; the W + K steps are two
     # HIP graphs (inputs picked by a device-side step counter).
     loop = serving_loops(args, gp, W, w, kv, ps, meta, meta0, qstate, slots, positions, params, k, v) \
-        if args.loop_steps > 0 else None
+        if args.loop_steps > 0 and args.workload == "qwen3_8b" else None
 
     # algorithmic bytes
     m = w.seq_lens.astype(np.int64)
@@ -293,8 +312,14 @@ def main():
     gbs = step_bytes / (step_ms * 1e-3) / 1e9
     dec_gbs = decode_bytes / (decode_ms * 1e-3) / 1e9
 
+    # resident (page, slot) pairs counted once: pages shared by a common prefix
+    # are read by every request that holds them, but held in HBM once
+    slots_all = np.concatenate([w.page_table[r][np.arange(int(w.seq_lens[r])) // b].astype(np.int64) * b
+                                + np.arange(int(w.seq_lens[r])) % b for r in range(R)])
+    unique_bytes = int(np.unique(slots_all).size) * Hkv * d * e * 2
+
     traffic = None
-    if os.path.exists(args.traffic_json):
+    if args.workload == "qwen3_8b" and os.path.exists(args.traffic_json):
         with open(args.traffic_json) as f:
             tj = json.load(f)
         if tj.get("kernel_source_hash") == _kernel_hash():
@@ -314,7 +339,7 @@ def main():
         cpu = cpu_baseline(w, args.cpu_seconds)
 
     line = {
-        "metric": "decode attn GB/s (% of HBM peak) + boundary events/s, Qwen3-8B layer shape",
+        "metric": "decode attn GB/s (% of HBM peak) + boundary events/s, " + WORKLOADS[args.workload][0],
         "value": round(gbs, 1),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -326,14 +351,13 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) K/V/q with 1% heavy keys; no model weights)",
-        "config": {"workload": "qwen3_8b_layer: 64 requests, 32 q / 8 kv heads, d 128, page 16, "
-                               "lengths U[1024,8192] under page budgets {64,128,256}, 4 at a boundary, "
-                               "200k free pages",
+        "config": {"workload": WORKLOADS[args.workload][1],
                    "resident_tokens": int(m.sum()), "boundary_requests": Rb},
         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
         "launch": "eager" if args.eager else "one HIP graph per step",
         "decode_attention": {"ms": round(decode_ms, 4), "GB/s": round(dec_gbs, 1),
                              "hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4), "bytes": decode_bytes,
+                             "unique_kv_bytes": unique_bytes,
                              "ms_inside_step": round(inline_decode_ms, 4),
                              "with_summaries_one_launch_ms": round(fused_ms, 4),
                              "with_summaries_two_launches_ms": round(separate_ms, 4)},

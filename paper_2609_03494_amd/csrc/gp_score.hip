@@ -34,23 +34,20 @@ template <>
 __device__ inline double ld<uint16_t>(const uint16_t *p) { return (double)bf16_to_f32(*p); }
 
 template <typename T>
-struct KRow;
-// Elements g*4 .. g*4+3 of a key row held as 16-byte units (g uniform).
+struct KRow;   // one element of a 16-byte unit of a key row, widened to fp64
 template <>
 struct KRow<uint16_t> {
     static constexpr int EPV = 8;
-    __device__ static inline void get_group(const uint4 *row, int g, double *f) {
-        const uint2 u = reinterpret_cast<const uint2 *>(row)[g];
-        f[0] = bf16_lo(u.x); f[1] = bf16_hi(u.x); f[2] = bf16_lo(u.y); f[3] = bf16_hi(u.y);
+    __device__ static inline double elem(const uint4 &u, int e) {
+        const uint32_t w = e < 2 ? u.x : e < 4 ? u.y : e < 6 ? u.z : u.w;
+        return (e & 1) ? bf16_hi(w) : bf16_lo(w);
     }
 };
 template <>
 struct KRow<float> {
     static constexpr int EPV = 4;
-    __device__ static inline void get_group(const uint4 *row, int g, double *f) {
-        const uint4 u = row[g];
-        f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y);
-        f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
+    __device__ static inline double elem(const uint4 &u, int e) {
+        return __uint_as_float(e == 0 ? u.x : e == 1 ? u.y : e == 2 ? u.z : u.w);
     }
 };
 
@@ -128,30 +125,31 @@ __global__ __launch_bounds__(256) void prep_kernel(ScoreArgs a) {
 
 // ------------------------------------------------------------------- logits --
 // Grid (KV head, blocks of kStatBlock candidates, boundary request), one wave
-// per workgroup, one candidate token per lane.  The lane reads its token's key
-// row once (all of it in flight at once) and parks it in LDS (rows padded to
-// avoid bank conflicts; a lane only ever reads its own row).  A loop over
-// groups of four head dimensions then forms the 2G logits with fp64 fused
-// multiply-adds: the loop counter and the summary addresses are wave-uniform,
-// so the 2G * 4 summary values of a group are scalar loads used directly as
-// FMA operands, with no LDS or vector-register traffic for them.  The block's
-// max m and sum of exp(z - m) per view go to the statistics array; the logits
-// array receives exp(z - m), so that the weights need a product, not an
-// exponential, per token.  A lane whose page id is invalid contributes zero
-// logits.
+// per workgroup.  The 2G x D logits of the block are a small fp64 matrix
+// product, done on the matrix cores with v_mfma_f64_16x16x4f64: the A operand
+// is the aligned summaries (row = view, padded to 16 rows with zeros), B the
+// keys of 16 candidates, so the block is four chains of D/4 MFMAs.  The
+// contraction over head dimensions is split four ways across lane groups: in
+// step s, lane group q (lanes 16q .. 16q+15) supplies dimension (D/4) q + s,
+// so each lane reads one contiguous quarter row of summaries (once) and of
+// each of its four keys.  The result leaves view 4j + q of candidate l % 16 in
+// register j of lane l.  Per view, the block's max m and sum of exp(z - m)
+// (16-lane reductions) go to the statistics array; the logits array receives
+// exp(z - m), so that the weights need a product, not an exponential, per
+// token.  A lane whose page id is invalid contributes zero logits.
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
 template <typename T, int D, int G>
 __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
     constexpr int V = 2 * G;
-    constexpr int EPV = KRow<T>::EPV;
-    constexpr int NV = D / EPV;                      // 16-byte units per key row
-    constexpr int ROW = NV + 1;                      // staged row stride, 16-byte units
-    constexpr int DG = 4;                            // head dimensions per loop step
-    constexpr int NG = D / DG;
-    static_assert(kStatBlock == 64, "one wave per statistics block");
-    __shared__ uint4 s_k[kStatBlock * ROW];
+    constexpr int S = D / 4;                         // MFMA steps (head dimensions per lane group)
+    constexpr int EPU = 16 / sizeof(T);              // key elements per 16-byte unit
+    constexpr int NU = S / EPU;                      // 16-byte units of a quarter key row
+    constexpr int NGRP = kStatBlock / 16;            // candidate groups of 16 per block
+    static_assert(kStatBlock == 64 && V <= 16 && S % EPU == 0, "layout");
 
     const int h = blockIdx.x, blk = blockIdx.y, i = blockIdx.z;
-    const int lane = threadIdx.x;
+    const int lane = threadIdx.x, col = lane & 15, q = lane >> 4;
     int r, P;
     if (!boundary_of(a, i, r, P)) return;
     const int C = (P - 1) * kPage;
@@ -160,51 +158,72 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
     const int slot = a.slot_ids[r];
     if (slot < 0 || slot >= a.M) return;
 
-    const int t = t0 + lane;
-    const bool live = t < C;
-    uint4 krow[NV];
+    // A: this lane's quarter row of summary `col` (zero rows pad the views to 16)
+    const double *qt = a.qt + (((size_t)i * a.Hkv + h) * V + col) * D + q * S;
+    double qa[S];
 #pragma unroll
-    for (int u = 0; u < NV; ++u) krow[u] = make_uint4(0u, 0u, 0u, 0u);
-    if (live) {
-        const int phys = a.page_table[(size_t)r * a.max_pages + t / kPage];
-        if (phys >= 0 && phys < a.pool_pages) {
-            const uint4 *kp = reinterpret_cast<const uint4 *>(reinterpret_cast<const T *>(a.k) +
-                              (((size_t)phys * a.Hkv + h) * kPage + (t % kPage)) * D);
-#pragma unroll
-            for (int u = 0; u < NV; ++u) krow[u] = kp[u];
+    for (int s2 = 0; s2 < S; s2 += 2) {
+        if (col < V) {
+            const double2 u = *reinterpret_cast<const double2 *>(qt + s2);
+            qa[s2] = u.x;
+            qa[s2 + 1] = u.y;
+        } else {
+            qa[s2] = 0.0;
+            qa[s2 + 1] = 0.0;
         }
     }
-    uint4 *myrow = s_k + lane * ROW;
+    // B: this lane's quarter row of candidate t0 + 16 g + col, for the 4 groups
+    uint4 kb[NGRP][NU];
 #pragma unroll
-    for (int u = 0; u < NV; ++u) myrow[u] = krow[u];
-
-    const double *__restrict__ qt = a.qt + ((size_t)i * a.Hkv + h) * V * D;
-    double z[V];
+    for (int g = 0; g < NGRP; ++g) {
+        const int t = t0 + 16 * g + col;
+        int phys = -1;
+        if (t < C) phys = a.page_table[(size_t)r * a.max_pages + t / kPage];
+        const bool ok = phys >= 0 && phys < a.pool_pages;
+        const uint4 *kp = reinterpret_cast<const uint4 *>(reinterpret_cast<const T *>(a.k) +
+                          (((size_t)(ok ? phys : 0) * a.Hkv + h) * kPage + (t % kPage)) * D + q * S);
 #pragma unroll
-    for (int v = 0; v < V; ++v) z[v] = 0.0;
-#pragma unroll 1
-    for (int g = 0; g < NG; ++g) {
-        double kf[DG];
-        KRow<T>::get_group(myrow, g, kf);
-        const double *qg = qt + g * DG;
+        for (int u = 0; u < NU; ++u) kb[g][u] = ok ? kp[u] : make_uint4(0u, 0u, 0u, 0u);
+    }
+    f64x4_t acc[NGRP];
 #pragma unroll
-        for (int e = 0; e < DG; ++e)
+    for (int g = 0; g < NGRP; ++g) acc[g] = f64x4_t{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-            for (int v = 0; v < V; ++v) z[v] = fma(qg[v * D + e], kf[e], z[v]);
+    for (int s2 = 0; s2 < S; ++s2) {
+#pragma unroll
+        for (int g = 0; g < NGRP; ++g) {
+            const double b = KRow<T>::elem(kb[g][s2 / EPU], s2 % EPU);
+            acc[g] = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[s2], b, acc[g], 0, 0, 0);
+        }
     }
 
-    double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax + t;
+    // statistics and exponentials per view (register j holds view 4j + q)
+    double *lgv = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax;
     double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch + blk) * V * 2;
 #pragma unroll
-    for (int v = 0; v < V; ++v) {
-        const double zv = z[v] * a.scale;
-        double mv = live ? zv : -__builtin_huge_val();
-        for (int off = 32; off >= 1; off >>= 1) mv = fmax(mv, __shfl_xor(mv, off, 64));
-        const double ev = live ? exp(zv - mv) : 0.0;
-        double sv = ev;
-        for (int off = 32; off >= 1; off >>= 1) sv += __shfl_xor(sv, off, 64);
-        if (live) lg[(size_t)v * a.cmax] = ev;
-        if (lane == 0) {
+    for (int j = 0; j < 4; ++j) {
+        const int v = 4 * j + q;
+        if (4 * j >= V) break;                       // uniform: no real view in this register
+        double z[NGRP];
+        double mv = -__builtin_huge_val();
+#pragma unroll
+        for (int g = 0; g < NGRP; ++g) {
+            z[g] = acc[g][j] * a.scale;
+            if (t0 + 16 * g + col < C) mv = fmax(mv, z[g]);
+        }
+        for (int off = 8; off >= 1; off >>= 1) mv = fmax(mv, __shfl_xor(mv, off, 16));
+        double sv = 0.0;
+#pragma unroll
+        for (int g = 0; g < NGRP; ++g) {
+            const int t = t0 + 16 * g + col;
+            if (t < C && v < V) {
+                const double ev = exp(z[g] - mv);
+                sv += ev;
+                lgv[(size_t)v * a.cmax + t] = ev;
+            }
+        }
+        for (int off = 8; off >= 1; off >>= 1) sv += __shfl_xor(sv, off, 16);
+        if (col == 0 && v < V) {
             pt[v * 2] = mv;
             pt[v * 2 + 1] = sv;
         }
