@@ -302,7 +302,7 @@ def main():
     # the same state and see the same seeded tokens; the W + K steps are two
     # HIP graphs (inputs picked by a device-side step counter).
     loop = serving_loops(args, gp, W, w, kv, ps, meta, meta0, qstate, slots, positions, params, k, v) \
-        if args.loop_steps > 0 and args.workload == "qwen3_8b" else None
+        if args.loop_steps > 0 else None
 
     # algorithmic bytes
     m = w.seq_lens.astype(np.int64)
@@ -494,7 +494,7 @@ def serving_loops(args, gp, W, w, kv, ps, meta, meta0, qstate, slots, positions,
     del snap
     res["steps"] = n_steps
     res["async_speedup"] = round(res["async"]["tokens_per_s"] / res["sync"]["tokens_per_s"], 4)
-    res["note"] = ("one layer of the Qwen3-8B layer workload run as a decode loop: per step, append "
+    res["note"] = ("one layer of the workload run as a decode loop: per step, append "
                    "(new K/V into the pages, summary EMA), decode attention, and the boundary event of "
                    "every request whose pages are full; async holds compressing requests for one step "
                    "and overlaps their compaction with the next step (App. E.3)")
