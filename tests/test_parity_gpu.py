@@ -552,42 +552,81 @@ def test_determinism_run_twice():
 
 # --------------------------------------------------- full benchmark shape --
 
-def test_full_qwen3_8b_sampled():
-    """The benchmark's workload at full size (64 requests, 32/8 heads, 200k free
-    pages), in the launch configuration the benchmark times: decode attention
-    checked on 8 sampled requests (all heads), the boundary event checked in
-    full on its 4 boundary requests."""
-    _say("full Qwen3-8B layer: generating inputs")
-    w = W.qwen3_8b()
+def _full_size_check(w, n_sample, seed=0):
+    """A workload at full size in the launch configuration the benchmark times:
+    decode attention on sampled requests (all heads), and the boundary event of
+    every boundary request -- counts, scores, decisions, page state and the
+    compacted rows -- against the oracle, which reads only the pages it needs."""
+    b = w.page_size
     dc = DeviceCase(w, poison_free_pages=False)
-    rng = np.random.default_rng(0)
-    sample = sorted(set(rng.choice(w.num_reqs, 6, replace=False).tolist()) | set(w.boundary[:2].tolist()))
-    _say("full Qwen3-8B layer: decode attention, sampled requests", sample)
+    rng = np.random.default_rng(seed)
+    sample = sorted(set(rng.choice(w.num_reqs, n_sample, replace=False).tolist()) | set(w.boundary[:2].tolist()))
+    _say("  decode attention, sampled requests", sample)
     _decode_check(w, dc, requests=sample)
-    _say("full Qwen3-8B layer: boundary event on", w.boundary.tolist())
-    # the oracle works on the boundary requests' pages only
-    res_g = dc.boundary(O.Params())
-    p32 = O.Params().as_f32(128)
+    _say("  boundary event on", len(w.boundary), "requests")
+    p32 = O.Params().as_f32(w.head_dim)
+    before = oracle_state(w)
     st = oracle_state(w)
-    counts = []
+    res_g = dc.boundary(O.Params())
+    counts, scores, fragile = [], [], set()
     for i, r in enumerate(w.boundary):
         P = int(w.num_pages[r])
-        toks = O.gather_tokens(PoolView(w, "k"), w.page_table[r], P * 16, 16)
-        c, s, a32 = O.score_request(toks, "bf16", P, 16, w.q_pre[r], w.qstate[w.slot_ids[r]],
-                                    int(w.positions[r]), p32, p32.scale)
-        for h in range(8):
+        toks = O.gather_tokens(PoolView(w, "k"), w.page_table[r], P * b, b)
+        c, sc, a32 = O.score_request(toks, w.dtype, P, b, w.q_pre[r], w.qstate[w.slot_ids[r]],
+                                     int(w.positions[r]), p32, p32.scale)
+        for h in range(w.num_kv_heads):
             for x in range(2):
-                if not O.top_p_fragile(a32[x, h], p32.p):
-                    assert res_g["k_counts"][0, i, h, x] == c[h, x]
-            np.testing.assert_allclose(res_g["scores"][0, i, h, : (P - 1) * 16], s[h], rtol=1e-5, atol=0)
+                g = int(res_g["k_counts"][0, i, h, x])
+                if O.top_p_fragile(a32[x, h], p32.p):
+                    fragile.add(i)
+                    assert abs(g - int(c[h, x])) <= 1
+                else:
+                    assert g == int(c[h, x]), f"K^{'SL'[x]} of boundary {i} head {h}"
+            np.testing.assert_allclose(res_g["scores"][0, i, h, : (P - 1) * b], sc[h], rtol=1e-5, atol=0)
         counts.append(c[None])
-    dec, delta = O.decide_and_allocate(st, w.boundary, counts, 16, p32)
-    assert np.array_equal(res_g["decisions"], dec)
+        scores.append(sc)
+    dec, delta = O.decide_and_allocate(st, w.boundary, counts, b, p32)
+    _say("  decisions", np.bincount(dec, minlength=4).tolist())
+    for i in np.nonzero(res_g["decisions"] != dec)[0]:
+        assert i in fragile, f"decision {i}: gpu {res_g['decisions'][i]} oracle {dec[i]}"
+    if (res_g["decisions"] != dec).any():
+        pytest.skip("a decision flipped on a fragile top-p count (excused); state not comparable")
     gs = dc.host_state()
-    np.testing.assert_array_equal(gs.page_table, st.page_table)
-    np.testing.assert_array_equal(gs.seq_lens, st.seq_lens)
+    for name in ("page_table", "num_pages", "seq_lens", "refcount"):
+        np.testing.assert_array_equal(getattr(gs, name), getattr(st, name), err_msg=name)
     assert gs.free_count == st.free_count
-    _say("decisions", dec.tolist())
+    np.testing.assert_array_equal(gs.free_list[: gs.free_count], st.free_list[: st.free_count])
+    # compacted rows of the requests that compressed
+    for i, r in enumerate(w.boundary):
+        if dec[i] not in (O.COMPRESS, O.FALLBACK):
+            continue
+        P = int(before.num_pages[r])
+        n = (P - 1) * b
+        kept = [O.select_retained(scores[i][h], P, b, p32.k_loc) for h in range(w.num_kv_heads)]
+        for which in ("k", "v"):
+            old = O.gather_tokens(PoolView(w, which), before.page_table[r], P * b, b)
+            have = dc.gather(gs.page_table[r], n, which)
+            for h in range(w.num_kv_heads):
+                kept_o = kept[h]
+                want = O.compact_tokens(old[:, h], kept_o, P, b, 1, p32.layout)[:n]
+                if np.array_equal(want, have[:, h]):
+                    continue
+                idx = row_index(old[:, h], have[:, h])
+                assert (idx >= 0).all(), f"compaction wrote rows that were never there (req {r})"
+                kept_g = np.setdiff1d(idx, np.arange(n, P * b))
+                assert kept_g.size == (P - 2) * b
+                band = threshold_band(scores[i][h], kept_o, P, b, p32.k_loc)
+                assert set(kept_g.tolist()) ^ set(kept_o.tolist()) <= band, (r, h, which)
+
+
+@pytest.mark.parametrize("name", ["qwen3_8b", "high_concurrency", "prefix_shared", "long_reasoning"])
+def test_full_size_sampled(name):
+    """The four large workloads at their full shapes (the long-reasoning one
+    with 6 of its 32 requests, at full lengths: generating all 32 takes most of
+    a minute).  qwen3_8b is exactly the benchmark's input."""
+    _say(f"full {name}: generating inputs")
+    w = W.long_reasoning(num_reqs=6) if name == "long_reasoning" else W.make(name)
+    _full_size_check(w, n_sample=6)
 
 
 # ------------------------------------------- selection on given scores --
