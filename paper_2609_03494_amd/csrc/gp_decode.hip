@@ -3,8 +3,11 @@
 //
 // Work item = (KV head h, chunk of the request's pages, request r): one
 // workgroup serves the whole GQA group of h (G query heads), so every K/V byte
-// is read from HBM once per step.  Chunks are about kDecodeChunkPages pages,
-// sized so that a request of max_pages pages splits evenly.  A request that
+// is read from HBM once per step.  A request of m tokens has cdiv(m, chunk
+// tokens) chunks, chunk tokens being about kDecodeChunkPages pages sized so
+// that a request of max_pages pages splits evenly; its pages are then divided
+// into that many nearly equal chunks, which keeps workgroup durations even.
+// A request that
 // spans several chunks leaves one (o, max, sum) partial per chunk, which a
 // second, small kernel merges; a request of a single chunk gets its output
 // from the first kernel.  Consecutive workgroups are the KV heads of one
@@ -126,9 +129,10 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     }
     if (chunk >= nchunks) return;
 
-    const int tok_begin = chunk * CHUNK;
-    const int tok_end = min(m, tok_begin + CHUNK);
-    const int page_begin = tok_begin / kPage, page_end = cdiv(tok_end, kPage);
+    // the request's pages split into nchunks nearly equal chunks (the chunk
+    // count is the merge's; equal lengths keep the workgroups' durations even)
+    const int npg = cdiv(m, kPage), cs = cdiv(npg, nchunks);
+    const int page_begin = min(npg, chunk * cs), page_end = min(npg, page_begin + cs);
 
     const int c = lane % LPT, row = lane / LPT;
     const T *qp = reinterpret_cast<const T *>(a.q) + ((size_t)r * Hq + (size_t)h * G) * D + c * EPL;
@@ -368,9 +372,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
         return;
     }
     if (chunk >= nchunks) return;
-    const int tok_begin = chunk * CHUNK;
-    const int tok_end = min(m, tok_begin + CHUNK);
-    const int page_begin = tok_begin / kPage, page_end = cdiv(tok_end, kPage);
+    // the request's pages split into nchunks nearly equal chunks (the chunk
+    // count is the merge's; equal lengths keep the workgroups' durations even)
+    const int npg = cdiv(m, kPage), cs = cdiv(npg, nchunks);
+    const int page_begin = min(npg, chunk * cs), page_end = min(npg, page_begin + cs);
 
     const int n = lane & 15, kg = lane >> 4;          // score layout: token n, key slice kg
     const int v_off = lane * DPL;                     // P.V: lane owns dims [lane * DPL, +DPL)
