@@ -21,7 +21,7 @@
 //           that moves (the border rows from the saved copy), then writes it to
 //           its new slot; in the shift layout rows move down by at most two
 //           pages (a shrink), so the only cross-chunk hazard is the one the
-//           32-row border copy covers.  In the fill layout only the survivors at
+//           border copy covers (16 rows, 32 under the Shrink policy).  In the fill layout only the survivors at
 //           or above the new resident length move, into evicted slots below it,
 //           so no row is written that another chunk reads and chunks with no
 //           moving row leave at once.  Workgroup 0 also pushes the released
@@ -271,18 +271,23 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
     }
     // the fill layout never overwrites a row that another chunk still reads
     if (!at_boundary || cc == 0 || cc >= cdiv(P * kPage, kCompactChunk) || a.layout == GP_LAYOUT_FILL) return;
-    // the kBorderRows rows below slot cc * kCompactChunk: the two pages before it
+    // the rows just below slot cc * kCompactChunk that the chunk above may
+    // overwrite: rows move down by at most one page in a Compress & Hold and
+    // two in a shrink, so one page is saved, or two under the Shrink policy
+    // (in the last pages of the kBorderRows-row buffer)
     constexpr int UPP = D * E / 16 * kPage;          // 16-byte units per page slice
-    constexpr int NBP = kBorderRows / kPage;         // pages saved per boundary
+    constexpr int NBP = kBorderRows / kPage;         // pages the buffer holds
+    const int nbp = a.policy == GP_POLICY_SHRINK ? NBP : 1;
     unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc + cc) * 2 * kBorderRows * D * E;
-    for (int u = tid; u < 2 * NBP * UPP; u += blockDim.x) {
-        const int kv = u / (NBP * UPP), rem = u % (NBP * UPP), pg = rem / UPP, w = rem % UPP;
-        const int lp = cc * kCompactChunk / kPage - NBP + pg;
+    for (int u = tid; u < 2 * nbp * UPP; u += blockDim.x) {
+        const int kv = u / (nbp * UPP), rem = u % (nbp * UPP), pg = rem / UPP, w = rem % UPP;
+        const int lp = cc * kCompactChunk / kPage - nbp + pg;
         const int phys = row[lp];
         if (phys < 0 || phys >= a.pool_pages) continue;
         const size_t src_off = (size_t)phys * a.Hkv * kPage * D * E + (size_t)h * kPage * D * E;
         const unsigned char *src = reinterpret_cast<const unsigned char *>(kv == 0 ? lt.k[l] : lt.v[l]) + src_off;
-        *reinterpret_cast<uint4 *>(bd + (size_t)u * 16) = *reinterpret_cast<const uint4 *>(src + (size_t)w * 16);
+        const size_t at = ((size_t)kv * NBP + (NBP - nbp + pg)) * UPP + w;
+        *reinterpret_cast<uint4 *>(bd + at * 16) = *reinterpret_cast<const uint4 *>(src + (size_t)w * 16);
     }
 }
 
@@ -564,6 +569,7 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
     const size_t head_bytes = (size_t)h * kPage * D * E;
     const bool fill = a.layout == GP_LAYOUT_FILL;
     const bool has_border = !fill && s0 + ROWS < total;
+    const int brows = a.policy == GP_POLICY_SHRINK ? kBorderRows : kPage;   // rows the select pass saved
     const int T = total - nev;              // resident length after the event
     int dst = -1;
     {
@@ -613,7 +619,7 @@ __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt
         const int rr = u / UPR, w = u % UPR;
         val[k] = make_uint4(0u, 0u, 0u, 0u);
         if (s_dst[rr] >= 0) {
-            if (has_border && rr >= ROWS - kBorderRows) {
+            if (has_border && rr >= ROWS - brows) {
                 const unsigned char *src = bd + ((size_t)(cc + 1) * 2 + kv) * kBorderRows * D * E +
                                            (size_t)(rr - (ROWS - kBorderRows)) * D * E + (size_t)w * 16;
                 val[k] = *reinterpret_cast<const uint4 *>(src);
