@@ -3,13 +3,14 @@
 // Grow by One Page, Sec. 4.2 fallback, App. E.2 prefix-preserving compaction).
 //
 // Three kernels, in stream order:
-//  pre      grid (KV head x layer, 1 + compaction chunks, boundary request).
+//  pre      grid (KV head x layer, 1 + column groups, boundary request).
 //           Column 0 selects, for every request at a boundary, the tokens a
 //           compression would evict (the selection needs only the scores, so it
 //           does not wait for the decision).  The other columns save the rows
-//           just below each compaction-chunk boundary ("border" rows), which a
-//           neighbouring chunk may overwrite before their owner reads them, and
-//           record which pages of the table row are shared (refcount > 1).
+//           just below each compaction-chunk boundary ("border" rows, 16
+//           boundaries per workgroup), which a neighbouring chunk may overwrite
+//           before their owner reads them, and record which pages of the table
+//           row are shared (refcount > 1).
 //  decide   one workgroup.  Delta from the integer working-set counts per
 //           request in parallel; then one thread walks the requests in list
 //           order over LDS-resident data to hand out pages from the free stack
@@ -21,8 +22,9 @@
 //           that moves (the border rows from the saved copy), then writes it to
 //           its new slot; in the shift layout rows move down by at most two
 //           pages (a shrink), so the only cross-chunk hazard is the one the
-//           border copy covers (16 rows, 32 under the Shrink policy).  In the fill layout only the survivors at
-//           or above the new resident length move, into evicted slots below it,
+//           border copy covers (16 rows, 32 under the Shrink policy).  In the
+//           fill layout only the survivors at or above the new resident length
+//           move, into evicted slots below it,
 //           so no row is written that another chunk reads and chunks with no
 //           moving row leave at once.  Workgroup 0 also pushes the released
 //           pages back on the stack, lowest id first.
@@ -250,13 +252,13 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
         }
         return;
     }
-    const int cc = x - 1;
+    const int col = x - 1;
     const int32_t *row = a.page_table + (size_t)(at_boundary ? r : 0) * a.max_pages;
-    if (blockIdx.x == 0 && cc < a.npc) {
-        // shared pages of block cc of the table row, as the call starts
+    if (blockIdx.x == 0 && col < a.npc) {
+        // shared pages of block col of the table row, as the call starts
         if (tid == 0) s_n = 0;
         __syncthreads();
-        const int j = cc * kPageBlock + tid;
+        const int j = col * kPageBlock + tid;
         if (j < a.max_pages) {
             int shared = 0;
             if (at_boundary && j < P) {
@@ -267,27 +269,35 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
             if (shared) atomicAdd(&s_n, 1);
         }
         __syncthreads();
-        if (tid == 0) a.nshc[(size_t)i * a.npc + cc] = s_n;
+        if (tid == 0) a.nshc[(size_t)i * a.npc + col] = s_n;
     }
     // the fill layout never overwrites a row that another chunk still reads
-    if (!at_boundary || cc == 0 || cc >= cdiv(P * kPage, kCompactChunk) || a.layout == GP_LAYOUT_FILL) return;
-    // the rows just below slot cc * kCompactChunk that the chunk above may
-    // overwrite: rows move down by at most one page in a Compress & Hold and
-    // two in a shrink, so one page is saved, or two under the Shrink policy
-    // (in the last pages of the kBorderRows-row buffer)
+    if (!at_boundary || a.layout == GP_LAYOUT_FILL) return;
+    // Border rows of the chunk boundaries cc in [col * kBordersPerGroup, +kBordersPerGroup)
+    // (cc >= 1, below the resident length): the rows just below slot
+    // cc * kCompactChunk that the chunk above may overwrite.  Rows move down
+    // by at most one page in a Compress & Hold and two in a shrink, so one
+    // page is saved, or two under the Shrink policy (in the last pages of the
+    // kBorderRows-row buffer).
     constexpr int UPP = D * E / 16 * kPage;          // 16-byte units per page slice
     constexpr int NBP = kBorderRows / kPage;         // pages the buffer holds
     const int nbp = a.policy == GP_POLICY_SHRINK ? NBP : 1;
-    unsigned char *bd = a.border + ((((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc + cc) * 2 * kBorderRows * D * E;
-    for (int u = tid; u < 2 * nbp * UPP; u += blockDim.x) {
-        const int kv = u / (nbp * UPP), rem = u % (nbp * UPP), pg = rem / UPP, w = rem % UPP;
+    const int cc0 = max(col * kBordersPerGroup, 1);
+    const int cc1 = min((col + 1) * kBordersPerGroup, cdiv(P * kPage, kCompactChunk));
+    if (cc0 >= cc1) return;
+    const int per_cc = 2 * nbp * UPP;                 // units saved per boundary
+    unsigned char *bd0 = a.border + (((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc * 2 * kBorderRows * D * E;
+    const unsigned char *pools[2] = {reinterpret_cast<const unsigned char *>(lt.k[l]),
+                                     reinterpret_cast<const unsigned char *>(lt.v[l])};
+    for (int u = tid; u < (cc1 - cc0) * per_cc; u += blockDim.x) {
+        const int cc = cc0 + u / per_cc, uu = u % per_cc;
+        const int kv = uu / (nbp * UPP), rem = uu % (nbp * UPP), pg = rem / UPP, w = rem % UPP;
         const int lp = cc * kCompactChunk / kPage - nbp + pg;
         const int phys = row[lp];
         if (phys < 0 || phys >= a.pool_pages) continue;
         const size_t src_off = (size_t)phys * a.Hkv * kPage * D * E + (size_t)h * kPage * D * E;
-        const unsigned char *src = reinterpret_cast<const unsigned char *>(kv == 0 ? lt.k[l] : lt.v[l]) + src_off;
-        const size_t at = ((size_t)kv * NBP + (NBP - nbp + pg)) * UPP + w;
-        *reinterpret_cast<uint4 *>(bd + at * 16) = *reinterpret_cast<const uint4 *>(src + (size_t)w * 16);
+        const size_t at = (((size_t)cc * 2 + kv) * NBP + (NBP - nbp + pg)) * UPP + w;
+        *reinterpret_cast<uint4 *>(bd0 + at * 16) = *reinterpret_cast<const uint4 *>(pools[kv] + src_off + (size_t)w * 16);
     }
 }
 
@@ -650,7 +660,8 @@ __global__ __launch_bounds__(256) void release_kernel(int32_t *seq_lens, int R) 
 template <int D, int E>
 hipError_t launch_de(const ApplyArgs &a, const LayerTable &lt, int stages, hipStream_t s) {
     // (KV head, layer) is the fastest grid index: each head stays on one XCD
-    dim3 gpre(a.Hkv * a.n_layers, 1 + a.ncc, a.Rb), gcomp(2 * a.Hkv * a.n_layers, a.ncc, a.Rb);
+    dim3 gpre(a.Hkv * a.n_layers, 1 + max(a.npc, cdiv(a.ncc, kBordersPerGroup)), a.Rb),
+        gcomp(2 * a.Hkv * a.n_layers, a.ncc, a.Rb);
     if (stages & kStageSelect) pre_kernel<D, E><<<gpre, 1024, 0, s>>>(a, lt);
     if (stages & kStageDecide) decide_kernel<<<1, 1024, 0, s>>>(a);
     if (stages & kStageCompact) compact_kernel<D, E><<<gcomp, 256, 0, s>>>(a, lt);
