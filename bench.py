@@ -242,6 +242,23 @@ def main():
     torch.cuda.synchronize()
     decode_ms = k0.elapsed_time(k1) / args.steps
 
+    # the same call with the caches cold: a 512 MiB scratch write before each
+    # launch evicts L2 and the 256 MB last-level cache, so no K/V byte can come
+    # from an earlier call (context for the back-to-back figure above)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    cold = []
+    for _ in range(args.steps):
+        flush.fill_(1)
+        c0 = torch.cuda.Event(enable_timing=True)
+        c1 = torch.cuda.Event(enable_timing=True)
+        c0.record(stream)
+        phase_decode()
+        c1.record(stream)
+        cold.append((c0, c1))
+    torch.cuda.synchronize()
+    decode_cold_ms = float(np.mean([x.elapsed_time(y) for x, y in cold]))
+    del flush
+
     # the summary update folded into decode attention (one launch) against the
     # two calls, K back-to-back launches each
     def timed_loop(fn):
@@ -359,6 +376,7 @@ def main():
                              "hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4), "bytes": decode_bytes,
                              "unique_kv_bytes": unique_bytes,
                              "ms_inside_step": round(inline_decode_ms, 4),
+                             "ms_caches_flushed": round(decode_cold_ms, 4),
                              "with_summaries_one_launch_ms": round(fused_ms, 4),
                              "with_summaries_two_launches_ms": round(separate_ms, 4)},
         "boundary": {"ms_after_decode": round(boundary_ms, 4),
