@@ -15,6 +15,13 @@ precision in which the GPU path stores them; sums taken on the way are fp64.
 Readings of points the paper leaves open (each one also listed in the design
 notes) are marked "reading:" below.
 
+Every function is pinned by tests against values fixed independently of it
+(closed forms, brute force on small inputs, library routines, hand-worked
+cases).  Parity unpinned: the end-to-end Delta values and the grow/compress
+split that the full pipeline yields on the synthetic workloads -- the paper
+prints no worked example for them (its grow ratio is measured on real model
+activations), so they are reported, not asserted.
+
 Storage conventions (the library's header fixes the same layout):
   K/V pools  [pool_pages][num_kv_heads][b][head_dim]
   page table [num_reqs][max_pages] int32, free-page stack free_list[:free_count]
