@@ -199,7 +199,7 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
     a.k_counts = k_counts;
     a.scores = scores;
     a.qt = reinterpret_cast<double *>(base + w.qt);
-    a.logits = reinterpret_cast<double *>(base + w.logits);
+    a.expz = reinterpret_cast<float *>(base + w.expz);
     a.part = reinterpret_cast<double *>(base + w.part);
     a.weights = reinterpret_cast<float *>(base + w.weights);
     a.Rb = num_bnd;

@@ -72,7 +72,7 @@ __host__ __device__ inline DecodeWs decode_ws(int R, int Hq, int Hkv, int D, int
 }
 
 struct ScoreWs {
-    size_t qt, logits, part, weights, total;
+    size_t qt, expz, part, weights, total;
     int cmax, nch;
 };
 
@@ -85,8 +85,8 @@ __host__ __device__ inline ScoreWs score_ws(int Rb, int Hq, int Hkv, int max_pag
     size_t off = 0;
     w.qt = off;       // [Rb][Hkv][2G][D] double: calibrated, rotated summaries
     off = align_up(off + (size_t)Rb * Hkv * 2 * G * 128 * sizeof(double));
-    w.logits = off;   // [Rb][Hkv][2G][cmax] double: exp(z - block max)
-    off = align_up(off + (size_t)Rb * Hkv * 2 * G * w.cmax * sizeof(double));
+    w.expz = off;     // [Rb][Hkv][2G][cmax] float: exp(z - block max), z the fp64 logit
+    off = align_up(off + (size_t)Rb * Hkv * 2 * G * w.cmax * sizeof(float));
     w.part = off;     // [Rb][Hkv][nch][2G][2] double: block max, block sum of exp
     off = align_up(off + (size_t)Rb * Hkv * w.nch * 2 * G * 2 * sizeof(double));
     w.weights = off;  // [Rb][Hkv][2][cmax] float
@@ -186,7 +186,8 @@ struct ScoreArgs {
     const int32_t *slot_ids, *positions, *bnd;
     int32_t *k_counts;
     float *scores;
-    double *qt, *logits, *part;
+    double *qt, *part;
+    float *expz;
     float *weights;
     int Rb, Hq, Hkv, M, max_pages, pool_pages, max_cand, cmax, nch, R;
     double scale, theta, p;

@@ -6,9 +6,10 @@
 //     GQA group (RMS calibration to the current query, then rotation at the
 //     current position; fp64, angles computed on the device in fp64).
 //  1. logits: per (boundary request, KV head, block of kStatBlock candidate
-//     tokens), one wave: each lane reads its token's key once and forms its
-//     2G logits in fp64; the block's max and sum of exponentials per view go
-//     to the workspace, and exp(z - block max) replaces the logit.
+//     tokens), one wave: the block's 2G logits per token in fp64; the block's
+//     max and sum of exponentials per view go to the workspace (fp64), and
+//     exp(z - block max) per token is stored in float32 (relative error below
+//     2^-24, about one rounding of the float32 weight it feeds).
 //  2. weights: merge the block statistics per view, scale each token's
 //     exponentials into softmax weights, average the G query heads of each
 //     view (fp64), round to float32 and write a^S, a^L (workspace) and
@@ -18,8 +19,9 @@
 //     p.  Per-bucket masses are accumulated as 2^-60 fixed-point integers, so
 //     sums are exact and independent of thread order.
 //
-// Bound: the key read (|C| * d * sizeof(elem) per KV head) plus 2G fp64
-// logits written and read back; kernel 1 does 2G fp64 FMAs per key element.
+// Bound: the key read (|C| * d * sizeof(elem) per KV head) plus 2G float32
+// exponentials written and read back; kernel 1 does 2G fp64 FMAs per key
+// element.
 #include "gp_internal.h"
 
 namespace gp {
@@ -134,9 +136,9 @@ __global__ __launch_bounds__(256) void prep_kernel(ScoreArgs a) {
 // so each lane reads one contiguous quarter row of summaries (once) and of
 // each of its four keys.  The result leaves view 4j + q of candidate l % 16 in
 // register j of lane l.  Per view, the block's max m and sum of exp(z - m)
-// (16-lane reductions) go to the statistics array; the logits array receives
-// exp(z - m), so that the weights need a product, not an exponential, per
-// token.  A lane whose page id is invalid contributes zero logits.
+// (16-lane reductions) go to the statistics array; exp(z - m) of each token
+// is stored (float32), so that the weights need a product, not an
+// exponential, per token.  A lane whose page id is invalid contributes zero logits.
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
 template <typename T, int D, int G>
@@ -198,7 +200,7 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
     }
 
     // statistics and exponentials per view (register j holds view 4j + q)
-    double *lgv = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax;
+    float *lgv = a.expz + ((size_t)i * a.Hkv + h) * V * a.cmax;
     double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch + blk) * V * 2;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -219,7 +221,7 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
             if (t < C && v < V) {
                 const double ev = exp(z[g] - mv);
                 sv += ev;
-                lgv[(size_t)v * a.cmax + t] = ev;
+                lgv[(size_t)v * a.cmax + t] = (float)ev;
             }
         }
         for (int off = 8; off >= 1; off >>= 1) sv += __shfl_xor(sv, off, 16);
@@ -254,17 +256,17 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
     const int used = cdiv(C, kStatBlock);
     const int b0 = t0 / kStatBlock;
     const double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch) * V * 2;
-    const double *lg = a.logits + ((size_t)i * a.Hkv + h) * V * a.cmax;
+    const float *lg = a.expz + ((size_t)i * a.Hkv + h) * V * a.cmax;
 
     // The kernel runs beside decode attention, where every memory round trip
     // is slow: the exponentials of this thread's tokens and the statistics
     // are all requested before any of them is used.
-    double e[TPT][V];
+    float e[TPT][V];
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
         const int t = t0 + k * 256 + tid;
 #pragma unroll
-        for (int v = 0; v < V; ++v) e[k][v] = t < C ? lg[(size_t)v * a.cmax + t] : 0.0;
+        for (int v = 0; v < V; ++v) e[k][v] = t < C ? lg[(size_t)v * a.cmax + t] : 0.0f;
     }
     // merge the block statistics: 32 lanes per view, views 8 at a time; lane
     // c0 holds blocks c0, c0 + 32, ... (the first NPL of them in registers)
@@ -315,7 +317,7 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 const int v = x * G + g;
-                acc += e[k][v] * s_f[bb][v];
+                acc += (double)e[k][v] * s_f[bb][v];
             }
             ax[x] = (float)(acc / G);
             w[(size_t)x * a.cmax + t] = ax[x];
