@@ -7,8 +7,9 @@ to the step's starting state (one device-to-device copy), update both query summ
 for every request, then boundary scoring, selection, the decision and compaction for the
 requests at a capacity boundary.  Inputs are seeded synthetic tensors resident
 in HBM before timing starts.  The step is captured once as a HIP graph and
-replayed (``--eager`` launches every call directly).  Scoring and selection
-read keys and scores only, so they run on a second stream beside decode
+replayed (``--eager`` launches every call directly).  Decode attention needs
+only the page metadata, and the summary update, scoring and selection only
+read what decode reads, so they run on a second stream beside decode
 attention; the decision and compaction wait for both (``--serial`` runs
 everything on one stream).
 
@@ -151,6 +152,8 @@ def main():
 
     def phase_pre():
         restore()
+
+    def phase_summaries():
         gp.gp_update_summaries(q_pre, slots, init, qstate, params.beta_s, params.beta_l)
 
     def phase_decode():
@@ -169,7 +172,8 @@ def main():
         gp.gp_boundary_compact(*bargs)
 
     side = torch.cuda.Stream()          # default priority, like the main stream
-    phase = dict(pre=phase_pre, decode=phase_decode, score=phase_score, apply=phase_apply)
+    phase = dict(pre=phase_pre, summaries=phase_summaries, decode=phase_decode, score=phase_score,
+                 apply=phase_apply)
 
     def step(marks=None):
         """One step on the current stream.  Scoring and selection only read,
@@ -186,13 +190,17 @@ def main():
 
         phase["pre"]()
         if args.serial:
+            phase["summaries"]()
             mark("d0")
             phase["decode"]()
             mark("d1")
             phase["score"]()
         else:
+            # decode attention needs only the page metadata: it forks right
+            # after the restore, beside the summary update and scoring
             side.wait_stream(cur)
             with torch.cuda.stream(side):
+                phase["summaries"]()
                 phase["score"]()
             mark("d0")
             phase["decode"]()
