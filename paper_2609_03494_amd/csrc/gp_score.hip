@@ -161,31 +161,32 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
     if (slot < 0 || slot >= a.M) return;
 
     // A: this lane's quarter row of summary `col` (zero rows pad the views to 16)
-    const double *qt = a.qt + (((size_t)i * a.Hkv + h) * V + col) * D + q * S;
+    // (every load below reads a valid address, clamped where the lane has no
+    // data, and the value is zeroed afterwards: the loads are all in flight at
+    // once instead of one masked load and wait at a time)
+    const double *qt = a.qt + (((size_t)i * a.Hkv + h) * V + min(col, V - 1)) * D + q * S;
     double qa[S];
 #pragma unroll
     for (int s2 = 0; s2 < S; s2 += 2) {
-        if (col < V) {
-            const double2 u = *reinterpret_cast<const double2 *>(qt + s2);
-            qa[s2] = u.x;
-            qa[s2 + 1] = u.y;
-        } else {
-            qa[s2] = 0.0;
-            qa[s2 + 1] = 0.0;
-        }
+        const double2 u = *reinterpret_cast<const double2 *>(qt + s2);
+        qa[s2] = col < V ? u.x : 0.0;
+        qa[s2 + 1] = col < V ? u.y : 0.0;
     }
     // B: this lane's quarter row of candidate t0 + 16 g + col, for the 4 groups
     uint4 kb[NGRP][NU];
 #pragma unroll
     for (int g = 0; g < NGRP; ++g) {
         const int t = t0 + 16 * g + col;
-        int phys = -1;
-        if (t < C) phys = a.page_table[(size_t)r * a.max_pages + t / kPage];
+        const int pe = a.page_table[(size_t)r * a.max_pages + min(t, C - 1) / kPage];
+        const int phys = t < C ? pe : -1;
         const bool ok = phys >= 0 && phys < a.pool_pages;
         const uint4 *kp = reinterpret_cast<const uint4 *>(reinterpret_cast<const T *>(a.k) +
                           (((size_t)(ok ? phys : 0) * a.Hkv + h) * kPage + (t % kPage)) * D + q * S);
 #pragma unroll
-        for (int u = 0; u < NU; ++u) kb[g][u] = ok ? kp[u] : make_uint4(0u, 0u, 0u, 0u);
+        for (int u = 0; u < NU; ++u) {
+            const uint4 x = kp[u];
+            kb[g][u] = ok ? x : make_uint4(0u, 0u, 0u, 0u);
+        }
     }
     f64x4_t acc[NGRP];
 #pragma unroll
@@ -266,7 +267,7 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
     for (int k = 0; k < TPT; ++k) {
         const int t = t0 + k * 256 + tid;
 #pragma unroll
-        for (int v = 0; v < V; ++v) e[k][v] = t < C ? lg[(size_t)v * a.cmax + t] : 0.0f;
+        for (int v = 0; v < V; ++v) e[k][v] = lg[(size_t)v * a.cmax + min(t, C - 1)];
     }
     // merge the block statistics: 32 lanes per view, views 8 at a time; lane
     // c0 holds blocks c0, c0 + 32, ... (the first NPL of them in registers)
@@ -277,8 +278,9 @@ __global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
 #pragma unroll
             for (int k = 0; k < NPL; ++k) {
                 const int c = c0 + 32 * k;
-                mk[k] = c < used ? pt[((size_t)c * V + v) * 2] : -__builtin_huge_val();
-                sk[k] = c < used ? pt[((size_t)c * V + v) * 2 + 1] : 0.0;
+                const double *pc = pt + ((size_t)min(c, used - 1) * V + v) * 2;
+                mk[k] = pc[0];
+                sk[k] = pc[1];
             }
             double M = -__builtin_huge_val();
 #pragma unroll
@@ -359,11 +361,15 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
 
     // the first 4 * 1024 weights stay in registers across the passes (every
     // candidate set up to 4096 tokens); longer ones re-read the rest
-    uint32_t cached[4];
+    // (loads at clamped indices, so that all four are in flight at once)
+    uint32_t cached[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+    if (C > 0) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int t = k * 1024 + tid;
-        cached[k] = t < C ? __float_as_uint(wv[t]) : 0xffffffffu;
+        for (int k = 0; k < 4; ++k) {
+            const int t = k * 1024 + tid;
+            const uint32_t u = __float_as_uint(wv[min(t, C - 1)]);
+            cached[k] = t < C ? u : 0xffffffffu;
+        }
     }
     uint32_t prefix = 0;
     unsigned long long above_mass = 0;
@@ -382,7 +388,8 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int t = base + k * 1024 + tid;
-                u[k] = base == 0 ? cached[k] : (t < C ? __float_as_uint(wv[t]) : 0xffffffffu);
+                const uint32_t y = base == 0 ? cached[k] : __float_as_uint(wv[min(t, C - 1)]);
+                u[k] = t < C ? y : 0xffffffffu;
             }
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -490,9 +497,17 @@ __global__ __launch_bounds__(256) void entropy_kernel(ScoreArgs a) {
     const int C = (P - 1) * kPage;
     const float *wv = a.weights + (((size_t)i * a.Hkv + h) * 2 + x) * a.cmax;
     double acc = 0.0;
-    for (int t = tid; t < C; t += blockDim.x) {
-        const double w = (double)wv[t];
-        if (w > 0.0) acc += w * log(w);
+    // four weights per round, loaded at clamped indices so that they are in
+    // flight together; the sum runs in the same order as one at a time
+    for (int t = tid; t < C; t += 4 * blockDim.x) {
+        float y[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) y[k] = wv[min(t + k * (int)blockDim.x, C - 1)];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const double w = (double)y[k];
+            if (t + k * (int)blockDim.x < C && w > 0.0) acc += w * log(w);
+        }
     }
     for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 64);
     if (lane == 0) s_red[wave] = acc;
