@@ -314,9 +314,35 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
     __shared__ int s_dec[kMaxBnd];
     __shared__ int s_pop[kMaxBnd];
     __shared__ long long s_cnt[4];
+    __shared__ unsigned long long s_D[kMaxBnd];     // sum of K^S - K^L (two's complement)
     __shared__ int s_fc0, s_popped;
     const int tid = threadIdx.x;
     const int Rb = a.Rb;
+
+    // The per-(layer, KV head) counts and the shared-page counts of every
+    // request are summed by the whole workgroup, one entry per thread, so
+    // that their loads are in flight together (integer sums: exact in any
+    // order).
+    for (int i = tid; i < Rb; i += blockDim.x) {
+        s_D[i] = 0;
+        s_nsh[i] = 0;
+    }
+    if (tid == 0) {
+        const int fc = *a.free_count;
+        s_fc0 = fc < 0 ? 0 : (fc > a.pool_pages ? a.pool_pages : fc);
+    }
+    __syncthreads();
+    const int LH = a.n_layers * a.Hkv;
+    for (int e = tid; e < Rb * LH; e += blockDim.x) {
+        const int i = e / LH, l = e % LH / a.Hkv, h = e % a.Hkv;
+        const int32_t *kc = a.k_counts + (((size_t)l * Rb + i) * a.Hkv + h) * 2;
+        atomicAdd(&s_D[i], (unsigned long long)((long long)kc[0] - (long long)kc[1]));
+    }
+    for (int e = tid; e < Rb * a.npc; e += blockDim.x) {
+        const int v = a.nshc[e];
+        if (v) atomicAdd(&s_nsh[e / a.npc], v);
+    }
+    __syncthreads();
 
     for (int i = tid; i < Rb; i += blockDim.x) {
         const int r = a.bnd[i];
@@ -328,12 +354,7 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
                 flags = F_BOUNDARY;
                 bool grow, shrink = false;
                 if (P >= 2) {
-                    long long D = 0;
-                    for (int l = 0; l < a.n_layers; ++l)
-                        for (int h = 0; h < a.Hkv; ++h) {
-                            const int32_t *kc = a.k_counts + (((size_t)l * Rb + i) * a.Hkv + h) * 2;
-                            D += (long long)kc[0] - (long long)kc[1];
-                        }
+                    const long long D = (long long)s_D[i];
                     // Delta = D / denom, denom = |C| * Hkv * layers.  Thresholds
                     // compare exactly as D against t * denom: t is a float and
                     // denom < 2^29, so the product is exact in fp64.
@@ -351,7 +372,7 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
                             break;
                         default: grow = above; break;
                     }
-                    for (int c = 0; c < a.npc; ++c) nsh += a.nshc[(size_t)i * a.npc + c];
+                    nsh = s_nsh[i];
                     last_shared = a.shflag[(size_t)i * a.max_pages + P - 1];
                 } else {
                     grow = a.policy == GP_POLICY_FIXED ? P < a.fixed_pages : true;
@@ -365,10 +386,6 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
         s_flags[i] = flags;
         s_nsh[i] = nsh;
         s_nsh_last[i] = last_shared;
-    }
-    if (tid == 0) {
-        const int fc = *a.free_count;
-        s_fc0 = fc < 0 ? 0 : (fc > a.pool_pages ? a.pool_pages : fc);
     }
     __syncthreads();
 

@@ -353,18 +353,51 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     __shared__ bf16x8_t s_q[KK][4][G];
     __shared__ int s_ids[kMaxChunkPages];
 
+    constexpr int RR = 4;                 // table-row entries per thread requested up front
     const int h = blockIdx.x, chunk = blockIdx.y, r = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int Hkv = a.Hkv, Hq = Hkv * G;
+    // The length, the page count and the request's page-table row (its first
+    // RR * blockDim entries) are requested together, before the chunk's page
+    // range is known, so the first K/V loads wait for one round trip only.
+    const int32_t *table = a.page_table + (size_t)r * a.max_pages;
     int m = a.seq_lens[r];
-    if (m < 0) return;                        // held: not in this step's batch
-    if (chunk == 0) fold_summaries<uint16_t, D, G>(a, r, h);
+    int P = a.num_pages[r];
+    int ent[RR];
+#pragma unroll
+    for (int u = 0; u < RR; ++u) ent[u] = table[min(tid + u * (int)blockDim.x, a.max_pages - 1)];
+    const uint16_t *qg = reinterpret_cast<const uint16_t *>(a.q) + ((size_t)r * Hq + (size_t)h * G) * D;
+    const int tq = min(tid, KK * 4 * G - 1);
+    const int q_kk = tq / (4 * G), q_kg = tq % (4 * G) / G, q_n = tq % G;
+    const bf16x8_t qv = *reinterpret_cast<const bf16x8_t *>(qg + (size_t)q_n * D + q_kk * 32 + q_kg * 8);
     const int CHUNK = a.chunk_pages * kPage;
 
-    int P = a.num_pages[r];
+    // (no early exit until the page ids are in LDS: a branch on the length
+    // would hold the row's loads back until the length has arrived)
+    const bool held = m < 0;                  // held: not in this step's batch
     P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
-    m = m > P * kPage ? P * kPage : m;
+    m = held ? 0 : (m > P * kPage ? P * kPage : m);
     const int nchunks = cdiv(m, CHUNK);
+    // the request's pages split into nchunks nearly equal chunks (the chunk
+    // count is the merge's; equal lengths keep the workgroups' durations even)
+    const int npg = cdiv(m, kPage), cs = nchunks > 0 ? cdiv(npg, nchunks) : 0;
+    const int page_begin = min(npg, chunk * cs), page_end = min(npg, page_begin + cs);
+
+    // page ids (from the row entries held, the rest of a long row re-read)
+    // and Q (MFMA A layout, rows < G) into LDS
+#pragma unroll
+    for (int u = 0; u < RR; ++u) {
+        const int j = tid + u * (int)blockDim.x;
+        if (j >= page_begin && j < page_end) s_ids[j - page_begin] = ent[u] >= 0 && ent[u] < a.pool_pages ? ent[u] : -1;
+    }
+    for (int j = max(page_begin, RR * (int)blockDim.x) + tid; j < page_end; j += blockDim.x) {
+        const int pid = table[j];
+        s_ids[j - page_begin] = pid >= 0 && pid < a.pool_pages ? pid : -1;
+    }
+    if (tid < KK * 4 * G) s_q[q_kk][q_kg][q_n] = qv;
+
+    if (held) return;
+    if (chunk == 0) fold_summaries<uint16_t, D, G>(a, r, h);
     uint16_t *out = reinterpret_cast<uint16_t *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     if (m == 0) {
         if (chunk == 0)
@@ -372,26 +405,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
         return;
     }
     if (chunk >= nchunks) return;
-    // the request's pages split into nchunks nearly equal chunks (the chunk
-    // count is the merge's; equal lengths keep the workgroups' durations even)
-    const int npg = cdiv(m, kPage), cs = cdiv(npg, nchunks);
-    const int page_begin = min(npg, chunk * cs), page_end = min(npg, page_begin + cs);
 
     const int n = lane & 15, kg = lane >> 4;          // score layout: token n, key slice kg
     const int v_off = lane * DPL;                     // P.V: lane owns dims [lane * DPL, +DPL)
     const int k_off = n * D + kg * 8;
-
-    // page ids and Q (MFMA A layout, rows < G) into LDS
-    const int32_t *table = a.page_table + (size_t)r * a.max_pages;
-    for (int k = tid; k < page_end - page_begin; k += blockDim.x) {
-        const int pid = table[page_begin + k];
-        s_ids[k] = pid >= 0 && pid < a.pool_pages ? pid : -1;
-    }
-    const uint16_t *qg = reinterpret_cast<const uint16_t *>(a.q) + ((size_t)r * Hq + (size_t)h * G) * D;
-    if (tid < KK * 4 * G) {
-        const int kk = tid / (4 * G), rem = tid % (4 * G), q_kg = rem / G, q_n = rem % G;
-        s_q[kk][q_kg][q_n] = *reinterpret_cast<const bf16x8_t *>(qg + (size_t)q_n * D + kk * 32 + q_kg * 8);
-    }
     __syncthreads();
 
     float mrun[GI], lrun[GI], o[G][DPL];
@@ -410,13 +427,13 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     const size_t head_off = (size_t)h * kPage * D;
     const size_t page_elems = (size_t)Hkv * kPage * D;
     uint4 kb[KK];
-    uint32_t vw[kPage];
+    uint32_t vwa[kPage], vwb[kPage];                 // values of this page and of the next
     auto load_k = [&](int phys) {
         const uint16_t *kp = kpool + (size_t)phys * page_elems + head_off + k_off;
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) kb[kk] = ld16(kp + kk * 32);
     };
-    auto load_v = [&](int phys) {
+    auto load_v = [&](int phys, uint32_t (&vw)[kPage]) {
         // one 2D-byte row per instruction: fully coalesced
         const uint16_t *vp = vpool + (size_t)phys * page_elems + head_off + v_off;
 #pragma unroll
@@ -427,13 +444,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
                 vw[t] = __builtin_nontemporal_load(vp + t * D);
         }
     };
-    int p = page_begin + wave;
-    int phys = p < page_end ? s_ids[p - page_begin] : -1;
-    if (phys >= 0) {
-        load_k(phys);
-        load_v(phys);
-    }
-    for (; p < page_end; p += NW) {
+    // One page of the wave: Q.K^T on the matrix cores, then the keys and
+    // values of the wave's next page are requested together (the values into
+    // the other buffer), then softmax and P.V on this page's values.
+    auto page = [&](int p, int &phys, uint32_t (&vw)[kPage], uint32_t (&vn)[kPage]) {
         const int ntok = phys >= 0 ? min(kPage, m - p * kPage) : 0;
         f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
         if (ntok > 0) {
@@ -444,10 +458,12 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
                 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, __builtin_bit_cast(bf16x8_t, kb[kk]), acc, 0, 0, 0);
             }
         }
-        // the keys of the next page go out as soon as these are consumed
         const int pn = p + NW;
         const int phys_next = pn < page_end ? s_ids[pn - page_begin] : -1;
-        if (phys_next >= 0) load_k(phys_next);
+        if (phys_next >= 0) {
+            load_k(phys_next);
+            load_v(phys_next, vn);
+        }
         const bool valid = n < ntok;
         float sc[GI], alpha[GI];
 #pragma unroll
@@ -489,9 +505,19 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
             }
         }
         wave_lds_sync();
-        // ... and its values once these are
-        if (phys_next >= 0) load_v(phys_next);
         phys = phys_next;
+    };
+    int p = page_begin + wave;
+    int phys = p < page_end ? s_ids[p - page_begin] : -1;
+    if (phys >= 0) {
+        load_k(phys);
+        load_v(phys, vwa);
+    }
+    // pages alternate between the two value buffers
+    for (; p < page_end; p += 2 * NW) {
+        page(p, phys, vwa, vwb);
+        if (p + NW >= page_end) break;
+        page(p + NW, phys, vwb, vwa);
     }
 
     // merge the waves: per-wave (max, sum) of each head, o of every dim
