@@ -353,51 +353,18 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     __shared__ bf16x8_t s_q[KK][4][G];
     __shared__ int s_ids[kMaxChunkPages];
 
-    constexpr int RR = 4;                 // table-row entries per thread requested up front
     const int h = blockIdx.x, chunk = blockIdx.y, r = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int Hkv = a.Hkv, Hq = Hkv * G;
-    // The length, the page count and the request's page-table row (its first
-    // RR * blockDim entries) are requested together, before the chunk's page
-    // range is known, so the first K/V loads wait for one round trip only.
-    const int32_t *table = a.page_table + (size_t)r * a.max_pages;
     int m = a.seq_lens[r];
-    int P = a.num_pages[r];
-    int ent[RR];
-#pragma unroll
-    for (int u = 0; u < RR; ++u) ent[u] = table[min(tid + u * (int)blockDim.x, a.max_pages - 1)];
-    const uint16_t *qg = reinterpret_cast<const uint16_t *>(a.q) + ((size_t)r * Hq + (size_t)h * G) * D;
-    const int tq = min(tid, KK * 4 * G - 1);
-    const int q_kk = tq / (4 * G), q_kg = tq % (4 * G) / G, q_n = tq % G;
-    const bf16x8_t qv = *reinterpret_cast<const bf16x8_t *>(qg + (size_t)q_n * D + q_kk * 32 + q_kg * 8);
+    if (m < 0) return;                        // held: not in this step's batch
+    if (chunk == 0) fold_summaries<uint16_t, D, G>(a, r, h);
     const int CHUNK = a.chunk_pages * kPage;
 
-    // (no early exit until the page ids are in LDS: a branch on the length
-    // would hold the row's loads back until the length has arrived)
-    const bool held = m < 0;                  // held: not in this step's batch
+    int P = a.num_pages[r];
     P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
-    m = held ? 0 : (m > P * kPage ? P * kPage : m);
+    m = m > P * kPage ? P * kPage : m;
     const int nchunks = cdiv(m, CHUNK);
-    // the request's pages split into nchunks nearly equal chunks (the chunk
-    // count is the merge's; equal lengths keep the workgroups' durations even)
-    const int npg = cdiv(m, kPage), cs = nchunks > 0 ? cdiv(npg, nchunks) : 0;
-    const int page_begin = min(npg, chunk * cs), page_end = min(npg, page_begin + cs);
-
-    // page ids (from the row entries held, the rest of a long row re-read)
-    // and Q (MFMA A layout, rows < G) into LDS
-#pragma unroll
-    for (int u = 0; u < RR; ++u) {
-        const int j = tid + u * (int)blockDim.x;
-        if (j >= page_begin && j < page_end) s_ids[j - page_begin] = ent[u] >= 0 && ent[u] < a.pool_pages ? ent[u] : -1;
-    }
-    for (int j = max(page_begin, RR * (int)blockDim.x) + tid; j < page_end; j += blockDim.x) {
-        const int pid = table[j];
-        s_ids[j - page_begin] = pid >= 0 && pid < a.pool_pages ? pid : -1;
-    }
-    if (tid < KK * 4 * G) s_q[q_kk][q_kg][q_n] = qv;
-
-    if (held) return;
-    if (chunk == 0) fold_summaries<uint16_t, D, G>(a, r, h);
     uint16_t *out = reinterpret_cast<uint16_t *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     if (m == 0) {
         if (chunk == 0)
@@ -405,10 +372,26 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
         return;
     }
     if (chunk >= nchunks) return;
+    // the request's pages split into nchunks nearly equal chunks (the chunk
+    // count is the merge's; equal lengths keep the workgroups' durations even)
+    const int npg = cdiv(m, kPage), cs = cdiv(npg, nchunks);
+    const int page_begin = min(npg, chunk * cs), page_end = min(npg, page_begin + cs);
 
     const int n = lane & 15, kg = lane >> 4;          // score layout: token n, key slice kg
     const int v_off = lane * DPL;                     // P.V: lane owns dims [lane * DPL, +DPL)
     const int k_off = n * D + kg * 8;
+
+    // page ids and Q (MFMA A layout, rows < G) into LDS
+    const int32_t *table = a.page_table + (size_t)r * a.max_pages;
+    for (int k = tid; k < page_end - page_begin; k += blockDim.x) {
+        const int pid = table[page_begin + k];
+        s_ids[k] = pid >= 0 && pid < a.pool_pages ? pid : -1;
+    }
+    const uint16_t *qg = reinterpret_cast<const uint16_t *>(a.q) + ((size_t)r * Hq + (size_t)h * G) * D;
+    if (tid < KK * 4 * G) {
+        const int kk = tid / (4 * G), rem = tid % (4 * G), q_kg = rem / G, q_n = rem % G;
+        s_q[kk][q_kg][q_n] = *reinterpret_cast<const bf16x8_t *>(qg + (size_t)q_n * D + kk * 32 + q_kg * 8);
+    }
     __syncthreads();
 
     float mrun[GI], lrun[GI], o[G][DPL];
