@@ -70,7 +70,7 @@ __device__ inline bool boundary_of(const ScoreArgs &a, int i, int &r, int &P) {
 // at the current position; angles pos * theta^(-2k/D) and their sine and
 // cosine are computed in fp64 on the device.
 template <typename T, int D, int G>
-__global__ __launch_bounds__(256) void prep_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(256, 5) void prep_kernel(ScoreArgs a) {
     constexpr int V = 2 * G;
     constexpr int H = D / 2;
     __shared__ double s_q[V][D];
@@ -240,7 +240,7 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
 // token's softmax weight in view (g, x) is its stored exp(z - m_b) times f_b.
 // The G query heads of a view are averaged in fp64 and rounded to float32.
 template <int G>
-__global__ __launch_bounds__(256) void weights_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G >= 8 ? 4 : 5))) void weights_kernel(ScoreArgs a) {
     constexpr int V = 2 * G;
     constexpr int BPC = kProbChunk / kStatBlock;     // statistics blocks per chunk
     constexpr int TPT = kProbChunk / 256;            // tokens per thread
@@ -333,19 +333,26 @@ __device__ inline unsigned long long fixed60(uint32_t bits) {
 }
 
 // -------------------------------------------------------------------- top-p --
-// One workgroup of 1024 threads per (boundary request, KV head, view).  Each of
-// the three radix passes histograms the weights that share the prefix found so
-// far (count and 2^-60 fixed-point mass per bucket), then the workgroup scans
-// the buckets from the top to find the one where the running mass reaches p.
-__global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
+// One workgroup of kTopPThreads threads per (boundary request, KV head, view).
+// Each of the three radix passes histograms the weights that share the prefix
+// found so far (count and 2^-60 fixed-point mass per bucket), then the
+// workgroup scans the buckets from the top to find the one where the running
+// mass reaches p.  The workgroup is small (one wave per SIMD) so that it can
+// start beside decode attention, which leaves a quarter of each SIMD's
+// registers free.
+constexpr int kTopPThreads = 256;
+__global__ __launch_bounds__(kTopPThreads, 5) void top_p_kernel(ScoreArgs a) {
+    constexpr int NT = kTopPThreads;
     constexpr int NB = 2048;
+    constexpr int CW = 4096 / NT;                   // weights per thread kept in registers
+    constexpr int NWV = NT / 64;
     __shared__ unsigned int s_cnt[NB];
     __shared__ unsigned long long s_mass[NB];
     __shared__ int s_bucket;
     __shared__ unsigned long long s_above_mass;
     __shared__ unsigned int s_above_cnt;
-    __shared__ unsigned long long s_wmass[16];
-    __shared__ unsigned int s_wcnt[16];
+    __shared__ unsigned long long s_wmass[NWV];
+    __shared__ unsigned int s_wcnt[NWV];
 
     const int h = blockIdx.x, x = blockIdx.y, i = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -359,14 +366,16 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
     const float *wv = a.weights + (((size_t)i * a.Hkv + h) * 2 + x) * a.cmax;
     const unsigned long long target = (unsigned long long)ldexp(a.p, 60);
 
-    // the first 4 * 1024 weights stay in registers across the passes (every
+    // the first CW * NT weights stay in registers across the passes (every
     // candidate set up to 4096 tokens); longer ones re-read the rest
-    // (loads at clamped indices, so that all four are in flight at once)
-    uint32_t cached[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+    // (loads at clamped indices, so that all of them are in flight at once)
+    uint32_t cached[CW];
+#pragma unroll
+    for (int k = 0; k < CW; ++k) cached[k] = 0xffffffffu;
     if (C > 0) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int t = k * 1024 + tid;
+        for (int k = 0; k < CW; ++k) {
+            const int t = k * NT + tid;
             const uint32_t u = __float_as_uint(wv[min(t, C - 1)]);
             cached[k] = t < C ? u : 0xffffffffu;
         }
@@ -378,27 +387,30 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
     const int nbits[3] = {11, 11, 9};
     for (int pass = 0; pass < 3; ++pass) {
         const int sh = shifts[pass], nb = 1 << nbits[pass];
-        for (int b = tid; b < nb; b += blockDim.x) {
+        for (int b = tid; b < nb; b += NT) {
             s_cnt[b] = 0;
             s_mass[b] = 0;
         }
         __syncthreads();
-        for (int base = 0; base < C; base += 1024 * 4) {
+        auto count = [&](uint32_t u) {
+            if (u != 0xffffffffu && (u >> (sh + nbits[pass])) == prefix) {
+                const int b = (u >> sh) & (nb - 1);
+                atomicAdd(&s_cnt[b], 1u);
+                atomicAdd(&s_mass[b], fixed60(u));
+            }
+        };
+#pragma unroll
+        for (int k = 0; k < CW; ++k) count(cached[k]);
+        for (int base = CW * NT; base < C; base += 4 * NT) {
             uint32_t u[4];
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
-                const int t = base + k * 1024 + tid;
-                const uint32_t y = base == 0 ? cached[k] : __float_as_uint(wv[min(t, C - 1)]);
+                const int t = base + k * NT + tid;
+                const uint32_t y = __float_as_uint(wv[min(t, C - 1)]);
                 u[k] = t < C ? y : 0xffffffffu;
             }
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                if (u[k] != 0xffffffffu && (u[k] >> (sh + nbits[pass])) == prefix) {
-                    const int b = (u[k] >> sh) & (nb - 1);
-                    atomicAdd(&s_cnt[b], 1u);
-                    atomicAdd(&s_mass[b], fixed60(u[k]));
-                }
-            }
+            for (int k = 0; k < 4; ++k) count(u[k]);
         }
         __syncthreads();
         // Scan of the buckets from the highest down, over the whole workgroup:
@@ -407,7 +419,7 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
         // reaches the mass still needed names that bucket, with the count and
         // mass strictly above it.
         {
-            const int per = nb >= 1024 ? nb / 1024 : 1;
+            const int per = nb >= NT ? nb / NT : 1;
             const bool owns = tid * per < nb;
             unsigned long long mm = 0;
             unsigned int cc = 0;
@@ -439,7 +451,7 @@ __global__ __launch_bounds__(1024) void top_p_kernel(ScoreArgs a) {
             const unsigned long long need = target > above_mass ? target - above_mass : 0ull;
             const unsigned long long em = im - mm;
             const unsigned int ec = ic - cc;
-            if (tid == 1023 && im < need) s_bucket = -1;    // the candidates fall short of p
+            if (tid == NT - 1 && im < need) s_bucket = -1;    // the candidates fall short of p
             if (owns && em < need && im >= need) {
                 unsigned long long cum = em;
                 unsigned int cnt = ec;
@@ -527,7 +539,7 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
     dim3 g0(a.Hkv, a.Rb), g1(a.Hkv, cdiv(a.cmax, kStatBlock), a.Rb), g2(a.Hkv, cdiv(a.cmax, kProbChunk), a.Rb), g3(a.Hkv, 2, a.Rb);
     if (a.cmax == 0) {
         // no request can have candidates: the counts are written as zero
-        top_p_kernel<<<g3, 1024, 0, s>>>(a);
+        top_p_kernel<<<g3, kTopPThreads, 0, s>>>(a);
         return hipGetLastError();
     }
     switch (G) {
@@ -544,7 +556,7 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
     if (a.metric == GP_METRIC_ENTROPY)
         entropy_kernel<<<g3, 256, 0, s>>>(a);
     else
-        top_p_kernel<<<g3, 1024, 0, s>>>(a);
+        top_p_kernel<<<g3, kTopPThreads, 0, s>>>(a);
     return hipGetLastError();
 }
 
