@@ -264,7 +264,9 @@ def main():
         c1.record(stream)
         cold.append((c0, c1))
     torch.cuda.synchronize()
-    decode_cold_ms = float(np.mean([x.elapsed_time(y) for x, y in cold]))
+    cold_t = np.array([x.elapsed_time(y) for x, y in cold])
+    decode_cold_ms = float(np.mean(cold_t))
+    decode_cold_pct = [round(float(x), 4) for x in np.percentile(cold_t, [10, 50, 90])]
     del flush
 
     # the summary update folded into decode attention (one launch) against the
@@ -317,6 +319,26 @@ def main():
         return float(np.mean([x.elapsed_time(y) for x, y in ev]))
 
     apply_layout_ms = {"shift": apply_ms(gp.GP_LAYOUT_SHIFT), "fill": apply_ms(gp.GP_LAYOUT_FILL)}
+
+    # the boundary calls alone, on one stream, as the step runs them (scoring +
+    # selection, then the decision + compaction), the state restored before
+    # each iteration outside the events; medians over K iterations
+    bev = []
+    for _ in range(args.steps):
+        restore()
+        b0, b1, b2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        b0.record(stream)
+        phase_score()
+        b1.record(stream)
+        phase_apply()
+        b2.record(stream)
+        bev.append((b0, b1, b2))
+    torch.cuda.synchronize()
+    t_score = float(np.median([x.elapsed_time(y) for x, y, _ in bev]))
+    t_apply = float(np.median([y.elapsed_time(z) for _, y, z in bev]))
+    bnd_np = np.asarray(w.boundary, dtype=np.int64)
+    cand = int(((w.num_pages[bnd_np].astype(np.int64) - 1) * b).sum())
+    score_bytes = cand * Hkv * d * e + cand * Hkv * 4         # K of every candidate once + the scores
 
     # the decode loop itself (App. E.3): every step appends each running
     # request's new token (K/V into its pages, one summary EMA step), decodes,
@@ -385,13 +407,18 @@ def main():
                              "unique_kv_bytes": unique_bytes,
                              "ms_inside_step": round(inline_decode_ms, 4),
                              "ms_caches_flushed": round(decode_cold_ms, 4),
+                             "ms_caches_flushed_p10_p50_p90": decode_cold_pct,
                              "with_summaries_one_launch_ms": round(fused_ms, 4),
                              "with_summaries_two_launches_ms": round(separate_ms, 4)},
         "boundary": {"ms_after_decode": round(boundary_ms, 4),
                      "events_per_s": round(Rb / (step_ms * 1e-3), 1),
                      "overlapped_with_decode": not args.serial,
                      "compress_grow_fallback_preempt": split,
-                     "apply_ms_all_compress": {k_: round(v_, 4) for k_, v_ in apply_layout_ms.items()}},
+                     "apply_ms_all_compress": {k_: round(v_, 4) for k_, v_ in apply_layout_ms.items()},
+                     "alone": {"score_select_ms": round(t_score, 4), "decide_compact_ms": round(t_apply, 4),
+                               "events_per_s": round(Rb / ((t_score + t_apply) * 1e-3), 1),
+                               "score_bytes": score_bytes,
+                               "score_GB/s": round(score_bytes / (t_score * 1e-3) / 1e9, 1)}},
         "serving_loop": loop,
         "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
