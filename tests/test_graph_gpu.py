@@ -13,8 +13,13 @@ from _harness import DeviceCase
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("fork", [False, True], ids=["one_stream", "score_on_side_stream"])
+@pytest.mark.parametrize("fork", [False, True, "bench"], ids=["one_stream", "score_on_side_stream",
+                                                         "bench_step_layout"])
 def test_graph_replays_match_eager(fork):
+    """fork="bench" is the benchmark's step: the summary update, scoring and
+    selection on a side stream beside decode attention, then the decision and
+    compaction as separate calls; its eager result must also equal the plain
+    one-stream sequence."""
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     import paper_2609_03494_amd as gp
@@ -42,13 +47,35 @@ def test_graph_replays_match_eager(fork):
                                   dc.ps.free_list, dc.ps.free_count)]
     k0, v0, qs0 = dc.layers[0].k.clone(), dc.layers[0].v.clone(), dc.qstate.clone()
 
-    def step():
+    def reset():
         for t, t0 in zip((dc.ps.page_table, dc.ps.num_pages, dc.ps.seq_lens, dc.ps.refcount,
                           dc.ps.free_list, dc.ps.free_count), state0):
             t.copy_(t0)
         dc.layers[0].k.copy_(k0)
         dc.layers[0].v.copy_(v0)
         dc.qstate.copy_(qs0)
+
+    bargs = (dc.layers, dc.ps, bnd, counts, scores, params, dec, delta, ctr, ws_a)
+
+    def step_bench():
+        reset()
+        cur = torch.cuda.current_stream()
+        aux.wait_stream(cur)
+        with torch.cuda.stream(aux):
+            gp.gp_update_summaries(dc.q_pre, dc.slot_ids, init, dc.qstate, p32.beta_s, p32.beta_l)
+            gp.gp_boundary_score(dc.layers[0], dc.ps, dc.q_pre, dc.qstate, dc.slot_ids, dc.positions,
+                                 bnd, params, counts, scores, ws_s)
+            gp.gp_boundary_select(*bargs)
+        gp.gp_decode_attention(dc.layers[0], dc.ps, dc.q_post, p32.scale, out, dc.ws_decode)
+        cur.wait_stream(aux)
+        gp.gp_boundary_decide(*bargs, hold=False)
+        gp.gp_boundary_compact(*bargs)
+
+    def step():
+        if fork == "bench":
+            step_bench()
+            return
+        reset()
         gp.gp_update_summaries(dc.q_pre, dc.slot_ids, init, dc.qstate, p32.beta_s, p32.beta_l)
         cur = torch.cuda.current_stream()
         if fork:
@@ -71,8 +98,29 @@ def test_graph_replays_match_eager(fork):
                                               dc.ps.seq_lens, dc.ps.free_list, dc.ps.free_count,
                                               dc.layers[0].k, dc.layers[0].v, dc.qstate)]
 
+    if fork == "bench":
+        # the plain sequence on one stream, with gp_boundary_apply
+        fork_saved, fork = fork, False
+        step()
+        plain = snapshot()
+        fork = fork_saved
     step()
     eager = snapshot()
+    names = ("out", "counts", "scores", "decisions", "delta", "page_table", "seq_lens", "free_list",
+             "free_count", "k_pool", "v_pool", "qstate")
+
+    def same_bits(a, b):
+        # compare bit patterns, so that NaN-poisoned slots compare equal
+        bits = {torch.bfloat16: torch.int16, torch.float32: torch.int32}.get(a.dtype)
+        ai, bi = (a.view(bits), b.view(bits)) if bits is not None else (a, b)
+        if not torch.equal(ai, bi):
+            print("differs in", int((ai != bi).sum()), "of", ai.numel(), flush=True)
+            return False
+        return True
+
+    if fork == "bench":
+        for name, a, b in zip(names, plain, eager):
+            assert same_bits(a, b), f"bench step layout: {name} differs from the one-stream sequence"
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -87,14 +135,6 @@ def test_graph_replays_match_eager(fork):
         torch.cuda.synchronize()
         g.replay()
         got = snapshot()
-        names = ("out", "counts", "scores", "decisions", "delta", "page_table", "seq_lens", "free_list",
-                 "free_count", "k_pool", "v_pool", "qstate")
         for name, a, b in zip(names, eager, got):
-            # compare bit patterns, so that NaN-poisoned slots compare equal
-            bits = {torch.bfloat16: torch.int16, torch.float32: torch.int32}.get(a.dtype)
-            ai, bi = (a.view(bits), b.view(bits)) if bits is not None else (a, b)
-            same = torch.equal(ai, bi)
-            if not same:
-                print(name, "differs in", int((ai != bi).sum()), "of", ai.numel(), flush=True)
-            assert same, f"replay {rep}: {name} differs"
+            assert same_bits(a, b), f"replay {rep}: {name} differs"
         del junk
