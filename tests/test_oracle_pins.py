@@ -518,3 +518,17 @@ def test_view_distributions_special_case_is_softmax():
         ref = torch.stack([torch.softmax(0.25 * torch.from_numpy(K[:, h]) @ torch.from_numpy(qt[h * G + g]), 0)
                            for g in range(G)]).mean(0).numpy()
         assert np.allclose(a[0, h], ref, rtol=0, atol=1e-15) and np.allclose(a[1, h], ref, rtol=0, atol=1e-15)
+
+
+def test_cpu_baseline_child_runs_the_oracle_on_worker_processes():
+    """The benchmark's all-core CPU leg: a GPU-free child process that forks
+    workers running the oracle's decode attention over the tiny workload."""
+    import json
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    cp = subprocess.run([sys.executable, "-m", "oracle.cpu_baseline", "tiny", "0.3", "2"], cwd=root,
+                        capture_output=True, text=True, timeout=120)
+    assert cp.returncode == 0, cp.stderr[-500:]
+    res = json.loads(cp.stdout.strip().splitlines()[-1])
+    assert res["workers"] == 2 and res["passes"] >= 2 and res["bytes"] > 0 and res["seconds"] > 0
