@@ -7,11 +7,12 @@ to the step's starting state (one device-to-device copy), update both query summ
 for every request, then boundary scoring, selection, the decision and compaction for the
 requests at a capacity boundary.  Inputs are seeded synthetic tensors resident
 in HBM before timing starts.  The step is captured once as a HIP graph and
-replayed (``--eager`` launches every call directly).  Decode attention needs
-only the page metadata, and the summary update, scoring and selection only
-read what decode reads, so they run on a second stream beside decode
-attention; the decision and compaction wait for both (``--serial`` runs
-everything on one stream).
+replayed (``--eager`` launches every call directly).  Decode attention reads
+a snapshot of the request metadata taken by one small copy at the start of the
+step, so the summary update, scoring, selection and the decision (which
+updates the live metadata) run on a second stream beside it; the compaction,
+which moves cached rows, waits for both (``--serial`` runs everything on one
+stream, decode on the live metadata).
 
 Prints one JSON line.  ``value`` is GB/s of the every-step traffic (summaries
 and decode attention, algorithmic bytes) over the whole step's time, boundary
@@ -159,7 +160,23 @@ def main():
     def phase_decode():
         gp.gp_decode_attention(kv, ps, q_post, params.scale, out, ws_d)
 
+    def phase_snapshot():
+        torch.mul(live_req_meta, 1, out=snap)
+
+    def phase_decode_snapshot():
+        gp.gp_decode_attention(kv, ps_dec, q_post, params.scale, out, ws_d)
+
     bargs = ([kv], ps, bnd, counts, scores, params, decisions, delta, counters, ws_a)
+    # Decode attention reads a per-step snapshot of the request metadata
+    # (page table, page counts, lengths), taken by one small copy at the start
+    # of the step, so that the decision, which updates the live copy, may run
+    # beside it; only the compaction, which moves cached rows, waits for it.
+    n_req_meta = views["page_table"].numel() + 2 * R      # the first three parts of `meta`
+    snap = torch.empty(n_req_meta, dtype=torch.int32, device=dev)
+    npt = views["page_table"].numel()
+    ps_dec = gp.PageState(snap[:npt].view(views["page_table"].shape), snap[npt: npt + R], snap[npt + R:],
+                          views["refcount"], views["free_list"], views["free_count"])
+    live_req_meta = meta[:n_req_meta]
 
     def phase_score():
         # scoring, then the eviction lists every boundary request would use if
@@ -171,15 +188,24 @@ def main():
         gp.gp_boundary_decide(*bargs, hold=False)
         gp.gp_boundary_compact(*bargs)
 
+    def phase_decide():
+        gp.gp_boundary_decide(*bargs, hold=False)
+
+    def phase_compact():
+        gp.gp_boundary_compact(*bargs)
+
     side = torch.cuda.Stream()          # default priority, like the main stream
     phase = dict(pre=phase_pre, summaries=phase_summaries, decode=phase_decode, score=phase_score,
-                 apply=phase_apply)
+                 apply=phase_apply, snapshot=phase_snapshot, decode_snapshot=phase_decode_snapshot,
+                 decide=phase_decide, compact=phase_compact)
 
     def step(marks=None):
-        """One step on the current stream.  Scoring and selection only read,
-        so unless --serial they run beside decode attention on a second stream
-        (fork and join by stream waits, which graph capture records as
-        dependencies); the decision and compaction wait for both."""
+        """One step on the current stream.  Unless --serial, the summary
+        update, scoring, selection and the decision run beside decode attention
+        on a second stream (fork and join by stream waits, which graph capture
+        records as dependencies): decode reads its own snapshot of the request
+        metadata, which the decision does not touch.  The compaction waits for
+        both."""
         cur = torch.cuda.current_stream()
 
         def mark(name):
@@ -195,18 +221,22 @@ def main():
             phase["decode"]()
             mark("d1")
             phase["score"]()
+            phase["apply"]()
         else:
-            # decode attention needs only the page metadata: it forks right
-            # after the restore, beside the summary update and scoring
+            # decode attention needs only the snapshot of the request metadata:
+            # it forks right after the restore and the snapshot, beside the
+            # summary update, scoring, selection and the decision
+            phase["snapshot"]()
             side.wait_stream(cur)
             with torch.cuda.stream(side):
                 phase["summaries"]()
                 phase["score"]()
+                phase["decide"]()
             mark("d0")
-            phase["decode"]()
+            phase["decode_snapshot"]()
             mark("d1")
             cur.wait_stream(side)
-        phase["apply"]()
+            phase["compact"]()
         mark("b1")
 
     # warm up every call (and the library's lazy state) eagerly first

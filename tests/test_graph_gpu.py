@@ -16,10 +16,10 @@ pytestmark = pytest.mark.gpu
 @pytest.mark.parametrize("fork", [False, True, "bench"], ids=["one_stream", "score_on_side_stream",
                                                          "bench_step_layout"])
 def test_graph_replays_match_eager(fork):
-    """fork="bench" is the benchmark's step: the summary update, scoring and
-    selection on a side stream beside decode attention, then the decision and
-    compaction as separate calls; its eager result must also equal the plain
-    one-stream sequence."""
+    """fork="bench" is the benchmark's step: decode attention reads a snapshot
+    of the request metadata while the summary update, scoring, selection and
+    the decision run on a side stream beside it, then the compaction; its eager
+    result must also equal the plain one-stream sequence."""
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     import paper_2609_03494_amd as gp
@@ -57,18 +57,25 @@ def test_graph_replays_match_eager(fork):
 
     bargs = (dc.layers, dc.ps, bnd, counts, scores, params, dec, delta, ctr, ws_a)
 
+    # decode's snapshot of the request metadata (the benchmark's step)
+    snap_pt, snap_np, snap_sl = (torch.empty_like(t) for t in (dc.ps.page_table, dc.ps.num_pages,
+                                                                dc.ps.seq_lens))
+    ps_dec = gp.PageState(snap_pt, snap_np, snap_sl, dc.ps.refcount, dc.ps.free_list, dc.ps.free_count)
+
     def step_bench():
         reset()
         cur = torch.cuda.current_stream()
+        for t, t0 in ((snap_pt, dc.ps.page_table), (snap_np, dc.ps.num_pages), (snap_sl, dc.ps.seq_lens)):
+            torch.mul(t0, 1, out=t)
         aux.wait_stream(cur)
         with torch.cuda.stream(aux):
             gp.gp_update_summaries(dc.q_pre, dc.slot_ids, init, dc.qstate, p32.beta_s, p32.beta_l)
             gp.gp_boundary_score(dc.layers[0], dc.ps, dc.q_pre, dc.qstate, dc.slot_ids, dc.positions,
                                  bnd, params, counts, scores, ws_s)
             gp.gp_boundary_select(*bargs)
-        gp.gp_decode_attention(dc.layers[0], dc.ps, dc.q_post, p32.scale, out, dc.ws_decode)
+            gp.gp_boundary_decide(*bargs, hold=False)      # updates the live metadata only
+        gp.gp_decode_attention(dc.layers[0], ps_dec, dc.q_post, p32.scale, out, dc.ws_decode)
         cur.wait_stream(aux)
-        gp.gp_boundary_decide(*bargs, hold=False)
         gp.gp_boundary_compact(*bargs)
 
     def step():
