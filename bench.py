@@ -8,8 +8,8 @@ for every request, then boundary scoring, selection, the decision and compaction
 requests at a capacity boundary.  Inputs are seeded synthetic tensors resident
 in HBM before timing starts.  The step is captured once as a HIP graph and
 replayed (``--eager`` launches every call directly).  Decode attention reads
-a snapshot of the request metadata taken by one small copy at the start of the
-step, so the summary update, scoring, selection and the decision (which
+a snapshot of the request metadata (written by the restore, in the same
+launch), so the summary update, scoring, selection and the decision (which
 updates the live metadata) run on a second stream beside it; the compaction,
 which moves cached rows, waits for both (``--serial`` runs everything on one
 stream, decode on the live metadata).
@@ -116,8 +116,12 @@ def main():
     parts = dict(page_table=w.page_table, num_pages=w.num_pages, seq_lens=w.seq_lens,
                  refcount=w.refcount, free_list=w.free_list, free_count=np.array([w.free_count]))
     flat = np.concatenate([np.asarray(v, np.int32).ravel() for v in parts.values()])
-    meta0 = i32(flat)
-    meta = meta0.clone()
+    # followed by decode attention's snapshot of the request metadata (page
+    # table, page counts, lengths), which the restore writes in the same launch
+    n_req_meta = int(w.page_table.size) + 2 * R
+    meta0_ext = i32(np.concatenate([flat, flat[:n_req_meta]]))
+    meta_ext = meta0_ext.clone()
+    meta0, meta = meta0_ext[: flat.size], meta_ext[: flat.size]
     views, off = {}, 0
     for name, arr in parts.items():
         n = int(np.asarray(arr).size)
@@ -149,7 +153,7 @@ def main():
         # evolving from step to step, as they would in serving.  An elementwise
         # kernel rather than a copy: in a HIP graph a memcpy node costs a few
         # microseconds of scheduling before the kernel that follows it
-        torch.mul(meta0, 1, out=meta)
+        torch.mul(meta0_ext, 1, out=meta_ext)
 
     def phase_pre():
         restore()
@@ -160,23 +164,19 @@ def main():
     def phase_decode():
         gp.gp_decode_attention(kv, ps, q_post, params.scale, out, ws_d)
 
-    def phase_snapshot():
-        torch.mul(live_req_meta, 1, out=snap)
-
     def phase_decode_snapshot():
         gp.gp_decode_attention(kv, ps_dec, q_post, params.scale, out, ws_d)
 
     bargs = ([kv], ps, bnd, counts, scores, params, decisions, delta, counters, ws_a)
     # Decode attention reads a per-step snapshot of the request metadata
-    # (page table, page counts, lengths), taken by one small copy at the start
-    # of the step, so that the decision, which updates the live copy, may run
-    # beside it; only the compaction, which moves cached rows, waits for it.
-    n_req_meta = views["page_table"].numel() + 2 * R      # the first three parts of `meta`
-    snap = torch.empty(n_req_meta, dtype=torch.int32, device=dev)
+    # (page table, page counts, lengths), so that the decision, which updates
+    # the live copy, may run beside it; only the compaction, which moves cached
+    # rows, waits for it.  The restore writes the snapshot too (one launch); a
+    # serving loop without a restore would take it with one small copy.
+    snap = meta_ext[meta.numel():]
     npt = views["page_table"].numel()
     ps_dec = gp.PageState(snap[:npt].view(views["page_table"].shape), snap[npt: npt + R], snap[npt + R:],
                           views["refcount"], views["free_list"], views["free_count"])
-    live_req_meta = meta[:n_req_meta]
 
     def phase_score():
         # scoring, then the eviction lists every boundary request would use if
@@ -196,7 +196,7 @@ def main():
 
     side = torch.cuda.Stream()          # default priority, like the main stream
     phase = dict(pre=phase_pre, summaries=phase_summaries, decode=phase_decode, score=phase_score,
-                 apply=phase_apply, snapshot=phase_snapshot, decode_snapshot=phase_decode_snapshot,
+                 apply=phase_apply, decode_snapshot=phase_decode_snapshot,
                  decide=phase_decide, compact=phase_compact)
 
     def step(marks=None):
@@ -223,10 +223,9 @@ def main():
             phase["score"]()
             phase["apply"]()
         else:
-            # decode attention needs only the snapshot of the request metadata:
-            # it forks right after the restore and the snapshot, beside the
+            # decode attention needs only the snapshot of the request metadata
+            # (written by the restore): it forks right after it, beside the
             # summary update, scoring, selection and the decision
-            phase["snapshot"]()
             side.wait_stream(cur)
             with torch.cuda.stream(side):
                 phase["summaries"]()
