@@ -204,6 +204,25 @@ gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *
                                 const void *q_post, int32_t num_q_heads, float scale,
                                 void *out, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* gp_decode_attention in its two launches, for a caller that orders other
+ * work after the first (Sec. 3.1, same outputs):
+ *   GP_DECODE_CHUNKS  reads q_post and the cache through the page table: the
+ *                     outputs of requests that fit in one chunk, partial
+ *                     (max, sum, o) of the others into ws;
+ *   GP_DECODE_MERGE   folds those partials into the remaining outputs: reads
+ *                     ws and the lengths and page counts of `ps`, never the
+ *                     cache.
+ * `stages` is either bit or both; both stages in order, on one ws and the
+ * same `ps` contents, give the bytes of gp_decode_attention.  Between them
+ * the cache may be written (e.g. compacted), not ws, `out` or the lengths
+ * and page counts.  Takes the decode workspace; GP_ERR_INVALID for any other
+ * `stages`. */
+enum { GP_DECODE_CHUNKS = 1, GP_DECODE_MERGE = 2 };
+gp_status_t gp_decode_attention_stages(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
+                                       const void *q_post, int32_t num_q_heads, float scale,
+                                       void *out, int32_t stages, void *ws, size_t ws_bytes,
+                                       hipStream_t stream);
+
 /* The summary update and decode attention of one step in a single launch
  * (Sec. 4.1 folds the update into the attention kernel): the results are
  * those of gp_update_summaries(q_pre, kv->dtype, ps->num_reqs, num_q_heads,

@@ -23,10 +23,11 @@ GP_COMPRESS, GP_GROW, GP_FALLBACK, GP_PREEMPT, GP_NOT_BOUNDARY = 0, 1, 2, 3, 4
 GP_SHRINK = 5
 GP_POLICY_GROWPAGE, GP_POLICY_FIXED, GP_POLICY_RANDOM, GP_POLICY_INVERSE, GP_POLICY_SHRINK = 0, 1, 2, 3, 4
 GP_METRIC_TOP_P, GP_METRIC_ENTROPY = 0, 1
+GP_DECODE_CHUNKS, GP_DECODE_MERGE = 1, 2
 GP_LAYOUT_SHIFT, GP_LAYOUT_FILL = 0, 1
 PAGE_SIZE = 16
 
-EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_step", "gp_boundary_score",
+EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_attention_stages", "gp_decode_step", "gp_boundary_score",
            "gp_boundary_apply", "gp_boundary_select", "gp_boundary_decide", "gp_boundary_compact",
            "gp_release_held", "gp_append_step", "gp_workspace_bytes", "gp_status_string")
 
@@ -81,6 +82,9 @@ def load() -> ctypes.CDLL:
     lib.gp_decode_attention.restype = ctypes.c_int
     lib.gp_decode_attention.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, i32,
                                         f32, vp, vp, sz, vp]
+    lib.gp_decode_attention_stages.restype = ctypes.c_int
+    lib.gp_decode_attention_stages.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, i32,
+                                               f32, vp, i32, vp, sz, vp]
     lib.gp_decode_step.restype = ctypes.c_int
     lib.gp_decode_step.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, vp, i32, f32,
                                    vp, vp, vp, vp, i32, f32, f32, vp, sz, vp]
@@ -226,6 +230,16 @@ def gp_decode_attention(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale:
                                     q_post.shape[1], scale, _ptr(out), _ptr(ws), ws.numel(),
                                     _stream(stream))
     _check(st, "gp_decode_attention")
+
+
+def gp_decode_attention_stages(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale: float,
+                               out: torch.Tensor, stages: int, ws: torch.Tensor, stream=None) -> None:
+    """Decode attention's chunk pass (GP_DECODE_CHUNKS) and/or merge (GP_DECODE_MERGE)."""
+    c_kv, c_ps = kv.c(), ps.c()
+    st = load().gp_decode_attention_stages(ctypes.byref(c_kv), ctypes.byref(c_ps), _ptr(q_post),
+                                           q_post.shape[1], scale, _ptr(out), stages, _ptr(ws), ws.numel(),
+                                           _stream(stream))
+    _check(st, "gp_decode_attention_stages")
 
 
 def gp_decode_step(kv: KVLayer, ps: PageState, q_post: torch.Tensor, q_pre: torch.Tensor, scale: float,

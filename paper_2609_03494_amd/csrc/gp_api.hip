@@ -103,7 +103,7 @@ struct FoldedSummaries {
 
 gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
                         int32_t num_q_heads, float scale, void *out, void *ws, size_t ws_bytes,
-                        const FoldedSummaries *sum, hipStream_t stream) {
+                        const FoldedSummaries *sum, int stages, hipStream_t stream) {
     gp_status_t st = check_layer(kv);
     if (st != GP_OK) return st;
     if ((st = check_state(ps, kv)) != GP_OK) return st;
@@ -144,7 +144,7 @@ gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, cons
     a.max_chunks = w.max_chunks;
     a.chunk_pages = w.chunk_pages;
     a.qscale = scale * 1.4426950408889634f;
-    return from_hip(launch_decode(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stream));
+    return from_hip(launch_decode(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stages, stream));
 }
 
 }  // namespace
@@ -152,7 +152,15 @@ gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, cons
 gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
                                 int32_t num_q_heads, float scale, void *out, void *ws, size_t ws_bytes,
                                 hipStream_t stream) {
-    return decode_call(kv, ps, q_post, num_q_heads, scale, out, ws, ws_bytes, nullptr, stream);
+    return decode_call(kv, ps, q_post, num_q_heads, scale, out, ws, ws_bytes, nullptr,
+                       GP_DECODE_CHUNKS | GP_DECODE_MERGE, stream);
+}
+
+gp_status_t gp_decode_attention_stages(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
+                                       int32_t num_q_heads, float scale, void *out, int32_t stages, void *ws,
+                                       size_t ws_bytes, hipStream_t stream) {
+    if (stages < 1 || stages > (GP_DECODE_CHUNKS | GP_DECODE_MERGE)) return GP_ERR_INVALID;
+    return decode_call(kv, ps, q_post, num_q_heads, scale, out, ws, ws_bytes, nullptr, stages, stream);
 }
 
 gp_status_t gp_decode_step(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
@@ -160,7 +168,8 @@ gp_status_t gp_decode_step(const gp_kv_layer_t *kv, const gp_page_state_t *ps, c
                            const int32_t *slot_ids, const uint8_t *init, float *qstate, int32_t num_slots,
                            float beta_s, float beta_l, void *ws, size_t ws_bytes, hipStream_t stream) {
     const FoldedSummaries sum{q_pre, slot_ids, init, qstate, num_slots, beta_s, beta_l};
-    return decode_call(kv, ps, q_post, num_q_heads, scale, out, ws, ws_bytes, &sum, stream);
+    return decode_call(kv, ps, q_post, num_q_heads, scale, out, ws, ws_bytes, &sum,
+                       GP_DECODE_CHUNKS | GP_DECODE_MERGE, stream);
 }
 
 gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_pre,

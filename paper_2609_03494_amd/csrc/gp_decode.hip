@@ -633,17 +633,18 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
 }
 
 template <typename T, int D>
-hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, hipStream_t s) {
+hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, int stages, hipStream_t s) {
     dim3 mgrid(a.Hkv, a.R);
     constexpr bool bf16 = sizeof(T) == 2;
+    const bool chunks = stages & GP_DECODE_CHUNKS, merge = (stages & GP_DECODE_MERGE) && a.max_chunks > 1;
     switch (G) {
 #define GP_CASE(GG)                                                  \
     case GG:                                                         \
-        if (bf16)                                                    \
+        if (chunks && bf16)                                          \
             decode_split_kernel<D, GG><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
-        else                                                         \
+        else if (chunks)                                             \
             decode_kernel<float, D, GG><<<grid, 256, 0, s>>>(a);     \
-        if (a.max_chunks > 1) merge_kernel<T, D, GG><<<mgrid, 256, 0, s>>>(a); \
+        if (merge) merge_kernel<T, D, GG><<<mgrid, 256, 0, s>>>(a);  \
         break;
         GP_CASE(1) GP_CASE(2) GP_CASE(4) GP_CASE(8)
 #undef GP_CASE
@@ -654,13 +655,14 @@ hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_decode(gp_dtype_t dt, int D, int G, const DecodeArgs &a, hipStream_t s) {
+hipError_t launch_decode(gp_dtype_t dt, int D, int G, const DecodeArgs &a, int stages, hipStream_t s) {
     // the KV heads of one chunk are neighbours in dispatch order: they read the
     // head slices of the same pages at about the same time
     dim3 grid(a.Hkv, a.max_chunks, a.R);
     if (dt == GP_BF16)
-        return D == 128 ? launch_g<uint16_t, 128>(G, a, grid, s) : launch_g<uint16_t, 64>(G, a, grid, s);
-    return D == 128 ? launch_g<float, 128>(G, a, grid, s) : launch_g<float, 64>(G, a, grid, s);
+        return D == 128 ? launch_g<uint16_t, 128>(G, a, grid, stages, s)
+                        : launch_g<uint16_t, 64>(G, a, grid, stages, s);
+    return D == 128 ? launch_g<float, 128>(G, a, grid, stages, s) : launch_g<float, 64>(G, a, grid, stages, s);
 }
 
 }  // namespace gp

@@ -71,6 +71,10 @@ def test_host_validation_without_launch(lib):
     ps2 = _lib._PageState(fake, fake, fake, fake, fake, fake, 4, 10, 99)
     assert lib.gp_decode_attention(ctypes.byref(kv), ctypes.byref(ps2), fake, 32, 0.1, fake, fake,
                                    1 << 30, None) == 1
+    # staged decode: stages must be GP_DECODE_CHUNKS, GP_DECODE_MERGE or both
+    for bad_stages in (0, 4, -1):
+        assert lib.gp_decode_attention_stages(ctypes.byref(kv), ctypes.byref(ps), fake, 32, 0.1, fake,
+                                              bad_stages, fake, 1 << 30, None) == 1
     # summaries: beta outside [0, 1]
     assert lib.gp_update_summaries(fake, 1, 4, 32, 128, fake, fake, fake, 512, 1.5, 0.9, None) == 1
     # score: max_cand too small for the table width

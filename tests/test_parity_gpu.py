@@ -292,6 +292,31 @@ def test_decode_back_to_back_calls_see_their_own_partials(dtype):
         assert torch.equal(out, alone[j % 2]), f"call {j}"
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_decode_stages_equal_the_whole_call(dtype):
+    """The chunk pass, then the merge, equal gp_decode_attention bit for bit,
+    also when the cache is overwritten (NaN) between the two stages: the merge
+    reads only the workspace and the lengths."""
+    _say(f"decode: chunk pass + merge vs the whole call, {dtype}, cache poisoned in between")
+    w = W._build(name="stages", seed=43, dtype=dtype, Hq=8 if dtype == "f32" else 32,
+                 Hkv=2 if dtype == "f32" else 8, d=128, n=np.array([0, 5, 700, 1100, 2100, 4500, 6100]),
+                 budgets=None, free_pages=8, heavy_mode="scaled", heavy_frac=0.02, summary_mode="random")
+    dc = DeviceCase(w)
+    scale = float(np.float32(1 / math.sqrt(w.head_dim)))
+    whole = torch.empty_like(dc.q_post)
+    gp.gp_decode_attention(dc.layers[0], dc.ps, dc.q_post, scale, whole, dc.ws_decode)
+    torch.cuda.synchronize()
+    staged = torch.full_like(dc.q_post, float("nan"))
+    gp.gp_decode_attention_stages(dc.layers[0], dc.ps, dc.q_post, scale, staged, gp.GP_DECODE_CHUNKS,
+                                  dc.ws_decode)
+    dc.layers[0].k.fill_(float("nan"))
+    dc.layers[0].v.fill_(float("nan"))
+    gp.gp_decode_attention_stages(dc.layers[0], dc.ps, dc.q_post, scale, staged, gp.GP_DECODE_MERGE,
+                                  dc.ws_decode)
+    torch.cuda.synchronize()
+    assert torch.equal(staged, whole)
+
+
 @pytest.mark.parametrize("case", ["tiny_fp32", "qwen3_bf16", "g8_prefix_bf16"])
 def test_decode_step_fused_equals_separate(case):
     # gp_decode_step folds the summary update into decode attention: summaries
