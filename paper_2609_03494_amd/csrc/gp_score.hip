@@ -126,32 +126,36 @@ __global__ __launch_bounds__(256, 5) void prep_kernel(ScoreArgs a) {
 }
 
 // ------------------------------------------------------------------- logits --
-// Grid (KV head, blocks of kStatBlock candidates, boundary request), one wave
-// per workgroup.  The 2G x D logits of the block are a small fp64 matrix
+// Grid (KV head, blocks of kStatBlock candidates, boundary request), two
+// waves per workgroup, 32 candidates each.  The 2G x D logits of the block are a small fp64 matrix
 // product, done on the matrix cores with v_mfma_f64_16x16x4f64: the A operand
 // is the aligned summaries (row = view, padded to 16 rows with zeros), B the
-// keys of 16 candidates, so the block is four chains of D/4 MFMAs.  The
+// keys of 16 candidates, so each wave runs two chains of D/4 MFMAs.  The
 // contraction over head dimensions is split four ways across lane groups: in
 // step s, lane group q (lanes 16q .. 16q+15) supplies dimension (D/4) q + s,
 // so each lane reads one contiguous quarter row of summaries (once) and of
-// each of its four keys.  The result leaves view 4j + q of candidate l % 16 in
+// each of its keys.  The result leaves view 4j + q of candidate l % 16 in
 // register j of lane l.  Per view, the block's max m and sum of exp(z - m)
-// (16-lane reductions) go to the statistics array; exp(z - m) of each token
+// (16-lane reductions, then across the two waves in LDS) go to the
+// statistics array; exp(z - m) of each token
 // is stored (float32), so that the weights need a product, not an
 // exponential, per token.  A lane whose page id is invalid contributes zero logits.
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
+constexpr int kLogitsWaves = 2;                 // waves per block of kStatBlock candidates
 
 template <typename T, int D, int G>
-__global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(64 * kLogitsWaves) void logits_kernel(ScoreArgs a) {
     constexpr int V = 2 * G;
     constexpr int S = D / 4;                         // MFMA steps (head dimensions per lane group)
     constexpr int EPU = 16 / sizeof(T);              // key elements per 16-byte unit
     constexpr int NU = S / EPU;                      // 16-byte units of a quarter key row
-    constexpr int NGRP = kStatBlock / 16;            // candidate groups of 16 per block
-    static_assert(kStatBlock == 64 && V <= 16 && S % EPU == 0, "layout");
+    constexpr int NW = kLogitsWaves;
+    constexpr int NGRP = kStatBlock / 16 / NW;       // candidate groups of 16 per wave
+    static_assert(kStatBlock == 64 && V <= 16 && S % EPU == 0 && NGRP * 16 * NW == kStatBlock, "layout");
+    __shared__ double s_wm[NW][16], s_ws[NW][16];
 
     const int h = blockIdx.x, blk = blockIdx.y, i = blockIdx.z;
-    const int lane = threadIdx.x, col = lane & 15, q = lane >> 4;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col = lane & 15, q = lane >> 4;
     int r, P;
     if (!boundary_of(a, i, r, P)) return;
     const int C = (P - 1) * kPage;
@@ -174,9 +178,10 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
     }
     // B: this lane's quarter row of candidate t0 + 16 g + col, for the 4 groups
     uint4 kb[NGRP][NU];
+    const int tw = t0 + 16 * NGRP * wave;            // this wave's first candidate
 #pragma unroll
     for (int g = 0; g < NGRP; ++g) {
-        const int t = t0 + 16 * g + col;
+        const int t = tw + 16 * g + col;
         const int pe = a.page_table[(size_t)r * a.max_pages + min(t, C - 1) / kPage];
         const int phys = t < C ? pe : -1;
         const bool ok = phys >= 0 && phys < a.pool_pages;
@@ -200,35 +205,70 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
         }
     }
 
-    // statistics and exponentials per view (register j holds view 4j + q)
+    // statistics and exponentials per view (register j holds view 4j + q):
+    // per wave over its candidates, then the block's max and sum across the
+    // waves through LDS
     float *lgv = a.expz + ((size_t)i * a.Hkv + h) * V * a.cmax;
     double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch + blk) * V * 2;
+    double z[4][NGRP], mv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        mv[j] = -__builtin_huge_val();
+        if (4 * j >= V) continue;                    // uniform: no real view in this register
+#pragma unroll
+        for (int g = 0; g < NGRP; ++g) {
+            z[j][g] = acc[g][j] * a.scale;
+            if (tw + 16 * g + col < C) mv[j] = fmax(mv[j], z[j][g]);
+        }
+        for (int off = 8; off >= 1; off >>= 1) mv[j] = fmax(mv[j], __shfl_xor(mv[j], off, 16));
+        if (NW > 1 && col == 0) s_wm[wave][4 * j + q] = mv[j];
+    }
+    if (NW > 1) {
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (4 * j >= V) continue;
+            double m = s_wm[0][4 * j + q];
+#pragma unroll
+            for (int w = 1; w < NW; ++w) m = fmax(m, s_wm[w][4 * j + q]);
+            mv[j] = m;
+        }
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         const int v = 4 * j + q;
-        if (4 * j >= V) break;                       // uniform: no real view in this register
-        double z[NGRP];
-        double mv = -__builtin_huge_val();
-#pragma unroll
-        for (int g = 0; g < NGRP; ++g) {
-            z[g] = acc[g][j] * a.scale;
-            if (t0 + 16 * g + col < C) mv = fmax(mv, z[g]);
-        }
-        for (int off = 8; off >= 1; off >>= 1) mv = fmax(mv, __shfl_xor(mv, off, 16));
+        if (4 * j >= V) continue;
         double sv = 0.0;
 #pragma unroll
         for (int g = 0; g < NGRP; ++g) {
-            const int t = t0 + 16 * g + col;
+            const int t = tw + 16 * g + col;
             if (t < C && v < V) {
-                const double ev = exp(z[g] - mv);
+                const double ev = exp(z[j][g] - mv[j]);
                 sv += ev;
                 lgv[(size_t)v * a.cmax + t] = (float)ev;
             }
         }
         for (int off = 8; off >= 1; off >>= 1) sv += __shfl_xor(sv, off, 16);
-        if (col == 0 && v < V) {
-            pt[v * 2] = mv;
+        if (NW > 1) {
+            if (col == 0) s_ws[wave][v] = sv;
+        } else if (col == 0 && v < V) {
+            pt[v * 2] = mv[j];
             pt[v * 2 + 1] = sv;
+        }
+    }
+    if (NW > 1) {
+        __syncthreads();
+        if (wave == 0 && col == 0) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int v = 4 * j + q;
+                if (4 * j >= V || v >= V) continue;
+                double tot = 0.0;
+#pragma unroll
+                for (int w = 0; w < NW; ++w) tot += s_ws[w][v];
+                pt[v * 2] = mv[j];
+                pt[v * 2 + 1] = tot;
+            }
         }
     }
 }
@@ -546,7 +586,7 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
 #define GP_CASE(GG)                                                   \
     case GG:                                                          \
         prep_kernel<T, D, GG><<<g0, 256, 0, s>>>(a);                  \
-        logits_kernel<T, D, GG><<<g1, kStatBlock, 0, s>>>(a);                \
+        logits_kernel<T, D, GG><<<g1, 64 * kLogitsWaves, 0, s>>>(a);                \
         weights_kernel<GG><<<g2, 256, 0, s>>>(a);                     \
         break;
         GP_CASE(1) GP_CASE(2) GP_CASE(4) GP_CASE(8)
