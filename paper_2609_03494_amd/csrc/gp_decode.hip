@@ -332,13 +332,14 @@ __device__ inline float row_sum16(float x) {
 }
 
 // Split decode (bf16): one workgroup of kDecodeWaves waves per (KV head,
-// chunk, request); the waves take the chunk's pages round-robin and keep one
-// page in flight each: the keys of a wave's next page are requested as soon
-// as the matrix cores have consumed the current ones, its values as soon as
-// P.V has.  In P.V each lane owns D/64 head dimensions for all 16 tokens of
-// the page, so a value load reads one whole 2D-byte row per instruction and
-// the accumulators take G * D / 64 registers; Q waits in LDS.  The waves
-// merge through LDS at the end.
+// chunk, request); the waves take the chunk's pages round-robin.  As soon as
+// the matrix cores have consumed a page's keys, the wave requests the keys and
+// the values of its next page (the values into the second of two buffers that
+// alternate), so a whole page is on its way while softmax and P.V run.  In
+// P.V each lane owns D/64 head dimensions for all 16 tokens of the page, so a
+// value load reads one whole 2D-byte row per instruction and the accumulators
+// take G * D / 64 registers; Q waits in LDS.  The waves merge through LDS at
+// the end.
 template <int D, int G>
 __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeArgs a) {
     constexpr int KK = D / 32;            // MFMA steps per page
