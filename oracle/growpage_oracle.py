@@ -9,8 +9,12 @@ Paper: "GrowPage: On-Demand KV Budgeting for Efficient LLM Reasoning Serving"
 (arXiv 2609.03494).  Each function names the passage it follows.  Arithmetic is
 fp64 on inputs widened exactly from their storage type (float32 or bfloat16).
 Where a floating-point value decides an integer (top-p working-set sizes,
-Top-K selection), the decision is taken on the values rounded to float32, the
-precision in which the GPU path stores them; sums taken on the way are fp64.
+Top-K selection), the decision is taken on the values rounded to float32: the
+boundary interface hands the token scores over as float32 (one score per
+candidate and KV head), so selection is defined on float32 scores, and the
+working-set sizes are taken on the float32 weights those scores are the
+maximum of, so that both decisions rest on the same numbers.  Sums taken on
+the way are fp64.
 
 Readings of points the paper leaves open (each one also listed in the design
 notes) are marked "reading:" below.

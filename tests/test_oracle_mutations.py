@@ -85,3 +85,61 @@ def test_dropped_grouped_head_is_caught(monkeypatch):
         return a
     _patch(monkeypatch, "view_distributions", bad)
     _fails(pins.test_view_distributions_special_case_is_softmax)
+
+
+def test_token_score_mean_instead_of_max_is_caught(monkeypatch):
+    _patch(monkeypatch, "token_scores",
+           lambda a_s, a_l: ((np.asarray(a_s, np.float64) + np.asarray(a_l, np.float64)) / 2).astype(np.float32))
+    _fails(pins.test_golden_token_scores)
+
+
+def test_token_score_short_view_alone_is_caught(monkeypatch):
+    _patch(monkeypatch, "token_scores", lambda a_s, a_l: np.asarray(a_s, np.float32).copy())
+    _fails(pins.test_golden_token_scores)
+
+
+def test_token_score_long_view_alone_is_caught(monkeypatch):
+    _patch(monkeypatch, "token_scores", lambda a_s, a_l: np.asarray(a_l, np.float32).copy())
+    _fails(pins.test_golden_token_scores)
+
+
+def _fragile_with(shift: int, eps_factor: float = 1.0):
+    """top_p_fragile that checks the running sums `shift` terms later than it
+    should, or with a band eps_factor times too wide."""
+    def bad(a32, p, eps=1e-6):
+        v = np.sort(np.asarray(a32, dtype=np.float32).astype(np.float64))[::-1]
+        csum = np.cumsum(v)
+        k = G.top_p_count(a32, p) + shift
+        e = eps * eps_factor
+        near = 0 <= k - 1 < csum.size and abs(csum[k - 1] - p) <= e
+        if 0 <= k - 2 < csum.size:
+            near = near or abs(csum[k - 2] - p) <= e
+        return bool(near)
+    return bad
+
+
+@pytest.mark.parametrize("shift", [1, -1])
+def test_top_p_fragile_index_off_by_one_is_caught(monkeypatch, shift):
+    _patch(monkeypatch, "top_p_fragile", _fragile_with(shift))
+    _fails(pins.test_golden_top_p_fragile)
+
+
+def test_top_p_fragile_band_ten_times_too_wide_is_caught(monkeypatch):
+    _patch(monkeypatch, "top_p_fragile", _fragile_with(0, 10.0))
+    _fails(pins.test_golden_top_p_fragile)
+
+
+def test_entropy_fragile_band_ten_times_too_wide_is_caught(monkeypatch):
+    orig = G.entropy_fragile
+    _patch(monkeypatch, "entropy_fragile", lambda a32, eps=1e-6: orig(a32, 10 * eps))
+    _fails(pins.test_golden_entropy_fragile)
+
+
+def test_entropy_fragile_at_integers_instead_of_midpoints_is_caught(monkeypatch):
+    def bad(a32, eps=1e-6):
+        v = np.asarray(a32, dtype=np.float32).astype(np.float64)
+        v = v[v > 0]
+        e = float(np.exp(-np.sum(v * np.log(v))))
+        return bool(abs(e - round(e)) <= eps * max(1.0, e))
+    _patch(monkeypatch, "entropy_fragile", bad)
+    _fails(pins.test_golden_entropy_fragile)

@@ -532,3 +532,69 @@ def test_cpu_baseline_child_runs_the_oracle_on_worker_processes():
     assert cp.returncode == 0, cp.stderr[-500:]
     res = json.loads(cp.stdout.strip().splitlines()[-1])
     assert res["workers"] == 2 and res["passes"] >= 2 and res["bytes"] > 0 and res["seconds"] > 0
+
+
+# ------------------------------------------- token scores and fragility ----
+
+def test_golden_token_scores():
+    """s = max(a^S, a^L) per KV head (Sec. 3.3, token-score equation) through
+    the whole scoring of one request: keys built so that each view's softmax is
+    a hand-chosen distribution (tests/golden/token_score_worked.json)."""
+    g = _golden("token_score_worked.json")
+    b, P = g["b"], g["P"]
+    heads = g["heads"]
+    Hkv = len(heads)
+    C = (P - 1) * b
+    tokens = np.zeros((P * b, Hkv, 2), np.float32)
+    for h, hd in enumerate(heads):
+        tokens[:C, h] = np.array(hd["keys"], np.float32)
+    tokens[C:] = 0.0                                       # the protected page is not scored
+    q_t = np.tile(np.float32([1.0, 0.0]), (Hkv, 1))          # [Hq = Hkv, d]
+    qbar = np.zeros((2, Hkv, 2), np.float32)
+    qbar[0, :, 0] = 1.0                                    # short summary (1, 0)
+    qbar[1, :, 1] = 1.0                                    # long summary (0, 1)
+    params = O.Params(p=0.85, scale=1.0)
+    counts, scores, a32 = O.score_request(tokens, "f32", P, b, q_t, qbar, 0, params, 1.0)
+    for h, hd in enumerate(heads):
+        np.testing.assert_allclose(a32[0, h], hd["a_s"], rtol=1e-6, atol=0)
+        np.testing.assert_allclose(a32[1, h], hd["a_l"], rtol=1e-6, atol=0)
+        np.testing.assert_allclose(scores[h], hd["scores"], rtol=1e-6, atol=0)
+    # the direct form on the golden weights
+    for hd in heads:
+        s = O.token_scores(np.float32(hd["a_s"]), np.float32(hd["a_l"]))
+        np.testing.assert_array_equal(s, np.float32(hd["scores"]))
+
+
+def test_golden_top_p_fragile():
+    """Fragility of the top-p size at the 1e-6 band, just inside and just
+    outside it on either side of the K-th and (K-1)-th running sums
+    (tests/golden/top_p_fragile_worked.json)."""
+    g = _golden("top_p_fragile_worked.json")
+    a = np.float32(g["a"])
+    for case in g["cases"]:
+        assert O.top_p_count(a, case["p"]) == case["K"], case
+        assert O.top_p_fragile(a, case["p"], g["eps"]) == case["fragile"], case
+        # order of the weights does not matter
+        assert O.top_p_fragile(a[::-1].copy(), case["p"], g["eps"]) == case["fragile"], case
+
+
+def test_golden_entropy_fragile():
+    """Fragility of the entropy size: exp(H) within 1e-6 (relative) of a rounding
+    midpoint, tested at 1.5 +- 5e-7 (inside) and 1.5 +- 2e-6 (outside), plus
+    integer and far-from-midpoint cases (tests/golden/entropy_fragile_worked.json).
+    The golden's own claims are checked too: its q solves the binary-entropy
+    closed form, and scipy's entropy of each vector is the exp(H) the file
+    states (the normalisation scipy applies moves it by far less than the
+    tolerance)."""
+    from scipy.stats import entropy as scipy_entropy
+    g = _golden("entropy_fragile_worked.json")
+    q = g["q_star"]
+    assert abs(-q * math.log(q) - (1 - q) * math.log(1 - q) - math.log(1.5)) < 1e-15
+    for case in g["cases"]:
+        a = np.float32(case["a"])
+        w = a.astype(np.float64)
+        e_lib = float(np.exp(scipy_entropy(w / w.sum())))
+        assert abs(e_lib - case["exp_H"]) <= 5e-8 * case["exp_H"], case
+        assert O.entropy_fragile(a, g["eps"]) == case["fragile"], case
+        if not case["fragile"]:
+            assert O.entropy_count(a) == int(math.floor(case["exp_H"] + 0.5)), case
