@@ -224,12 +224,14 @@ gp_status_t gp_decode_attention_stages(const gp_kv_layer_t *kv, const gp_page_st
                                        hipStream_t stream);
 
 /* The summary update and decode attention of one step in a single launch
- * (Sec. 4.1 folds the update into the attention kernel): the results are
- * those of gp_update_summaries(q_pre, kv->dtype, ps->num_reqs, num_q_heads,
- * kv->head_dim, slot_ids, init, qstate, num_slots, beta_s, beta_l) followed by
- * gp_decode_attention(kv, ps, q_post, num_q_heads, scale, out, ws), bit for
- * bit.  q_pre has the layout and dtype of q_post.  Takes the decode
- * workspace. */
+ * (Sec. 4.1 folds the update into the attention kernel).  On a batch with no
+ * held request the results are those of gp_update_summaries(q_pre, kv->dtype,
+ * ps->num_reqs, num_q_heads, kv->head_dim, slot_ids, init, qstate, num_slots,
+ * beta_s, beta_l) followed by gp_decode_attention(kv, ps, q_post, num_q_heads,
+ * scale, out, ws), bit for bit.  A held request (seq_lens[r] < 0) is out of
+ * the step: no output and no summary update (gp_update_summaries, which does
+ * not see the lengths, would update it).  q_pre has the layout and dtype of
+ * q_post.  Takes the decode workspace. */
 gp_status_t gp_decode_step(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
                            const void *q_pre, int32_t num_q_heads, float scale, void *out,
                            const int32_t *slot_ids, const uint8_t *init, float *qstate, int32_t num_slots,
@@ -313,12 +315,19 @@ gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers,
  *             With hold != 0 a request that compresses or shrinks is left HELD
  *             (seq_lens[r] = -(new m) - 1) so that a decode step launched while
  *             its compaction runs leaves it out; otherwise as in apply.
- *  - compact: moves the rows and returns released pages to the stack.  Reads
- *             and writes only the pages of requests that compress or shrink,
- *             so it may run beside the next step's decode of the others.
- * gp_boundary_apply == select, decide (hold 0), compact on one stream.  The
- * workspace holds the event until compact has completed: an event that
- * overlaps the previous one's compaction needs a second workspace. */
+ *  - compact: moves the rows of the requests that compress or shrink, and
+ *             pushes the pages the event released onto the free stack
+ *             (free_list and *free_count).  The cached rows it reads and
+ *             writes are those of the moving requests only, so it may run
+ *             beside the next step's append and decode of the other requests.
+ * gp_boundary_apply == select, decide (hold 0), compact on one stream.
+ * Ordering: decide pops the free stack and compact pushes onto it, so the
+ * next event's decide -- and anything else that reads or changes free_list,
+ * free_count or the refcounts -- must be stream-ordered after the previous
+ * event's compact (otherwise a push and a pop race and a page can be handed
+ * out twice).  The workspace holds the event until compact has completed: an
+ * event whose select runs while the previous one's compact is still running
+ * needs a second workspace. */
 gp_status_t gp_boundary_select(const gp_kv_layer_t *layers, int32_t n_layers,
                                const gp_page_state_t *ps, const int32_t *bnd, int32_t num_bnd,
                                const int32_t *k_counts, const float *scores, int32_t max_cand,

@@ -595,12 +595,17 @@ def compact_tokens(tokens: np.ndarray, kept: np.ndarray, P: int, b: int, drop: i
 # ----------------------------------------------------------------------------
 
 def boundary_step(layers, dtype, state: PageState, q_pre, qstate, slot_ids, positions, bnd,
-                  params: Params, b: int = 16, draws=None):
+                  params: Params, b: int = 16, draws=None, counts=None):
     """Score, decide, select and compact, for every boundary request, over one or
     more layers.  ``layers`` is a list of (k_pool, v_pool) dense arrays
     [pool_pages, Hkv, b, d] (storage type) that are modified in place, and
     qstate a list with each layer's summary pool.
     ``q_pre`` and ``qstate`` are one array each, or a list with one per layer.
+    ``counts`` (optional, [Rb] of [layers, Hkv, 2]): working-set sizes to decide
+    with in place of the ones the scoring yields -- a test hook for sizes that
+    another implementation obtained where the rounding band excuses a
+    difference of one; scores and everything after the decision are computed
+    as usual.
     Returns dict(decisions, delta, counts, scores, kept, counters)."""
     n_layers = len(layers)
     q_layers = list(q_pre) if isinstance(q_pre, (list, tuple)) else [q_pre] * n_layers
@@ -630,6 +635,8 @@ def boundary_step(layers, dtype, state: PageState, q_pre, qstate, slot_ids, posi
         counts_all.append(np.stack(per_layer_c))
         scores_all.append(per_layer_s)
         weights_all.append(per_layer_w)
+    if counts is not None:
+        counts_all = [np.asarray(c, np.int64).copy() for c in counts]
     old_tables = {int(r): state.page_table[int(r)].copy() for r in bnd}
     old_pages = {int(r): int(state.num_pages[int(r)]) for r in bnd}
     dec, delta = decide_and_allocate(state, bnd, counts_all, b, params, draws)

@@ -14,6 +14,11 @@ import paper_2609_03494_amd as gp
 import workloads as W
 
 DEV = "cuda"
+# floor of the element-wise fp32 decode bar, relative to sum_i a_i |v_i,d|:
+# 2^-18 = 64 units of float32 rounding, the worst-case error of a sequential
+# fp32 sum of 64 terms (the kernels sum at most a page of tokens per lane and
+# step, over at most a few dozen steps, and merge partials in short trees)
+FP32_FLOOR = 2.0 ** -18
 
 
 def torch_dtype(w: W.Workload):
@@ -177,6 +182,27 @@ def assert_rows_close(got: np.ndarray, ref: np.ndarray, rtol: float, what: str):
     assert np.isfinite(got).all(), f"{what}: non-finite values"
     assert worst <= rtol, f"{what}: worst row-relative error {worst:.3e} > {rtol:.1e}"
     return worst
+
+
+class AbsPool:
+    """|values| of a pool view: decode attention over it gives, per output
+    element, sum_i a_i |v_i,d|, the magnitude at which the fp32 sums of that
+    element round."""
+
+    def __init__(self, view):
+        self.view = view
+
+    def __getitem__(self, pid):
+        return np.abs(self.view[pid])
+
+
+def fp32_elementwise_ok(got: np.ndarray, ref: np.ndarray, ref_abs: np.ndarray, rtol: float = 1e-5,
+                        floor: float = FP32_FLOOR) -> bool:
+    """Element-wise fp32 bar: |got - ref| <= rtol |ref| + floor * sum_i a_i |v_i,d|.
+    The floor term is the rounding scale of the weighted sum that produces the
+    element (a sum over the resident tokens of terms of size a_i |v_i,d|); it
+    keeps elements that nearly cancel from demanding more than fp32 can give."""
+    return bool((np.abs(got - ref) <= rtol * np.abs(ref) + floor * ref_abs).all())
 
 
 def bf16_rounding_ok(got: np.ndarray, ref: np.ndarray, extra: float = 1e-5) -> bool:

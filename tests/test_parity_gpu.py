@@ -19,8 +19,8 @@ import torch
 import oracle as O
 import paper_2609_03494_amd as gp
 import workloads as W
-from _harness import (DEV, DeviceCase, PoolView, assert_rows_close, bf16_rounding_ok, oracle_state,
-                      row_index, threshold_band, to_numpy)
+from _harness import (DEV, AbsPool, DeviceCase, PoolView, assert_rows_close, bf16_rounding_ok,
+                      fp32_elementwise_ok, oracle_state, row_index, threshold_band, to_numpy)
 
 pytestmark = pytest.mark.gpu
 
@@ -59,19 +59,29 @@ def _betas():
     return p.beta_s, p.beta_l
 
 
-def _decode_check(w, dc, requests=None):
+def _decode_compare(w, got, requests=None, seq_lens=None, what="decode"):
+    """GPU decode outputs (fp64 view, [R, Hq, d]) against the oracle's."""
     scale = float(np.float32(1.0 / math.sqrt(w.head_dim)))
-    got = dc.decode(scale)
     pool_k, pool_v = PoolView(w, "k"), PoolView(w, "v")
     reqs = list(range(w.num_reqs)) if requests is None else list(requests)
-    ref = O.decode_attention(pool_k, pool_v, w.dtype, w.page_table, w.seq_lens, w.q_post,
+    sl = w.seq_lens if seq_lens is None else seq_lens
+    ref = O.decode_attention(pool_k, pool_v, w.dtype, w.page_table, sl, w.q_post,
                              w.num_q_heads, scale, requests=reqs)
     got, ref = got[reqs], ref[reqs]
     if w.dtype == "f32":
-        return assert_rows_close(got, ref, 1e-5, "decode fp32")
-    worst = assert_rows_close(got, ref, 2e-2, "decode bf16")
-    assert bf16_rounding_ok(got, ref), "decode bf16: beyond bf16 rounding of the exact value"
+        ref_abs = O.decode_attention(pool_k, AbsPool(pool_v), w.dtype, w.page_table, sl, w.q_post,
+                                     w.num_q_heads, scale, requests=reqs)[reqs]
+        worst = assert_rows_close(got, ref, 1e-5, f"{what} fp32")
+        assert fp32_elementwise_ok(got, ref, ref_abs), f"{what} fp32: element-wise bar"
+        return worst
+    worst = assert_rows_close(got, ref, 2e-2, f"{what} bf16")
+    assert bf16_rounding_ok(got, ref), f"{what} bf16: beyond bf16 rounding of the exact value"
     return worst
+
+
+def _decode_check(w, dc, requests=None):
+    scale = float(np.float32(1.0 / math.sqrt(w.head_dim)))
+    return _decode_compare(w, dc.decode(scale), requests)
 
 
 def _fragile(a32, p32):
@@ -106,8 +116,11 @@ def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=N
                           draws=draws)
     got = dc.boundary(params, bnd=bnd, draws=draws)
     b = w.page_size
-    # working-set sizes and scores, per layer
-    fragile = set()
+    # working-set sizes and scores, per layer; where a size is fragile (the
+    # oracle's running sum passes p within 1e-6) the GPU's may differ by one,
+    # and the oracle then decides with the GPU's size
+    adjusted = [np.asarray(c, np.int64).copy() for c in ref["counts"]]
+    moved = 0
     for i, r in enumerate(bnd):
         P = int(before_state.num_pages[r])
         C = (P - 1) * b if int(before_state.seq_lens[r]) == P * b and P >= 2 else 0
@@ -116,22 +129,27 @@ def _boundary_check(w, params, qstate_host=None, dc=None, bnd=None, free_count=N
                 for x in range(2):
                     g, o = int(got["k_counts"][ell, i, h, x]), int(ref["counts"][i][ell, h, x])
                     a32 = ref["weights"][i][ell][x, h]
-                    if a32.size and _fragile(a32, p32):
-                        fragile.add(i)
-                        assert abs(g - o) <= 1, (i, ell, h, x, g, o)
-                    else:
-                        assert g == o, f"K^{'SL'[x]} of boundary {i} layer {ell} head {h}: gpu {g} oracle {o}"
+                    if g != o:
+                        assert a32.size and _fragile(a32, p32) and abs(g - o) == 1, \
+                            f"K^{'SL'[x]} of boundary {i} layer {ell} head {h}: gpu {g} oracle {o}"
+                        adjusted[i][ell, h, x] = g
+                        moved += 1
                 if C:
                     np.testing.assert_allclose(got["scores"][ell, i, h, :C], ref["scores"][i][ell][h],
                                                rtol=1e-5, atol=0,
                                                err_msg=f"scores boundary {i} layer {ell} head {h}")
+    if moved:
+        # the same event in the oracle from the starting state, deciding with
+        # the GPU's sizes where they differ (inside the band); everything after
+        # the decision is then compared exactly
+        _say(f"  {moved} fragile working-set size(s) differ by one; oracle re-decides with them")
+        pools = [(k.copy(), v.copy()) for k, v in pools0]
+        st = before_state.copy()
+        ref = O.boundary_step(pools, w.dtype, st, q_layers, s_layers, w.slot_ids, w.positions, bnd, p32,
+                              draws=draws, counts=adjusted)
     # decisions
     dec_g, dec_o = got["decisions"], ref["decisions"]
-    for i in range(len(bnd)):
-        if dec_g[i] != dec_o[i]:
-            assert i in fragile, f"decision {i}: gpu {dec_g[i]} oracle {dec_o[i]}"
-    if (dec_g != dec_o).any():
-        pytest.skip("a decision flipped on a fragile top-p count (excused); state not comparable")
+    np.testing.assert_array_equal(dec_g, dec_o)
     np.testing.assert_array_equal(got["delta"], ref["delta"])
     np.testing.assert_array_equal(got["counters"], ref["counters"])
     # page state, bit-exact
@@ -356,8 +374,72 @@ def test_decode_step_fused_equals_separate(case):
     np.testing.assert_array_equal(qs_f.view(np.int32), ref_qs.view(np.int32))
     np.testing.assert_array_equal(qs_f.view(np.int32), qs_s.view(np.int32))
     np.testing.assert_array_equal(out_f, out_s)
+    # the fused outputs against the oracle's decode attention directly
+    sl = w.seq_lens.copy()
+    if empty is not None:
+        sl[empty] = 0
+    _decode_compare(w, O.widen(out_f, w.dtype), seq_lens=sl, what="fused decode step")
     if empty is not None:
         assert (O.widen(out_f[empty], w.dtype) == 0).all()
+
+
+def test_decode_step_fused_with_held_request_against_oracle():
+    """gp_decode_step on a batch with a held request (App. E.3): the held row of
+    the output is not written and its summaries stay as they were; every other
+    request matches the oracle's update_summaries + decode_attention."""
+    _say("decode step (fused summaries): a held request is left out")
+    w = W.qwen3_8b(seed=33, num_reqs=7, len_lo=30, len_hi=2500, budget_choices=(4, 40, 200), free_pages=32)
+    scale = float(np.float32(1.0 / math.sqrt(w.head_dim)))
+    bs, bl = _betas()
+    held = 3
+    dc = DeviceCase(w)
+    dc.ps.seq_lens[held] = -int(w.seq_lens[held]) - 1
+    out = torch.full_like(dc.q_post, float("nan"))
+    init = np.zeros(w.num_reqs, np.uint8)
+    init[0] = 1
+    gp.gp_decode_step(dc.layers[0], dc.ps, dc.q_post, dc.q_pre, scale, out, dc.slot_ids,
+                      torch.from_numpy(init).to(DEV), dc.qstate, bs, bl, dc.ws_decode)
+    torch.cuda.synchronize()
+    got = O.widen(to_numpy(out), w.dtype)
+    assert np.isnan(got[held]).all(), "the held request's output row was written"
+    active = [r for r in range(w.num_reqs) if r != held]
+    _decode_compare(w, got, requests=active, what="fused decode step")
+    idx = np.array(active)
+    ref_qs = O.update_summaries(w.q_pre[idx], w.dtype, w.slot_ids[idx], init[idx], w.qstate, bs, bl)
+    np.testing.assert_array_equal(dc.qstate.cpu().numpy().view(np.int32), ref_qs.view(np.int32))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_g1_decode_and_boundary(dtype):
+    """GQA ratio 1 (one query head per KV head): decode attention, and boundary
+    events at tau = 0 and with every request compressing."""
+    _say(f"G = 1: decode and boundary, {dtype}")
+    d = 128 if dtype == "bf16" else 64
+    w = W._build(name="g1", seed=44, dtype=dtype, Hq=4, Hkv=4, d=d,
+                 n=np.array([33, 48, 401, 1024, 2001, 2048, 3001]), budgets=None, free_pages=8,
+                 heavy_mode="scaled", heavy_frac=0.02, summary_mode="random")
+    assert len(w.boundary) == 3
+    _decode_check(w, DeviceCase(w))
+    for tau in (0.0, math.inf):
+        _boundary_check(w, O.Params(tau=tau))
+
+
+@pytest.mark.parametrize("tau", [math.inf, -math.inf])
+def test_boundary_tables_beyond_2048_pages(tau):
+    """Requests of 2050 and 3000 pages at a boundary (table 3004 pages wide):
+    the selection's second pass over pages beyond the 2048 it keeps in
+    registers, top-p over more candidates than it caches, and compaction over
+    188 chunks; plus decode attention over the same requests."""
+    _say(f"boundary: requests of 2050 and 3000 pages, tau {tau}")
+    n = np.array([2050 * 16, 2600 * 16 + 5, 3000 * 16])
+    w = W._build(name="wide", seed=45, dtype="bf16", Hq=8, Hkv=2, d=128, n=n, budgets=None,
+                 free_pages=40, heavy_mode="scaled", heavy_frac=0.01, summary_mode="random")
+    assert w.boundary.tolist() == [0, 2] and w.max_pages > 3000
+    dc = DeviceCase(w)
+    _decode_check(w, dc)
+    res = _boundary_check(w, O.Params(tau=tau), dc=dc)
+    want = O.COMPRESS if tau > 0 else O.GROW
+    assert (res["decisions"] == want).all()
 
 
 def test_boundary_tiny_all_branches():
@@ -593,29 +675,31 @@ def _full_size_check(w, n_sample, seed=0):
     before = oracle_state(w)
     st = oracle_state(w)
     res_g = dc.boundary(O.Params())
-    counts, scores, fragile = [], [], set()
+    counts, scores, moved = [], [], 0
     for i, r in enumerate(w.boundary):
         P = int(w.num_pages[r])
         toks = O.gather_tokens(PoolView(w, "k"), w.page_table[r], P * b, b)
         c, sc, a32 = O.score_request(toks, w.dtype, P, b, w.q_pre[r], w.qstate[w.slot_ids[r]],
                                      int(w.positions[r]), p32, p32.scale)
+        c = np.asarray(c, np.int64).copy()
         for h in range(w.num_kv_heads):
             for x in range(2):
                 g = int(res_g["k_counts"][0, i, h, x])
-                if O.top_p_fragile(a32[x, h], p32.p):
-                    fragile.add(i)
-                    assert abs(g - int(c[h, x])) <= 1
-                else:
-                    assert g == int(c[h, x]), f"K^{'SL'[x]} of boundary {i} head {h}"
+                if g != int(c[h, x]):
+                    # inside the rounding band the oracle decides with the GPU's size
+                    assert O.top_p_fragile(a32[x, h], p32.p, 1e-6) and abs(g - int(c[h, x])) == 1, \
+                        f"K^{'SL'[x]} of boundary {i} head {h}: gpu {g} oracle {int(c[h, x])}"
+                    c[h, x] = g
+                    moved += 1
             np.testing.assert_allclose(res_g["scores"][0, i, h, : (P - 1) * b], sc[h], rtol=1e-5, atol=0)
         counts.append(c[None])
         scores.append(sc)
+    if moved:
+        _say(f"  {moved} fragile working-set size(s) differ by one; the oracle decides with the GPU's")
     dec, delta = O.decide_and_allocate(st, w.boundary, counts, b, p32)
     _say("  decisions", np.bincount(dec, minlength=4).tolist())
-    for i in np.nonzero(res_g["decisions"] != dec)[0]:
-        assert i in fragile, f"decision {i}: gpu {res_g['decisions'][i]} oracle {dec[i]}"
-    if (res_g["decisions"] != dec).any():
-        pytest.skip("a decision flipped on a fragile top-p count (excused); state not comparable")
+    np.testing.assert_array_equal(res_g["decisions"], dec)
+    np.testing.assert_array_equal(res_g["delta"], delta)
     gs = dc.host_state()
     for name in ("page_table", "num_pages", "seq_lens", "refcount"):
         np.testing.assert_array_equal(getattr(gs, name), getattr(st, name), err_msg=name)
