@@ -21,7 +21,9 @@
  *    memory and are read during the call only.
  *  - The library allocates and frees nothing, never synchronises the stream
  *    and keeps no global state: every call only enqueues kernels on `stream`
- *    and returns.  Results are valid once the stream has reached them.
+ *    and returns.  Results are valid once the stream has reached them.  (One
+ *    exception: gp_decode_attention_noalloc keeps its partials in a static
+ *    8 MiB device array, one per device, and caches that array's address.)
  *  - Host-side validation returns a status without launching anything.  A
  *    launch failure returns GP_ERR_HIP.  Device-side state that breaks the
  *    layout contract (page ids out of range, seq_len above the pages held) is
@@ -79,7 +81,8 @@ typedef enum {
     GP_ERR_INVALID = 1,      /* null pointer, negative size, inconsistent shapes */
     GP_ERR_UNSUPPORTED = 2,  /* page size, head_dim or GQA ratio not built       */
     GP_ERR_WORKSPACE = 3,    /* ws_bytes below gp_workspace_bytes()              */
-    GP_ERR_HIP = 4           /* a kernel launch failed                           */
+    GP_ERR_HIP = 4,          /* a kernel launch failed                           */
+    GP_ERR_SCRATCH = 5       /* beyond the static scratch of a no-allocation call */
 } gp_status_t;
 
 typedef enum { GP_F32 = 0, GP_BF16 = 1 } gp_dtype_t;
@@ -203,6 +206,22 @@ gp_status_t gp_update_summaries(const void *q_pre, gp_dtype_t dtype, int32_t num
 gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
                                 const void *q_post, int32_t num_q_heads, float scale,
                                 void *out, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* gp_decode_attention without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments and results as
+ * gp_decode_attention; the split partials go to a static device array of
+ * 8 MiB (one per device, held until the process ends), so the call allocates
+ * nothing.  A batch whose decode workspace (gp_workspace_bytes(GP_OP_DECODE,
+ * ...)) exceeds 8 MiB returns GP_ERR_SCRATCH without launching.  `stream`
+ * must belong to the current device (else GP_ERR_INVALID).  Every call on a
+ * device shares that device's array: calls that overlap on one device (on
+ * different streams, or a later call before an earlier one has completed on
+ * another stream) race and give undefined results; calls in one stream's
+ * order are safe.  Nothing in the array needs to start at zero. */
+gp_status_t gp_decode_attention_noalloc(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
+                                        const void *q_post, int32_t num_q_heads, float scale,
+                                        void *out, hipStream_t stream);
 
 /* gp_decode_attention in its two launches, for a caller that orders other
  * work after the first (Sec. 3.1, same outputs):

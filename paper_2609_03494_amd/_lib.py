@@ -26,8 +26,10 @@ GP_METRIC_TOP_P, GP_METRIC_ENTROPY = 0, 1
 GP_DECODE_CHUNKS, GP_DECODE_MERGE = 1, 2
 GP_LAYOUT_SHIFT, GP_LAYOUT_FILL = 0, 1
 PAGE_SIZE = 16
+GP_ERR_SCRATCH = 5
 
-EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_attention_stages", "gp_decode_step", "gp_boundary_score",
+EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_attention_noalloc",
+           "gp_decode_attention_stages", "gp_decode_step", "gp_boundary_score",
            "gp_boundary_apply", "gp_boundary_select", "gp_boundary_decide", "gp_boundary_compact",
            "gp_release_held", "gp_append_step", "gp_workspace_bytes", "gp_status_string")
 
@@ -82,6 +84,9 @@ def load() -> ctypes.CDLL:
     lib.gp_decode_attention.restype = ctypes.c_int
     lib.gp_decode_attention.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, i32,
                                         f32, vp, vp, sz, vp]
+    lib.gp_decode_attention_noalloc.restype = ctypes.c_int
+    lib.gp_decode_attention_noalloc.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp,
+                                                i32, f32, vp, vp]
     lib.gp_decode_attention_stages.restype = ctypes.c_int
     lib.gp_decode_attention_stages.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, i32,
                                                f32, vp, i32, vp, sz, vp]
@@ -230,6 +235,16 @@ def gp_decode_attention(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale:
                                     q_post.shape[1], scale, _ptr(out), _ptr(ws), ws.numel(),
                                     _stream(stream))
     _check(st, "gp_decode_attention")
+
+
+def gp_decode_attention_noalloc(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale: float,
+                                out: torch.Tensor, stream=None) -> None:
+    """gp_decode_attention with its partials in the library's static scratch
+    (no workspace, nothing allocated)."""
+    c_kv, c_ps = kv.c(), ps.c()
+    st = load().gp_decode_attention_noalloc(ctypes.byref(c_kv), ctypes.byref(c_ps), _ptr(q_post),
+                                            q_post.shape[1], scale, _ptr(out), _stream(stream))
+    _check(st, "gp_decode_attention_noalloc")
 
 
 def gp_decode_attention_stages(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale: float,

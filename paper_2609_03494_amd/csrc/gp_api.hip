@@ -3,11 +3,45 @@
 // then enqueues its kernels on the caller's stream and returns.
 #include <math.h>
 
+#include <mutex>
+
 #include "gp_internal.h"
 
 using namespace gp;
 
+// Scratch of gp_decode_attention_noalloc, for callers that cannot allocate:
+// the decode partials live in this array, one copy per device, held until the
+// process ends.  In host code `scratch` only names the symbol; its device
+// address comes from hipGetSymbolAddress (scratch_address below).
+constexpr size_t kScratchBytes = size_t(8) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices];     // device address of `scratch`, per device
+
+// The address of `scratch` on the device `stream` runs on, which must be the
+// current device; looked up once per device, with that device current.
+gp_status_t scratch_address(hipStream_t stream, void **out) {
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return GP_ERR_HIP;
+    if (stream) {
+        hipDevice_t sd = 0;
+        if (hipStreamGetDevice(stream, &sd) != hipSuccess) return GP_ERR_HIP;
+        if (sd != cur) return GP_ERR_INVALID;
+    }
+    if (cur < 0 || cur >= kMaxDevices) return GP_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[cur]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return GP_ERR_HIP;
+        g_scratch_ptr[cur] = p;
+    }
+    *out = g_scratch_ptr[cur];
+    return GP_OK;
+}
 
 bool dims_ok(int Hq, int Hkv, int D) {
     if (Hkv <= 0 || Hq <= 0 || Hq % Hkv) return false;
@@ -46,6 +80,8 @@ const char *gp_status_string(gp_status_t s) {
         case GP_ERR_UNSUPPORTED: return "unsupported shape (page size 16, head_dim 64/128, GQA ratio 1/2/4/8)";
         case GP_ERR_WORKSPACE: return "workspace too small";
         case GP_ERR_HIP: return "HIP launch failed";
+        case GP_ERR_SCRATCH:
+            return "problem needs more than the 8 MiB static scratch of gp_decode_attention_noalloc";
     }
     return "unknown status";
 }
@@ -101,9 +137,10 @@ struct FoldedSummaries {
     float beta_s, beta_l;
 };
 
+// noalloc: ws and ws_bytes are ignored; the partials go to the static scratch.
 gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
                         int32_t num_q_heads, float scale, void *out, void *ws, size_t ws_bytes,
-                        const FoldedSummaries *sum, int stages, hipStream_t stream) {
+                        const FoldedSummaries *sum, int stages, hipStream_t stream, bool noalloc = false) {
     gp_status_t st = check_layer(kv);
     if (st != GP_OK) return st;
     if ((st = check_state(ps, kv)) != GP_OK) return st;
@@ -115,12 +152,17 @@ gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, cons
             return GP_ERR_INVALID;
     }
     if (ps->num_reqs == 0) return GP_OK;
-    if (!q_post || !out || !ws) return GP_ERR_INVALID;
+    if (!q_post || !out || (!ws && !noalloc)) return GP_ERR_INVALID;
     if (sum && (!sum->q_pre || !sum->slot_ids || !sum->init || !sum->qstate)) return GP_ERR_INVALID;
     const DecodeWs w = decode_ws(ps->num_reqs, num_q_heads, kv->num_kv_heads, kv->head_dim, ps->max_pages);
-    if (ws_bytes < w.total) return GP_ERR_WORKSPACE;
     if (ps->num_reqs > 65535 || w.max_chunks > kMaxDecodeChunks || w.chunk_pages > kMaxChunkPages)
         return GP_ERR_UNSUPPORTED;
+    if (noalloc) {
+        if (w.total > kScratchBytes) return GP_ERR_SCRATCH;
+        if ((st = scratch_address(stream, &ws)) != GP_OK) return st;
+        ws_bytes = kScratchBytes;
+    }
+    if (ws_bytes < w.total) return GP_ERR_WORKSPACE;
     DecodeArgs a;
     a.k = kv->k;
     a.v = kv->v;
@@ -154,6 +196,13 @@ gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *
                                 hipStream_t stream) {
     return decode_call(kv, ps, q_post, num_q_heads, scale, out, ws, ws_bytes, nullptr,
                        GP_DECODE_CHUNKS | GP_DECODE_MERGE, stream);
+}
+
+gp_status_t gp_decode_attention_noalloc(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
+                                        const void *q_post, int32_t num_q_heads, float scale, void *out,
+                                        hipStream_t stream) {
+    return decode_call(kv, ps, q_post, num_q_heads, scale, out, nullptr, 0, nullptr,
+                       GP_DECODE_CHUNKS | GP_DECODE_MERGE, stream, true);
 }
 
 gp_status_t gp_decode_attention_stages(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,

@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for code in range(5):
+    for code in range(6):
         assert gp.status_string(code)
 
 
@@ -118,6 +118,11 @@ def test_host_validation_without_launch(lib):
                                   fake, fake, fake, fake, 1 << 30, None) == 2
     assert lib.gp_boundary_decide(arr, 65, ctypes.byref(ps), fake, 2, fake, fake, 144, ctypes.byref(p),
                                   fake, fake, fake, fake, 1 << 30, None, 1) == 2
+    # no-allocation decode: null layer; a batch whose partials exceed the 8 MiB
+    # static scratch is refused on the host (GP_ERR_SCRATCH) before any device call
+    assert lib.gp_decode_attention_noalloc(None, ctypes.byref(ps), fake, 32, 0.1, fake, None) == 1
+    big = _lib._PageState(fake, fake, fake, fake, fake, fake, 2048, 8192, 100)
+    assert lib.gp_decode_attention_noalloc(ctypes.byref(kv), ctypes.byref(big), fake, 32, 0.1, fake, None) == 5
     # zero requests is a no-op that succeeds
     ps0 = _lib._PageState(fake, fake, fake, fake, fake, fake, 0, 10, 100)
     assert lib.gp_decode_attention(ctypes.byref(kv), ctypes.byref(ps0), fake, 32, 0.1, fake, fake, 0,
