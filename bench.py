@@ -321,6 +321,33 @@ def main():
     fused_ms = timed_loop(fused_step)
     separate_ms = timed_loop(separate_step)
 
+    # the step's new token folded in as well (one launch: K/V append into the
+    # pages, summaries, decode attention, lengths advanced) against the loop
+    # prologue and decode attention as two launches; both restore the page
+    # metadata and positions before each call so that every call does the same
+    # work
+    tok = W.step_inputs(w, 1, seed=1)[0]
+    k_tok, v_tok = bf(tok["k_new"][0]), bf(tok["v_new"][0])
+    pos0 = positions.clone()
+
+    def token_fused():
+        restore()
+        positions.copy_(pos0)
+        gp.gp_decode_step(kv, ps, q_post, q_pre, params.scale, out, slots, init, qstate,
+                          params.beta_s, params.beta_l, ws_d, k_new=k_tok, v_new=v_tok, positions=positions)
+
+    def token_separate():
+        restore()
+        positions.copy_(pos0)
+        gp.gp_append_step([kv], ps, positions, k_tok[None], v_tok[None], q_pre[None], slots, init,
+                          qstate[None], params.beta_s, params.beta_l)
+        gp.gp_decode_attention(kv, ps, q_post, params.scale, out, ws_d)
+
+    token_fused_ms = timed_loop(token_fused)
+    token_separate_ms = timed_loop(token_separate)
+    restore()
+    positions.copy_(pos0)
+
     # instrumented pass (eager launches, events between phases): how much of a
     # step the boundary work adds after decode attention has finished
     marks = {"d0": [], "d1": [], "b1": []}
@@ -438,7 +465,9 @@ def main():
                              "ms_caches_flushed": round(decode_cold_ms, 4),
                              "ms_caches_flushed_p10_p50_p90": decode_cold_pct,
                              "with_summaries_one_launch_ms": round(fused_ms, 4),
-                             "with_summaries_two_launches_ms": round(separate_ms, 4)},
+                             "with_summaries_two_launches_ms": round(separate_ms, 4),
+                             "with_token_and_summaries_one_launch_ms": round(token_fused_ms, 4),
+                             "append_step_then_decode_two_launches_ms": round(token_separate_ms, 4)},
         "boundary": {"ms_after_decode": round(boundary_ms, 4),
                      "events_per_s": round(Rb / (step_ms * 1e-3), 1),
                      "overlapped_with_decode": not args.serial,

@@ -229,8 +229,8 @@ gp_status_t gp_decode_attention_noalloc(const gp_kv_layer_t *kv, const gp_page_s
  *                     outputs of requests that fit in one chunk, partial
  *                     (max, sum, o) of the others into ws;
  *   GP_DECODE_MERGE   folds those partials into the remaining outputs: reads
- *                     ws and the lengths and page counts of `ps`, never the
- *                     cache.
+ *                     ws (which also records each request's length), never
+ *                     the cache.
  * `stages` is either bit or both; both stages in order, on one ws and the
  * same `ps` contents, give the bytes of gp_decode_attention.  Between them
  * the cache may be written (e.g. compacted), not ws, `out` or the lengths
@@ -242,19 +242,38 @@ gp_status_t gp_decode_attention_stages(const gp_kv_layer_t *kv, const gp_page_st
                                        void *out, int32_t stages, void *ws, size_t ws_bytes,
                                        hipStream_t stream);
 
-/* The summary update and decode attention of one step in a single launch
- * (Sec. 4.1 folds the update into the attention kernel).  On a batch with no
- * held request the results are those of gp_update_summaries(q_pre, kv->dtype,
- * ps->num_reqs, num_q_heads, kv->head_dim, slot_ids, init, qstate, num_slots,
- * beta_s, beta_l) followed by gp_decode_attention(kv, ps, q_post, num_q_heads,
- * scale, out, ws), bit for bit.  A held request (seq_lens[r] < 0) is out of
- * the step: no output and no summary update (gp_update_summaries, which does
- * not see the lengths, would update it).  q_pre has the layout and dtype of
- * q_post.  Takes the decode workspace. */
+/* The step's new token, the summary update and decode attention in a single
+ * launch (Sec. 4.1 folds the per-step work into the attention kernel).
+ *  - Without a token (k_new == v_new == NULL): on a batch with no held request
+ *    the results are those of gp_update_summaries(q_pre, kv->dtype,
+ *    ps->num_reqs, num_q_heads, kv->head_dim, slot_ids, init, qstate,
+ *    num_slots, beta_s, beta_l) followed by gp_decode_attention(kv, ps,
+ *    q_post, num_q_heads, scale, out, ws), bit for bit.
+ *  - With a token (k_new, v_new [num_reqs][num_kv_heads][head_dim] in the KV
+ *    dtype, post-RoPE): every request with room (0 <= m_r < P_r * page_size)
+ *    takes it -- its K and V are written at slot m_r of the paged cache, the
+ *    summaries of its slot take one EMA step with q_pre (or are set to it if
+ *    init[r] != 0), and decode attention runs over its m_r + 1 tokens;
+ *    requests with full pages (at a boundary, awaiting a decision) take no
+ *    token, keep their summaries and attend over their m_r tokens.  With
+ *    advance != 0, seq_lens[r] and positions[r] of the requests that took the
+ *    token then grow by one; pass advance = 0 for every layer but the last
+ *    when each layer of a model calls this (the lengths are shared by the
+ *    layers).  One layer with advance != 0 equals gp_append_step(kv, 1, ps,
+ *    positions, k_new, v_new, q_pre, ...) followed by gp_decode_attention, bit
+ *    for bit.  positions may be NULL when advance == 0.
+ *  - A held request (seq_lens[r] < 0) is out of the step: no token, no
+ *    summary update, no output (gp_update_summaries, which does not see the
+ *    lengths, would update it).
+ * q_pre has the layout and dtype of q_post.  Takes the decode workspace.
+ * GP_ERR_INVALID if only one of k_new, v_new is given, or advance != 0 with a
+ * token and no positions. */
 gp_status_t gp_decode_step(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
                            const void *q_pre, int32_t num_q_heads, float scale, void *out,
                            const int32_t *slot_ids, const uint8_t *init, float *qstate, int32_t num_slots,
-                           float beta_s, float beta_l, void *ws, size_t ws_bytes, hipStream_t stream);
+                           float beta_s, float beta_l, const void *k_new, const void *v_new,
+                           int32_t *positions, int32_t advance, void *ws, size_t ws_bytes,
+                           hipStream_t stream);
 
 /* Boundary scoring of one layer (Sec. 3.2 and 3.3; App. E.1).
  * For boundary request i (r = bnd[i], at a boundary, P = num_pages[r]):

@@ -92,7 +92,7 @@ def load() -> ctypes.CDLL:
                                                f32, vp, i32, vp, sz, vp]
     lib.gp_decode_step.restype = ctypes.c_int
     lib.gp_decode_step.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, vp, i32, f32,
-                                   vp, vp, vp, vp, i32, f32, f32, vp, sz, vp]
+                                   vp, vp, vp, vp, i32, f32, f32, vp, vp, vp, i32, vp, sz, vp]
     lib.gp_boundary_score.restype = ctypes.c_int
     lib.gp_boundary_score.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, vp, i32,
                                       vp, vp, vp, i32, i32, ctypes.POINTER(_Params), vp, vp, i32, vp,
@@ -259,13 +259,16 @@ def gp_decode_attention_stages(kv: KVLayer, ps: PageState, q_post: torch.Tensor,
 
 def gp_decode_step(kv: KVLayer, ps: PageState, q_post: torch.Tensor, q_pre: torch.Tensor, scale: float,
                    out: torch.Tensor, slot_ids: torch.Tensor, init: torch.Tensor, qstate: torch.Tensor,
-                   beta_s: float, beta_l: float, ws: torch.Tensor, stream=None) -> None:
-    """Summary update and decode attention of one step in one launch."""
+                   beta_s: float, beta_l: float, ws: torch.Tensor, k_new: torch.Tensor | None = None,
+                   v_new: torch.Tensor | None = None, positions: torch.Tensor | None = None,
+                   advance: bool = True, stream=None) -> None:
+    """The step's new token (k_new, v_new [R][Hkv][d], optional), the summary
+    update and decode attention in one launch."""
     c_kv, c_ps = kv.c(), ps.c()
     st = load().gp_decode_step(ctypes.byref(c_kv), ctypes.byref(c_ps), _ptr(q_post), _ptr(q_pre),
                                q_post.shape[1], scale, _ptr(out), _ptr(slot_ids), _ptr(init),
-                               _ptr(qstate), qstate.shape[0], beta_s, beta_l, _ptr(ws), ws.numel(),
-                               _stream(stream))
+                               _ptr(qstate), qstate.shape[0], beta_s, beta_l, _ptr(k_new), _ptr(v_new),
+                               _ptr(positions), int(bool(advance)), _ptr(ws), ws.numel(), _stream(stream))
     _check(st, "gp_decode_step")
 
 

@@ -135,6 +135,10 @@ struct FoldedSummaries {
     float *qstate;
     int32_t num_slots;
     float beta_s, beta_l;
+    // the step's new token (k_new == nullptr: none)
+    const void *k_new, *v_new;
+    int32_t *positions;
+    int32_t advance;
 };
 
 // noalloc: ws and ws_bytes are ignored; the partials go to the static scratch.
@@ -154,6 +158,8 @@ gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, cons
     if (ps->num_reqs == 0) return GP_OK;
     if (!q_post || !out || (!ws && !noalloc)) return GP_ERR_INVALID;
     if (sum && (!sum->q_pre || !sum->slot_ids || !sum->init || !sum->qstate)) return GP_ERR_INVALID;
+    if (sum && (!sum->k_new != !sum->v_new)) return GP_ERR_INVALID;
+    if (sum && sum->k_new && sum->advance && !sum->positions) return GP_ERR_INVALID;
     const DecodeWs w = decode_ws(ps->num_reqs, num_q_heads, kv->num_kv_heads, kv->head_dim, ps->max_pages);
     if (ps->num_reqs > 65535 || w.max_chunks > kMaxDecodeChunks || w.chunk_pages > kMaxChunkPages)
         return GP_ERR_UNSUPPORTED;
@@ -178,7 +184,15 @@ gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, cons
     a.M = sum ? sum->num_slots : 0;
     a.beta_s = sum ? sum->beta_s : 0.0;
     a.beta_l = sum ? sum->beta_l : 0.0;
+    a.k_w = kv->k;
+    a.v_w = kv->v;
+    a.k_new = sum ? sum->k_new : nullptr;
+    a.v_new = sum ? sum->v_new : nullptr;
+    a.seq_lens_w = ps->seq_lens;
+    a.positions = sum ? sum->positions : nullptr;
+    a.advance = sum && sum->k_new ? (sum->advance != 0) : 0;
     a.partial = reinterpret_cast<float *>(static_cast<unsigned char *>(ws) + w.partial);
+    a.lens = reinterpret_cast<int32_t *>(static_cast<unsigned char *>(ws) + w.lens);
     a.R = ps->num_reqs;
     a.Hkv = kv->num_kv_heads;
     a.max_pages = ps->max_pages;
@@ -215,8 +229,11 @@ gp_status_t gp_decode_attention_stages(const gp_kv_layer_t *kv, const gp_page_st
 gp_status_t gp_decode_step(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
                            const void *q_pre, int32_t num_q_heads, float scale, void *out,
                            const int32_t *slot_ids, const uint8_t *init, float *qstate, int32_t num_slots,
-                           float beta_s, float beta_l, void *ws, size_t ws_bytes, hipStream_t stream) {
-    const FoldedSummaries sum{q_pre, slot_ids, init, qstate, num_slots, beta_s, beta_l};
+                           float beta_s, float beta_l, const void *k_new, const void *v_new,
+                           int32_t *positions, int32_t advance, void *ws, size_t ws_bytes,
+                           hipStream_t stream) {
+    const FoldedSummaries sum{q_pre, slot_ids, init, qstate, num_slots, beta_s, beta_l,
+                              k_new, v_new, positions, advance};
     return decode_call(kv, ps, q_post, num_q_heads, scale, out, ws, ws_bytes, &sum,
                        GP_DECODE_CHUNKS | GP_DECODE_MERGE, stream);
 }

@@ -69,6 +69,32 @@ __device__ inline uint4 stream16(const void *p) {
     return make_uint4(x[0], x[1], x[2], x[3]);
 }
 
+// The request's view of one step: resident tokens m, pages P (clamped to the
+// table), whether the step's new token goes in (room: a token is given and the
+// last page has a free slot, Sec. 3.1 paged cache) and the tokens attended.
+struct StepView {
+    int m, P, m_attn;
+    bool room;
+};
+__device__ inline StepView step_view(const DecodeArgs &a, int r, int m) {
+    StepView v;
+    int P = a.num_pages[r];
+    v.P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
+    v.m = m > v.P * kPage ? v.P * kPage : m;
+    v.room = a.k_new != nullptr && v.m < v.P * kPage;
+    v.m_attn = v.m + (v.room ? 1 : 0);
+    return v;
+}
+
+// For the merge pass: the tokens attended (-1: held) and whether a token went
+// in, written once per request by the workgroup of (KV head 0, chunk 0).
+__device__ inline void record_step(const DecodeArgs &a, int r, int h, int chunk, int m_attn, bool room) {
+    if (h == 0 && chunk == 0 && threadIdx.x == 0) {
+        a.lens[r] = m_attn;
+        a.lens[a.R + r] = room ? 1 : 0;
+    }
+}
+
 // gp_decode_step: the summary update of query heads [h G, h G + G) of request
 // r, done by the workgroup of the pair's first chunk (Sec. 4.1 folds the
 // update into the attention kernel).  Same arithmetic as the update kernel.
@@ -109,17 +135,23 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     __shared__ float s_m[NW][G], s_l[NW][G];
     __shared__ float s_o[NW][G][D];
 
+    __shared__ float s_new[2][D];             // the step's new token (K, V) of head h
+
     const int h = blockIdx.x, chunk = blockIdx.y, r = blockIdx.z;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int Hkv = a.Hkv;
     const int Hq = Hkv * G;
-    int m = a.seq_lens[r];
-    if (m < 0) return;                        // held: not in this step's batch
-    if (chunk == 0) fold_summaries<T, D, G>(a, r, h);
-
-    int P = a.num_pages[r];
-    P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
-    m = m > P * kPage ? P * kPage : m;
+    const int m_in = a.seq_lens[r];
+    if (m_in < 0) {                           // held: not in this step's batch
+        record_step(a, r, h, chunk, -1, false);
+        return;
+    }
+    const StepView sv = step_view(a, r, m_in);
+    record_step(a, r, h, chunk, sv.m_attn, sv.room);
+    // with a new token, only the requests that take it update their summaries
+    if (chunk == 0 && (a.k_new == nullptr || sv.room)) fold_summaries<T, D, G>(a, r, h);
+    const int P = sv.P;
+    const int m = sv.m_attn;
     const int nchunks = cdiv(m, CHUNK);
     T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     if (m == 0) {
@@ -133,6 +165,25 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     // count is the merge's; equal lengths keep the workgroups' durations even)
     const int npg = cdiv(m, kPage), cs = cdiv(npg, nchunks);
     const int page_begin = min(npg, chunk * cs), page_end = min(npg, page_begin + cs);
+
+    // the new token: the workgroup whose pages hold slot m_in writes it into
+    // the cache and takes its K and V from LDS (the cache slot is not read back)
+    const int p_new = sv.room ? sv.m / kPage : -1, slot_new = sv.m % kPage;
+    const bool owns_new = p_new >= page_begin && p_new < page_end;
+    if (owns_new) {
+        const T *kn = reinterpret_cast<const T *>(a.k_new) + ((size_t)r * Hkv + h) * D;
+        const T *vn = reinterpret_cast<const T *>(a.v_new) + ((size_t)r * Hkv + h) * D;
+        const int pid = a.page_table[(size_t)r * a.max_pages + p_new];
+        const bool okp = pid >= 0 && pid < a.pool_pages;
+        const size_t dst = (((size_t)(okp ? pid : 0) * Hkv + h) * kPage + slot_new) * D;
+        for (int i = threadIdx.x; i < 2 * D; i += blockDim.x) {
+            const int kvsel = i / D, dd = i % D;
+            const T x = kvsel ? vn[dd] : kn[dd];
+            s_new[kvsel][dd] = Tr::load(&x);
+            if (okp) (kvsel ? reinterpret_cast<T *>(a.v_w) : reinterpret_cast<T *>(a.k_w))[dst + dd] = x;
+        }
+    }
+    __syncthreads();
 
     const int c = lane % LPT, row = lane / LPT;
     const T *qp = reinterpret_cast<const T *>(a.q) + ((size_t)r * Hq + (size_t)h * G) * D + c * EPL;
@@ -181,10 +232,15 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
         for (int u = 0; u < 2; ++u) {
             if (!ok[u]) continue;   // wave-uniform
             float s[LPP][G];
+            const bool patch = p0 + u * NW == p_new;     // wave-uniform
 #pragma unroll
             for (int j = 0; j < LPP; ++j) {
                 float kf[EPL];
                 Tr::unpack(kr[u][j], kf);
+                if (patch && j * TPL + row == slot_new) {
+#pragma unroll
+                    for (int e = 0; e < EPL; ++e) kf[e] = s_new[0][c * EPL + e];
+                }
 #pragma unroll
                 for (int g = 0; g < G; ++g) {
                     float acc = 0.0f;
@@ -231,6 +287,10 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
                 const bool valid = full || (j * TPL + row) < ntok[u];
                 float vf[EPL];
                 Tr::unpack(vr[u][j], vf);
+                if (patch && j * TPL + row == slot_new) {
+#pragma unroll
+                    for (int e = 0; e < EPL; ++e) vf[e] = s_new[1][c * EPL + e];
+                }
 #pragma unroll
                 for (int e = 0; e < EPL; ++e) vf[e] = valid ? vf[e] : 0.0f;
 #pragma unroll
@@ -340,36 +400,82 @@ __device__ inline float row_sum16(float x) {
 // value load reads one whole 2D-byte row per instruction and the accumulators
 // take G * D / 64 registers; Q waits in LDS.  The waves merge through LDS at
 // the end.
-template <int D, int G>
+template <int D, int G, bool STEP>
 __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeArgs a) {
     constexpr int KK = D / 32;            // MFMA steps per page
     constexpr int DPL = D / 64;           // head dims per lane in P.V (2 or 1)
     constexpr int HR = (G + 3) / 4;       // lane rows that carry real heads
     constexpr int GI = G < 4 ? G : 4;     // heads per lane row
     constexpr int NW = kDecodeWaves;
+    constexpr int NT = 64 * NW;
+    constexpr int FE = STEP ? (G * D + NT - 1) / NT : 1;   // summary elements per thread
     __shared__ float s_m[NW][G], s_l[NW][G];
     __shared__ float s_o[NW][G][D];
     __shared__ float s_p[NW][kPage][G];
     __shared__ float s_alpha[NW][G];
     __shared__ bf16x8_t s_q[KK][4][G];
     __shared__ int s_ids[kMaxChunkPages];
+    __shared__ __attribute__((aligned(16))) uint16_t s_new[STEP ? 2 : 1][STEP ? D : 8];   // new token K, V
 
     const int h = blockIdx.x, chunk = blockIdx.y, r = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int Hkv = a.Hkv, Hq = Hkv * G;
-    int m = a.seq_lens[r];
-    if (m < 0) return;                        // held: not in this step's batch
-    if (chunk == 0) fold_summaries<uint16_t, D, G>(a, r, h);
+    const int m_in = a.seq_lens[r];
+    if (m_in < 0) {                           // held: not in this step's batch
+        record_step(a, r, h, chunk, -1, false);
+        return;
+    }
+    const StepView sv = step_view(a, r, m_in);
+    record_step(a, r, h, chunk, sv.m_attn, sv.room);
     const int CHUNK = a.chunk_pages * kPage;
 
-    int P = a.num_pages[r];
-    P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
-    m = m > P * kPage ? P * kPage : m;
+    // gp_decode_step: the summaries of query heads [h G, h G + G) are updated
+    // by the first chunk's workgroup (with a new token: only if the request
+    // takes it).  The old values and the query are requested here, with the
+    // other loads of the prologue; the update is stored when the workgroup ends.
+    float f_q[FE], f_s[FE], f_l[FE];
+    float *fS = nullptr;
+    bool f_init = false;
+    if constexpr (STEP) {
+        if (chunk == 0 && a.qstate && (a.k_new == nullptr || sv.room)) {
+            const int slot = a.slot_ids[r];
+            if (slot >= 0 && slot < a.M) {
+                fS = a.qstate + (size_t)slot * 2 * Hq * D + (size_t)h * G * D;
+                f_init = a.init[r] != 0;
+                const uint16_t *qp = reinterpret_cast<const uint16_t *>(a.q_pre) + ((size_t)r * Hq + (size_t)h * G) * D;
+#pragma unroll
+                for (int e = 0; e < FE; ++e) {
+                    const int i = min(tid + e * NT, G * D - 1);
+                    f_q[e] = bf16_to_f32(qp[i]);
+                    f_s[e] = fS[i];
+                    f_l[e] = fS[(size_t)Hq * D + i];
+                }
+            }
+        }
+    }
+    auto finish_fold = [&]() {
+        if constexpr (STEP) {
+            if (fS) {
+                const double cs_ = 1.0 - a.beta_s, cl_ = 1.0 - a.beta_l;
+#pragma unroll
+                for (int e = 0; e < FE; ++e) {
+                    const int i = tid + e * NT;
+                    if (i < G * D) {
+                        fS[i] = f_init ? f_q[e] : ema_step(f_s[e], f_q[e], a.beta_s, cs_);
+                        fS[(size_t)Hq * D + i] = f_init ? f_q[e] : ema_step(f_l[e], f_q[e], a.beta_l, cl_);
+                    }
+                }
+            }
+        }
+    };
+
+    const int m = sv.m_attn;
     const int nchunks = cdiv(m, CHUNK);
     uint16_t *out = reinterpret_cast<uint16_t *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     if (m == 0) {
         if (chunk == 0)
             for (int i = tid; i < G * D; i += blockDim.x) out[i] = 0;
+        finish_fold();
         return;
     }
     if (chunk >= nchunks) return;
@@ -393,7 +499,34 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
         const int kk = tid / (4 * G), rem = tid % (4 * G), q_kg = rem / G, q_n = rem % G;
         s_q[kk][q_kg][q_n] = *reinterpret_cast<const bf16x8_t *>(qg + (size_t)q_n * D + kk * 32 + q_kg * 8);
     }
+    // gp_decode_step with a new token: the workgroup whose pages hold slot
+    // m_in stages the token's K and V of head h in LDS (its waves take them
+    // from there, not from the cache) and writes them into the cache
+    const int p_new = STEP && sv.room ? sv.m / kPage : -1, slot_new = sv.m % kPage;
+    const bool owns_new = STEP && p_new >= page_begin && p_new < page_end;
+    constexpr int NU16 = D / 8;                       // 16-byte units of one row
+    uint4 nv = make_uint4(0u, 0u, 0u, 0u);
+    if constexpr (STEP) {
+        if (owns_new && tid < 2 * NU16) {
+            const int kvsel = tid / NU16, u = tid % NU16;
+            const uint16_t *src = reinterpret_cast<const uint16_t *>(kvsel ? a.v_new : a.k_new) +
+                                  ((size_t)r * Hkv + h) * D + u * 8;
+            nv = *reinterpret_cast<const uint4 *>(src);
+            *reinterpret_cast<uint4 *>(&s_new[kvsel][u * 8]) = nv;
+        }
+    }
     __syncthreads();
+    if constexpr (STEP) {
+        if (owns_new && tid < 2 * NU16) {
+            const int kvsel = tid / NU16, u = tid % NU16;
+            const int phys = s_ids[p_new - page_begin];
+            if (phys >= 0) {
+                uint16_t *dst = reinterpret_cast<uint16_t *>(kvsel ? a.v_w : a.k_w) +
+                                (((size_t)phys * Hkv + h) * kPage + slot_new) * D + u * 8;
+                *reinterpret_cast<uint4 *>(dst) = nv;
+            }
+        }
+    }
 
     float mrun[GI], lrun[GI], o[G][DPL];
 #pragma unroll
@@ -433,6 +566,18 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     // the other buffer), then softmax and P.V on this page's values.
     auto page = [&](int p, int &phys, uint32_t (&vw)[kPage], uint32_t (&vn)[kPage]) {
         const int ntok = phys >= 0 ? min(kPage, m - p * kPage) : 0;
+        if constexpr (STEP) {
+            if (p == p_new) {     // wave-uniform: the new token's slot comes from LDS
+                if (n == slot_new) {
+#pragma unroll
+                    for (int kk = 0; kk < KK; ++kk) kb[kk] = *reinterpret_cast<const uint4 *>(&s_new[0][kk * 32 + kg * 8]);
+                }
+                const uint32_t nvv = DPL == 2 ? *reinterpret_cast<const uint32_t *>(&s_new[1][v_off])
+                                              : (uint32_t)s_new[1][v_off];
+#pragma unroll
+                for (int t = 0; t < kPage; ++t) vw[t] = t == slot_new ? nvv : vw[t];
+            }
+        }
         f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
         if (ntok > 0) {
 #pragma unroll
@@ -544,6 +689,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
             }
         }
     }
+    finish_fold();
 }
 
 // Second pass for requests that span several chunks: one workgroup per
@@ -560,10 +706,14 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     __shared__ float s_f[MAXC][G];                 // exp2(m_k - M) / L per chunk and head
     __shared__ float s_ml[MAXC][G][2];
     const int h = blockIdx.x, r = blockIdx.y;
-    int P = a.num_pages[r];
-    P = P < 0 ? 0 : (P > a.max_pages ? a.max_pages : P);
-    int m = a.seq_lens[r];
-    m = m < 0 ? 0 : (m > P * kPage ? P * kPage : m);     // held requests: nothing to merge
+    // tokens attended, as the chunk pass recorded them (-1: held, nothing to merge)
+    const int m = a.lens[r];
+    if (m < 0) return;
+    if (a.advance && h == 0 && threadIdx.x == 0 && a.lens[a.R + r]) {
+        // gp_decode_step: the request took the step's token
+        a.seq_lens_w[r] = m;
+        if (a.positions) a.positions[r] += 1;
+    }
     const int nchunks = cdiv(m, CHUNK);
     if (nchunks <= 1) return;
     const int Hq = a.Hkv * G;
@@ -637,12 +787,19 @@ template <typename T, int D>
 hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, int stages, hipStream_t s) {
     dim3 mgrid(a.Hkv, a.R);
     constexpr bool bf16 = sizeof(T) == 2;
-    const bool chunks = stages & GP_DECODE_CHUNKS, merge = (stages & GP_DECODE_MERGE) && a.max_chunks > 1;
+    // the step variant (summaries and/or the new token folded in) is its own
+    // instantiation, so plain decode attention carries none of its code
+    const bool step = a.qstate != nullptr || a.k_new != nullptr;
+    // the merge pass also advances the lengths when a token went in
+    const bool chunks = stages & GP_DECODE_CHUNKS,
+               merge = (stages & GP_DECODE_MERGE) && (a.max_chunks > 1 || (a.k_new && a.advance));
     switch (G) {
 #define GP_CASE(GG)                                                  \
     case GG:                                                         \
-        if (chunks && bf16)                                          \
-            decode_split_kernel<D, GG><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
+        if (chunks && bf16 && step)                                  \
+            decode_split_kernel<D, GG, true><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
+        else if (chunks && bf16)                                     \
+            decode_split_kernel<D, GG, false><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
         else if (chunks)                                             \
             decode_kernel<float, D, GG><<<grid, 256, 0, s>>>(a);     \
         if (merge) merge_kernel<T, D, GG><<<mgrid, 256, 0, s>>>(a);  \

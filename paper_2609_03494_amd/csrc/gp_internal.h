@@ -46,7 +46,7 @@ __device__ inline float ema_step(float prev, float x, double beta, double one_mi
 }
 
 struct DecodeWs {
-    size_t partial, total;
+    size_t partial, lens, total;
     int max_chunks, chunk_pages;
 };
 
@@ -67,6 +67,8 @@ __host__ __device__ inline DecodeWs decode_ws(int R, int Hq, int Hkv, int D, int
     size_t off = 0;
     w.partial = off;    // float: [R][Hkv][max_chunks][G][D + 2] (o, max, sum)
     off = align_up(off + (size_t)R * Hkv * w.max_chunks * G * (D + 2) * sizeof(float));
+    w.lens = off;       // int32: [R] tokens attended (-1: held), [R] token appended (0/1)
+    off = align_up(off + (size_t)R * 2 * sizeof(int32_t));
     w.total = off;
     return w;
 }
@@ -152,7 +154,15 @@ struct DecodeArgs {
     float *qstate;
     int M;
     double beta_s, beta_l;
+    // the step's new token folded into the launch (gp_decode_step with k_new):
+    // written at slot m_r of every request with room and attended to; with
+    // advance != 0 the merge pass then advances seq_lens and positions
+    void *k_w, *v_w;              // the pools, written at the new token's slot
+    const void *k_new, *v_new;    // [R][Hkv][D]; nullptr: no token
+    int32_t *seq_lens_w, *positions;
+    int advance;
     float *partial;
+    int32_t *lens;                // [R] tokens attended (-1: held), then [R] appended flags
     int R, Hkv, max_pages, pool_pages, max_chunks, chunk_pages;
     float qscale;   // scale * log2(e)
 };

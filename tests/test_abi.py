@@ -99,11 +99,16 @@ def test_host_validation_without_launch(lib):
                                      fake, fake, fake, fake, 1 << 30, None) == 1, fields
     # fused step: beta outside [0, 1], null summary pool, then a small workspace
     assert lib.gp_decode_step(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 32, 0.1, fake, fake, fake,
-                              fake, 512, 0.9, -0.5, fake, 1 << 30, None) == 1
+                              fake, 512, 0.9, -0.5, None, None, None, 0, fake, 1 << 30, None) == 1
     assert lib.gp_decode_step(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 32, 0.1, fake, fake, fake,
-                              None, 512, 0.9, 0.999, fake, 1 << 30, None) == 1
+                              None, 512, 0.9, 0.999, None, None, None, 0, fake, 1 << 30, None) == 1
     assert lib.gp_decode_step(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 32, 0.1, fake, fake, fake,
-                              fake, 512, 0.9, 0.999, fake, 16, None) == 3
+                              fake, 512, 0.9, 0.999, None, None, None, 0, fake, 16, None) == 3
+    # fused step with a token: K without V, or advancing without positions
+    assert lib.gp_decode_step(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 32, 0.1, fake, fake, fake,
+                              fake, 512, 0.9, 0.999, fake, None, fake, 1, fake, 1 << 30, None) == 1
+    assert lib.gp_decode_step(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 32, 0.1, fake, fake, fake,
+                              fake, 512, 0.9, 0.999, fake, fake, None, 1, fake, 1 << 30, None) == 1
     # release: null state; append: beta outside [0, 1], too many layers, null summaries
     assert lib.gp_release_held(None, None) == 1
     assert lib.gp_append_step(arr, 1, ctypes.byref(ps), fake, fake, fake, fake, 32, fake, None, fake, 512,

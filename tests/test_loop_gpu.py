@@ -13,7 +13,8 @@ import torch
 import oracle as O
 import paper_2609_03494_amd as gp
 import workloads as W
-from _harness import (DEV, DeviceCase, assert_rows_close, bf16_rounding_ok, library_params, oracle_state,
+from _harness import (DEV, AbsPool, DeviceCase, assert_rows_close, bf16_rounding_ok, fp32_elementwise_ok,
+                      library_params, oracle_state,
                       to_numpy, to_torch, torch_dtype)
 
 pytestmark = pytest.mark.gpu
@@ -190,6 +191,118 @@ def test_append_step_matches_oracle(dtype):
                 want = O.gather_tokens(pools[l][x], st.page_table[r], m, b)
                 have = dc.gather(st.page_table[r], m, which, layer=l)
                 assert np.array_equal(want, have), f"{which} of request {r}, layer {l}"
+
+
+# ------------------------------------- the token folded into the decode step --
+
+def _step_case(case):
+    if case == "f32":
+        return _small(dtype="f32")
+    if case == "bf16_qwen3":
+        return W.qwen3_8b(seed=71, num_reqs=9, len_lo=30, len_hi=5000, budget_choices=(4, 40, 400),
+                          boundary_frac=0.25, free_pages=32)
+    return W.prefix_shared(num_reqs=5, prefix_len=256, tail_lo=20, tail_hi=700, free_pages=40)
+
+
+@pytest.mark.parametrize("case", ["f32", "bf16_qwen3", "bf16_g8"])
+def test_decode_step_with_token_against_oracle(case):
+    """gp_decode_step with the step's token folded in (Sec. 4.1): K and V
+    written at slot m_r of every request with room, the summaries of those
+    requests updated, decode attention over m_r + 1 tokens, lengths and
+    positions advanced; a held request and requests with full pages as in the
+    loop, a request with nothing resident attends to the new token alone.
+    Against the oracle's append_token + update_summaries + decode_attention,
+    and bit for bit against gp_append_step followed by gp_decode_attention."""
+    w = _step_case(case)
+    b, R, dt = w.page_size, w.num_reqs, w.dtype
+    inp = W.step_inputs(w, 1, seed=5)[0]
+    full = [r for r in range(R) if w.seq_lens[r] == w.num_pages[r] * b]
+    # (no empty request under a shared prefix: its first page is shared, so its
+    # token would land in a page other requests read)
+    empty = 1 if case != "bf16_g8" else None
+    held = max(r for r in range(R) if r not in full and r != empty)
+    assert full and empty not in full
+    init = np.zeros(R, np.uint8)
+    init[0] = 1
+    p32 = O.Params().as_f32(w.head_dim)
+    scale = float(np.float32(1.0 / math.sqrt(w.head_dim)))
+    _say(f"decode step with the token folded in: {case}, full {full}, held {held}, empty {empty}")
+    # oracle
+    st = oracle_state(w)
+    if empty is not None:
+        st.seq_lens[empty] = 0
+    pools = [(w.dense_pool("k"), w.dense_pool("v"))]
+    pos = w.positions.copy()
+    active = [r for r in range(R) if r != held]
+    app = [r for r in active if O.append_token(pools, st, r, [(inp["k_new"][0][r], inp["v_new"][0][r])], b)]
+    for r in app:
+        pos[r] += 1
+    idx = np.array(app)
+    qs_ref = O.update_summaries(inp["q_pre"][idx], dt, w.slot_ids[idx], init[idx], w.qstate,
+                                p32.beta_s, p32.beta_l)
+    ref = O.decode_attention(pools[0][0], pools[0][1], dt, st.page_table, st.seq_lens, inp["q_post"],
+                             w.num_q_heads, scale, requests=active)[active]
+
+    def run(fused, advance=True):
+        dc = DeviceCase(w)
+        if empty is not None:
+            dc.ps.seq_lens[empty] = 0
+        dc.ps.seq_lens[held] = -int(w.seq_lens[held]) - 1
+        positions = dc.positions.clone()
+        q_pre, q_post = to_torch(inp["q_pre"], dt), to_torch(inp["q_post"], dt)
+        k_new, v_new = to_torch(inp["k_new"][0], dt), to_torch(inp["v_new"][0], dt)
+        ini = torch.from_numpy(init).to(DEV)
+        out = torch.full_like(q_post, float("nan"))
+        if fused:
+            gp.gp_decode_step(dc.layers[0], dc.ps, q_post, q_pre, scale, out, dc.slot_ids, ini, dc.qstate,
+                              p32.beta_s, p32.beta_l, dc.ws_decode, k_new=k_new, v_new=v_new,
+                              positions=positions, advance=advance)
+        else:
+            gp.gp_append_step(dc.layers, dc.ps, positions, k_new[None].contiguous(), v_new[None].contiguous(),
+                              q_pre[None].contiguous(), dc.slot_ids, ini, dc.qstate[None], p32.beta_s,
+                              p32.beta_l)
+            gp.gp_decode_attention(dc.layers[0], dc.ps, q_post, scale, out, dc.ws_decode)
+        torch.cuda.synchronize()
+        return dc, positions, out
+
+    dc, positions, out = run(True)
+    got = O.widen(to_numpy(out), dt)
+    assert np.isnan(got[held]).all(), "the held request's output row was written"
+    g = got[active]
+    if dt == "f32":
+        ref_abs = O.decode_attention(pools[0][0], AbsPool(pools[0][1]), dt, st.page_table, st.seq_lens,
+                                     inp["q_post"], w.num_q_heads, scale, requests=active)[active]
+        assert_rows_close(g, ref, 1e-5, "decode step fp32")
+        assert fp32_elementwise_ok(g, ref, ref_abs), "decode step fp32: element-wise bar"
+    else:
+        assert_rows_close(g, ref, 2e-2, "decode step bf16")
+        assert bf16_rounding_ok(g, ref), "decode step bf16: beyond bf16 rounding of the exact value"
+    np.testing.assert_array_equal(dc.qstate.cpu().numpy().view(np.int32), qs_ref.view(np.int32))
+    sl = dc.ps.seq_lens.cpu().numpy()
+    want_sl = st.seq_lens.copy()
+    want_sl[held] = -int(w.seq_lens[held]) - 1
+    np.testing.assert_array_equal(sl, want_sl)
+    np.testing.assert_array_equal(positions.cpu().numpy(), pos)
+    for r in active:
+        m = int(st.seq_lens[r])
+        for x, which in enumerate(("k", "v")):
+            want = O.gather_tokens(pools[0][x], st.page_table[r], m, b)
+            assert np.array_equal(want, dc.gather(st.page_table[r], m, which)), f"{which} of request {r}"
+    # the two launches of the loop prologue give the same bytes
+    dc2, positions2, out2 = run(False)
+    assert _bytes(out2) == _bytes(out)        # bytes: the held row is NaN in both
+    assert _bytes(dc2.qstate) == _bytes(dc.qstate) and torch.equal(positions2, positions)
+    assert torch.equal(dc2.ps.seq_lens, dc.ps.seq_lens)
+    assert _bytes(dc2.layers[0].k) == _bytes(dc.layers[0].k) and _bytes(dc2.layers[0].v) == _bytes(dc.layers[0].v)
+    # advance = 0 (every layer but the last): the same outputs, the token in the
+    # cache, lengths and positions as they were
+    dc3, positions3, out3 = run(True, advance=False)
+    assert _bytes(out3) == _bytes(out)
+    assert _bytes(dc3.layers[0].k) == _bytes(dc.layers[0].k) and _bytes(dc3.layers[0].v) == _bytes(dc.layers[0].v)
+    assert torch.equal(positions3, dc3.positions)
+    sl3 = dc3.ps.seq_lens.cpu().numpy()
+    assert (empty is None or sl3[empty] == 0) and sl3[held] == -int(w.seq_lens[held]) - 1
+    assert all(sl3[r] == w.seq_lens[r] for r in range(R) if r not in (empty, held))
 
 
 # -------------------------------------------------- the decode loop itself --
