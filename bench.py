@@ -348,6 +348,32 @@ def main():
     restore()
     positions.copy_(pos0)
 
+    # a workload with a shared prefix: decode attention that reads the shared
+    # pages once per block of requests (the prefix pass on a second stream
+    # beside the private tails, then the merge), K back-to-back calls
+    shared = None
+    prefix_pages = int(w.meta.get("prefix_len", 0)) // b
+    if prefix_pages:
+        groups = [(0, R, prefix_pages)]
+        side2 = torch.cuda.Stream()
+
+        def shared_call():
+            cur = torch.cuda.current_stream()
+            side2.wait_stream(cur)
+            with torch.cuda.stream(side2):
+                gp.gp_decode_attention_shared(kv, ps, q_post, params.scale, out, groups, ws_d,
+                                              stages=gp.GP_DECODE_PREFIX)
+            gp.gp_decode_attention_shared(kv, ps, q_post, params.scale, out, groups, ws_d,
+                                          stages=gp.GP_DECODE_CHUNKS)
+            cur.wait_stream(side2)
+            gp.gp_decode_attention_shared(kv, ps, q_post, params.scale, out, groups, ws_d,
+                                          stages=gp.GP_DECODE_MERGE)
+
+        for _ in range(2):
+            shared_call()
+        shared_ms = timed_loop(shared_call)
+        shared = {"ms": shared_ms, "groups": groups}
+
     # instrumented pass (eager launches, events between phases): how much of a
     # step the boundary work adds after decode attention has finished
     marks = {"d0": [], "d1": [], "b1": []}
@@ -421,6 +447,16 @@ def main():
                                 + np.arange(int(w.seq_lens[r])) % b for r in range(R)])
     unique_bytes = int(np.unique(slots_all).size) * Hkv * d * e * 2
 
+    if shared is not None:
+        sh_gbs = unique_bytes / (shared["ms"] * 1e-3) / 1e9
+        shared = {"ms": round(shared["ms"], 4), "unique_GB/s": round(sh_gbs, 1),
+                  "unique_hbm_frac": round(sh_gbs / HBM_PEAK_GBS, 4),
+                  "plain_call_unique_hbm_frac": round(unique_bytes / (decode_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                  "groups": shared["groups"],
+                  "note": "gp_decode_attention_shared: the prefix pass (shared pages read once per block of "
+                          "requests, on the matrix cores) on a second stream beside the private tails, then "
+                          "the merge"}
+
     traffic = None
     if args.workload == "qwen3_8b" and os.path.exists(args.traffic_json):
         with open(args.traffic_json) as f:
@@ -467,7 +503,8 @@ def main():
                              "with_summaries_one_launch_ms": round(fused_ms, 4),
                              "with_summaries_two_launches_ms": round(separate_ms, 4),
                              "with_token_and_summaries_one_launch_ms": round(token_fused_ms, 4),
-                             "append_step_then_decode_two_launches_ms": round(token_separate_ms, 4)},
+                             "append_step_then_decode_two_launches_ms": round(token_separate_ms, 4),
+                             "shared_prefix": shared},
         "boundary": {"ms_after_decode": round(boundary_ms, 4),
                      "events_per_s": round(Rb / (step_ms * 1e-3), 1),
                      "overlapped_with_decode": not args.serial,

@@ -207,6 +207,41 @@ gp_status_t gp_decode_attention(const gp_kv_layer_t *kv, const gp_page_state_t *
                                 const void *q_post, int32_t num_q_heads, float scale,
                                 void *out, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Decode attention over batches whose requests share a common prefix of
+ * pages (App. E.2: a shared prefix sits in reference-counted blocks that every
+ * request holding it reads; Sec. 3.1 attention-output equation).  Same
+ * arguments and outputs as gp_decode_attention, plus prefix groups (HOST
+ * array, read during the call): requests [first_req, first_req + num_reqs)
+ * share the first prefix_pages pages of request first_req's table.  The
+ * shared pages are read once per block of 8 * 16 / G requests of a group
+ * (not once per request), in a prefix pass on the matrix cores; each
+ * request's private pages follow in the usual split pass, and the two
+ * partial results are merged.  Whether a request reads the prefix pass is
+ * decided on the device: it must not be held, hold at least prefix_pages
+ * pages and prefix_pages * page_size tokens, and have the leader's page ids
+ * on all prefix pages; any other member (e.g. one whose shared pages a
+ * compaction has replaced by private copies, App. E.2) is served like a
+ * request of no group, so the groups only decide the speed, never the
+ * result.  The outputs equal gp_decode_attention's to float32 rounding of the
+ * sums (P.V of the prefix runs in another order; the bf16 output may differ
+ * in its last bit).  Groups: at most 16, in order of first_req, disjoint;
+ * bfloat16 pools only (GP_ERR_UNSUPPORTED otherwise).  Takes the decode
+ * workspace.
+ * `stages` (any non-empty combination of GP_DECODE_PREFIX, GP_DECODE_CHUNKS,
+ * GP_DECODE_MERGE; all three = the whole call, run in that order) lets a
+ * caller overlap the two passes: PREFIX (the shared pages, on the matrix
+ * cores) and CHUNKS (the private pages, bound by HBM) read the same inputs
+ * and write disjoint parts of ws, so they may run concurrently on two
+ * streams; MERGE reads ws and must be ordered after both.  Between the
+ * stages nothing but ws may be written. */
+typedef struct {
+    int32_t first_req, num_reqs, prefix_pages;
+} gp_prefix_group_t;
+gp_status_t gp_decode_attention_shared(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
+                                       const void *q_post, int32_t num_q_heads, float scale, void *out,
+                                       const gp_prefix_group_t *groups, int32_t num_groups, int32_t stages,
+                                       void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* gp_decode_attention without a workspace argument, for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc).  Same arguments and results as
@@ -236,7 +271,7 @@ gp_status_t gp_decode_attention_noalloc(const gp_kv_layer_t *kv, const gp_page_s
  * the cache may be written (e.g. compacted), not ws, `out` or the lengths
  * and page counts.  Takes the decode workspace; GP_ERR_INVALID for any other
  * `stages`. */
-enum { GP_DECODE_CHUNKS = 1, GP_DECODE_MERGE = 2 };
+enum { GP_DECODE_CHUNKS = 1, GP_DECODE_MERGE = 2, GP_DECODE_PREFIX = 4 };
 gp_status_t gp_decode_attention_stages(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
                                        const void *q_post, int32_t num_q_heads, float scale,
                                        void *out, int32_t stages, void *ws, size_t ws_bytes,

@@ -23,12 +23,12 @@ GP_COMPRESS, GP_GROW, GP_FALLBACK, GP_PREEMPT, GP_NOT_BOUNDARY = 0, 1, 2, 3, 4
 GP_SHRINK = 5
 GP_POLICY_GROWPAGE, GP_POLICY_FIXED, GP_POLICY_RANDOM, GP_POLICY_INVERSE, GP_POLICY_SHRINK = 0, 1, 2, 3, 4
 GP_METRIC_TOP_P, GP_METRIC_ENTROPY = 0, 1
-GP_DECODE_CHUNKS, GP_DECODE_MERGE = 1, 2
+GP_DECODE_CHUNKS, GP_DECODE_MERGE, GP_DECODE_PREFIX = 1, 2, 4
 GP_LAYOUT_SHIFT, GP_LAYOUT_FILL = 0, 1
 PAGE_SIZE = 16
 GP_ERR_SCRATCH = 5
 
-EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_attention_noalloc",
+EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_attention_noalloc", "gp_decode_attention_shared",
            "gp_decode_attention_stages", "gp_decode_step", "gp_boundary_score",
            "gp_boundary_apply", "gp_boundary_select", "gp_boundary_decide", "gp_boundary_compact",
            "gp_release_held", "gp_append_step", "gp_workspace_bytes", "gp_status_string")
@@ -52,6 +52,10 @@ class _PageState(ctypes.Structure):
                 ("free_list", ctypes.c_void_p), ("free_count", ctypes.c_void_p),
                 ("num_reqs", ctypes.c_int32), ("max_pages", ctypes.c_int32),
                 ("pool_pages", ctypes.c_int32)]
+
+
+class _PrefixGroup(ctypes.Structure):
+    _fields_ = [("first_req", ctypes.c_int32), ("num_reqs", ctypes.c_int32), ("prefix_pages", ctypes.c_int32)]
 
 
 class _Params(ctypes.Structure):
@@ -87,6 +91,9 @@ def load() -> ctypes.CDLL:
     lib.gp_decode_attention_noalloc.restype = ctypes.c_int
     lib.gp_decode_attention_noalloc.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp,
                                                 i32, f32, vp, vp]
+    lib.gp_decode_attention_shared.restype = ctypes.c_int
+    lib.gp_decode_attention_shared.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, i32,
+                                               f32, vp, ctypes.POINTER(_PrefixGroup), i32, i32, vp, sz, vp]
     lib.gp_decode_attention_stages.restype = ctypes.c_int
     lib.gp_decode_attention_stages.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, i32,
                                                f32, vp, i32, vp, sz, vp]
@@ -245,6 +252,21 @@ def gp_decode_attention_noalloc(kv: KVLayer, ps: PageState, q_post: torch.Tensor
     st = load().gp_decode_attention_noalloc(ctypes.byref(c_kv), ctypes.byref(c_ps), _ptr(q_post),
                                             q_post.shape[1], scale, _ptr(out), _stream(stream))
     _check(st, "gp_decode_attention_noalloc")
+
+
+def gp_decode_attention_shared(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale: float,
+                               out: torch.Tensor, groups, ws: torch.Tensor,
+                               stages: int = GP_DECODE_PREFIX | GP_DECODE_CHUNKS | GP_DECODE_MERGE,
+                               stream=None) -> None:
+    """Decode attention with shared-prefix groups: ``groups`` is a list of
+    (first_req, num_reqs, prefix_pages); ``stages`` any of GP_DECODE_PREFIX,
+    GP_DECODE_CHUNKS, GP_DECODE_MERGE."""
+    arr = (_PrefixGroup * max(len(groups), 1))(*[_PrefixGroup(*map(int, g)) for g in groups])
+    c_kv, c_ps = kv.c(), ps.c()
+    st = load().gp_decode_attention_shared(ctypes.byref(c_kv), ctypes.byref(c_ps), _ptr(q_post),
+                                           q_post.shape[1], scale, _ptr(out), arr, len(groups), int(stages),
+                                           _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "gp_decode_attention_shared")
 
 
 def gp_decode_attention_stages(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale: float,

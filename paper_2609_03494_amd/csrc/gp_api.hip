@@ -142,9 +142,11 @@ struct FoldedSummaries {
 };
 
 // noalloc: ws and ws_bytes are ignored; the partials go to the static scratch.
+// groups (host, num_groups of them): the shared-prefix decode.
 gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,
                         int32_t num_q_heads, float scale, void *out, void *ws, size_t ws_bytes,
-                        const FoldedSummaries *sum, int stages, hipStream_t stream, bool noalloc = false) {
+                        const FoldedSummaries *sum, int stages, hipStream_t stream, bool noalloc = false,
+                        const gp_prefix_group_t *groups = nullptr, int32_t num_groups = 0) {
     gp_status_t st = check_layer(kv);
     if (st != GP_OK) return st;
     if ((st = check_state(ps, kv)) != GP_OK) return st;
@@ -169,7 +171,30 @@ gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, cons
         ws_bytes = kScratchBytes;
     }
     if (ws_bytes < w.total) return GP_ERR_WORKSPACE;
-    DecodeArgs a;
+    DecodeArgs a = {};
+    if (num_groups < 0 || num_groups > kMaxPrefixGroups || (num_groups > 0 && !groups)) return GP_ERR_INVALID;
+    if (num_groups > 0 && kv->dtype != GP_BF16) return GP_ERR_UNSUPPORTED;
+    {
+        // groups: in order of first request, disjoint, inside the batch, a
+        // prefix of at least one page and at most the table width
+        int end = 0, blk = 0;
+        const int rpb = kPrefixWaves * (16 / (num_q_heads / kv->num_kv_heads));
+        for (int g = 0; g < num_groups; ++g) {
+            const gp_prefix_group_t &gr = groups[g];
+            if (gr.first_req < end || gr.num_reqs < 1 || gr.first_req + gr.num_reqs > ps->num_reqs ||
+                gr.prefix_pages < 1 || gr.prefix_pages > ps->max_pages)
+                return GP_ERR_INVALID;
+            end = gr.first_req + gr.num_reqs;
+            a.g_first[g] = gr.first_req;
+            a.g_num[g] = gr.num_reqs;
+            a.g_pages[g] = gr.prefix_pages;
+            a.g_blk0[g] = blk;
+            blk += cdiv(gr.num_reqs, rpb);
+        }
+        a.g_blk0[num_groups] = blk;
+        a.ngroups = num_groups;
+        if (blk > 65535) return GP_ERR_UNSUPPORTED;
+    }
     a.k = kv->k;
     a.v = kv->v;
     a.page_table = ps->page_table;
@@ -198,6 +223,7 @@ gp_status_t decode_call(const gp_kv_layer_t *kv, const gp_page_state_t *ps, cons
     a.max_pages = ps->max_pages;
     a.pool_pages = kv->pool_pages;
     a.max_chunks = w.max_chunks;
+    a.slots = w.slots;
     a.chunk_pages = w.chunk_pages;
     a.qscale = scale * 1.4426950408889634f;
     return from_hip(launch_decode(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stages, stream));
@@ -217,6 +243,17 @@ gp_status_t gp_decode_attention_noalloc(const gp_kv_layer_t *kv, const gp_page_s
                                         hipStream_t stream) {
     return decode_call(kv, ps, q_post, num_q_heads, scale, out, nullptr, 0, nullptr,
                        GP_DECODE_CHUNKS | GP_DECODE_MERGE, stream, true);
+}
+
+gp_status_t gp_decode_attention_shared(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
+                                       const void *q_post, int32_t num_q_heads, float scale, void *out,
+                                       const gp_prefix_group_t *groups, int32_t num_groups, int32_t stages,
+                                       void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (num_groups < 0 || (num_groups > 0 && !groups)) return GP_ERR_INVALID;
+    if (stages < 1 || stages > (GP_DECODE_PREFIX | GP_DECODE_CHUNKS | GP_DECODE_MERGE)) return GP_ERR_INVALID;
+    // without groups it is plain decode attention (no prefix stage)
+    return decode_call(kv, ps, q_post, num_q_heads, scale, out, ws, ws_bytes, nullptr, stages, stream, false,
+                       groups, num_groups);
 }
 
 gp_status_t gp_decode_attention_stages(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_post,

@@ -86,13 +86,26 @@ __device__ inline StepView step_view(const DecodeArgs &a, int r, int m) {
     return v;
 }
 
-// For the merge pass: the tokens attended (-1: held) and whether a token went
-// in, written once per request by the workgroup of (KV head 0, chunk 0).
-__device__ inline void record_step(const DecodeArgs &a, int r, int h, int chunk, int m_attn, bool room) {
+// For the merge pass: the tokens attended (-1: held), whether a token went in
+// and how many partial slots the merge folds (0: the output is written by the
+// chunk pass), written once per request by the workgroup of (KV head 0,
+// chunk 0).
+__device__ inline void record_step(const DecodeArgs &a, int r, int h, int chunk, int m_attn, bool room,
+                                   int merge_slots) {
     if (h == 0 && chunk == 0 && threadIdx.x == 0) {
         a.lens[r] = m_attn;
         a.lens[a.R + r] = room ? 1 : 0;
+        a.lens[2 * a.R + r] = merge_slots;
     }
+}
+
+// gp_decode_attention_shared: whether request r (not held, at least pp pages
+// and pp * page_size tokens, within its table) may read a prefix pass of pp
+// pages; the prefix pass and the tail pass also require the leader's page ids
+// on every prefix page.  Both passes evaluate this on their own.
+__device__ inline bool prefix_reader(const DecodeArgs &a, int r, int pp) {
+    const int m = a.seq_lens[r], P = a.num_pages[r];
+    return m >= pp * kPage && P >= pp && P <= a.max_pages && m <= P * kPage;
 }
 
 // gp_decode_step: the summary update of query heads [h G, h G + G) of request
@@ -143,16 +156,15 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     const int Hq = Hkv * G;
     const int m_in = a.seq_lens[r];
     if (m_in < 0) {                           // held: not in this step's batch
-        record_step(a, r, h, chunk, -1, false);
+        record_step(a, r, h, chunk, -1, false, 0);
         return;
     }
     const StepView sv = step_view(a, r, m_in);
-    record_step(a, r, h, chunk, sv.m_attn, sv.room);
     // with a new token, only the requests that take it update their summaries
     if (chunk == 0 && (a.k_new == nullptr || sv.room)) fold_summaries<T, D, G>(a, r, h);
-    const int P = sv.P;
     const int m = sv.m_attn;
     const int nchunks = cdiv(m, CHUNK);
+    record_step(a, r, h, chunk, sv.m_attn, sv.room, nchunks > 1 ? nchunks : 0);
     T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     if (m == 0) {
         if (chunk == 0)
@@ -328,7 +340,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 
     // merge the waves: thread -> (g, dim) pairs
     const bool single = nchunks == 1;
-    float *part = a.partial + (((size_t)r * Hkv + h) * a.max_chunks + chunk) * G * (D + 2);
+    float *part = a.partial + (((size_t)r * Hkv + h) * a.slots + chunk) * G * (D + 2);
     for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
         const int g = i / D, dd = i % D;
         float M = kNegInf;
@@ -400,8 +412,13 @@ __device__ inline float row_sum16(float x) {
 // value load reads one whole 2D-byte row per instruction and the accumulators
 // take G * D / 64 registers; Q waits in LDS.  The waves merge through LDS at
 // the end.
-template <int D, int G, bool STEP>
+// MODE 0: decode attention; 1: gp_decode_step (summaries and/or the new token
+// folded in); 2: the private tails of gp_decode_attention_shared (a request
+// that reads its group's shared prefix pass covers the pages after the prefix
+// only, and its partials follow the prefix's).
+template <int D, int G, int MODE>
 __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeArgs a) {
+    constexpr bool STEP = MODE == 1, PREFIX = MODE == 2;
     constexpr int KK = D / 32;            // MFMA steps per page
     constexpr int DPL = D / 64;           // head dims per lane in P.V (2 or 1)
     constexpr int HR = (G + 3) / 4;       // lane rows that carry real heads
@@ -421,12 +438,34 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int Hkv = a.Hkv, Hq = Hkv * G;
     const int m_in = a.seq_lens[r];
+    // PREFIX: a request whose prefix pages the prefix pass read starts after
+    // them, in the partial slots after the prefix chunks' (the pass wrote
+    // matched[r] for every request of a group)
+    int base_page = 0, slot0 = 0;
+    bool pmatch = false;
+    if constexpr (PREFIX) {
+        int gsel = -1;
+        for (int g = 0; g < a.ngroups; ++g)
+            if (r >= a.g_first[g] && r < a.g_first[g] + a.g_num[g]) gsel = g;
+        if (gsel >= 0) {                                  // uniform
+            // the prefix pass's test for this request, evaluated here as well
+            const int pp = a.g_pages[gsel];
+            bool ok = prefix_reader(a, r, pp);
+            const int32_t *row = a.page_table + (size_t)r * a.max_pages;
+            const int32_t *lrow = a.page_table + (size_t)a.g_first[gsel] * a.max_pages;
+            for (int j = tid; ok && j < pp; j += blockDim.x) ok = row[j] == lrow[j];
+            pmatch = __syncthreads_and(ok);
+            if (pmatch) {
+                base_page = pp;
+                slot0 = cdiv(pp, a.chunk_pages);
+            }
+        }
+    }
     if (m_in < 0) {                           // held: not in this step's batch
-        record_step(a, r, h, chunk, -1, false);
+        record_step(a, r, h, chunk, -1, false, 0);
         return;
     }
     const StepView sv = step_view(a, r, m_in);
-    record_step(a, r, h, chunk, sv.m_attn, sv.room);
     const int CHUNK = a.chunk_pages * kPage;
 
     // gp_decode_step: the summaries of query heads [h G, h G + G) are updated
@@ -470,10 +509,12 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     };
 
     const int m = sv.m_attn;
-    const int nchunks = cdiv(m, CHUNK);
+    const int mt = m - base_page * kPage;         // tokens this pass covers
+    const int nchunks = cdiv(mt, CHUNK);
+    record_step(a, r, h, chunk, m, sv.room, (pmatch || nchunks > 1) ? slot0 + nchunks : 0);
     uint16_t *out = reinterpret_cast<uint16_t *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
-    if (m == 0) {
-        if (chunk == 0)
+    if (mt == 0) {
+        if (chunk == 0 && !pmatch)
             for (int i = tid; i < G * D; i += blockDim.x) out[i] = 0;
         finish_fold();
         return;
@@ -481,8 +522,9 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     if (chunk >= nchunks) return;
     // the request's pages split into nchunks nearly equal chunks (the chunk
     // count is the merge's; equal lengths keep the workgroups' durations even)
-    const int npg = cdiv(m, kPage), cs = cdiv(npg, nchunks);
-    const int page_begin = min(npg, chunk * cs), page_end = min(npg, page_begin + cs);
+    const int npg = cdiv(mt, kPage), cs = cdiv(npg, nchunks);
+    const int page_begin = base_page + min(npg, chunk * cs);
+    const int page_end = base_page + min(npg, chunk * cs + cs);
 
     const int n = lane & 15, kg = lane >> 4;          // score layout: token n, key slice kg
     const int v_off = lane * DPL;                     // P.V: lane owns dims [lane * DPL, +DPL)
@@ -665,8 +707,8 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
         for (int e = 0; e < DPL; ++e) s_o[wave][g][v_off + e] = o[g][e];
     __syncthreads();
 
-    const bool single = nchunks == 1;
-    float *part = a.partial + (((size_t)r * Hkv + h) * a.max_chunks + chunk) * G * (D + 2);
+    const bool single = nchunks == 1 && !pmatch;
+    float *part = a.partial + (((size_t)r * Hkv + h) * a.slots + slot0 + chunk) * G * (D + 2);
     for (int i = tid; i < G * D; i += blockDim.x) {
         const int g = i / D, dd = i % D;
         float M = kNegInf;
@@ -701,12 +743,12 @@ constexpr int kFastMerge = 8;   // chunks a merge folds without staging
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     using Tr = Traits<T>;
-    const int CHUNK = a.chunk_pages * kPage;
-    constexpr int MAXC = kMaxDecodeChunks;
+    constexpr int MAXC = kMaxDecodeChunks + 1;       // partial slots (a shared prefix takes one more)
     __shared__ float s_f[MAXC][G];                 // exp2(m_k - M) / L per chunk and head
     __shared__ float s_ml[MAXC][G][2];
     const int h = blockIdx.x, r = blockIdx.y;
-    // tokens attended, as the chunk pass recorded them (-1: held, nothing to merge)
+    // tokens attended and partial slots, as the chunk pass recorded them
+    // (-1: held; 0 slots: the chunk pass wrote the output)
     const int m = a.lens[r];
     if (m < 0) return;
     if (a.advance && h == 0 && threadIdx.x == 0 && a.lens[a.R + r]) {
@@ -714,11 +756,11 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
         a.seq_lens_w[r] = m;
         if (a.positions) a.positions[r] += 1;
     }
-    const int nchunks = cdiv(m, CHUNK);
-    if (nchunks <= 1) return;
+    const int nchunks = a.lens[2 * a.R + r];
+    if (nchunks == 0) return;
     const int Hq = a.Hkv * G;
     T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
-    const float *base = a.partial + ((size_t)r * a.Hkv + h) * a.max_chunks * G * (D + 2);
+    const float *base = a.partial + ((size_t)r * a.Hkv + h) * a.slots * G * (D + 2);
     const int tid = threadIdx.x;
     if (nchunks <= kFastMerge) {
         // few chunks: every thread loads all it needs at once (one round trip,
@@ -783,23 +825,284 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Shared-prefix pass (gp_decode_attention_shared; App. E.2 keeps a common
+// prefix in reference-counted blocks that many requests read).  Work item =
+// (KV head h, prefix chunk c, block of 4 * 16 / G requests of one group).  The
+// chunk's pages are read once per workgroup, staged in LDS (keys row-major,
+// values transposed), and each of the four waves serves 16 query rows (16 / G
+// requests x G heads): Q.K^T on v_mfma_f32_16x16x32_bf16 as in the split
+// kernel, online softmax per row over two pages at a time, and P.V on
+// v_mfma_f32_16x16x32_bf16 with P split into two bfloat16 terms (hi + lo carry
+// 16 significant bits, so P.V keeps float32-level accuracy while the values
+// stay exact bfloat16).  The
+// chunk's (o, max, sum) per row go to the partial slot c of each request; the
+// private tails follow in the next slots and the merge folds them together.
+// A request reads the pass only if it is not held, holds at least the
+// prefix's tokens and its table matches the group leader's on every prefix
+// page (matched[r], written by the (h 0, c 0) workgroups for the tail pass);
+// otherwise the tail pass covers all of its pages.
+// Bound: HBM on the tails; the prefix pages are read once per block of
+// requests instead of once per request.
+typedef short bf16x4s_t __attribute__((ext_vector_type(4)));
+
+__device__ inline bf16x4s_t split_hi(const float (&p)[4], float (&lo)[4]) {
+    bf16x4s_t hi;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const uint16_t b = f32_to_bf16(p[e]);
+        hi[e] = (short)b;
+        lo[e] = p[e] - bf16_to_f32(b);
+    }
+    return hi;
+}
+__device__ inline bf16x4s_t to_bf16x4(const float (&x)[4]) {
+    bf16x4s_t r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = (short)f32_to_bf16(x[e]);
+    return r;
+}
+
+// The prefix pass runs in workgroups of kPrefixWaves waves; a round stages
+// kPrefixBatch pages (the next round's travel in registers while this one is
+// computed from LDS), and the waves take them two at a time (32 tokens: one
+// 16x16x32 MFMA per output tile and bf16 term of P.V).
+constexpr int kPrefixBatch = 4;
+
+template <int D, int G>
+__global__ __launch_bounds__(64 * kPrefixWaves) void prefix_kernel(DecodeArgs a) {
+    constexpr int KK = D / 32;            // Q.K^T MFMA steps per page
+    constexpr int NW = kPrefixWaves;
+    constexpr int NT = 64 * NW;
+    constexpr int RPW = 16 / G;           // requests per wave (16 query rows)
+    constexpr int RPB = NW * RPW;         // requests per workgroup
+    constexpr int KS = D + 8;             // key row stride in LDS (elements; 16 bytes of padding)
+    constexpr int VS = 2 * kPage + 8;     // transposed value row stride: 32 tokens + padding
+    constexpr int DT = D / 16;            // P.V output tiles of 16 dims
+    constexpr int UPP = kPage * D / 8;    // 16-byte units of one page of one head (keys or values)
+    constexpr int NB = kPrefixBatch;      // pages per round (even)
+    constexpr int UPT = 2 * UPP * NB / NT;   // units a thread stages per round
+    static_assert(NB % 2 == 0 && (2 * UPP * NB) % NT == 0, "staging layout");
+    __shared__ __attribute__((aligned(16))) uint16_t s_k[NB][kPage][KS];
+    __shared__ __attribute__((aligned(16))) uint16_t s_vt[NB / 2][D][VS];
+    __shared__ float s_p[NW][16][2 * kPage + 1];
+    __shared__ int s_ids[kMaxChunkPages];
+    __shared__ int s_match[RPB];
+
+    const int h = blockIdx.x, c = blockIdx.y, blk = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int n = lane & 15, kg = lane >> 4;
+    int gi = 0;
+    while (gi + 1 < a.ngroups && blk >= a.g_blk0[gi + 1]) ++gi;
+    const int first = a.g_first[gi], nreq = a.g_num[gi], ppages = a.g_pages[gi];
+    const int r0 = first + (blk - a.g_blk0[gi]) * RPB;
+    const int p_begin = c * a.chunk_pages, p_end = min(ppages, p_begin + a.chunk_pages);
+    const int Hkv = a.Hkv, Hq = Hkv * G;
+    const int32_t *lead = a.page_table + (size_t)first * a.max_pages;
+
+    // which requests of the block read the pass (the same test in every
+    // workgroup of the block, so they agree without talking)
+    for (int j = tid; j < RPB; j += NT) {
+        const int r = r0 + j;
+        s_match[j] = r < first + nreq && prefix_reader(a, r, ppages) ? 1 : 0;
+    }
+    for (int k = tid; k < p_end - p_begin; k += NT) {
+        const int pid = lead[p_begin + k];
+        s_ids[k] = pid >= 0 && pid < a.pool_pages ? pid : -1;
+    }
+    __syncthreads();
+    for (int e = tid; e < RPB * ppages; e += NT) {
+        const int j = e / ppages, pg = e % ppages;
+        if (s_match[j] && a.page_table[(size_t)(r0 + j) * a.max_pages + pg] != lead[pg]) s_match[j] = 0;
+    }
+    __syncthreads();
+    if (p_begin >= ppages) return;
+    int any = 0;
+    for (int j = 0; j < RPB; ++j) any |= s_match[j];
+    if (!any) return;                                    // uniform
+
+    // this wave's 16 query rows: row rho = request (wave * RPW + rho / G), head rho % G
+    const int jq = wave * RPW + n / G;
+    const bool rowq = s_match[jq] != 0;
+    bf16x8_t qa[KK];
+    {
+        const uint16_t *qp = reinterpret_cast<const uint16_t *>(a.q) +
+                             ((size_t)(rowq ? r0 + jq : first) * Hq + (size_t)h * G + n % G) * D;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const bf16x8_t x = *reinterpret_cast<const bf16x8_t *>(qp + kk * 32 + kg * 8);
+            qa[kk] = rowq ? x : bf16x8_t{};
+        }
+    }
+
+    const uint16_t *kpool = reinterpret_cast<const uint16_t *>(a.k);
+    const uint16_t *vpool = reinterpret_cast<const uint16_t *>(a.v);
+    const size_t head_off = (size_t)h * kPage * D;
+    const size_t page_elems = (size_t)Hkv * kPage * D;
+    const int npage = p_end - p_begin;
+    // staging: unit e of a round (e = tid + q * NT) is page e / (2 UPP), keys
+    // if (e % (2 UPP)) < UPP else values, token and dims from e % UPP
+    uint4 nxt[UPT];
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int q = 0; q < UPT; ++q) {
+            const int e = tid + q * NT, b = e / (2 * UPP), w2 = e % (2 * UPP), u = w2 % UPP;
+            const int k = k0 + b;
+            const int phys = k < npage ? s_ids[k] : -1;
+            const uint16_t *pool = w2 < UPP ? kpool : vpool;
+            const uint16_t *src = pool + (size_t)(phys >= 0 ? phys : 0) * page_elems + head_off +
+                                  (u / (D / 8)) * D + (u % (D / 8)) * 8;
+            const uint4 x = *reinterpret_cast<const uint4 *>(src);
+            nxt[q] = phys >= 0 ? x : make_uint4(0u, 0u, 0u, 0u);
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int q = 0; q < UPT; ++q) {
+            const int e = tid + q * NT, b = e / (2 * UPP), w2 = e % (2 * UPP), u = w2 % UPP;
+            const int tok = u / (D / 8), dim = (u % (D / 8)) * 8;
+            if (w2 < UPP) {
+                *reinterpret_cast<uint4 *>(&s_k[b][tok][dim]) = nxt[q];
+            } else {
+                const uint32_t w4[4] = {nxt[q].x, nxt[q].y, nxt[q].z, nxt[q].w};
+                const int col = (b & 1) * kPage + tok;      // token within the page pair
+#pragma unroll
+                for (int e2 = 0; e2 < 4; ++e2) {
+                    s_vt[b >> 1][dim + 2 * e2][col] = (uint16_t)(w4[e2] & 0xffffu);
+                    s_vt[b >> 1][dim + 2 * e2 + 1][col] = (uint16_t)(w4[e2] >> 16);
+                }
+            }
+        }
+    };
+
+    float mrun[4], lrun[4];
+    f32x4_t o[DT];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        mrun[i] = kNegInf;
+        lrun[i] = 0.0f;
+    }
+#pragma unroll
+    for (int t = 0; t < DT; ++t) o[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+    fetch(0);
+    stage();
+    __syncthreads();
+    for (int k0 = 0; k0 < npage; k0 += NB) {
+        if (k0 + NB < npage) fetch(k0 + NB);             // in flight while this round is computed
+        for (int b = 0; b < NB && k0 + b < npage; b += 2) {
+            // S = Q K^T for 16 rows x 32 tokens (two pages; the second may be
+            // past the chunk's end or invalid: its scores are masked)
+            const bool v0 = s_ids[k0 + b] >= 0;
+            const bool v1 = k0 + b + 1 < npage && s_ids[k0 + b + 1] >= 0;
+            bf16x8_t kb0[KK], kb1[KK];
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                kb0[kk] = *reinterpret_cast<const bf16x8_t *>(&s_k[b][n][kk * 32 + kg * 8]);
+                kb1[kk] = *reinterpret_cast<const bf16x8_t *>(&s_k[b + 1][n][kk * 32 + kg * 8]);
+            }
+            f32x4_t acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], kb0[kk], acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], kb1[kk], acc1, 0, 0, 0);
+            }
+            // online softmax of rows 4 kg + i over the 32 tokens
+            float p0[4], p1[4], alpha[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float s0 = v0 ? acc0[i] * a.qscale : kNegInf;
+                const float s1 = v1 ? acc1[i] * a.qscale : kNegInf;
+                const float mn = fmaxf(mrun[i], fmaxf(row_max16(s0), row_max16(s1)));
+                // arguments are <= 0: the hardware exp2 needs no range fix-up
+                alpha[i] = mn == kNegInf ? 1.0f : __builtin_amdgcn_exp2f(mrun[i] - mn);
+                mrun[i] = mn;
+                p0[i] = mn == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(s0 - mn);
+                p1[i] = mn == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(s1 - mn);
+                lrun[i] = lrun[i] * alpha[i] + p0[i] + p1[i];
+            }
+            wave_lds_sync();                               // the previous pair's reads of s_p are done
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                s_p[wave][kg * 4 + i][n] = p0[i];
+                s_p[wave][kg * 4 + i][kPage + n] = p1[i];
+            }
+            wave_lds_sync();
+            // P as the A operand: row n, tokens 8 kg .. 8 kg + 7, in two bf16 terms
+            bf16x8_t a_hi, a_lo;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float x = s_p[wave][n][kg * 8 + e];
+                a_hi[e] = (__bf16)x;                      // round to nearest even
+                a_lo[e] = (__bf16)(x - (float)a_hi[e]);   // x - hi is exact in float32
+            }
+            // skip the rescale while no row's maximum has moved (wave-uniform)
+            bool moved = false;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) moved = moved || alpha[i] != 1.0f;
+            if (__builtin_amdgcn_read_exec() && __any(moved)) {
+#pragma unroll
+                for (int t = 0; t < DT; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) o[t][i] *= alpha[i];
+            }
+#pragma unroll
+            for (int t = 0; t < DT; ++t) {
+                const bf16x8_t vb = *reinterpret_cast<const bf16x8_t *>(&s_vt[b >> 1][t * 16 + n][kg * 8]);
+                o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_hi, vb, o[t], 0, 0, 0);
+                o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_lo, vb, o[t], 0, 0, 0);
+            }
+        }
+        __syncthreads();                                  // every wave is done with this round
+        if (k0 + NB < npage) {
+            stage();
+            __syncthreads();
+        }
+    }
+
+    // partials of rows 4 kg + i: o of dims 16 t + n, (max, sum) written by lane n = 0
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float l = row_sum16(lrun[i]);
+        const int rho = kg * 4 + i, j = wave * RPW + rho / G, g = rho % G;
+        if (!s_match[j]) continue;
+        float *part = a.partial + (((size_t)(r0 + j) * Hkv + h) * a.slots + c) * G * (D + 2) + (size_t)g * (D + 2);
+#pragma unroll
+        for (int t = 0; t < DT; ++t) part[t * 16 + n] = o[t][i];
+        if (n == 0) {
+            part[D] = mrun[i];
+            part[D + 1] = l;
+        }
+    }
+}
+
 template <typename T, int D>
 hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, int stages, hipStream_t s) {
     dim3 mgrid(a.Hkv, a.R);
     constexpr bool bf16 = sizeof(T) == 2;
-    // the step variant (summaries and/or the new token folded in) is its own
-    // instantiation, so plain decode attention carries none of its code
-    const bool step = a.qstate != nullptr || a.k_new != nullptr;
-    // the merge pass also advances the lengths when a token went in
-    const bool chunks = stages & GP_DECODE_CHUNKS,
-               merge = (stages & GP_DECODE_MERGE) && (a.max_chunks > 1 || (a.k_new && a.advance));
+    // the step variant (summaries and/or the new token folded in) and the
+    // tails of the shared-prefix decode are their own instantiations, so plain
+    // decode attention carries none of their code
+    const int mode = a.ngroups > 0 ? 2 : (a.qstate != nullptr || a.k_new != nullptr) ? 1 : 0;
+    // the merge pass also advances the lengths when a token went in, and folds
+    // the prefix partials of a shared-prefix call
+    const bool chunks = stages & GP_DECODE_CHUNKS, prefix = (stages & GP_DECODE_PREFIX) && mode == 2,
+               merge = (stages & GP_DECODE_MERGE) && (a.max_chunks > 1 || (a.k_new && a.advance) || mode == 2);
+    // prefix pass grid: (KV head, prefix chunk, request block)
+    int max_pc = 0;
+    for (int g = 0; g < a.ngroups; ++g) max_pc = max(max_pc, cdiv(a.g_pages[g], a.chunk_pages));
+    const dim3 pgrid(a.Hkv, max(max_pc, 1), max(a.g_blk0[a.ngroups], 1));
     switch (G) {
 #define GP_CASE(GG)                                                  \
     case GG:                                                         \
-        if (chunks && bf16 && step)                                  \
-            decode_split_kernel<D, GG, true><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
+        if (prefix && bf16)                                          \
+            prefix_kernel<D, GG><<<pgrid, 64 * kPrefixWaves, 0, s>>>(a); \
+        if (chunks && bf16 && mode == 2)                             \
+            decode_split_kernel<D, GG, 2><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
+        else if (chunks && bf16 && mode == 1)                        \
+            decode_split_kernel<D, GG, 1><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
         else if (chunks && bf16)                                     \
-            decode_split_kernel<D, GG, false><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
+            decode_split_kernel<D, GG, 0><<<grid, 64 * kDecodeWaves, 0, s>>>(a); \
         else if (chunks)                                             \
             decode_kernel<float, D, GG><<<grid, 256, 0, s>>>(a);     \
         if (merge) merge_kernel<T, D, GG><<<mgrid, 256, 0, s>>>(a);  \

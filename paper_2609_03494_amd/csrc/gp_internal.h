@@ -47,7 +47,7 @@ __device__ inline float ema_step(float prev, float x, double beta, double one_mi
 
 struct DecodeWs {
     size_t partial, lens, total;
-    int max_chunks, chunk_pages;
+    int max_chunks, chunk_pages, slots;
 };
 
 // Work split of decode attention: every request is cut into chunks of about
@@ -65,10 +65,15 @@ __host__ __device__ inline DecodeWs decode_ws(int R, int Hq, int Hkv, int D, int
     w.chunk_pages = decode_chunk_pages(max_pages);
     w.max_chunks = cdiv(max_pages, w.chunk_pages);
     size_t off = 0;
-    w.partial = off;    // float: [R][Hkv][max_chunks][G][D + 2] (o, max, sum)
-    off = align_up(off + (size_t)R * Hkv * w.max_chunks * G * (D + 2) * sizeof(float));
-    w.lens = off;       // int32: [R] tokens attended (-1: held), [R] token appended (0/1)
-    off = align_up(off + (size_t)R * 2 * sizeof(int32_t));
+    // partial slots per (request, KV head): the chunks of the request, plus one
+    // more for a shared prefix (its chunks have the decode chunk size, so a
+    // request of a prefix group needs at most one slot more than its pages)
+    w.slots = w.max_chunks + 1;
+    w.partial = off;    // float: [R][Hkv][slots][G][D + 2] (o, max, sum)
+    off = align_up(off + (size_t)R * Hkv * w.slots * G * (D + 2) * sizeof(float));
+    w.lens = off;       // int32: [R] tokens attended (-1: held), [R] token appended (0/1),
+                        //        [R] partial slots the merge folds (0: none)
+    off = align_up(off + (size_t)R * 3 * sizeof(int32_t));
     w.total = off;
     return w;
 }
@@ -142,6 +147,9 @@ __host__ __device__ inline ApplyWs apply_ws(int Rb, int Hkv, int D, int elem, in
 
 // ------------------------------------------------------------ launch args --
 
+constexpr int kMaxPrefixGroups = 16;      // prefix groups one shared decode call takes
+constexpr int kPrefixWaves = 4;           // waves per workgroup of the shared-prefix pass
+
 struct DecodeArgs {
     const void *k, *v;
     const int32_t *page_table, *num_pages, *seq_lens;
@@ -162,8 +170,14 @@ struct DecodeArgs {
     int32_t *seq_lens_w, *positions;
     int advance;
     float *partial;
-    int32_t *lens;                // [R] tokens attended (-1: held), then [R] appended flags
-    int R, Hkv, max_pages, pool_pages, max_chunks, chunk_pages;
+    int32_t *lens;                // [R] tokens attended (-1: held), [R] appended flags, [R] merge slots
+    // shared-prefix decode (gp_decode_attention_shared): requests
+    // [g_first, g_first + g_num) share the first g_pages pages of g_first's
+    // table; workgroup blocks [g_blk0[g], g_blk0[g + 1]) of the prefix pass
+    int ngroups;
+    int g_first[kMaxPrefixGroups], g_num[kMaxPrefixGroups], g_pages[kMaxPrefixGroups];
+    int g_blk0[kMaxPrefixGroups + 1];
+    int R, Hkv, max_pages, pool_pages, max_chunks, chunk_pages, slots;
     float qscale;   // scale * log2(e)
 };
 

@@ -442,6 +442,95 @@ def test_boundary_tables_beyond_2048_pages(tau):
     assert (res["decisions"] == want).all()
 
 
+# ------------------------------------------- decode over a shared prefix --
+
+def _shared_case(case):
+    if case == "g4":
+        return W.prefix_shared(num_reqs=24, prefix_len=320, tail_lo=20, tail_hi=900, free_pages=60,
+                               num_q_heads=32)
+    return W.prefix_shared(num_reqs=20, prefix_len=320, tail_lo=20, tail_hi=1500, free_pages=60)
+
+
+@pytest.mark.parametrize("case", ["g8", "g4", "g8_mixed", "g8_two_groups"])
+def test_decode_shared_prefix(case):
+    """gp_decode_attention_shared (App. E.2 shared prefix blocks read once per
+    block of requests) against the oracle.  "mixed": one member's prefix page
+    replaced by a private copy (a compaction does that), one member holding
+    fewer tokens than the prefix, one held member -- those must fall back to
+    reading their own pages; "two_groups": the batch split into two groups,
+    the second with a shorter declared prefix."""
+    w = _shared_case("g4" if case == "g4" else "g8")
+    b, R = w.page_size, w.num_reqs
+    pp = w.meta["prefix_len"] // b
+    dc = DeviceCase(w)
+    k_pool, v_pool = w.dense_pool("k"), w.dense_pool("v")
+    table, seq = w.page_table.copy(), w.seq_lens.copy()
+    held = None
+    if case == "g8_mixed":
+        # request 5: its prefix page 3 becomes a private copy with the same rows
+        new = int(w.free_list[w.free_count - 1])
+        old = int(table[5, 3])
+        k_pool[new], v_pool[new] = k_pool[old], v_pool[old]
+        table[5, 3] = new
+        for x in (dc.layers[0].k, dc.layers[0].v):
+            x[new] = x[old]
+        dc.ps.page_table[5, 3] = new
+        # request 7 holds fewer tokens than the prefix; request 9 is held
+        seq[7] = 100
+        dc.ps.seq_lens[7] = 100
+        held = 9
+        dc.ps.seq_lens[held] = -int(seq[held]) - 1
+    groups = [(0, R, pp)] if case != "g8_two_groups" else [(0, 9, pp), (9, R - 9, 7)]
+    scale = float(np.float32(1.0 / math.sqrt(w.head_dim)))
+    _say(f"decode, shared prefix of {pp} pages: {case}, {R} requests, groups {groups}")
+    out = torch.full_like(dc.q_post, float("nan"))
+    gp.gp_decode_attention_shared(dc.layers[0], dc.ps, dc.q_post, scale, out, groups, dc.ws_decode)
+    plain = torch.full_like(dc.q_post, float("nan"))
+    gp.gp_decode_attention(dc.layers[0], dc.ps, dc.q_post, scale, plain, dc.ws_decode)
+    torch.cuda.synchronize()
+    got = O.widen(to_numpy(out), w.dtype)
+    active = [r for r in range(R) if r != held]
+    ref = O.decode_attention(k_pool, v_pool, w.dtype, table, seq, w.q_post, w.num_q_heads, scale,
+                             requests=active)[active]
+    assert_rows_close(got[active], ref, 2e-2, "shared decode bf16")
+    assert bf16_rounding_ok(got[active], ref), "shared decode bf16: beyond bf16 rounding of the exact value"
+    if held is not None:
+        assert np.isnan(got[held]).all(), "the held request's output row was written"
+    # against the plain call: one bf16 step apart at most, plus the float32
+    # accumulation-order term of elements that nearly cancel (1e-5 of the row)
+    pl = O.widen(to_numpy(plain), w.dtype)[active]
+    tol = np.abs(pl) * 2.0 ** -7 + 1e-5 * np.abs(pl).max(axis=-1, keepdims=True)
+    assert (np.abs(got[active] - pl) <= tol).all()
+
+
+def test_decode_shared_prefix_stages_on_two_streams():
+    """The prefix pass on a second stream beside the tail pass, then the merge:
+    the bytes of the whole call (the two passes write disjoint partials)."""
+    w = _shared_case("g8")
+    pp = w.meta["prefix_len"] // w.page_size
+    dc = DeviceCase(w)
+    scale = float(np.float32(1.0 / math.sqrt(w.head_dim)))
+    groups = [(0, w.num_reqs, pp)]
+    _say("decode, shared prefix: prefix pass on a second stream beside the tails")
+    whole = torch.full_like(dc.q_post, float("nan"))
+    gp.gp_decode_attention_shared(dc.layers[0], dc.ps, dc.q_post, scale, whole, groups, dc.ws_decode)
+    torch.cuda.synchronize()
+    ws2 = torch.zeros_like(dc.ws_decode)
+    split = torch.full_like(dc.q_post, float("nan"))
+    cur, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    side.wait_stream(cur)
+    with torch.cuda.stream(side):
+        gp.gp_decode_attention_shared(dc.layers[0], dc.ps, dc.q_post, scale, split, groups, ws2,
+                                      stages=gp.GP_DECODE_PREFIX)
+    gp.gp_decode_attention_shared(dc.layers[0], dc.ps, dc.q_post, scale, split, groups, ws2,
+                                  stages=gp.GP_DECODE_CHUNKS)
+    cur.wait_stream(side)
+    gp.gp_decode_attention_shared(dc.layers[0], dc.ps, dc.q_post, scale, split, groups, ws2,
+                                  stages=gp.GP_DECODE_MERGE)
+    torch.cuda.synchronize()
+    assert to_numpy(split).tobytes() == to_numpy(whole).tobytes()
+
+
 def test_boundary_tiny_all_branches():
     params = {"tau=0": O.Params(), "grow": O.Params(tau=-math.inf), "compress": O.Params(tau=math.inf)}
     for name, p in params.items():
