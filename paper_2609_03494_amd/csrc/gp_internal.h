@@ -216,6 +216,7 @@ struct ScoreArgs {
     int Rb, Hq, Hkv, M, max_pages, pool_pages, max_cand, cmax, nch, R;
     double scale, theta, p;
     int metric;       // GP_METRIC_*
+    int lg_iters;     // statistics blocks per logits workgroup (set at launch)
 };
 
 struct ApplyArgs {

@@ -5,11 +5,12 @@
 //  0. prep: per (boundary request, KV head) the 2G aligned summaries of its
 //     GQA group (RMS calibration to the current query, then rotation at the
 //     current position; fp64, angles computed on the device in fp64).
-//  1. logits: per (boundary request, KV head, block of kStatBlock candidate
-//     tokens), one wave: the block's 2G logits per token in fp64; the block's
-//     max and sum of exponentials per view go to the workspace (fp64), and
-//     exp(z - block max) per token is stored in float32 (relative error below
-//     2^-24, about one rounding of the float32 weight it feeds).
+//  1. logits: per (boundary request, KV head, set of blocks of kStatBlock
+//     candidate tokens), one wave: each block's 2G logits per token in fp64
+//     on the fp64 matrix cores; the block's max and sum of exponentials per
+//     view go to the workspace (fp64), and exp(z - block max) per token is
+//     stored in float32 (relative error about 2^-24: one rounding of the
+//     float32 weight it feeds).
 //  2. weights: merge the block statistics per view, scale each token's
 //     exponentials into softmax weights, average the G query heads of each
 //     view (fp64), round to float32 and write a^S, a^L (workspace) and
@@ -52,6 +53,49 @@ struct KRow<float> {
         return __uint_as_float(e == 0 ? u.x : e == 1 ? u.y : e == 2 ? u.z : u.w);
     }
 };
+
+// exp(x) for x <= 0 in fp64, to a relative error below 2^-36: x = n ln 2 + r
+// with |r| <= ln 2 / 2 (n = rint(x / ln 2), ln 2 in two parts so that r is
+// exact to fp64 rounding), exp(r) by its Taylor polynomial of degree 9
+// (truncation below 0.35^10 / 10! < 2^-37), then scaled by 2^n; results
+// below the smallest fp64 denormal flush to zero in the scaling.  The
+// exponentials feed float32 values and an fp64 sum, so this is far below
+// the rounding they then take.
+// (The coefficients are pinned to scalar registers, so that each Horner step
+// is one three-operand FMA rather than a copy of the constant and an FMA.)
+__device__ inline double sreg(double c) {
+    double r;
+    asm("" : "=s"(r) : "0"(c));
+    return r;
+}
+__device__ inline double exp_nonpos(double x) {
+    const double n = __builtin_rint(x * sreg(1.4426950408889634));
+    double r = __builtin_fma(-n, sreg(6.93147180369123816490e-01), x);
+    r = __builtin_fma(-n, sreg(1.90821492927058770002e-10), r);
+    double p = sreg(1.0 / 362880.0);
+    p = __builtin_fma(p, r, sreg(1.0 / 40320.0));
+    p = __builtin_fma(p, r, sreg(1.0 / 5040.0));
+    p = __builtin_fma(p, r, sreg(1.0 / 720.0));
+    p = __builtin_fma(p, r, sreg(1.0 / 120.0));
+    p = __builtin_fma(p, r, sreg(1.0 / 24.0));
+    p = __builtin_fma(p, r, sreg(1.0 / 6.0));
+    p = __builtin_fma(p, r, 0.5);
+    p = __builtin_fma(p, r, 1.0);
+    p = __builtin_fma(p, r, 1.0);
+    return __builtin_ldexp(p, (int)fmax(n, -2100.0));
+}
+
+// max without the NaN canonicalisation of fmax (the operands are finite or -inf)
+__device__ inline double max_f64(double a, double b) { return a > b ? a : b; }
+
+// x from the lane N places down in its row of 16 (rotating), for an fp64 value
+template <int N>
+__device__ inline double dpp_ror_f64(double x) {
+    const long long b = __builtin_bit_cast(long long, x);
+    const int lo = __builtin_amdgcn_mov_dpp((int)b, 0x120 + N, 0xf, 0xf, false);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), 0x120 + N, 0xf, 0xf, false);
+    return __builtin_bit_cast(double, ((long long)hi << 32) | (unsigned)lo);
+}
 
 __device__ inline bool boundary_of(const ScoreArgs &a, int i, int &r, int &P) {
     r = a.bnd[i];
@@ -126,148 +170,163 @@ __global__ __launch_bounds__(256, 5) void prep_kernel(ScoreArgs a) {
 }
 
 // ------------------------------------------------------------------- logits --
-// Grid (KV head, blocks of kStatBlock candidates, boundary request), two
-// waves per workgroup, 32 candidates each.  The 2G x D logits of the block are a small fp64 matrix
-// product, done on the matrix cores with v_mfma_f64_16x16x4f64: the A operand
-// is the aligned summaries (row = view, padded to 16 rows with zeros), B the
-// keys of 16 candidates, so each wave runs two chains of D/4 MFMAs.  The
-// contraction over head dimensions is split four ways across lane groups: in
-// step s, lane group q (lanes 16q .. 16q+15) supplies dimension (D/4) q + s,
-// so each lane reads one contiguous quarter row of summaries (once) and of
-// each of its keys.  The result leaves view 4j + q of candidate l % 16 in
-// register j of lane l.  Per view, the block's max m and sum of exp(z - m)
-// (16-lane reductions, then across the two waves in LDS) go to the
-// statistics array; exp(z - m) of each token
-// is stored (float32), so that the weights need a product, not an
-// exponential, per token.  A lane whose page id is invalid contributes zero logits.
-typedef double f64x4_t __attribute__((ext_vector_type(4)));
-constexpr int kLogitsWaves = 2;                 // waves per block of kStatBlock candidates
+// Grid (KV head, split, boundary request), one wave per workgroup.  Workgroup
+// y of a request handles statistics blocks y, y + splits, y + 2 splits, ...
+// (at most kLogitsMaxIters) of kStatBlock = 64 candidates each.  The 2G x D
+// logits of a block are a small fp64 matrix product on the matrix cores,
+// v_mfma_f64_4x4x4f64: four independent 4 x 4 x 4 products per instruction
+// (16 cycles for 512 flops, the same rate per flop as 16x16x4, but with no
+// padding rows at 2G <= 8 views).  Lane l = 16 k + 4 b + j holds row j of
+// block b's A and column j of its B for contraction index k, and element
+// (k, j) of its result.  The four blocks are four groups of 4 candidates
+// (B = their keys), A is one quarter of the views (4 vh .. 4 vh + 3, the same
+// in all blocks), so one key operand feeds ceil(2G / 4) instructions and each
+// key element is loaded and widened once.  The four lanes of a candidate (k =
+// 0..3) read adjacent 16-byte units of its key row, so that one load
+// instruction touches one 64-byte segment per candidate: unit u of lane k is
+// unit 4 u + k of the row, and contraction step s of lane group k takes head
+// dimension dim(k, s) = 4 E (s / E) + E k + s % E (E elements per unit).  The
+// summaries come from LDS, laid out [k][view][s] in that order, with paddings
+// that put the 16 doubles of one read on distinct banks.
+//
+// A block is taken in two halves of 32 candidates (two groups of 16, one key
+// register set each); while one half is multiplied the keys of the next half
+// are in flight, and the page ids of all the workgroup's blocks are read
+// once at the start, so the wave waits for memory once, not once per block.
+// Per view, the block's max m and sum of exp(z - m) (fp64, 16-lane DPP
+// reductions) go to the statistics array, and exp(z - m) of each token is
+// stored (float32), so that the weights need a product, not an exponential,
+// per token.  A candidate whose page id is invalid contributes zero logits.
+constexpr int kLogitsMaxIters = 32;
 
 template <typename T, int D, int G>
-__global__ __launch_bounds__(64 * kLogitsWaves) void logits_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
     constexpr int V = 2 * G;
+    constexpr int VH = (V + 3) / 4;                  // view quarters (MFMAs per key operand)
+    constexpr int VR = 4 * VH;                       // view rows in LDS (rows >= V are zero)
     constexpr int S = D / 4;                         // MFMA steps (head dimensions per lane group)
     constexpr int EPU = 16 / sizeof(T);              // key elements per 16-byte unit
     constexpr int NU = S / EPU;                      // 16-byte units of a quarter key row
-    constexpr int NW = kLogitsWaves;
-    constexpr int NGRP = kStatBlock / 16 / NW;       // candidate groups of 16 per wave
-    static_assert(kStatBlock == 64 && V <= 16 && S % EPU == 0 && NGRP * 16 * NW == kStatBlock, "layout");
-    __shared__ double s_wm[NW][16], s_ws[NW][16];
+    constexpr int SP = S + 1;                        // view row stride (doubles)
+    constexpr int KS = VR * SP + (8 - (VR * SP) % 32 + 32) % 32;   // k stride, = 8 mod 32 doubles
+    static_assert(kStatBlock == 64 && kPage == 16 && S % EPU == 0, "layout");
+    __shared__ double s_a[4 * KS];
+    __shared__ int s_pg[4 * kLogitsMaxIters];
 
-    const int h = blockIdx.x, blk = blockIdx.y, i = blockIdx.z;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col = lane & 15, q = lane >> 4;
+    const int h = blockIdx.x, y = blockIdx.y, i = blockIdx.z, ny = gridDim.y;
+    const int lane = threadIdx.x;
+    const int k = lane >> 4, cand = lane & 15;      // contraction / output row; candidate 4 b + j
     int r, P;
     if (!boundary_of(a, i, r, P)) return;
     const int C = (P - 1) * kPage;
-    const int t0 = blk * kStatBlock;
-    if (t0 >= C) return;
+    const int nblk = cdiv(C, kStatBlock);
+    if (y >= nblk) return;
     const int slot = a.slot_ids[r];
     if (slot < 0 || slot >= a.M) return;
+    const int nit = min(cdiv(nblk - y, ny), min(a.lg_iters, kLogitsMaxIters));
 
-    // A: this lane's quarter row of summary `col` (zero rows pad the views to 16)
-    // (every load below reads a valid address, clamped where the lane has no
-    // data, and the value is zeroed afterwards: the loads are all in flight at
-    // once instead of one masked load and wait at a time)
-    const double *qt = a.qt + (((size_t)i * a.Hkv + h) * V + min(col, V - 1)) * D + q * S;
-    double qa[S];
-#pragma unroll
-    for (int s2 = 0; s2 < S; s2 += 2) {
-        const double2 u = *reinterpret_cast<const double2 *>(qt + s2);
-        qa[s2] = col < V ? u.x : 0.0;
-        qa[s2 + 1] = col < V ? u.y : 0.0;
+    // the page ids of this workgroup's blocks (-1: no candidates there or an
+    // invalid id) and the aligned summaries
+    for (int e = lane; e < 4 * nit; e += 64) {
+        const int pg = 4 * (y + ny * (e / 4)) + e % 4;
+        const int pe = pg < P - 1 ? a.page_table[(size_t)r * a.max_pages + pg] : -1;
+        s_pg[e] = pe >= 0 && pe < a.pool_pages ? pe : -1;
     }
-    // B: this lane's quarter row of candidate t0 + 16 g + col, for the 4 groups
-    uint4 kb[NGRP][NU];
-    const int tw = t0 + 16 * NGRP * wave;            // this wave's first candidate
-#pragma unroll
-    for (int g = 0; g < NGRP; ++g) {
-        const int t = tw + 16 * g + col;
-        const int pe = a.page_table[(size_t)r * a.max_pages + min(t, C - 1) / kPage];
-        const int phys = t < C ? pe : -1;
-        const bool ok = phys >= 0 && phys < a.pool_pages;
-        const uint4 *kp = reinterpret_cast<const uint4 *>(reinterpret_cast<const T *>(a.k) +
-                          (((size_t)(ok ? phys : 0) * a.Hkv + h) * kPage + (t % kPage)) * D + q * S);
-#pragma unroll
-        for (int u = 0; u < NU; ++u) {
-            const uint4 x = kp[u];
-            kb[g][u] = ok ? x : make_uint4(0u, 0u, 0u, 0u);
-        }
+    const double *qt = a.qt + ((size_t)i * a.Hkv + h) * V * D;
+    for (int e = lane; e < 4 * VR * S; e += 64) {
+        const int q = e / (VR * S), rem = e % (VR * S), v = rem / S, s2 = rem % S;
+        const int d = 4 * EPU * (s2 / EPU) + EPU * q + s2 % EPU;
+        s_a[q * KS + v * SP + s2] = v < V ? qt[(size_t)v * D + d] : 0.0;
     }
-    f64x4_t acc[NGRP];
-#pragma unroll
-    for (int g = 0; g < NGRP; ++g) acc[g] = f64x4_t{0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-    for (int s2 = 0; s2 < S; ++s2) {
-#pragma unroll
-        for (int g = 0; g < NGRP; ++g) {
-            const double b = KRow<T>::elem(kb[g][s2 / EPU], s2 % EPU);
-            acc[g] = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[s2], b, acc[g], 0, 0, 0);
-        }
-    }
+    __syncthreads();
 
-    // statistics and exponentials per view (register j holds view 4j + q):
-    // per wave over its candidates, then the block's max and sum across the
-    // waves through LDS
-    float *lgv = a.expz + ((size_t)i * a.Hkv + h) * V * a.cmax;
-    double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch + blk) * V * 2;
-    double z[4][NGRP], mv[4];
+    // keys of half `hf` of block `it`: lane (k, cand) reads units k, 4 + k,
+    // ... of token cand of the block's pages 2 hf and 2 hf + 1.  The loads are
+    // unconditional (an invalid page reads page 0, and its logits are zeroed
+    // after the product), and the last half prefetches itself again, so that
+    // every wait for the current keys leaves the next half's loads in flight.
+    const T *kbase = reinterpret_cast<const T *>(a.k) + (size_t)h * kPage * D + (size_t)cand * D + k * EPU;
+    auto load_keys = [&](int it, int hf, uint4 (&kb)[2][NU]) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        mv[j] = -__builtin_huge_val();
-        if (4 * j >= V) continue;                    // uniform: no real view in this register
+        for (int g = 0; g < 2; ++g) {
+            const int pe = s_pg[4 * it + 2 * hf + g];
+            const uint4 *kp = reinterpret_cast<const uint4 *>(kbase + (size_t)max(pe, 0) * a.Hkv * kPage * D);
 #pragma unroll
-        for (int g = 0; g < NGRP; ++g) {
-            z[j][g] = acc[g][j] * a.scale;
-            if (tw + 16 * g + col < C) mv[j] = fmax(mv[j], z[j][g]);
+            for (int u = 0; u < NU; ++u) kb[g][u] = kp[4 * u];
         }
-        for (int off = 8; off >= 1; off >>= 1) mv[j] = fmax(mv[j], __shfl_xor(mv[j], off, 16));
-        if (NW > 1 && col == 0) s_wm[wave][4 * j + q] = mv[j];
-    }
-    if (NW > 1) {
-        __syncthreads();
+    };
+    const double *arow = s_a + k * KS + (lane & 3) * SP;    // A: view 4 vh + (lane & 3), dims dim(k, s)
+    auto multiply = [&](const uint4 (&kb)[2][NU], double (&acc)[VH][2]) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if (4 * j >= V) continue;
-            double m = s_wm[0][4 * j + q];
+        for (int vh = 0; vh < VH; ++vh) acc[vh][0] = acc[vh][1] = 0.0;
 #pragma unroll
-            for (int w = 1; w < NW; ++w) m = fmax(m, s_wm[w][4 * j + q]);
-            mv[j] = m;
-        }
-    }
+        for (int s2 = 0; s2 < S; ++s2) {
+            double av[VH];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int v = 4 * j + q;
-        if (4 * j >= V) continue;
-        double sv = 0.0;
+            for (int vh = 0; vh < VH; ++vh) av[vh] = arow[4 * vh * SP + s2];
 #pragma unroll
-        for (int g = 0; g < NGRP; ++g) {
-            const int t = tw + 16 * g + col;
-            if (t < C && v < V) {
-                const double ev = exp(z[j][g] - mv[j]);
-                sv += ev;
-                lgv[(size_t)v * a.cmax + t] = (float)ev;
+            for (int g = 0; g < 2; ++g) {
+                const double bv = KRow<T>::elem(kb[g][s2 / EPU], s2 % EPU);
+#pragma unroll
+                for (int vh = 0; vh < VH; ++vh)
+                    acc[vh][g] = __builtin_amdgcn_mfma_f64_4x4x4f64(av[vh], bv, acc[vh][g], 0, 0, 0);
             }
         }
-        for (int off = 8; off >= 1; off >>= 1) sv += __shfl_xor(sv, off, 16);
-        if (NW > 1) {
-            if (col == 0) s_ws[wave][v] = sv;
-        } else if (col == 0 && v < V) {
-            pt[v * 2] = mv[j];
-            pt[v * 2 + 1] = sv;
+    };
+    float *lgv = a.expz + ((size_t)i * a.Hkv + h) * V * a.cmax;
+    uint4 k0[2][NU], k1[2][NU];
+    load_keys(0, 0, k0);
+    for (int it = 0; it < nit; ++it) {
+        const int blk = y + ny * it;
+        double acc[VH][4];
+        {
+            double a2[VH][2];
+            load_keys(it, 1, k1);
+            __builtin_amdgcn_sched_barrier(0);      // the next half's loads go out first
+            multiply(k0, a2);
+#pragma unroll
+            for (int vh = 0; vh < VH; ++vh) acc[vh][0] = a2[vh][0], acc[vh][1] = a2[vh][1];
+            load_keys(min(it + 1, nit - 1), 0, k0);
+            __builtin_amdgcn_sched_barrier(0);
+            multiply(k1, a2);
+#pragma unroll
+            for (int vh = 0; vh < VH; ++vh) acc[vh][2] = a2[vh][0], acc[vh][3] = a2[vh][1];
         }
-    }
-    if (NW > 1) {
-        __syncthreads();
-        if (wave == 0 && col == 0) {
+
+        // this lane's logits: view 4 vh + k of candidate 16 g + cand of the block
+        const int t0 = blk * kStatBlock + cand;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int v = 4 * j + q;
-                if (4 * j >= V || v >= V) continue;
-                double tot = 0.0;
+        for (int vh = 0; vh < VH; ++vh) {
+            const int v = 4 * vh + k;
+            double z[4], m = -__builtin_huge_val();
 #pragma unroll
-                for (int w = 0; w < NW; ++w) tot += s_ws[w][v];
-                pt[v * 2] = mv[j];
-                pt[v * 2 + 1] = tot;
+            for (int g = 0; g < 4; ++g) {
+                const bool ok = s_pg[4 * it + g] >= 0;
+                z[g] = ok ? acc[vh][g] * a.scale : 0.0;
+                if (t0 + 16 * g < C) m = max_f64(m, z[g]);
+            }
+            m = max_f64(m, dpp_ror_f64<8>(m));
+            m = max_f64(m, dpp_ror_f64<4>(m));
+            m = max_f64(m, dpp_ror_f64<2>(m));
+            m = max_f64(m, dpp_ror_f64<1>(m));
+            double sv = 0.0;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int t = t0 + 16 * g;
+                if (t < C) {
+                    const double ev = exp_nonpos(z[g] - m);
+                    sv += ev;
+                    if (v < V) lgv[(size_t)v * a.cmax + t] = (float)ev;
+                }
+            }
+            sv += dpp_ror_f64<8>(sv);
+            sv += dpp_ror_f64<4>(sv);
+            sv += dpp_ror_f64<2>(sv);
+            sv += dpp_ror_f64<1>(sv);
+            if (cand == 0 && v < V) {
+                double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch + blk) * V * 2;
+                pt[v * 2] = m;
+                pt[v * 2 + 1] = sv;
             }
         }
     }
@@ -576,7 +635,13 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
     // the KV head is the fastest grid index everywhere: workgroups are handed to
     // the XCDs round-robin, so head h's workgroups all run on one XCD and read
     // back what the previous kernel left in that XCD's L2
-    dim3 g0(a.Hkv, a.Rb), g1(a.Hkv, cdiv(a.cmax, kStatBlock), a.Rb), g2(a.Hkv, cdiv(a.cmax, kProbChunk), a.Rb), g3(a.Hkv, 2, a.Rb);
+    // logits: each one-wave workgroup takes lg_iters statistics blocks, enough
+    // that the grid is about 16384 workgroups (64 per CU) when the candidate
+    // sets are long, one block each when they are short
+    ScoreArgs b = a;
+    const int nblocks = a.Hkv * a.nch * a.Rb;
+    b.lg_iters = std::min(kLogitsMaxIters, std::max(1, cdiv(nblocks, 16384)));
+    dim3 g0(a.Hkv, a.Rb), g1(a.Hkv, cdiv(a.nch, b.lg_iters), a.Rb), g2(a.Hkv, cdiv(a.cmax, kProbChunk), a.Rb), g3(a.Hkv, 2, a.Rb);
     if (a.cmax == 0) {
         // no request can have candidates: the counts are written as zero
         top_p_kernel<<<g3, kTopPThreads, 0, s>>>(a);
@@ -586,7 +651,7 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
 #define GP_CASE(GG)                                                   \
     case GG:                                                          \
         prep_kernel<T, D, GG><<<g0, 256, 0, s>>>(a);                  \
-        logits_kernel<T, D, GG><<<g1, 64 * kLogitsWaves, 0, s>>>(a);                \
+        logits_kernel<T, D, GG><<<g1, 64, 0, s>>>(b);                 \
         weights_kernel<GG><<<g2, 256, 0, s>>>(a);                     \
         break;
         GP_CASE(1) GP_CASE(2) GP_CASE(4) GP_CASE(8)
