@@ -68,6 +68,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU sample")
+    ap.add_argument("--ceiling-mib", type=int, default=4096, help="buffer of the streaming-read ceiling")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "decode_traffic_qwen3_8b.json"))
     ap.add_argument("--eager", action="store_true", help="launch every call directly (no HIP graphs)")
     ap.add_argument("--serial", action="store_true",
@@ -298,6 +299,23 @@ def main():
     decode_cold_pct = [round(float(x), 4) for x in np.percentile(cold_t, [10, 50, 90])]
     del flush
 
+    # streaming-read ceiling: the plain read kernel of the library over a
+    # buffer far larger than the caches, K back-to-back launches
+    ceil_buf = torch.ones(args.ceiling_mib << 20, dtype=torch.uint8, device=dev)
+    ceil_out = torch.zeros(1, dtype=torch.int32, device=dev)
+    for _ in range(2):
+        gp.gp_stream_read(ceil_buf, ceil_out)
+    torch.cuda.synchronize()
+    c0 = torch.cuda.Event(enable_timing=True)
+    c1 = torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(args.steps):
+        gp.gp_stream_read(ceil_buf, ceil_out)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    ceiling_gbs = ceil_buf.numel() / (c0.elapsed_time(c1) / args.steps * 1e-3) / 1e9
+    del ceil_buf, ceil_out
+
     # the summary update folded into decode attention (one launch) against the
     # two calls, K back-to-back launches each
     def timed_loop(fn):
@@ -517,6 +535,13 @@ def main():
         "serving_loop": loop,
         "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
+        "stream_read_ceiling": {"GB/s": round(ceiling_gbs, 1), "hbm_frac": round(ceiling_gbs / HBM_PEAK_GBS, 4),
+                                "bytes": args.ceiling_mib << 20,
+                                "decode_over_ceiling": round(dec_gbs / ceiling_gbs, 4),
+                                "kernel": "gp_stream_read: one pass of non-temporal 16-byte loads, 8 in flight "
+                                          "per thread, 16 workgroups of 256 per CU (the best of a sweep of "
+                                          "4/8/16 loads in flight, 4/8/16 workgroups per CU, plain or "
+                                          "non-temporal loads)"},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -448,6 +448,14 @@ size_t gp_workspace_bytes(int32_t op, int32_t num_reqs, int32_t num_bnd, int32_t
                           int32_t num_kv_heads, int32_t head_dim, int32_t max_pages,
                           int32_t page_size, gp_dtype_t dtype, int32_t n_layers);
 
+/* Measurement reference, not a step of the method: reads bytes (a multiple of
+ * 16; device memory, 16-byte aligned) once with plain streaming loads and
+ * XORs every word into *out (device, 4 bytes, caller-owned; not cleared
+ * here).  Its bandwidth is the streaming-read ceiling the decode and scoring
+ * kernels are set against.  GP_ERR_INVALID for a null pointer or a size that
+ * is not a multiple of 16. */
+gp_status_t gp_stream_read(const void *src, size_t bytes, uint32_t *out, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *gp_status_string(gp_status_t status);
 

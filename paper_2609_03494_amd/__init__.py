@@ -13,6 +13,6 @@ from ._lib import (  # noqa: F401
     GP_ERR_SCRATCH, LIB_PATH, PAGE_SIZE,
     GP_LAYOUT_FILL, GP_LAYOUT_SHIFT, GrowPageError, KVLayer, PageState, Params, gp_append_step, gp_boundary_apply, gp_boundary_compact,
     gp_boundary_decide, gp_boundary_score, gp_boundary_select, gp_release_held,
-    gp_decode_attention, gp_decode_attention_noalloc, gp_decode_attention_shared, gp_decode_attention_stages, gp_decode_step, gp_update_summaries, gp_workspace_bytes, load, status_string,
+    gp_decode_attention, gp_decode_attention_noalloc, gp_decode_attention_shared, gp_decode_attention_stages, gp_decode_step, gp_stream_read, gp_update_summaries, gp_workspace_bytes, load, status_string,
     workspace,
 )

@@ -31,7 +31,7 @@ GP_ERR_SCRATCH = 5
 EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_attention_noalloc", "gp_decode_attention_shared",
            "gp_decode_attention_stages", "gp_decode_step", "gp_boundary_score",
            "gp_boundary_apply", "gp_boundary_select", "gp_boundary_decide", "gp_boundary_compact",
-           "gp_release_held", "gp_append_step", "gp_workspace_bytes", "gp_status_string")
+           "gp_release_held", "gp_append_step", "gp_workspace_bytes", "gp_status_string", "gp_stream_read")
 
 
 class GrowPageError(RuntimeError):
@@ -83,6 +83,8 @@ def load() -> ctypes.CDLL:
     lib.gp_status_string.argtypes = [ctypes.c_int]
     lib.gp_workspace_bytes.restype = sz
     lib.gp_workspace_bytes.argtypes = [i32] * 8 + [ctypes.c_int, i32]
+    lib.gp_stream_read.restype = ctypes.c_int
+    lib.gp_stream_read.argtypes = [vp, sz, vp, vp]
     lib.gp_update_summaries.restype = ctypes.c_int
     lib.gp_update_summaries.argtypes = [vp, ctypes.c_int, i32, i32, i32, vp, vp, vp, i32, f32, f32, vp]
     lib.gp_decode_attention.restype = ctypes.c_int
@@ -242,6 +244,13 @@ def gp_decode_attention(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale:
                                     q_post.shape[1], scale, _ptr(out), _ptr(ws), ws.numel(),
                                     _stream(stream))
     _check(st, "gp_decode_attention")
+
+
+def gp_stream_read(src: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+    """The streaming-read reference kernel over src's bytes (XOR into out[0],
+    an int32 device tensor)."""
+    st = load().gp_stream_read(_ptr(src), src.numel() * src.element_size(), _ptr(out), _stream(stream))
+    _check(st, "gp_stream_read")
 
 
 def gp_decode_attention_noalloc(kv: KVLayer, ps: PageState, q_post: torch.Tensor, scale: float,

@@ -21,7 +21,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libgrowpage.so")
 SOURCES = ["gp_api.hip", "gp_summaries.hip", "gp_decode.hip", "gp_score.hip", "gp_apply.hip",
-           "gp_append.hip"]
+           "gp_append.hip", "gp_calib.hip"]
 ARCH = os.environ.get("GP_OFFLOAD_ARCH", "gfx950")
 
 

@@ -86,6 +86,12 @@ const char *gp_status_string(gp_status_t s) {
     return "unknown status";
 }
 
+gp_status_t gp_stream_read(const void *src, size_t bytes, uint32_t *out, hipStream_t stream) {
+    if (!src || !out || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(src) % 16 != 0) return GP_ERR_INVALID;
+    if (bytes == 0) return GP_OK;
+    return from_hip(launch_stream_read(src, bytes, out, stream));
+}
+
 size_t gp_workspace_bytes(int32_t op, int32_t num_reqs, int32_t num_bnd, int32_t num_q_heads,
                           int32_t num_kv_heads, int32_t head_dim, int32_t max_pages,
                           int32_t page_size, gp_dtype_t dtype, int32_t n_layers) {

@@ -256,6 +256,7 @@ constexpr int kStageSelect = 1, kStageDecide = 2, kStageCompact = 4;
 hipError_t launch_apply(gp_dtype_t dt, int D, const ApplyArgs &a, const LayerPtrs *layers, int stages,
                         hipStream_t s);
 hipError_t launch_release(int32_t *seq_lens, int R, hipStream_t s);
+hipError_t launch_stream_read(const void *src, size_t bytes, uint32_t *out, hipStream_t s);
 
 // ---------------------------------------------------------- device helpers --
 

@@ -132,3 +132,23 @@ def test_host_validation_without_launch(lib):
     ps0 = _lib._PageState(fake, fake, fake, fake, fake, fake, 0, 10, 100)
     assert lib.gp_decode_attention(ctypes.byref(kv), ctypes.byref(ps0), fake, 32, 0.1, fake, fake, 0,
                                    None) == 0
+    # streaming-read reference: null pointers, sizes not a multiple of 16
+    assert lib.gp_stream_read(None, 16, fake, None) == 1
+    assert lib.gp_stream_read(fake, 24, fake, None) == 1
+    assert lib.gp_stream_read(fake, 0, fake, None) == 0
+
+
+@pytest.mark.gpu
+def test_stream_read_checksum(lib):
+    """The streaming-read reference reads every word: its XOR checksum equals
+    the host's, for a size with a ragged tail beyond the unrolled loop."""
+    import numpy as np
+    import torch
+    rng = np.random.default_rng(3)
+    for n_words in (4, 4 * 1000003, 4 * (1 << 22)):
+        host = rng.integers(0, 2**32, size=n_words, dtype=np.uint64).astype(np.uint32)
+        src = torch.from_numpy(host.view(np.int32)).cuda()
+        out = torch.zeros(1, dtype=torch.int32, device="cuda")
+        gp.gp_stream_read(src, out)
+        torch.cuda.synchronize()
+        assert int(out.cpu().numpy().view(np.uint32)[0]) == int(np.bitwise_xor.reduce(host))
