@@ -233,6 +233,7 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
 // -------------------------------------------------------------------- pre --
 template <int D, int E>
 __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
+    __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     __shared__ int s_n;
     const int x = blockIdx.y, i = blockIdx.z;
     const int h = blockIdx.x % a.Hkv, l = blockIdx.x / a.Hkv;
@@ -307,6 +308,7 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
 enum { F_BOUNDARY = 1, F_GROW = 2, F_SHRINK = 4 };
 
 __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
+    __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     __shared__ int s_P[kMaxBnd];
     __shared__ int s_flags[kMaxBnd];
     __shared__ int s_nsh[kMaxBnd];     // shared pages to replace (after the decision)
@@ -517,6 +519,7 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
 // (3) the rows themselves, then the stores.
 template <int D, int E>
 __global__ __launch_bounds__(256) void compact_kernel(ApplyArgs a, LayerTable lt) {
+    __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     constexpr int UPR = D * E / 16;                 // 16-byte units per row
     constexpr int ROWS = kCompactChunk;
     constexpr int UNITS = ROWS * UPR / 256;         // 16-byte units per thread

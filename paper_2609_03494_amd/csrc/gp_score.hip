@@ -115,6 +115,7 @@ __device__ inline bool boundary_of(const ScoreArgs &a, int i, int &r, int &P) {
 // cosine are computed in fp64 on the device.
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256, 5) void prep_kernel(ScoreArgs a) {
+    __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     constexpr int V = 2 * G;
     constexpr int H = D / 2;
     __shared__ double s_q[V][D];
@@ -201,6 +202,7 @@ constexpr int kLogitsMaxIters = 32;
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
+    __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     constexpr int V = 2 * G;
     constexpr int VH = (V + 3) / 4;                  // view quarters (MFMAs per key operand)
     constexpr int VR = 4 * VH;                       // view rows in LDS (rows >= V are zero)
@@ -340,6 +342,7 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
 // The G query heads of a view are averaged in fp64 and rounded to float32.
 template <int G>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G >= 8 ? 4 : 5))) void weights_kernel(ScoreArgs a) {
+    __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     constexpr int V = 2 * G;
     constexpr int BPC = kProbChunk / kStatBlock;     // statistics blocks per chunk
     constexpr int TPT = kProbChunk / 256;            // tokens per thread
@@ -441,6 +444,7 @@ __device__ inline unsigned long long fixed60(uint32_t bits) {
 // registers free.
 constexpr int kTopPThreads = 256;
 __global__ __launch_bounds__(kTopPThreads, 5) void top_p_kernel(ScoreArgs a) {
+    __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     constexpr int NT = kTopPThreads;
     constexpr int NB = 2048;
     constexpr int CW = 4096 / NT;                   // weights per thread kept in registers
