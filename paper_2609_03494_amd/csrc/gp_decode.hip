@@ -443,6 +443,8 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     // matched[r] for every request of a group)
     int base_page = 0, slot0 = 0;
     bool pmatch = false;
+    int spec_n = 0, spec_pid = -1;                    // PREFIX: page ids requested ahead
+    bool spec_hit = false;
     if constexpr (PREFIX) {
         int gsel = -1;
         for (int g = 0; g < a.ngroups; ++g)
@@ -450,15 +452,29 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
         if (gsel >= 0) {                                  // uniform
             // the prefix pass's test for this request, evaluated here as well
             const int pp = a.g_pages[gsel];
-            bool ok = prefix_reader(a, r, pp);
+            const bool reader = prefix_reader(a, r, pp);
             const int32_t *row = a.page_table + (size_t)r * a.max_pages;
             const int32_t *lrow = a.page_table + (size_t)a.g_first[gsel] * a.max_pages;
-            for (int j = tid; ok && j < pp; j += blockDim.x) ok = row[j] == lrow[j];
+            // while the table rows are compared, the page ids of this chunk's
+            // range as it is when the rows match (the usual case) are already
+            // requested: one memory round trip less before the pages
+            if (reader) {
+                const int mt_s = m_in - pp * kPage, nch_s = cdiv(mt_s, a.chunk_pages * kPage);
+                if (mt_s > 0 && chunk < nch_s) {
+                    const int npg_s = cdiv(mt_s, kPage), cs_s = cdiv(npg_s, nch_s);
+                    const int pb = pp + min(npg_s, chunk * cs_s), pe = pp + min(npg_s, chunk * cs_s + cs_s);
+                    spec_n = pe - pb;
+                    if (spec_n <= (int)blockDim.x && tid < spec_n) spec_pid = row[pb + tid];
+                }
+            }
+            bool ok = reader;
+            for (int j = tid; j < pp; j += blockDim.x) ok = ok && row[j] == lrow[j];
             pmatch = __syncthreads_and(ok);
             if (pmatch) {
                 base_page = pp;
                 slot0 = cdiv(pp, a.chunk_pages);
             }
+            spec_hit = pmatch && spec_n > 0 && spec_n <= (int)blockDim.x;
         }
     }
     if (m_in < 0) {                           // held: not in this step's batch
@@ -532,9 +548,14 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
 
     // page ids and Q (MFMA A layout, rows < G) into LDS
     const int32_t *table = a.page_table + (size_t)r * a.max_pages;
-    for (int k = tid; k < page_end - page_begin; k += blockDim.x) {
-        const int pid = table[page_begin + k];
-        s_ids[k] = pid >= 0 && pid < a.pool_pages ? pid : -1;
+    if (PREFIX && spec_hit) {
+        // (the same range: the prefix pages matched, as the request assumed)
+        if (tid < page_end - page_begin) s_ids[tid] = spec_pid >= 0 && spec_pid < a.pool_pages ? spec_pid : -1;
+    } else {
+        for (int k = tid; k < page_end - page_begin; k += blockDim.x) {
+            const int pid = table[page_begin + k];
+            s_ids[k] = pid >= 0 && pid < a.pool_pages ? pid : -1;
+        }
     }
     const uint16_t *qg = reinterpret_cast<const uint16_t *>(a.q) + ((size_t)r * Hq + (size_t)h * G) * D;
     if (tid < KK * 4 * G) {
