@@ -538,10 +538,11 @@ def main():
         "stream_read_ceiling": {"GB/s": round(ceiling_gbs, 1), "hbm_frac": round(ceiling_gbs / HBM_PEAK_GBS, 4),
                                 "bytes": args.ceiling_mib << 20,
                                 "decode_over_ceiling": round(dec_gbs / ceiling_gbs, 4),
-                                "kernel": "gp_stream_read: one pass of non-temporal 16-byte loads, 8 in flight "
-                                          "per thread, 16 workgroups of 256 per CU (the best of a sweep of "
-                                          "4/8/16 loads in flight, 4/8/16 workgroups per CU, plain or "
-                                          "non-temporal loads)"},
+                                "kernel": "gp_stream_read: one pass of non-temporal 16-byte loads, one "
+                                          "contiguous chunk per workgroup, 16 loads in flight per thread, 8 "
+                                          "workgroups of 256 per CU, per-workgroup partials folded by a "
+                                          "one-workgroup kernel (the best of a sweep of grid-stride or "
+                                          "contiguous chunks, 4/8/16 loads in flight, 4-64 workgroups per CU)"},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -452,8 +452,10 @@ size_t gp_workspace_bytes(int32_t op, int32_t num_reqs, int32_t num_bnd, int32_t
  * 16; device memory, 16-byte aligned) once with plain streaming loads and
  * XORs every word into *out (device, 4 bytes, caller-owned; not cleared
  * here).  Its bandwidth is the streaming-read ceiling the decode and scoring
- * kernels are set against.  GP_ERR_INVALID for a null pointer or a size that
- * is not a multiple of 16. */
+ * kernels are set against.  The per-workgroup partial words go through one
+ * device-wide array in the library, so calls that overlap on one device (on
+ * different streams) race; calls in one stream do not.  GP_ERR_INVALID for a
+ * null pointer or a size that is not a multiple of 16. */
 gp_status_t gp_stream_read(const void *src, size_t bytes, uint32_t *out, hipStream_t stream);
 
 /* Static description of a status code. */
