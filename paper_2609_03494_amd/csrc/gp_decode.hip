@@ -849,9 +849,10 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
 // ---------------------------------------------------------------------------
 // Shared-prefix pass (gp_decode_attention_shared; App. E.2 keeps a common
 // prefix in reference-counted blocks that many requests read).  Work item =
-// (KV head h, prefix chunk c, block of 4 * 16 / G requests of one group).  The
-// chunk's pages are read once per workgroup, staged in LDS (keys row-major,
-// values transposed), and each of the four waves serves 16 query rows (16 / G
+// (KV head h, prefix slot c, block of 4 * 16 / G requests of one group).  The
+// prefix is split evenly over its slots; a slot's pages are read once per
+// workgroup, staged in LDS (keys row-major, values transposed), and each of
+// the four waves serves 16 query rows (16 / G
 // requests x G heads): Q.K^T on v_mfma_f32_16x16x32_bf16 as in the split
 // kernel, online softmax per row over two pages at a time, and P.V on
 // v_mfma_f32_16x16x32_bf16 with P split into two bfloat16 terms (hi + lo carry
@@ -917,7 +918,10 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void prefix_kernel(DecodeArgs a)
     while (gi + 1 < a.ngroups && blk >= a.g_blk0[gi + 1]) ++gi;
     const int first = a.g_first[gi], nreq = a.g_num[gi], ppages = a.g_pages[gi];
     const int r0 = first + (blk - a.g_blk0[gi]) * RPB;
-    const int p_begin = c * a.chunk_pages, p_end = min(ppages, p_begin + a.chunk_pages);
+    // the prefix split evenly over its cdiv(ppages, chunk_pages) slots (cs <=
+    // chunk_pages; the last slot is never empty)
+    const int nps = cdiv(ppages, a.chunk_pages), cs = cdiv(ppages, nps);
+    const int p_begin = c * cs, p_end = min(ppages, p_begin + cs);
     const int Hkv = a.Hkv, Hq = Hkv * G;
     const int32_t *lead = a.page_table + (size_t)first * a.max_pages;
 

@@ -171,9 +171,12 @@ __global__ __launch_bounds__(256, 5) void prep_kernel(ScoreArgs a) {
 }
 
 // ------------------------------------------------------------------- logits --
-// Grid (KV head, split, boundary request), one wave per workgroup.  Workgroup
-// y of a request handles statistics blocks y, y + splits, y + 2 splits, ...
-// (at most kLogitsMaxIters) of kStatBlock = 64 candidates each.  The 2G x D
+// Grid (KV head, split / kLogitsWaves, boundary request); each wave of a
+// workgroup is one split, and the waves share the summaries in LDS (with one
+// wave per workgroup the LDS copy of the summaries, not registers, would cap
+// the waves per CU).  Split y of a request handles statistics blocks y,
+// y + splits, y + 2 splits, ... (at most kLogitsMaxIters) of kStatBlock = 64
+// candidates each.  The 2G x D
 // logits of a block are a small fp64 matrix product on the matrix cores,
 // v_mfma_f64_4x4x4f64: four independent 4 x 4 x 4 products per instruction
 // (16 cycles for 512 flops, the same rate per flop as 16x16x4, but with no
@@ -199,9 +202,13 @@ __global__ __launch_bounds__(256, 5) void prep_kernel(ScoreArgs a) {
 // stored (float32), so that the weights need a product, not an exponential,
 // per token.  A candidate whose page id is invalid contributes zero logits.
 constexpr int kLogitsMaxIters = 32;
+#ifndef GP_LOGITS_WAVES
+#define GP_LOGITS_WAVES 2
+#endif
+constexpr int kLogitsWaves = GP_LOGITS_WAVES;   // waves per workgroup, sharing the summaries in LDS
 
 template <typename T, int D, int G>
-__global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(64 * kLogitsWaves) void logits_kernel(ScoreArgs a) {
     __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     constexpr int V = 2 * G;
     constexpr int VH = (V + 3) / 4;                  // view quarters (MFMAs per key operand)
@@ -213,34 +220,39 @@ __global__ __launch_bounds__(64) void logits_kernel(ScoreArgs a) {
     constexpr int KS = VR * SP + (8 - (VR * SP) % 32 + 32) % 32;   // k stride, = 8 mod 32 doubles
     static_assert(kStatBlock == 64 && kPage == 16 && S % EPU == 0, "layout");
     __shared__ double s_a[4 * KS];
-    __shared__ int s_pg[4 * kLogitsMaxIters];
+    __shared__ int s_pgs[kLogitsWaves][4 * kLogitsMaxIters];
 
-    const int h = blockIdx.x, y = blockIdx.y, i = blockIdx.z, ny = gridDim.y;
-    const int lane = threadIdx.x;
+    // wave w of the workgroup takes block set y = blockIdx.y * waves + w
+    const int h = blockIdx.x, i = blockIdx.z;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int y = blockIdx.y * kLogitsWaves + wave, ny = gridDim.y * kLogitsWaves;
+    int *s_pg = s_pgs[wave];
     const int k = lane >> 4, cand = lane & 15;      // contraction / output row; candidate 4 b + j
     int r, P;
-    if (!boundary_of(a, i, r, P)) return;
-    const int C = (P - 1) * kPage;
-    const int nblk = cdiv(C, kStatBlock);
-    if (y >= nblk) return;
+    if (!boundary_of(a, i, r, P)) return;          // uniform over the workgroup
     const int slot = a.slot_ids[r];
     if (slot < 0 || slot >= a.M) return;
-    const int nit = min(cdiv(nblk - y, ny), min(a.lg_iters, kLogitsMaxIters));
+    const int C = (P - 1) * kPage;
+    const int nblk = cdiv(C, kStatBlock);
+    if (blockIdx.y * kLogitsWaves >= nblk) return;  // no wave of the workgroup has a block
+    const bool active = y < nblk;
+    const int nit = active ? min(cdiv(nblk - y, ny), min(a.lg_iters, kLogitsMaxIters)) : 0;
 
-    // the page ids of this workgroup's blocks (-1: no candidates there or an
-    // invalid id) and the aligned summaries
+    // the page ids of this wave's blocks (-1: no candidates there or an
+    // invalid id) and the aligned summaries (all waves)
     for (int e = lane; e < 4 * nit; e += 64) {
         const int pg = 4 * (y + ny * (e / 4)) + e % 4;
         const int pe = pg < P - 1 ? a.page_table[(size_t)r * a.max_pages + pg] : -1;
         s_pg[e] = pe >= 0 && pe < a.pool_pages ? pe : -1;
     }
     const double *qt = a.qt + ((size_t)i * a.Hkv + h) * V * D;
-    for (int e = lane; e < 4 * VR * S; e += 64) {
+    for (int e = threadIdx.x; e < 4 * VR * S; e += 64 * kLogitsWaves) {
         const int q = e / (VR * S), rem = e % (VR * S), v = rem / S, s2 = rem % S;
         const int d = 4 * EPU * (s2 / EPU) + EPU * q + s2 % EPU;
         s_a[q * KS + v * SP + s2] = v < V ? qt[(size_t)v * D + d] : 0.0;
     }
     __syncthreads();
+    if (!active) return;
 
     // keys of half `hf` of block `it`: lane (k, cand) reads units k, 4 + k,
     // ... of token cand of the block's pages 2 hf and 2 hf + 1.  The loads are
@@ -639,13 +651,13 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
     // the KV head is the fastest grid index everywhere: workgroups are handed to
     // the XCDs round-robin, so head h's workgroups all run on one XCD and read
     // back what the previous kernel left in that XCD's L2
-    // logits: each one-wave workgroup takes lg_iters statistics blocks, enough
-    // that the grid is about 16384 workgroups (64 per CU) when the candidate
-    // sets are long, one block each when they are short
+    // logits: each wave takes lg_iters statistics blocks, enough that there
+    // are about 16384 waves (64 per CU) when the candidate sets are long, one
+    // block each when they are short
     ScoreArgs b = a;
     const int nblocks = a.Hkv * a.nch * a.Rb;
     b.lg_iters = std::min(kLogitsMaxIters, std::max(1, cdiv(nblocks, 16384)));
-    dim3 g0(a.Hkv, a.Rb), g1(a.Hkv, cdiv(a.nch, b.lg_iters), a.Rb), g2(a.Hkv, cdiv(a.cmax, kProbChunk), a.Rb), g3(a.Hkv, 2, a.Rb);
+    dim3 g0(a.Hkv, a.Rb), g1(a.Hkv, cdiv(cdiv(a.nch, b.lg_iters), kLogitsWaves), a.Rb), g2(a.Hkv, cdiv(a.cmax, kProbChunk), a.Rb), g3(a.Hkv, 2, a.Rb);
     if (a.cmax == 0) {
         // no request can have candidates: the counts are written as zero
         top_p_kernel<<<g3, kTopPThreads, 0, s>>>(a);
@@ -655,7 +667,7 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
 #define GP_CASE(GG)                                                   \
     case GG:                                                          \
         prep_kernel<T, D, GG><<<g0, 256, 0, s>>>(a);                  \
-        logits_kernel<T, D, GG><<<g1, 64, 0, s>>>(b);                 \
+        logits_kernel<T, D, GG><<<g1, 64 * kLogitsWaves, 0, s>>>(b);  \
         weights_kernel<GG><<<g2, 256, 0, s>>>(a);                     \
         break;
         GP_CASE(1) GP_CASE(2) GP_CASE(4) GP_CASE(8)

@@ -448,18 +448,27 @@ def _shared_case(case):
     if case == "g4":
         return W.prefix_shared(num_reqs=24, prefix_len=320, tail_lo=20, tail_hi=900, free_pages=60,
                                num_q_heads=32)
+    if case == "g8_long_prefix":
+        # a 128-page prefix over three partial slots (43 + 43 + 42 pages)
+        return W.prefix_shared(num_reqs=10, prefix_len=2048, tail_lo=20, tail_hi=600, free_pages=60)
+    if case == "g8_two_page_prefix":
+        # fewer prefix pages than the prefix pass has waves
+        return W.prefix_shared(num_reqs=12, prefix_len=32, tail_lo=20, tail_hi=900, free_pages=60)
     return W.prefix_shared(num_reqs=20, prefix_len=320, tail_lo=20, tail_hi=1500, free_pages=60)
 
 
-@pytest.mark.parametrize("case", ["g8", "g4", "g8_mixed", "g8_two_groups"])
+@pytest.mark.parametrize("case", ["g8", "g4", "g8_mixed", "g8_two_groups", "g8_long_prefix",
+                                  "g8_two_page_prefix"])
 def test_decode_shared_prefix(case):
     """gp_decode_attention_shared (App. E.2 shared prefix blocks read once per
     block of requests) against the oracle.  "mixed": one member's prefix page
     replaced by a private copy (a compaction does that), one member holding
     fewer tokens than the prefix, one held member -- those must fall back to
     reading their own pages; "two_groups": the batch split into two groups,
-    the second with a shorter declared prefix."""
-    w = _shared_case("g4" if case == "g4" else "g8")
+    the second with a shorter declared prefix; "long_prefix": a prefix over
+    several partial slots; "two_page_prefix": fewer prefix pages than the
+    waves that share them."""
+    w = _shared_case(case if case in ("g4", "g8_long_prefix", "g8_two_page_prefix") else "g8")
     b, R = w.page_size, w.num_reqs
     pp = w.meta["prefix_len"] // b
     dc = DeviceCase(w)
