@@ -69,6 +69,15 @@ __device__ inline uint4 stream16(const void *p) {
     return make_uint4(x[0], x[1], x[2], x[3]);
 }
 
+// s_waitcnt immediates: vmcnt(0) (vmcnt in bits 3:0 and 15:14, the others at
+// their maximum), lgkmcnt(0); and the cache-policy operand of a direct-to-LDS
+// load that marks it non-temporal
+constexpr int kWaitVm0 = 0x0F70;
+constexpr int kWaitLgkm0 = 0xC07F;
+constexpr int kCpolNT = 2;
+typedef const __attribute__((address_space(1))) void global_cvoid_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
 // The request's view of one step: resident tokens m, pages P (clamped to the
 // table), whether the step's new token goes in (room: a token is given and the
 // last page has a free slot, Sec. 3.1 paged cache) and the tokens attended.
@@ -426,13 +435,18 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     constexpr int NW = kDecodeWaves;
     constexpr int NT = 64 * NW;
     constexpr int FE = STEP ? (G * D + NT - 1) / NT : 1;   // summary elements per thread
+    constexpr int UPP = kPage * D / 8;                // 16-byte units of one page of one head (keys or values)
+    constexpr int STAGE_BYTES = NW * 2 * UPP * 16, MERGE_BYTES = NW * G * D * 4;
     __shared__ float s_m[NW][G], s_l[NW][G];
-    __shared__ float s_o[NW][G][D];
     __shared__ float s_p[NW][kPage][G];
     __shared__ float s_alpha[NW][G];
     __shared__ bf16x8_t s_q[KK][4][G];
     __shared__ int s_ids[kMaxChunkPages];
     __shared__ __attribute__((aligned(16))) uint16_t s_new[STEP ? 2 : 1][STEP ? D : 8];   // new token K, V
+    // per wave one page of keys and one of values while the pages are read,
+    // then the waves' o for the merge
+    __shared__ __attribute__((aligned(16))) char s_big[STAGE_BYTES > MERGE_BYTES ? STAGE_BYTES : MERGE_BYTES];
+    auto s_o = reinterpret_cast<float (*)[G][D]>(s_big);
 
     const int h = blockIdx.x, chunk = blockIdx.y, r = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -544,7 +558,6 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
 
     const int n = lane & 15, kg = lane >> 4;          // score layout: token n, key slice kg
     const int v_off = lane * DPL;                     // P.V: lane owns dims [lane * DPL, +DPL)
-    const int k_off = n * D + kg * 8;
 
     // page ids and Q (MFMA A layout, rows < G) into LDS
     const int32_t *table = a.page_table + (size_t)r * a.max_pages;
@@ -607,28 +620,65 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     const size_t head_off = (size_t)h * kPage * D;
     const size_t page_elems = (size_t)Hkv * kPage * D;
     uint4 kb[KK];
-    uint32_t vwa[kPage], vwb[kPage];                 // values of this page and of the next
-    auto load_k = [&](int phys) {
-        const uint16_t *kp = kpool + (size_t)phys * page_elems + head_off + k_off;
+    // Keys and values go straight to the wave's two LDS pages (no registers
+    // in flight, so the request for the next page can go out as soon as this
+    // one has been read out), each load instruction one contiguous 64 x
+    // 16-byte run of the page (RPI whole rows).  Keys are swizzled: lane l of
+    // instruction q takes row R = q RPI + l / UPR, unit (l % UPR) ^ (R % UPR),
+    // so that unit u of row R sits at R UPR + (u ^ (R % UPR)) and the 16 rows
+    // a score-layout read touches fall on distinct banks; values keep the row
+    // layout (a P.V read is one whole row).  (Loading the keys in the score
+    // layout itself, sixteen rows of 64 bytes per instruction, reads paged
+    // keys about 7 % slower.)
+    constexpr int UPR = D / 8;                        // 16-byte units per row
+    constexpr int RPI = 64 / UPR;                     // rows per load instruction
+    constexpr int KLD = kPage / RPI;                  // load instructions per page (keys or values)
+    uint4 *kstage = reinterpret_cast<uint4 *>(s_big) + (size_t)wave * 2 * UPP;
+    uint4 *vstage = kstage + UPP;
+    auto load_kv = [&](int phys) {
+        const size_t off = (size_t)phys * page_elems + head_off;
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) kb[kk] = ld16(kp + kk * 32);
+        for (int q = 0; q < KLD; ++q) {
+            const int R = q * RPI + lane / UPR, u = (lane % UPR) ^ (R % UPR);
+            __builtin_amdgcn_global_load_lds((global_cvoid_t *)(kpool + off + R * D + u * 8),
+                                             (lds_void_t *)(kstage + q * 64), 16, 0, kCpolNT);
+        }
+#pragma unroll
+        for (int q = 0; q < KLD; ++q)
+            __builtin_amdgcn_global_load_lds((global_cvoid_t *)(vpool + off + (size_t)(q * 64 + lane) * 8),
+                                             (lds_void_t *)(vstage + q * 64), 16, 0, kCpolNT);
     };
-    auto load_v = [&](int phys, uint32_t (&vw)[kPage]) {
-        // one 2D-byte row per instruction: fully coalesced
-        const uint16_t *vp = vpool + (size_t)phys * page_elems + head_off + v_off;
+    // once the page has landed: the score-layout key operand of step kk (unit
+    // 4 kk + kg of row n) and this lane's dims of every value row; the stages
+    // are free again when the reads are done
+    auto read_kv = [&](uint32_t (&vw)[kPage]) {
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) kb[kk] = kstage[n * UPR + ((4 * kk + kg) ^ (n % UPR))];
 #pragma unroll
         for (int t = 0; t < kPage; ++t) {
             if constexpr (DPL == 2)
-                vw[t] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(vp + t * D));
+                vw[t] = reinterpret_cast<const uint32_t *>(vstage)[t * (D / 2) + lane];
             else
-                vw[t] = __builtin_nontemporal_load(vp + t * D);
+                vw[t] = reinterpret_cast<const uint16_t *>(vstage)[t * D + lane];
         }
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+        __builtin_amdgcn_sched_barrier(0);
     };
     // One page of the wave: Q.K^T on the matrix cores, then the keys and
     // values of the wave's next page are requested together (the values into
     // the other buffer), then softmax and P.V on this page's values.
-    auto page = [&](int p, int &phys, uint32_t (&vw)[kPage], uint32_t (&vn)[kPage]) {
+    auto page = [&](int p, int &phys) {
         const int ntok = phys >= 0 ? min(kPage, m - p * kPage) : 0;
+        uint32_t vw[kPage];                          // this lane's dims of the page's value rows
+        if (phys >= 0) {                             // wave-uniform
+            read_kv(vw);
+        } else {
+#pragma unroll
+            for (int t = 0; t < kPage; ++t) vw[t] = 0u;
+        }
         if constexpr (STEP) {
             if (p == p_new) {     // wave-uniform: the new token's slot comes from LDS
                 if (n == slot_new) {
@@ -652,10 +702,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
         }
         const int pn = p + NW;
         const int phys_next = pn < page_end ? s_ids[pn - page_begin] : -1;
-        if (phys_next >= 0) {
-            load_k(phys_next);
-            load_v(phys_next, vn);
-        }
+        if (phys_next >= 0) load_kv(phys_next);
         const bool valid = n < ntok;
         float sc[GI], alpha[GI];
 #pragma unroll
@@ -701,20 +748,14 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
     };
     int p = page_begin + wave;
     int phys = p < page_end ? s_ids[p - page_begin] : -1;
-    if (phys >= 0) {
-        load_k(phys);
-        load_v(phys, vwa);
-    }
-    // pages alternate between the two value buffers
-    for (; p < page_end; p += 2 * NW) {
-        page(p, phys, vwa, vwb);
-        if (p + NW >= page_end) break;
-        page(p + NW, phys, vwb, vwa);
-    }
+    if (phys >= 0) load_kv(phys);
+    for (; p < page_end; p += NW) page(p, phys);
 
-    // merge the waves: per-wave (max, sum) of each head, o of every dim
+    // merge the waves: per-wave (max, sum) of each head, o of every dim (o
+    // goes where the stages were, once every wave is done with them)
 #pragma unroll
     for (int i = 0; i < GI; ++i) lrun[i] = row_sum16(lrun[i]);
+    __syncthreads();
     if (kg < HR && n == 0) {
 #pragma unroll
         for (int i = 0; i < GI; ++i) {
