@@ -892,68 +892,52 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
 // prefix in reference-counted blocks that many requests read).  Work item =
 // (KV head h, prefix slot c, block of 4 * 16 / G requests of one group).  The
 // prefix is split evenly over its slots; a slot's pages are read once per
-// workgroup, staged in LDS (keys row-major, values transposed), and each of
-// the four waves serves 16 query rows (16 / G
-// requests x G heads): Q.K^T on v_mfma_f32_16x16x32_bf16 as in the split
-// kernel, online softmax per row over two pages at a time, and P.V on
-// v_mfma_f32_16x16x32_bf16 with P split into two bfloat16 terms (hi + lo carry
-// 16 significant bits, so P.V keeps float32-level accuracy while the values
-// stay exact bfloat16).  The
-// chunk's (o, max, sum) per row go to the partial slot c of each request; the
+// workgroup, kPrefixBatch at a time, straight into LDS by direct-to-LDS loads
+// (the next batch in flight while this one is computed), and each of the four
+// waves serves 16 query rows (16 / G requests x G heads) over all of them.
+// Per page a wave computes S^T = K.Q^T on v_mfma_f32_16x16x32_bf16 (the keys
+// as the A operand), so that every lane holds four tokens of one query row; an
+// online softmax per row; and O^T += V^T.P^T on v_mfma_f32_16x16x16bf16_1k,
+// with V^T read by ds_read_b64_tr_b16 and P, already in the B layout, split
+// into two bfloat16 terms (hi + lo carry 16 significant bits, so P.V keeps
+// float32-level accuracy while the values stay exact bfloat16).  Every lane
+// holds output dims of one row, so the rescale needs no lane exchange.  The
+// slot's (o, max, sum) per row go to partial slot c of each request; the
 // private tails follow in the next slots and the merge folds them together.
 // A request reads the pass only if it is not held, holds at least the
 // prefix's tokens and its table matches the group leader's on every prefix
-// page (matched[r], written by the (h 0, c 0) workgroups for the tail pass);
-// otherwise the tail pass covers all of its pages.
+// page; otherwise the tail pass covers all of its pages (both passes make the
+// same test).
 // Bound: HBM on the tails; the prefix pages are read once per block of
 // requests instead of once per request.
 typedef short bf16x4s_t __attribute__((ext_vector_type(4)));
 
-__device__ inline bf16x4s_t split_hi(const float (&p)[4], float (&lo)[4]) {
-    bf16x4s_t hi;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const uint16_t b = f32_to_bf16(p[e]);
-        hi[e] = (short)b;
-        lo[e] = p[e] - bf16_to_f32(b);
-    }
-    return hi;
-}
-__device__ inline bf16x4s_t to_bf16x4(const float (&x)[4]) {
-    bf16x4s_t r;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) r[e] = (short)f32_to_bf16(x[e]);
-    return r;
-}
-
-// The prefix pass runs in workgroups of kPrefixWaves waves; a round stages
-// kPrefixBatch pages (the next round's travel in registers while this one is
-// computed from LDS), and the waves take them two at a time (32 tokens: one
-// 16x16x32 MFMA per output tile and bf16 term of P.V).
+// The pass stages kPrefixBatch pages (keys and values) per round and keeps
+// two rounds in LDS.
 constexpr int kPrefixBatch = 4;
 
 template <int D, int G>
 __global__ __launch_bounds__(64 * kPrefixWaves) void prefix_kernel(DecodeArgs a) {
-    constexpr int KK = D / 32;            // Q.K^T MFMA steps per page
+    constexpr int KK = D / 32;            // S^T MFMA steps per page
     constexpr int NW = kPrefixWaves;
     constexpr int NT = 64 * NW;
     constexpr int RPW = 16 / G;           // requests per wave (16 query rows)
     constexpr int RPB = NW * RPW;         // requests per workgroup
-    constexpr int KS = D + 8;             // key row stride in LDS (elements; 16 bytes of padding)
-    constexpr int VS = 2 * kPage + 8;     // transposed value row stride: 32 tokens + padding
-    constexpr int DT = D / 16;            // P.V output tiles of 16 dims
-    constexpr int UPP = kPage * D / 8;    // 16-byte units of one page of one head (keys or values)
-    constexpr int NB = kPrefixBatch;      // pages per round (even)
-    constexpr int UPT = 2 * UPP * NB / NT;   // units a thread stages per round
-    static_assert(NB % 2 == 0 && (2 * UPP * NB) % NT == 0, "staging layout");
-    __shared__ __attribute__((aligned(16))) uint16_t s_k[NB][kPage][KS];
-    __shared__ __attribute__((aligned(16))) uint16_t s_vt[NB / 2][D][VS];
-    __shared__ float s_p[NW][16][2 * kPage + 1];
+    constexpr int DT = D / 16;            // O^T tiles of 16 dims
+    constexpr int UPR = D / 8;            // 16-byte units per row
+    constexpr int UPP = kPage * UPR;      // units of one page of one head (keys or values)
+    constexpr int NB = kPrefixBatch;      // pages per round
+    constexpr int RPI = 64 / UPR;         // rows per load instruction
+    constexpr int IPP = 2 * UPP / 64;     // load instructions per page (keys, then values)
+    constexpr int IPW = NB * IPP / NW;    // load instructions per wave and round
+    static_assert((NB * IPP) % NW == 0 && UPP % 64 == 0, "staging layout");
+    __shared__ __attribute__((aligned(16))) uint4 s_stage[2][NB][2][UPP];   // [round % 2][page][keys, values]
     __shared__ int s_ids[kMaxChunkPages];
     __shared__ int s_match[RPB];
 
     const int h = blockIdx.x, c = blockIdx.y, blk = blockIdx.z;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 15, kg = lane >> 4;
     int gi = 0;
     while (gi + 1 < a.ngroups && blk >= a.g_blk0[gi + 1]) ++gi;
@@ -987,17 +971,19 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void prefix_kernel(DecodeArgs a)
     for (int j = 0; j < RPB; ++j) any |= s_match[j];
     if (!any) return;                                    // uniform
 
-    // this wave's 16 query rows: row rho = request (wave * RPW + rho / G), head rho % G
+    // this wave's 16 query rows (row n = request wave * RPW + n / G, head
+    // n % G) as the B operand of S^T = K Q^T: lane (n, kg) holds dims
+    // 32 kk + 8 kg .. + 7
     const int jq = wave * RPW + n / G;
     const bool rowq = s_match[jq] != 0;
-    bf16x8_t qa[KK];
+    bf16x8_t qb[KK];
     {
         const uint16_t *qp = reinterpret_cast<const uint16_t *>(a.q) +
                              ((size_t)(rowq ? r0 + jq : first) * Hq + (size_t)h * G + n % G) * D;
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
             const bf16x8_t x = *reinterpret_cast<const bf16x8_t *>(qp + kk * 32 + kg * 8);
-            qa[kk] = rowq ? x : bf16x8_t{};
+            qb[kk] = rowq ? x : bf16x8_t{};
         }
     }
 
@@ -1006,138 +992,116 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void prefix_kernel(DecodeArgs a)
     const size_t head_off = (size_t)h * kPage * D;
     const size_t page_elems = (size_t)Hkv * kPage * D;
     const int npage = p_end - p_begin;
-    // staging: unit e of a round (e = tid + q * NT) is page e / (2 UPP), keys
-    // if (e % (2 UPP)) < UPP else values, token and dims from e % UPP
-    uint4 nxt[UPT];
-    auto fetch = [&](int k0) {
+    // Round rr's pages rr NB .. rr NB + NB - 1 go to stage rr % 2, each load
+    // instruction one contiguous run of RPI rows; the waves split the
+    // instructions.  Unit u of row R sits at R UPR + (u ^ fk(R)) for keys,
+    // fk(R) = R % UPR (a score-layout read of 16 rows hits 16 bank groups),
+    // and at R UPR + (u ^ fv(R)) for values, fv(R) = 2 (R % (UPR / 2)) (the
+    // transposed reads of 4 rows x 2 units hit distinct bank groups).  An
+    // invalid page id reads page 0 (its scores are masked).
+    auto issue = [&](int rr) {
 #pragma unroll
-        for (int q = 0; q < UPT; ++q) {
-            const int e = tid + q * NT, b = e / (2 * UPP), w2 = e % (2 * UPP), u = w2 % UPP;
-            const int k = k0 + b;
-            const int phys = k < npage ? s_ids[k] : -1;
-            const uint16_t *pool = w2 < UPP ? kpool : vpool;
-            const uint16_t *src = pool + (size_t)(phys >= 0 ? phys : 0) * page_elems + head_off +
-                                  (u / (D / 8)) * D + (u % (D / 8)) * 8;
-            const uint4 x = *reinterpret_cast<const uint4 *>(src);
-            nxt[q] = phys >= 0 ? x : make_uint4(0u, 0u, 0u, 0u);
-        }
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int q = 0; q < UPT; ++q) {
-            const int e = tid + q * NT, b = e / (2 * UPP), w2 = e % (2 * UPP), u = w2 % UPP;
-            const int tok = u / (D / 8), dim = (u % (D / 8)) * 8;
-            if (w2 < UPP) {
-                *reinterpret_cast<uint4 *>(&s_k[b][tok][dim]) = nxt[q];
-            } else {
-                const uint32_t w4[4] = {nxt[q].x, nxt[q].y, nxt[q].z, nxt[q].w};
-                const int col = (b & 1) * kPage + tok;      // token within the page pair
-#pragma unroll
-                for (int e2 = 0; e2 < 4; ++e2) {
-                    s_vt[b >> 1][dim + 2 * e2][col] = (uint16_t)(w4[e2] & 0xffffu);
-                    s_vt[b >> 1][dim + 2 * e2 + 1][col] = (uint16_t)(w4[e2] >> 16);
-                }
+        for (int i = 0; i < IPW; ++i) {
+            const int e = wave * IPW + i, j = e / IPP, w2 = e % IPP;
+            const int k = rr * NB + j;
+            if (k < npage) {                             // wave-uniform
+                const bool isv = w2 >= IPP / 2;
+                const int q = isv ? w2 - IPP / 2 : w2;
+                const int R = q * RPI + lane / UPR, s = lane % UPR;
+                const int u = s ^ (isv ? 2 * (R % (UPR / 2)) : R % UPR);
+                const uint16_t *src = (isv ? vpool : kpool) + (size_t)max(s_ids[k], 0) * page_elems + head_off +
+                                      (size_t)R * D + u * 8;
+                __builtin_amdgcn_global_load_lds((global_cvoid_t *)src,
+                                                 (lds_void_t *)(&s_stage[rr & 1][j][isv][q * 64]), 16, 0, kCpolNT);
             }
         }
     };
 
-    float mrun[4], lrun[4];
-    f32x4_t o[DT];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        mrun[i] = kNegInf;
-        lrun[i] = 0.0f;
-    }
+    float mrun = kNegInf, lrun = 0.0f;   // row n: running max (log2 units), this lane's share of the sum
+    f32x4_t o[DT];                       // O^T tile t: lane (n, kg) holds dims 16 t + 4 kg + e of row n
 #pragma unroll
     for (int t = 0; t < DT; ++t) o[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-
-    fetch(0);
-    stage();
-    __syncthreads();
-    for (int k0 = 0; k0 < npage; k0 += NB) {
-        if (k0 + NB < npage) fetch(k0 + NB);             // in flight while this round is computed
-        for (int b = 0; b < NB && k0 + b < npage; b += 2) {
-            // S = Q K^T for 16 rows x 32 tokens (two pages; the second may be
-            // past the chunk's end or invalid: its scores are masked)
-            const bool v0 = s_ids[k0 + b] >= 0;
-            const bool v1 = k0 + b + 1 < npage && s_ids[k0 + b + 1] >= 0;
-            bf16x8_t kb0[KK], kb1[KK];
+    auto page = [&](const uint4 *ks, const uint4 *vs, bool valid) {
+        bf16x8_t kc[KK];
 #pragma unroll
-            for (int kk = 0; kk < KK; ++kk) {
-                kb0[kk] = *reinterpret_cast<const bf16x8_t *>(&s_k[b][n][kk * 32 + kg * 8]);
-                kb1[kk] = *reinterpret_cast<const bf16x8_t *>(&s_k[b + 1][n][kk * 32 + kg * 8]);
-            }
-            f32x4_t acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int kk = 0; kk < KK; ++kk)
+            kc[kk] = __builtin_bit_cast(bf16x8_t, ks[n * UPR + ((4 * kk + kg) ^ (n % UPR))]);
+        f32x4_t st = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-            for (int kk = 0; kk < KK; ++kk) {
-                acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], kb0[kk], acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], kb1[kk], acc1, 0, 0, 0);
-            }
-            // online softmax of rows 4 kg + i over the 32 tokens
-            float p0[4], p1[4], alpha[4];
+        for (int kk = 0; kk < KK; ++kk) st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc[kk], qb[kk], st, 0, 0, 0);
+        // online softmax of row n; this lane has tokens 4 kg + e
+        float s[4], ml = kNegInf;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float s0 = v0 ? acc0[i] * a.qscale : kNegInf;
-                const float s1 = v1 ? acc1[i] * a.qscale : kNegInf;
-                const float mn = fmaxf(mrun[i], fmaxf(row_max16(s0), row_max16(s1)));
-                // arguments are <= 0: the hardware exp2 needs no range fix-up
-                alpha[i] = mn == kNegInf ? 1.0f : __builtin_amdgcn_exp2f(mrun[i] - mn);
-                mrun[i] = mn;
-                p0[i] = mn == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(s0 - mn);
-                p1[i] = mn == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(s1 - mn);
-                lrun[i] = lrun[i] * alpha[i] + p0[i] + p1[i];
-            }
-            wave_lds_sync();                               // the previous pair's reads of s_p are done
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                s_p[wave][kg * 4 + i][n] = p0[i];
-                s_p[wave][kg * 4 + i][kPage + n] = p1[i];
-            }
-            wave_lds_sync();
-            // P as the A operand: row n, tokens 8 kg .. 8 kg + 7, in two bf16 terms
-            bf16x8_t a_hi, a_lo;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float x = s_p[wave][n][kg * 8 + e];
-                a_hi[e] = (__bf16)x;                      // round to nearest even
-                a_lo[e] = (__bf16)(x - (float)a_hi[e]);   // x - hi is exact in float32
-            }
-            // skip the rescale while no row's maximum has moved (wave-uniform)
-            bool moved = false;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) moved = moved || alpha[i] != 1.0f;
-            if (__builtin_amdgcn_read_exec() && __any(moved)) {
-#pragma unroll
-                for (int t = 0; t < DT; ++t)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) o[t][i] *= alpha[i];
-            }
-#pragma unroll
-            for (int t = 0; t < DT; ++t) {
-                const bf16x8_t vb = *reinterpret_cast<const bf16x8_t *>(&s_vt[b >> 1][t * 16 + n][kg * 8]);
-                o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_hi, vb, o[t], 0, 0, 0);
-                o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_lo, vb, o[t], 0, 0, 0);
-            }
+        for (int e = 0; e < 4; ++e) {
+            s[e] = valid ? st[e] * a.qscale : kNegInf;
+            ml = fmaxf(ml, s[e]);
         }
-        __syncthreads();                                  // every wave is done with this round
-        if (k0 + NB < npage) {
-            stage();
-            __syncthreads();
+        ml = fmaxf(ml, __shfl_xor(ml, 16, 64));
+        ml = fmaxf(ml, __shfl_xor(ml, 32, 64));
+        const float mn = fmaxf(mrun, ml);
+        // arguments are <= 0: the hardware exp2 needs no range fix-up
+        const float alpha = mn == kNegInf ? 1.0f : __builtin_amdgcn_exp2f(mrun - mn);
+        float p[4], psum = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            p[e] = mn == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(s[e] - mn);
+            psum += p[e];
+        }
+        lrun = lrun * alpha + psum;
+        mrun = mn;
+        if (__any(alpha != 1.0f)) {                      // skip while no row's max has moved
+#pragma unroll
+            for (int t = 0; t < DT; ++t)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[t][e] *= alpha;
+        }
+        // P^T as the B operand (tokens 4 kg + e of row n) in two bf16 terms
+        bf16x4s_t phi, plo;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const __bf16 hb = (__bf16)p[e];              // round to nearest even
+            phi[e] = __builtin_bit_cast(short, hb);
+            plo[e] = __builtin_bit_cast(short, (__bf16)(p[e] - (float)hb));   // p - hi is exact in float32
+        }
+        // V^T tile t as the A operand by transposed reads: lane j of group kg
+        // names row R = 4 kg + j / 4, dims 16 t + 4 (j % 4) (unit 2 t + (j % 4)
+        // / 2, half (j % 4) % 2); lane n receives the values of tokens
+        // 4 kg .. 4 kg + 3 at dim 16 t + n
+        const int R = 4 * kg + n / 4, qd = n % 4;
+        const char *vrow = reinterpret_cast<const char *>(vs + R * UPR) + (qd & 1) * 8;
+        const int fv = 2 * (R % (UPR / 2));
+#pragma unroll
+        for (int t = 0; t < DT; ++t) {
+            const bf16x4s_t vt = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) bf16x4s_t *)(vrow + ((2 * t + qd / 2) ^ fv) * 16));
+            o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, phi, o[t], 0, 0, 0);
+            o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, plo, o[t], 0, 0, 0);
+        }
+    };
+
+    issue(0);
+    for (int rr = 0; rr * NB < npage; ++rr) {
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);            // this wave's part of round rr has landed
+        __syncthreads();                                 // all of it; every wave is done with round rr - 1
+        if ((rr + 1) * NB < npage) issue(rr + 1);        // into the stage round rr - 1 used
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            const int k = rr * NB + j;
+            if (k < npage) page(s_stage[rr & 1][j][0], s_stage[rr & 1][j][1], s_ids[k] >= 0);
         }
     }
 
-    // partials of rows 4 kg + i: o of dims 16 t + n, (max, sum) written by lane n = 0
+    // partials of row n: o of dims 16 t + 4 kg + e, (max, sum) by the kg 0 lanes
+    lrun += __shfl_xor(lrun, 16, 64);
+    lrun += __shfl_xor(lrun, 32, 64);
+    if (rowq) {
+        float *part = a.partial + (((size_t)(r0 + jq) * Hkv + h) * a.slots + c) * G * (D + 2) +
+                      (size_t)(n % G) * (D + 2);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const float l = row_sum16(lrun[i]);
-        const int rho = kg * 4 + i, j = wave * RPW + rho / G, g = rho % G;
-        if (!s_match[j]) continue;
-        float *part = a.partial + (((size_t)(r0 + j) * Hkv + h) * a.slots + c) * G * (D + 2) + (size_t)g * (D + 2);
-#pragma unroll
-        for (int t = 0; t < DT; ++t) part[t * 16 + n] = o[t][i];
-        if (n == 0) {
-            part[D] = mrun[i];
-            part[D + 1] = l;
+        for (int t = 0; t < DT; ++t) *reinterpret_cast<f32x4_t *>(part + 16 * t + 4 * kg) = o[t];
+        if (kg == 0) {
+            part[D] = mrun;
+            part[D + 1] = lrun;
         }
     }
 }
