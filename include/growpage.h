@@ -333,6 +333,28 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
                               const gp_params_t *params, int32_t *k_counts, float *scores,
                               int32_t max_cand, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* gp_boundary_score in two stream-ordered parts (stages, a bit mask), so that
+ * the selection, which needs only the scores, can run beside the working-set
+ * counts (the asynchronous overlap of App. E.3 applied inside one event):
+ *  - GP_SCORE_WEIGHTS: calibration and rotation of the summaries, the
+ *    per-view softmax weights in the workspace and scores[] (Sec. 3.2,
+ *    Sec. 3.3 token score);
+ *  - GP_SCORE_COUNTS:  k_counts[] from the weights in the workspace (Sec. 3.2
+ *    working-set ratio; top-p or entropy by params->metric).
+ * Same arguments and workspace in both calls; COUNTS after WEIGHTS on one
+ * stream, or after an event that orders it so; both stages in one call is
+ * gp_boundary_score.  The two write disjoint outputs, and COUNTS only reads
+ * the workspace and the page state.  GP_ERR_INVALID for an empty or unknown
+ * mask. */
+enum { GP_SCORE_WEIGHTS = 1, GP_SCORE_COUNTS = 2 };
+gp_status_t gp_boundary_score_stages(const gp_kv_layer_t *kv, const gp_page_state_t *ps,
+                                     const void *q_pre, const float *qstate, int32_t num_slots,
+                                     const int32_t *slot_ids, const int32_t *positions,
+                                     const int32_t *bnd, int32_t num_bnd, int32_t num_q_heads,
+                                     const gp_params_t *params, int32_t *k_counts, float *scores,
+                                     int32_t max_cand, void *ws, size_t ws_bytes, hipStream_t stream,
+                                     int32_t stages);
+
 /* Decision, allocation, selection and compaction for the boundary requests,
  * over n_layers layers (layers[l], k_counts[l][num_bnd][Hkv][2] and
  * scores[l][num_bnd][Hkv][max_cand] from gp_boundary_score).

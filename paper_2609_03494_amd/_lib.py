@@ -25,11 +25,12 @@ GP_POLICY_GROWPAGE, GP_POLICY_FIXED, GP_POLICY_RANDOM, GP_POLICY_INVERSE, GP_POL
 GP_METRIC_TOP_P, GP_METRIC_ENTROPY = 0, 1
 GP_DECODE_CHUNKS, GP_DECODE_MERGE, GP_DECODE_PREFIX = 1, 2, 4
 GP_LAYOUT_SHIFT, GP_LAYOUT_FILL = 0, 1
+GP_SCORE_WEIGHTS, GP_SCORE_COUNTS = 1, 2
 PAGE_SIZE = 16
 GP_ERR_SCRATCH = 5
 
 EXPORTS = ("gp_update_summaries", "gp_decode_attention", "gp_decode_attention_noalloc", "gp_decode_attention_shared",
-           "gp_decode_attention_stages", "gp_decode_step", "gp_boundary_score",
+           "gp_decode_attention_stages", "gp_decode_step", "gp_boundary_score", "gp_boundary_score_stages",
            "gp_boundary_apply", "gp_boundary_select", "gp_boundary_decide", "gp_boundary_compact",
            "gp_release_held", "gp_append_step", "gp_workspace_bytes", "gp_status_string", "gp_stream_read")
 
@@ -106,6 +107,8 @@ def load() -> ctypes.CDLL:
     lib.gp_boundary_score.argtypes = [ctypes.POINTER(_KVLayer), ctypes.POINTER(_PageState), vp, vp, i32,
                                       vp, vp, vp, i32, i32, ctypes.POINTER(_Params), vp, vp, i32, vp,
                                       sz, vp]
+    lib.gp_boundary_score_stages.restype = ctypes.c_int
+    lib.gp_boundary_score_stages.argtypes = lib.gp_boundary_score.argtypes + [i32]
     lib.gp_boundary_apply.restype = ctypes.c_int
     apply_args = [ctypes.POINTER(_KVLayer), i32, ctypes.POINTER(_PageState), vp, i32,
                   vp, vp, i32, ctypes.POINTER(_Params), vp, vp, vp, vp, sz, vp]
@@ -306,14 +309,17 @@ def gp_decode_step(kv: KVLayer, ps: PageState, q_post: torch.Tensor, q_pre: torc
 def gp_boundary_score(kv: KVLayer, ps: PageState, q_pre: torch.Tensor, qstate: torch.Tensor,
                       slot_ids: torch.Tensor, positions: torch.Tensor, bnd: torch.Tensor,
                       params: Params, k_counts: torch.Tensor, scores: torch.Tensor,
-                      ws: torch.Tensor, stream=None) -> None:
+                      ws: torch.Tensor, stream=None, stages=None) -> None:
+    """stages None: gp_boundary_score; else gp_boundary_score_stages with that
+    mask (GP_SCORE_WEIGHTS, GP_SCORE_COUNTS)."""
     c_kv, c_ps, c_p = kv.c(), ps.c(), params.c()
-    st = load().gp_boundary_score(ctypes.byref(c_kv), ctypes.byref(c_ps), _ptr(q_pre), _ptr(qstate),
-                                  qstate.shape[0], _ptr(slot_ids), _ptr(positions), _ptr(bnd),
-                                  bnd.shape[0], q_pre.shape[1], ctypes.byref(c_p), _ptr(k_counts),
-                                  _ptr(scores), scores.shape[-1], _ptr(ws), ws.numel(),
-                                  _stream(stream))
-    _check(st, "gp_boundary_score")
+    args = (ctypes.byref(c_kv), ctypes.byref(c_ps), _ptr(q_pre), _ptr(qstate), qstate.shape[0], _ptr(slot_ids),
+            _ptr(positions), _ptr(bnd), bnd.shape[0], q_pre.shape[1], ctypes.byref(c_p), _ptr(k_counts),
+            _ptr(scores), scores.shape[-1], _ptr(ws), ws.numel(), _stream(stream))
+    if stages is None:
+        _check(load().gp_boundary_score(*args), "gp_boundary_score")
+    else:
+        _check(load().gp_boundary_score_stages(*args, stages), "gp_boundary_score_stages")
 
 
 def _apply_like(name, layers, ps, bnd, k_counts, scores, params, decisions, delta, counters, ws, stream,

@@ -281,12 +281,13 @@ gp_status_t gp_decode_step(const gp_kv_layer_t *kv, const gp_page_state_t *ps, c
                        GP_DECODE_CHUNKS | GP_DECODE_MERGE, stream);
 }
 
-gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_pre,
-                              const float *qstate, int32_t num_slots, const int32_t *slot_ids,
-                              const int32_t *positions, const int32_t *bnd, int32_t num_bnd,
-                              int32_t num_q_heads, const gp_params_t *params, int32_t *k_counts,
-                              float *scores, int32_t max_cand, void *ws, size_t ws_bytes,
-                              hipStream_t stream) {
+gp_status_t gp_boundary_score_stages(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_pre,
+                                     const float *qstate, int32_t num_slots, const int32_t *slot_ids,
+                                     const int32_t *positions, const int32_t *bnd, int32_t num_bnd,
+                                     int32_t num_q_heads, const gp_params_t *params, int32_t *k_counts,
+                                     float *scores, int32_t max_cand, void *ws, size_t ws_bytes,
+                                     hipStream_t stream, int32_t stages) {
+    if (stages <= 0 || (stages & ~(GP_SCORE_WEIGHTS | GP_SCORE_COUNTS)) != 0) return GP_ERR_INVALID;
     gp_status_t st = check_layer(kv);
     if (st != GP_OK) return st;
     if ((st = check_state(ps, kv)) != GP_OK) return st;
@@ -334,7 +335,18 @@ gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps
     a.theta = params->rope_theta;
     a.p = params->p;
     a.metric = params->metric;
-    return from_hip(launch_score(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stream));
+    return from_hip(launch_score(kv->dtype, kv->head_dim, num_q_heads / kv->num_kv_heads, a, stages, stream));
+}
+
+gp_status_t gp_boundary_score(const gp_kv_layer_t *kv, const gp_page_state_t *ps, const void *q_pre,
+                              const float *qstate, int32_t num_slots, const int32_t *slot_ids,
+                              const int32_t *positions, const int32_t *bnd, int32_t num_bnd,
+                              int32_t num_q_heads, const gp_params_t *params, int32_t *k_counts,
+                              float *scores, int32_t max_cand, void *ws, size_t ws_bytes,
+                              hipStream_t stream) {
+    return gp_boundary_score_stages(kv, ps, q_pre, qstate, num_slots, slot_ids, positions, bnd, num_bnd,
+                                    num_q_heads, params, k_counts, scores, max_cand, ws, ws_bytes, stream,
+                                    GP_SCORE_WEIGHTS | GP_SCORE_COUNTS);
 }
 
 namespace {

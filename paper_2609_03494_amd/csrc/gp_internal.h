@@ -249,7 +249,7 @@ struct LayerPtrs {
 hipError_t launch_summaries(gp_dtype_t dt, const SummaryArgs &a, hipStream_t s);
 hipError_t launch_append(gp_dtype_t dt, int D, const AppendArgs &a, hipStream_t s);
 hipError_t launch_decode(gp_dtype_t dt, int D, int G, const DecodeArgs &a, int stages, hipStream_t s);
-hipError_t launch_score(gp_dtype_t dt, int D, int G, const ScoreArgs &a, hipStream_t s);
+hipError_t launch_score(gp_dtype_t dt, int D, int G, const ScoreArgs &a, int stages, hipStream_t s);
 // Stages of the boundary apply (selection, decision, compaction).
 constexpr int kStageSelect = 1, kStageDecide = 2, kStageCompact = 4;
 

@@ -647,7 +647,7 @@ __global__ __launch_bounds__(256) void entropy_kernel(ScoreArgs a) {
 }
 
 template <typename T, int D>
-hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
+hipError_t launch_gd(int G, const ScoreArgs &a, int stages, hipStream_t s) {
     // the KV head is the fastest grid index everywhere: workgroups are handed to
     // the XCDs round-robin, so head h's workgroups all run on one XCD and read
     // back what the previous kernel left in that XCD's L2
@@ -658,11 +658,13 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
     const int nblocks = a.Hkv * a.nch * a.Rb;
     b.lg_iters = std::min(kLogitsMaxIters, std::max(1, cdiv(nblocks, 16384)));
     dim3 g0(a.Hkv, a.Rb), g1(a.Hkv, cdiv(cdiv(a.nch, b.lg_iters), kLogitsWaves), a.Rb), g2(a.Hkv, cdiv(a.cmax, kProbChunk), a.Rb), g3(a.Hkv, 2, a.Rb);
+    const bool weights = stages & GP_SCORE_WEIGHTS, counts = stages & GP_SCORE_COUNTS;
     if (a.cmax == 0) {
         // no request can have candidates: the counts are written as zero
-        top_p_kernel<<<g3, kTopPThreads, 0, s>>>(a);
+        if (counts) top_p_kernel<<<g3, kTopPThreads, 0, s>>>(a);
         return hipGetLastError();
     }
+    if (weights) {
     switch (G) {
 #define GP_CASE(GG)                                                   \
     case GG:                                                          \
@@ -674,19 +676,23 @@ hipError_t launch_gd(int G, const ScoreArgs &a, hipStream_t s) {
 #undef GP_CASE
         default: return hipErrorInvalidValue;
     }
-    if (a.metric == GP_METRIC_ENTROPY)
-        entropy_kernel<<<g3, 256, 0, s>>>(a);
-    else
-        top_p_kernel<<<g3, kTopPThreads, 0, s>>>(a);
+    }
+    if (counts) {
+        if (a.metric == GP_METRIC_ENTROPY)
+            entropy_kernel<<<g3, 256, 0, s>>>(a);
+        else
+            top_p_kernel<<<g3, kTopPThreads, 0, s>>>(a);
+    }
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_score(gp_dtype_t dt, int D, int G, const ScoreArgs &a, hipStream_t s) {
+hipError_t launch_score(gp_dtype_t dt, int D, int G, const ScoreArgs &a, int stages, hipStream_t s) {
     if (a.Rb == 0) return hipSuccess;
-    if (dt == GP_BF16) return D == 128 ? launch_gd<uint16_t, 128>(G, a, s) : launch_gd<uint16_t, 64>(G, a, s);
-    return D == 128 ? launch_gd<float, 128>(G, a, s) : launch_gd<float, 64>(G, a, s);
+    if (dt == GP_BF16)
+        return D == 128 ? launch_gd<uint16_t, 128>(G, a, stages, s) : launch_gd<uint16_t, 64>(G, a, stages, s);
+    return D == 128 ? launch_gd<float, 128>(G, a, stages, s) : launch_gd<float, 64>(G, a, stages, s);
 }
 
 }  // namespace gp

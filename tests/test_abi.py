@@ -81,6 +81,12 @@ def test_host_validation_without_launch(lib):
     p = _lib._Params(0.9, 0.999, 0.99, 0.0, 0.088, 1e6, 4, 0)
     assert lib.gp_boundary_score(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 512, fake, fake, fake,
                                  2, 32, ctypes.byref(p), fake, fake, 16, fake, 1 << 30, None) == 1
+    # staged score: the mask must be GP_SCORE_WEIGHTS, GP_SCORE_COUNTS or both
+    pv = _lib._Params(0.9, 0.999, 0.99, 0.0, 0.088, 1e6, 4, 0)
+    for bad_stages in (0, 4, -1):
+        assert lib.gp_boundary_score_stages(ctypes.byref(kv), ctypes.byref(ps), fake, fake, 512, fake, fake, fake,
+                                            2, 32, ctypes.byref(pv), fake, fake, 144, fake, 1 << 30, None,
+                                            bad_stages) == 1
     # apply: too many layers
     arr = (_lib._KVLayer * 1)(kv)
     assert lib.gp_boundary_apply(arr, 65, ctypes.byref(ps), fake, 2, fake, fake, 144, ctypes.byref(p),

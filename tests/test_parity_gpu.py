@@ -20,7 +20,8 @@ import oracle as O
 import paper_2609_03494_amd as gp
 import workloads as W
 from _harness import (DEV, AbsPool, DeviceCase, PoolView, assert_rows_close, bf16_rounding_ok,
-                      fp32_elementwise_ok, oracle_state, row_index, threshold_band, to_numpy)
+                      fp32_elementwise_ok, library_params, oracle_state, row_index, threshold_band, to_numpy,
+                      torch_dtype)
 
 pytestmark = pytest.mark.gpu
 
@@ -538,6 +539,49 @@ def test_decode_shared_prefix_stages_on_two_streams():
                                   stages=gp.GP_DECODE_MERGE)
     torch.cuda.synchronize()
     assert to_numpy(split).tobytes() == to_numpy(whole).tobytes()
+
+
+@pytest.mark.parametrize("metric", ["top_p", "entropy"])
+def test_boundary_score_stages_match_the_whole_call(metric):
+    """gp_boundary_score_stages: the weights stage, then the counts stage on a
+    second stream beside the selection (which reads the scores only), give the
+    bytes of one gp_boundary_score call -- counts, scores and the selection's
+    eviction lists alike."""
+    _say(f"boundary: scoring in two stages, metric {metric}")
+    w = W.qwen3_8b(seed=11, num_reqs=10, len_lo=300, len_hi=3000, budget_choices=(8, 60, 200),
+                   boundary_frac=0.5, free_pages=30)
+    dc = DeviceCase(w)
+    bnd = torch.from_numpy(w.boundary.astype(np.int32)).to(DEV)
+    Rb, Hkv = int(bnd.shape[0]), w.num_kv_heads
+    gparams = library_params(O.Params(metric=metric), w.head_dim, None)
+    max_cand = (w.max_pages - 1) * w.page_size
+    dt = torch_dtype(w)
+    ws_s = gp.workspace(gp.GP_OP_SCORE, w.num_reqs, Rb, w.num_q_heads, Hkv, w.head_dim, w.max_pages, dt)
+    outs = []
+    for staged in (False, True):
+        counts = torch.full((Rb, Hkv, 2), -7, dtype=torch.int32, device=DEV)
+        scores = torch.full((Rb, Hkv, max_cand), -1.0, device=DEV)
+        ws_a = gp.workspace(gp.GP_OP_APPLY, w.num_reqs, Rb, w.num_q_heads, Hkv, w.head_dim, w.max_pages, dt)
+        args = (dc.layers[0], dc.ps, dc.q_pre_layers[0], dc.qstate_layers[0], dc.slot_ids, dc.positions, bnd,
+                gparams, counts, scores, ws_s)
+        sel = ([dc.layers[0]], dc.ps, bnd, counts, scores, gparams, torch.zeros(Rb, dtype=torch.int32, device=DEV),
+               torch.zeros(Rb, device=DEV), torch.zeros(4, dtype=torch.int64, device=DEV), ws_a)
+        if staged:
+            gp.gp_boundary_score(*args, stages=gp.GP_SCORE_WEIGHTS)
+            cur, side = torch.cuda.current_stream(), torch.cuda.Stream()
+            side.wait_stream(cur)
+            with torch.cuda.stream(side):
+                gp.gp_boundary_score(*args, stages=gp.GP_SCORE_COUNTS)
+            gp.gp_boundary_select(*sel)
+            cur.wait_stream(side)
+        else:
+            gp.gp_boundary_score(*args)
+            gp.gp_boundary_select(*sel)
+        torch.cuda.synchronize()
+        outs.append((to_numpy(counts).tobytes(), to_numpy(scores).tobytes(), to_numpy(ws_a).tobytes()))
+    assert outs[0][0] == outs[1][0], "counts"
+    assert outs[0][1] == outs[1][1], "scores"
+    assert outs[0][2] == outs[1][2], "selection workspace"
 
 
 def test_boundary_tiny_all_branches():
