@@ -455,11 +455,19 @@ def _shared_case(case):
     if case == "g8_two_page_prefix":
         # fewer prefix pages than the prefix pass has waves
         return W.prefix_shared(num_reqs=12, prefix_len=32, tail_lo=20, tail_hi=900, free_pages=60)
+    if case in ("d64_g2", "d64_g1"):
+        # head_dim 64 (eight 16-byte units per row: the staging swizzles by row
+        # mod 8 and mod 4) with 8 or 16 requests per row group
+        rng = np.random.default_rng(61)
+        n = 480 + rng.integers(20, 700, size=18)
+        Hq = 4 if case == "d64_g2" else 2
+        return W._build(name="prefix_d64", seed=62, dtype="bf16", Hq=Hq, Hkv=2, d=64, n=n, budgets=None,
+                        free_pages=40, heavy_mode="scaled", heavy_frac=0.02, summary_mode="random", prefix_len=480)
     return W.prefix_shared(num_reqs=20, prefix_len=320, tail_lo=20, tail_hi=1500, free_pages=60)
 
 
 @pytest.mark.parametrize("case", ["g8", "g4", "g8_mixed", "g8_two_groups", "g8_long_prefix",
-                                  "g8_two_page_prefix"])
+                                  "g8_two_page_prefix", "d64_g2", "d64_g1"])
 def test_decode_shared_prefix(case):
     """gp_decode_attention_shared (App. E.2 shared prefix blocks read once per
     block of requests) against the oracle.  "mixed": one member's prefix page
@@ -469,7 +477,7 @@ def test_decode_shared_prefix(case):
     the second with a shorter declared prefix; "long_prefix": a prefix over
     several partial slots; "two_page_prefix": fewer prefix pages than the
     waves that share them."""
-    w = _shared_case(case if case in ("g4", "g8_long_prefix", "g8_two_page_prefix") else "g8")
+    w = _shared_case(case if case in ("g4", "g8_long_prefix", "g8_two_page_prefix", "d64_g2", "d64_g1") else "g8")
     b, R = w.page_size, w.num_reqs
     pp = w.meta["prefix_len"] // b
     dc = DeviceCase(w)
