@@ -426,8 +426,10 @@ __device__ inline float row_sum16(float x) {
 // that reads its group's shared prefix pass covers the pages after the prefix
 // only, and its partials follow the prefix's).
 template <int D, int G, int MODE>
-__global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_eu(4))) void decode_split_kernel(
+    DecodeArgs a) {
     constexpr bool STEP = MODE == 1, PREFIX = MODE == 2;
+    constexpr bool PVM = G >= kDecodePvmMinG;   // P.V on the matrix cores (see the page step)
     constexpr int KK = D / 32;            // MFMA steps per page
     constexpr int DPL = D / 64;           // head dims per lane in P.V (2 or 1)
     constexpr int HR = (G + 3) / 4;       // lane rows that carry real heads
@@ -644,9 +646,13 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
                                              (lds_void_t *)(kstage + q * 64), 16, 0, kCpolNT);
         }
 #pragma unroll
-        for (int q = 0; q < KLD; ++q)
-            __builtin_amdgcn_global_load_lds((global_cvoid_t *)(vpool + off + (size_t)(q * 64 + lane) * 8),
+        for (int q = 0; q < KLD; ++q) {
+            // PVM: values swizzled by fv(R) = 2 (R % (UPR / 2)) for the
+            // transposed reads; otherwise the plain row layout
+            const int R = q * RPI + lane / UPR, u = PVM ? (lane % UPR) ^ (2 * (R % (UPR / 2))) : lane % UPR;
+            __builtin_amdgcn_global_load_lds((global_cvoid_t *)(vpool + off + R * D + u * 8),
                                              (lds_void_t *)(vstage + q * 64), 16, 0, kCpolNT);
+        }
     };
     // once the page has landed: the score-layout key operand of step kk (unit
     // 4 kk + kg of row n) and this lane's dims of every value row; the stages
@@ -746,27 +752,173 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void decode_split_kernel(DecodeA
         wave_lds_sync();
         phys = phys_next;
     };
+    // PVM (G >= kDecodePvmMinG): S^T = K.Q^T, so that lane (n, kg) holds
+    // tokens 4 kg + e of head n -- the B layout of the P.V product -- and
+    // O^T += V^T.P^T on v_mfma_f32_16x16x16bf16_1k, V^T by transposed LDS
+    // reads, P in two bfloat16 terms (hi + lo carry 16 significant bits): the
+    // per-page P.V costs the matrix cores what it costs at any G, where the
+    // vector-ALU form grows with G.  Heads n >= G of the 16 columns carry zero
+    // queries and are never written.
+    constexpr int DT = D / 16;                        // O^T tiles of 16 dims
+    f32x4_t ot[PVM ? DT : 1];
+    float pm_run = kNegInf, pl_run = 0.0f;            // head n: running max, this lane's share of the sum
+#pragma unroll
+    for (int t = 0; t < (PVM ? DT : 1); ++t) ot[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    typedef short bf16x4v_t __attribute__((ext_vector_type(4)));
+    // keys and values of a page go out as two requests here, so that the
+    // keys' stage is refilled as soon as its operands are read and the
+    // values' once P.V has read them
+    auto load_k_only = [&](int phys) {
+        const size_t off = (size_t)phys * page_elems + head_off;
+#pragma unroll
+        for (int q = 0; q < KLD; ++q) {
+            const int R = q * RPI + lane / UPR, u = (lane % UPR) ^ (R % UPR);
+            __builtin_amdgcn_global_load_lds((global_cvoid_t *)(kpool + off + R * D + u * 8),
+                                             (lds_void_t *)(kstage + q * 64), 16, 0, kCpolNT);
+        }
+    };
+    auto load_v_only = [&](int phys) {
+        const size_t off = (size_t)phys * page_elems + head_off;
+#pragma unroll
+        for (int q = 0; q < KLD; ++q) {
+            const int R = q * RPI + lane / UPR, u = (lane % UPR) ^ (2 * (R % (UPR / 2)));
+            __builtin_amdgcn_global_load_lds((global_cvoid_t *)(vpool + off + R * D + u * 8),
+                                             (lds_void_t *)(vstage + q * 64), 16, 0, kCpolNT);
+        }
+    };
+    auto page_pvm = [&](int p, int &phys) {
+        const int ntok = phys >= 0 ? min(kPage, m - p * kPage) : 0;
+        const int pn = p + NW;
+        const int phys_next = pn < page_end ? s_ids[pn - page_begin] : -1;
+        if (phys >= 0) {                              // wave-uniform
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) kb[kk] = kstage[n * UPR + ((4 * kk + kg) ^ (n % UPR))];
+            __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (phys_next >= 0) load_k_only(phys_next);
+        if constexpr (STEP) {
+            if (p == p_new && n == slot_new) {        // the new token's key comes from LDS
+#pragma unroll
+                for (int kk = 0; kk < KK; ++kk) kb[kk] = *reinterpret_cast<const uint4 *>(&s_new[0][kk * 32 + kg * 8]);
+            }
+        }
+        f32x4_t st = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (ntok > 0) {
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                bf16x8_t qb = {};
+                if (n < G) qb = s_q[kk][kg][n];
+                st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kb[kk]), qb, st, 0, 0, 0);
+            }
+        }
+        // online softmax of head n over tokens 4 kg + e
+        float sc[4], ml = kNegInf;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            sc[e] = 4 * kg + e < ntok ? st[e] * a.qscale : kNegInf;
+            ml = fmaxf(ml, sc[e]);
+        }
+        ml = fmaxf(ml, __shfl_xor(ml, 16, 64));
+        ml = fmaxf(ml, __shfl_xor(ml, 32, 64));
+        const float mn = fmaxf(pm_run, ml);
+        const float alpha = mn == kNegInf ? 1.0f : exp2f(pm_run - mn);
+        float psum = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            sc[e] = mn == kNegInf ? 0.0f : exp2f(sc[e] - mn);
+            psum += sc[e];
+        }
+        pl_run = pl_run * alpha + psum;
+        pm_run = mn;
+        if (__any(alpha != 1.0f)) {                   // skip while no head's max has moved
+#pragma unroll
+            for (int t = 0; t < DT; ++t)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) ot[t][e] *= alpha;
+        }
+        bf16x4v_t phi, plo;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const __bf16 hb = (__bf16)sc[e];              // round to nearest even
+            phi[e] = __builtin_bit_cast(short, hb);
+            plo[e] = __builtin_bit_cast(short, (__bf16)(sc[e] - (float)hb));   // p - hi is exact in float32
+        }
+        if (ntok > 0) {
+            // V^T tile t as the A operand by transposed reads: lane j of group
+            // kg names row R = 4 kg + j / 4, dims 16 t + 4 (j % 4); lane n
+            // receives tokens 4 kg .. + 3 at dim 16 t + n.  Slots past the last
+            // token may hold anything (0 x inf would reach o), so they read as
+            // zero; the step's new token comes from LDS.
+            const int R = 4 * kg + n / 4, qd = n % 4, fv = 2 * (R % (UPR / 2));
+            const char *vrow = reinterpret_cast<const char *>(vstage + R * UPR) + (qd & 1) * 8;
+#pragma unroll
+            for (int t = 0; t < DT; ++t) {
+                bf16x4v_t vt = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) bf16x4v_t *)(vrow + ((2 * t + qd / 2) ^ fv) * 16));
+                if (ntok < kPage) {                   // wave-uniform
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (4 * kg + e >= ntok) vt[e] = 0;
+                }
+                if constexpr (STEP) {
+                    if (p == p_new && kg == slot_new / 4) vt[slot_new % 4] = (short)s_new[1][16 * t + n];
+                }
+                ot[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, phi, ot[t], 0, 0, 0);
+                ot[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, plo, ot[t], 0, 0, 0);
+            }
+            __builtin_amdgcn_s_waitcnt(kWaitLgkm0);   // the values' stage is read
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (phys_next >= 0) load_v_only(phys_next);
+        phys = phys_next;
+    };
     int p = page_begin + wave;
     int phys = p < page_end ? s_ids[p - page_begin] : -1;
     if (phys >= 0) load_kv(phys);
-    for (; p < page_end; p += NW) page(p, phys);
+    if constexpr (PVM) {
+        for (; p < page_end; p += NW) page_pvm(p, phys);
+    } else {
+        for (; p < page_end; p += NW) page(p, phys);
+    }
 
     // merge the waves: per-wave (max, sum) of each head, o of every dim (o
     // goes where the stages were, once every wave is done with them)
+    if constexpr (PVM) {
+        pl_run += __shfl_xor(pl_run, 16, 64);
+        pl_run += __shfl_xor(pl_run, 32, 64);
+    } else {
 #pragma unroll
-    for (int i = 0; i < GI; ++i) lrun[i] = row_sum16(lrun[i]);
-    __syncthreads();
-    if (kg < HR && n == 0) {
-#pragma unroll
-        for (int i = 0; i < GI; ++i) {
-            s_m[wave][kg * 4 + i] = mrun[i];
-            s_l[wave][kg * 4 + i] = lrun[i];
-        }
+        for (int i = 0; i < GI; ++i) lrun[i] = row_sum16(lrun[i]);
     }
+    __syncthreads();
+    if constexpr (PVM) {
+        if (n < G) {
+            if (kg == 0) {
+                s_m[wave][n] = pm_run;
+                s_l[wave][n] = pl_run;
+            }
 #pragma unroll
-    for (int g = 0; g < G; ++g)
+            for (int t = 0; t < DT; ++t)
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) s_o[wave][g][v_off + e] = o[g][e];
+                for (int e = 0; e < 4; ++e) s_o[wave][n][16 * t + 4 * kg + e] = ot[t][e];
+        }
+    } else {
+        if (kg < HR && n == 0) {
+#pragma unroll
+            for (int i = 0; i < GI; ++i) {
+                s_m[wave][kg * 4 + i] = mrun[i];
+                s_l[wave][kg * 4 + i] = lrun[i];
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) s_o[wave][g][v_off + e] = o[g][e];
+    }
     __syncthreads();
 
     const bool single = nchunks == 1 && !pmatch;

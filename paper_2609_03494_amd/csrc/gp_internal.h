@@ -15,6 +15,10 @@ constexpr int kPage = 16;                 // tokens per page
 #ifndef GP_DECODE_CHUNK_PAGES
 #define GP_DECODE_CHUNK_PAGES 64
 #endif
+#ifndef GP_DECODE_PVM_MIN_G
+#define GP_DECODE_PVM_MIN_G 4
+#endif
+constexpr int kDecodePvmMinG = GP_DECODE_PVM_MIN_G;   // GQA ratios whose decode P.V runs on the matrix cores
 constexpr int kDecodeChunkPages = GP_DECODE_CHUNK_PAGES;   // pages per decode work item, about (split-K)
 constexpr int kMaxChunkPages = 64;                         // pages per decode chunk at most (LDS id table)
 #ifndef GP_DECODE_WAVES
