@@ -413,14 +413,15 @@ __device__ inline float row_sum16(float x) {
 }
 
 // Split decode (bf16): one workgroup of kDecodeWaves waves per (KV head,
-// chunk, request); the waves take the chunk's pages round-robin.  As soon as
-// the matrix cores have consumed a page's keys, the wave requests the keys and
-// the values of its next page (the values into the second of two buffers that
-// alternate), so a whole page is on its way while softmax and P.V run.  In
-// P.V each lane owns D/64 head dimensions for all 16 tokens of the page, so a
-// value load reads one whole 2D-byte row per instruction and the accumulators
-// take G * D / 64 registers; Q waits in LDS.  The waves merge through LDS at
-// the end.
+// chunk, request); the waves take the chunk's pages round-robin.  Each wave
+// owns one LDS page of keys and one of values, filled by direct-to-LDS loads;
+// as soon as a stage has been read out, the wave requests the same part of its
+// next page, so a page is on its way while softmax and P.V run.  Q waits in
+// LDS.  For G >= kDecodePvmMinG, P.V runs on the matrix cores (S^T = K.Q^T
+// puts P in the B layout; V^T comes by transposed LDS reads); for smaller G on
+// the vector ALUs, each lane owning D/64 head dimensions for all 16 tokens of
+// the page (accumulators G * D / 64 registers).  The waves merge through LDS
+// at the end.
 // MODE 0: decode attention; 1: gp_decode_step (summaries and/or the new token
 // folded in); 2: the private tails of gp_decode_attention_shared (a request
 // that reads its group's shared prefix pass covers the pages after the prefix
