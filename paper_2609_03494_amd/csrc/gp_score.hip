@@ -448,17 +448,17 @@ __device__ inline unsigned long long fixed60(uint32_t bits) {
 
 // -------------------------------------------------------------------- top-p --
 // One workgroup of kTopPThreads threads per (boundary request, KV head, view).
-// Each of the three radix passes histograms the weights that share the prefix
+// Each of the three radix passes (10-bit digits of the weights' float32 bit
+// patterns below bit 30) histograms the weights that share the prefix
 // found so far (count and 2^-60 fixed-point mass per bucket), then the
 // workgroup scans the buckets from the top to find the one where the running
-// mass reaches p.  The workgroup is small (one wave per SIMD) so that it can
-// start beside decode attention, which leaves a quarter of each SIMD's
-// registers free.
+// mass reaches p.  The workgroup is small (one wave per SIMD, 12 KB of LDS)
+// so that it starts on any CU with room beside decode attention.
 constexpr int kTopPThreads = 256;
 __global__ __launch_bounds__(kTopPThreads, 5) void top_p_kernel(ScoreArgs a) {
     __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     constexpr int NT = kTopPThreads;
-    constexpr int NB = 2048;
+    constexpr int NB = 1024;
     constexpr int CW = 4096 / NT;                   // weights per thread kept in registers
     constexpr int NWV = NT / 64;
     __shared__ unsigned int s_cnt[NB];
@@ -498,8 +498,10 @@ __global__ __launch_bounds__(kTopPThreads, 5) void top_p_kernel(ScoreArgs a) {
     uint32_t prefix = 0;
     unsigned long long above_mass = 0;
     unsigned int above_cnt = 0;
-    const int shifts[3] = {20, 9, 0};
-    const int nbits[3] = {11, 11, 9};
+    // the weights are at most 1, so bits 31 and 30 of their float32 patterns
+    // are clear (0x3f800000 and below) and three 10-bit digits cover the rest
+    const int shifts[3] = {20, 10, 0};
+    const int nbits[3] = {10, 10, 10};
     for (int pass = 0; pass < 3; ++pass) {
         const int sh = shifts[pass], nb = 1 << nbits[pass];
         for (int b = tid; b < nb; b += NT) {
