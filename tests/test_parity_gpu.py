@@ -266,6 +266,31 @@ def test_decode_g8_prefix_shared():
     _decode_check(w, DeviceCase(w))
 
 
+@pytest.mark.parametrize("hq", [8, 32, 64])
+def test_decode_ignores_slots_past_the_last_token(hq):
+    """Slots of a request's last page past its last token hold anything -- here
+    NaN and +-inf in K and V -- and must not reach the output: the vector-ALU
+    P.V (G = 1) skips them, the matrix-core P.V (G = 4, 8) multiplies them by
+    zero weights, so it has to read them as zero first."""
+    _say(f"decode: poisoned slots past the last token, {hq} q / 8 kv heads")
+    rng = np.random.default_rng(hq)
+    n = rng.integers(20, 1200, size=12)
+    n[n % 16 == 0] += 5                                   # every last page partly filled
+    w = W._build(name="tail_poison", seed=50 + hq, dtype="bf16", Hq=hq, Hkv=8, d=128, n=n, budgets=None,
+                 free_pages=8, heavy_mode="scaled", heavy_frac=0.02, summary_mode="random")
+    dc = DeviceCase(w)
+    b = w.page_size
+    bad = (float("nan"), float("inf"), -float("inf"))
+    for r in range(w.num_reqs):
+        m = int(w.seq_lens[r])
+        if m % b == 0:
+            continue
+        pid = int(w.page_table[r, (m - 1) // b])
+        for j, x in enumerate((dc.layers[0].k, dc.layers[0].v)):
+            x[pid, :, m % b:, :] = bad[(r + j) % 3]
+    _decode_check(w, dc)
+
+
 def test_decode_empty_request_gives_zero():
     _say("decode: a request with no resident token")
     w = W.qwen3_8b(num_reqs=3, len_lo=40, len_hi=90, budget_choices=(8,), free_pages=4)
