@@ -308,11 +308,12 @@ def test_decode_empty_request_gives_zero():
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_decode_back_to_back_calls_see_their_own_partials(dtype):
-    """Requests of several chunks are merged by the workgroup that finishes
-    last, through partials that other workgroups wrote from other XCDs.  Two
+    """Requests of several chunks leave per-chunk partials in the workspace,
+    written by workgroups on every XCD, which the merge launch folds.  Two
     calls with different queries alternate on one stream with no
     synchronisation between them (same workspace, same partial slots); every
-    output must equal, bit for bit, that of the same call run alone."""
+    output must equal, bit for bit, that of the same call run alone, so no
+    call reads partials that another left behind."""
     _say(f"decode: 64 alternating back-to-back calls, {dtype}, requests of 1..7 chunks")
     w = W._build(name="b2b", seed=41, dtype=dtype, Hq=8 if dtype == "f32" else 32,
                  Hkv=2 if dtype == "f32" else 8, d=128, n=np.array([5, 700, 1100, 2100, 3000, 4500, 5200, 6100]),
