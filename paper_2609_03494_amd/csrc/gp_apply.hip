@@ -241,9 +241,12 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
     const int r = a.bnd[i];
     int P = 0;
     bool at_boundary = false;
-    if (r >= 0 && r < a.R) {
-        P = a.num_pages[r];
-        at_boundary = P >= 2 && P <= a.max_pages && a.seq_lens[r] == P * kPage;
+    if (a.R > 0) {
+        // page count and length in one round trip (clamped index)
+        const int rc = min(max(r, 0), a.R - 1);
+        const int Pr = a.num_pages[rc], m = a.seq_lens[rc];
+        at_boundary = (r >= 0) & (r < a.R) & (Pr >= 2) & (Pr <= a.max_pages) & (m == Pr * kPage);
+        P = at_boundary ? Pr : 0;
     }
     if (x == 0) {
         if (at_boundary) {
@@ -321,19 +324,26 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
     const int tid = threadIdx.x;
     const int Rb = a.Rb;
 
-    // The per-(layer, KV head) counts and the shared-page counts of every
-    // request are summed by the whole workgroup, one entry per thread, so
-    // that their loads are in flight together (integer sums: exact in any
-    // order).
+    // The free count, this thread's first boundary request with its page
+    // count and length (clamped index) and its first shared-page count are
+    // requested before anything waits: they arrive while the counts below
+    // are summed.
+    const int fc = tid == 0 ? *a.free_count : 0;
+    const int r_first = tid < Rb ? a.bnd[tid] : -1;
+    const int rc_first = min(max(r_first, 0), a.R - 1);
+    const int P_first = tid < Rb && a.R > 0 ? a.num_pages[rc_first] : 0;
+    const int m_first = tid < Rb && a.R > 0 ? a.seq_lens[rc_first] : -1;
+    const int nshc_first = tid < Rb * a.npc ? a.nshc[tid] : 0;
     for (int i = tid; i < Rb; i += blockDim.x) {
         s_D[i] = 0;
         s_nsh[i] = 0;
     }
-    if (tid == 0) {
-        const int fc = *a.free_count;
-        s_fc0 = fc < 0 ? 0 : (fc > a.pool_pages ? a.pool_pages : fc);
-    }
+    if (tid == 0) s_fc0 = fc < 0 ? 0 : (fc > a.pool_pages ? a.pool_pages : fc);
     __syncthreads();
+    // The per-(layer, KV head) counts and the shared-page counts of every
+    // request are summed by the whole workgroup, one entry per thread, so
+    // that their loads are in flight together (integer sums: exact in any
+    // order).
     const int LH = a.n_layers * a.Hkv;
     for (int e = tid; e < Rb * LH; e += blockDim.x) {
         const int i = e / LH, l = e % LH / a.Hkv, h = e % a.Hkv;
@@ -341,18 +351,22 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
         atomicAdd(&s_D[i], (unsigned long long)((long long)kc[0] - (long long)kc[1]));
     }
     for (int e = tid; e < Rb * a.npc; e += blockDim.x) {
-        const int v = a.nshc[e];
+        const int v = e == tid ? nshc_first : a.nshc[e];
         if (v) atomicAdd(&s_nsh[e / a.npc], v);
     }
     __syncthreads();
 
     for (int i = tid; i < Rb; i += blockDim.x) {
-        const int r = a.bnd[i];
+        const bool first = i == tid;
+        const int r = first ? r_first : a.bnd[i];
         int P = 0, flags = 0, nsh = 0, last_shared = 0;
         float dl = 0.0f;
+        const int rc = min(max(r, 0), a.R - 1);     // page count and length in one round trip
+        const int Pr = first ? P_first : (a.R > 0 ? a.num_pages[rc] : 0);
+        const int mr = first ? m_first : (a.R > 0 ? a.seq_lens[rc] : -1);
         if (r >= 0 && r < a.R) {
-            P = a.num_pages[r];
-            if (P >= 0 && P <= a.max_pages && a.seq_lens[r] == P * kPage) {
+            P = Pr;
+            if (P >= 0 && P <= a.max_pages && mr == P * kPage) {
                 flags = F_BOUNDARY;
                 bool grow, shrink = false;
                 if (P >= 2) {

@@ -962,6 +962,61 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     __shared__ float s_f[MAXC][G];                 // exp2(m_k - M) / L per chunk and head
     __shared__ float s_ml[MAXC][G][2];
     const int h = blockIdx.x, r = blockIdx.y;
+    const int tid = threadIdx.x;
+    const int kmax = a.max_chunks + (a.ngroups > 0 ? 1 : 0);   // slots any request can fill
+    if (kmax <= kFastMerge) {
+        // few slots: every thread requests its elements of every slot a
+        // request can fill together with the lengths (one round trip; the
+        // recorded count then decides which slots are folded)
+        constexpr int EPT = (G * D + 255) / 256;     // elements per thread
+        const float *base = a.partial + ((size_t)r * a.Hkv + h) * a.slots * G * (D + 2);
+        float mk[EPT][kFastMerge], lk[EPT][kFastMerge], ok[EPT][kFastMerge];
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            const int i = min(tid + 256 * e, G * D - 1);
+            const int g = i / D, dd = i % D;
+#pragma unroll
+            for (int k = 0; k < kFastMerge; ++k) {
+                mk[e][k] = kNegInf;
+                lk[e][k] = 0.0f;
+                ok[e][k] = 0.0f;
+                if (k < kmax) {
+                    const float *pp = base + ((size_t)k * G + g) * (D + 2);
+                    mk[e][k] = pp[D];
+                    lk[e][k] = pp[D + 1];
+                    ok[e][k] = pp[dd];
+                }
+            }
+        }
+        const int m = a.lens[r], took = a.lens[a.R + r], nslots = a.lens[2 * a.R + r];
+        if (m < 0) return;
+        if (a.advance && h == 0 && tid == 0 && took) {
+            a.seq_lens_w[r] = m;
+            if (a.positions) a.positions[r] += 1;
+        }
+        if (nslots == 0) return;
+        T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * a.Hkv * G + (size_t)h * G) * D;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            const int i = tid + 256 * e;
+            float M = kNegInf;
+#pragma unroll
+            for (int k = 0; k < kFastMerge; ++k)
+                if (k < nslots) M = fmaxf(M, mk[e][k]);
+            float L = 0.0f, Os = 0.0f;
+#pragma unroll
+            for (int k = 0; k < kFastMerge; ++k) {
+                // slots past the count hold whatever an earlier call left
+                if (k < nslots) {
+                    const float f = mk[e][k] == kNegInf ? 0.0f : exp2f(mk[e][k] - M);
+                    L += lk[e][k] * f;
+                    Os += ok[e][k] * f;
+                }
+            }
+            if (i < G * D) Tr::store(out + i, L > 0.0f ? Os / L : 0.0f);
+        }
+        return;
+    }
     // tokens attended and partial slots, as the chunk pass recorded them
     // (-1: held; 0 slots: the chunk pass wrote the output)
     const int m = a.lens[r];
@@ -976,7 +1031,6 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     const int Hq = a.Hkv * G;
     T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     const float *base = a.partial + ((size_t)r * a.Hkv + h) * a.slots * G * (D + 2);
-    const int tid = threadIdx.x;
     if (nchunks <= kFastMerge) {
         // few chunks: every thread loads all it needs at once (one round trip,
         // the (max, sum) of a head are the same address for a whole wave) and

@@ -97,12 +97,23 @@ __device__ inline double dpp_ror_f64(double x) {
     return __builtin_bit_cast(double, ((long long)hi << 32) | (unsigned)lo);
 }
 
-__device__ inline bool boundary_of(const ScoreArgs &a, int i, int &r, int &P) {
+// slot (optional): the request's summary slot, which must lie in [0, M).
+__device__ inline bool boundary_of(const ScoreArgs &a, int i, int &r, int &P, int *slot = nullptr) {
     r = a.bnd[i];
-    if (r < 0 || r >= a.R) return false;
-    P = a.num_pages[r];
-    if (P < 2 || P > a.max_pages) return false;
-    return a.seq_lens[r] == P * kPage;
+    if (a.R <= 0) return false;
+    // the page count, the length (and the slot) are requested together, at a
+    // clamped index: beside decode attention every round trip costs
+    // microseconds
+    const int rc = min(max(r, 0), a.R - 1);
+    P = a.num_pages[rc];
+    const int m = a.seq_lens[rc];
+    bool ok = true;
+    if (slot) {
+        *slot = a.slot_ids[rc];
+        ok = (*slot >= 0) & (*slot < a.M);
+    }
+    // one test of all the values (no branch between the loads)
+    return ok & (r >= 0) & (r < a.R) & (P >= 2) & (P <= a.max_pages) & (m == P * kPage);
 }
 
 // Products and sums are rounded one at a time, as in a plain fp64 evaluation.
@@ -123,23 +134,37 @@ __global__ __launch_bounds__(256, 5) void prep_kernel(ScoreArgs a) {
     __shared__ double s_cos[H], s_sin[H];
     __shared__ double s_ss[3 * G];
     const int h = blockIdx.x, i = blockIdx.y;
-    int r, P;
-    if (!boundary_of(a, i, r, P)) return;
-    const int slot = a.slot_ids[r];
-    if (slot < 0 || slot >= a.M) return;
+    int r, P, slot;
+    if (!boundary_of(a, i, r, P, &slot)) return;
+    // the query, the position and the summaries are requested together (every
+    // element of a thread at a clamped index)
     const int tid = threadIdx.x;
     const int Hq = a.Hkv * G;
     const float *qs = a.qstate + (size_t)slot * 2 * Hq * D;
     const T *qp = reinterpret_cast<const T *>(a.q_pre) + (size_t)r * Hq * D;
-    for (int e = tid; e < V * D; e += blockDim.x) {
-        const int v = e / D, d = e % D, x = v / G, g = v % G;
-        s_q[v][d] = (double)qs[((size_t)x * Hq + h * G + g) * D + d];
+    constexpr int NQ = (G * D + 255) / 256, NS = (V * D + 255) / 256;   // elements per thread
+    double qv[NQ], sv[NS];
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+        const int e = min(tid + 256 * j, G * D - 1), g = e / D, d = e % D;
+        qv[j] = ld<T>(qp + (size_t)(h * G + g) * D + d);
     }
-    for (int e = tid; e < G * D; e += blockDim.x) {
-        const int g = e / D, d = e % D;
-        s_qt[g][d] = ld<T>(qp + (size_t)(h * G + g) * D + d);
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+        const int e = min(tid + 256 * j, V * D - 1), v = e / D, d = e % D, x = v / G, g = v % G;
+        sv[j] = (double)qs[((size_t)x * Hq + h * G + g) * D + d];
     }
     const double pos = (double)a.positions[r];
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+        const int e = tid + 256 * j;
+        if (e < G * D) s_qt[e / D][e % D] = qv[j];
+    }
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+        const int e = tid + 256 * j;
+        if (e < V * D) s_q[e / D][e % D] = sv[j];
+    }
     for (int k = tid; k < H; k += blockDim.x) {
         const double ang = pos * pow(a.theta, (-2.0 * k) / D);
         s_cos[k] = cos(ang);
@@ -228,10 +253,8 @@ __global__ __launch_bounds__(64 * kLogitsWaves) void logits_kernel(ScoreArgs a) 
     const int y = blockIdx.y * kLogitsWaves + wave, ny = gridDim.y * kLogitsWaves;
     int *s_pg = s_pgs[wave];
     const int k = lane >> 4, cand = lane & 15;      // contraction / output row; candidate 4 b + j
-    int r, P;
-    if (!boundary_of(a, i, r, P)) return;          // uniform over the workgroup
-    const int slot = a.slot_ids[r];
-    if (slot < 0 || slot >= a.M) return;
+    int r, P, slot;
+    if (!boundary_of(a, i, r, P, &slot)) return;   // uniform over the workgroup
     const int C = (P - 1) * kPage;
     const int nblk = cdiv(C, kStatBlock);
     if (blockIdx.y * kLogitsWaves >= nblk) return;  // no wave of the workgroup has a block
@@ -239,17 +262,39 @@ __global__ __launch_bounds__(64 * kLogitsWaves) void logits_kernel(ScoreArgs a) 
     const int nit = active ? min(cdiv(nblk - y, ny), min(a.lg_iters, kLogitsMaxIters)) : 0;
 
     // the page ids of this wave's blocks (-1: no candidates there or an
-    // invalid id) and the aligned summaries (all waves)
-    for (int e = lane; e < 4 * nit; e += 64) {
-        const int pg = 4 * (y + ny * (e / 4)) + e % 4;
-        const int pe = pg < P - 1 ? a.page_table[(size_t)r * a.max_pages + pg] : -1;
-        s_pg[e] = pe >= 0 && pe < a.pool_pages ? pe : -1;
+    // invalid id) and the aligned summaries (all waves), all requested at
+    // once (clamped indices, values dropped afterwards where unused)
+    constexpr int PPL = 4 * kLogitsMaxIters / 64;               // page ids per lane
+    static_assert(4 * kLogitsMaxIters % 64 == 0, "page ids per lane");
+    constexpr int NT = 64 * kLogitsWaves;
+    constexpr int NA = (4 * VR * S + NT - 1) / NT;              // summary elements per thread
+    int pev[PPL];
+#pragma unroll
+    for (int j = 0; j < PPL; ++j) {
+        const int e = lane + 64 * j, pg = 4 * (y + ny * (e / 4)) + e % 4;
+        pev[j] = a.page_table[(size_t)r * a.max_pages + min(pg, P - 2)];
     }
     const double *qt = a.qt + ((size_t)i * a.Hkv + h) * V * D;
-    for (int e = threadIdx.x; e < 4 * VR * S; e += 64 * kLogitsWaves) {
+    double av[NA];
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+        const int e = min((int)threadIdx.x + NT * j, 4 * VR * S - 1);
         const int q = e / (VR * S), rem = e % (VR * S), v = rem / S, s2 = rem % S;
         const int d = 4 * EPU * (s2 / EPU) + EPU * q + s2 % EPU;
-        s_a[q * KS + v * SP + s2] = v < V ? qt[(size_t)v * D + d] : 0.0;
+        av[j] = qt[(size_t)min(v, V - 1) * D + d];
+    }
+#pragma unroll
+    for (int j = 0; j < PPL; ++j) {
+        const int e = lane + 64 * j, pg = 4 * (y + ny * (e / 4)) + e % 4;
+        if (e < 4 * nit) s_pg[e] = pg < P - 1 && pev[j] >= 0 && pev[j] < a.pool_pages ? pev[j] : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+        const int e = threadIdx.x + NT * j;
+        if (e < 4 * VR * S) {
+            const int q = e / (VR * S), rem = e % (VR * S), v = rem / S, s2 = rem % S;
+            s_a[q * KS + v * SP + s2] = v < V ? av[j] : 0.0;
+        }
     }
     __syncthreads();
     if (!active) return;

@@ -22,15 +22,22 @@ __device__ inline float load_q<uint16_t>(const uint16_t *p, size_t i) { return b
 template <typename T>
 __global__ __launch_bounds__(256) void summaries_kernel(SummaryArgs a) {
     const int r = blockIdx.y;
-    const int slot = a.slot_ids[r];
-    if (slot < 0 || slot >= a.M) return;
-    const bool init = a.init[r] != 0;
+    const int i0 = blockIdx.x * blockDim.x + threadIdx.x;
+    // the slot, the init flag and the thread's first query element are
+    // requested together (the first at a clamped index), so the kernel makes
+    // two memory round trips, not four: it heads the boundary chain of a step
     const T *q = reinterpret_cast<const T *>(a.q) + (size_t)r * a.HqD;
+    const float x0 = load_q<T>(q, min(i0, a.HqD - 1));
+    const int slot = a.slot_ids[r];
+    const int init_flag = a.init[r];
+    __asm__ volatile("" ::"v"(x0), "v"(slot), "v"(init_flag));   // all three issued before any wait
+    const bool init = init_flag != 0;
+    if (slot < 0 || slot >= a.M) return;
     float *S = a.qstate + (size_t)slot * 2 * a.HqD;
     float *L = S + a.HqD;
     const double cs = 1.0 - a.beta_s, cl = 1.0 - a.beta_l;
-    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < a.HqD; i += gridDim.x * blockDim.x) {
-        const float x = load_q<T>(q, i);
+    for (int i = i0; i < a.HqD; i += gridDim.x * blockDim.x) {
+        const float x = i == i0 ? x0 : load_q<T>(q, i);
         if (init) {
             S[i] = x;
             L[i] = x;
