@@ -317,7 +317,7 @@ gp_status_t gp_boundary_score_stages(const gp_kv_layer_t *kv, const gp_page_stat
     a.bnd = bnd;
     a.k_counts = k_counts;
     a.scores = scores;
-    a.qt = reinterpret_cast<double *>(base + w.qt);
+    a.cand = reinterpret_cast<int32_t *>(base + w.cand);
     a.expz = reinterpret_cast<float *>(base + w.expz);
     a.part = reinterpret_cast<double *>(base + w.part);
     a.weights = reinterpret_cast<float *>(base + w.weights);

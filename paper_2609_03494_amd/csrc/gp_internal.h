@@ -83,7 +83,7 @@ __host__ __device__ inline DecodeWs decode_ws(int R, int Hq, int Hkv, int D, int
 }
 
 struct ScoreWs {
-    size_t qt, expz, part, weights, total;
+    size_t cand, expz, part, weights, total;
     int cmax, nch;
 };
 
@@ -94,8 +94,8 @@ __host__ __device__ inline ScoreWs score_ws(int Rb, int Hq, int Hkv, int max_pag
     w.cmax = max_pages > 1 ? (max_pages - 1) * kPage : 0;
     w.nch = cdiv(w.cmax > 0 ? w.cmax : 1, kStatBlock);
     size_t off = 0;
-    w.qt = off;       // [Rb][Hkv][2G][D] double: calibrated, rotated summaries
-    off = align_up(off + (size_t)Rb * Hkv * 2 * G * 128 * sizeof(double));
+    w.cand = off;     // [Rb] int32: candidates of the event (0: not a boundary), written by the logits
+    off = align_up(off + (size_t)Rb * sizeof(int32_t));
     w.expz = off;     // [Rb][Hkv][2G][cmax] float: exp(z - block max), z the fp64 logit
     off = align_up(off + (size_t)Rb * Hkv * 2 * G * w.cmax * sizeof(float));
     w.part = off;     // [Rb][Hkv][nch][2G][2] double: block max, block sum of exp
@@ -214,7 +214,8 @@ struct ScoreArgs {
     const int32_t *slot_ids, *positions, *bnd;
     int32_t *k_counts;
     float *scores;
-    double *qt, *part;
+    double *part;
+    int32_t *cand;    // [Rb] candidates per event, 0 if the entry is not a boundary (logits -> later kernels)
     float *expz;
     float *weights;
     int Rb, Hq, Hkv, M, max_pages, pool_pages, max_cand, cmax, nch, R;

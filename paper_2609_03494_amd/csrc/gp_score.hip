@@ -2,26 +2,26 @@
 // App. E.1 "demand estimation at capacity boundaries").
 //
 // Three kernels per layer:
-//  0. prep: per (boundary request, KV head) the 2G aligned summaries of its
-//     GQA group (RMS calibration to the current query, then rotation at the
-//     current position; fp64, angles computed on the device in fp64).
-//  1. logits: per (boundary request, KV head, set of blocks of kStatBlock
-//     candidate tokens), one wave: each block's 2G logits per token in fp64
+//  0. logits: per (boundary request, KV head, set of blocks of kStatBlock
+//     candidate tokens), one wave: first the 2G aligned summaries of the GQA
+//     group (RMS calibration to the current query, then rotation at the
+//     current position; fp64, angles computed on the device in fp64), then
+//     each block's 2G logits per token in fp64
 //     on the fp64 matrix cores; the block's max and sum of exponentials per
 //     view go to the workspace (fp64), and exp(z - block max) per token is
 //     stored in float32 (relative error about 2^-24: one rounding of the
 //     float32 weight it feeds).
-//  2. weights: merge the block statistics per view, scale each token's
+//  1. weights: merge the block statistics per view, scale each token's
 //     exponentials into softmax weights, average the G query heads of each
 //     view (fp64), round to float32 and write a^S, a^L (workspace) and
 //     s = max(a^S, a^L) (output).
-//  3. top-p: per (request, KV head, view) a three-pass radix select on the
+//  2. top-p: per (request, KV head, view) a three-pass radix select on the
 //     float32 bit patterns finds the smallest k whose k largest weights reach
 //     p.  Per-bucket masses are accumulated as 2^-60 fixed-point integers, so
 //     sums are exact and independent of thread order.
 //
 // Bound: the key read (|C| * d * sizeof(elem) per KV head) plus 2G float32
-// exponentials written and read back; kernel 1 does 2G fp64 FMAs per key
+// exponentials written and read back; kernel 0 does 2G fp64 FMAs per key
 // element.
 #include "gp_internal.h"
 
@@ -85,6 +85,10 @@ __device__ inline double exp_nonpos(double x) {
     return __builtin_ldexp(p, (int)fmax(n, -2100.0));
 }
 
+// LDS traffic between lanes of one wave: wait for the wave's LDS operations
+// and keep the compiler from moving memory accesses across this point.
+__device__ inline void wave_lds_sync() { __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 // max without the NaN canonicalisation of fmax (the operands are finite or -inf)
 __device__ inline double max_f64(double a, double b) { return a > b ? a : b; }
 
@@ -118,82 +122,6 @@ __device__ inline bool boundary_of(const ScoreArgs &a, int i, int &r, int &P, in
 
 // Products and sums are rounded one at a time, as in a plain fp64 evaluation.
 #pragma clang fp contract(off)
-
-// --------------------------------------------------------------------- prep --
-// One workgroup per (boundary request, KV head): the 2G summaries of its GQA
-// group scaled to the RMS of the current query (RMS calibration) and rotated
-// at the current position; angles pos * theta^(-2k/D) and their sine and
-// cosine are computed in fp64 on the device.
-template <typename T, int D, int G>
-__global__ __launch_bounds__(256, 5) void prep_kernel(ScoreArgs a) {
-    __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
-    constexpr int V = 2 * G;
-    constexpr int H = D / 2;
-    __shared__ double s_q[V][D];
-    __shared__ double s_qt[G][D];
-    __shared__ double s_cos[H], s_sin[H];
-    __shared__ double s_ss[3 * G];
-    const int h = blockIdx.x, i = blockIdx.y;
-    int r, P, slot;
-    if (!boundary_of(a, i, r, P, &slot)) return;
-    // the query, the position and the summaries are requested together (every
-    // element of a thread at a clamped index)
-    const int tid = threadIdx.x;
-    const int Hq = a.Hkv * G;
-    const float *qs = a.qstate + (size_t)slot * 2 * Hq * D;
-    const T *qp = reinterpret_cast<const T *>(a.q_pre) + (size_t)r * Hq * D;
-    constexpr int NQ = (G * D + 255) / 256, NS = (V * D + 255) / 256;   // elements per thread
-    double qv[NQ], sv[NS];
-#pragma unroll
-    for (int j = 0; j < NQ; ++j) {
-        const int e = min(tid + 256 * j, G * D - 1), g = e / D, d = e % D;
-        qv[j] = ld<T>(qp + (size_t)(h * G + g) * D + d);
-    }
-#pragma unroll
-    for (int j = 0; j < NS; ++j) {
-        const int e = min(tid + 256 * j, V * D - 1), v = e / D, d = e % D, x = v / G, g = v % G;
-        sv[j] = (double)qs[((size_t)x * Hq + h * G + g) * D + d];
-    }
-    const double pos = (double)a.positions[r];
-#pragma unroll
-    for (int j = 0; j < NQ; ++j) {
-        const int e = tid + 256 * j;
-        if (e < G * D) s_qt[e / D][e % D] = qv[j];
-    }
-#pragma unroll
-    for (int j = 0; j < NS; ++j) {
-        const int e = tid + 256 * j;
-        if (e < V * D) s_q[e / D][e % D] = sv[j];
-    }
-    for (int k = tid; k < H; k += blockDim.x) {
-        const double ang = pos * pow(a.theta, (-2.0 * k) / D);
-        s_cos[k] = cos(ang);
-        s_sin[k] = sin(ang);
-    }
-    __syncthreads();
-    // 3G sums of squares, 8 lanes each
-    if (tid < 3 * G * 8) {
-        const int which = tid / 8, part = tid % 8;
-        const double *src = which < V ? s_q[which] : s_qt[which - V];
-        double acc = 0.0;
-#pragma unroll
-        for (int d = part * (D / 8); d < (part + 1) * (D / 8); ++d) acc += src[d] * src[d];
-        acc += __shfl_xor(acc, 1, 8);
-        acc += __shfl_xor(acc, 2, 8);
-        acc += __shfl_xor(acc, 4, 8);
-        if (part == 0) s_ss[which] = acc;
-    }
-    __syncthreads();
-    double *out = a.qt + ((size_t)i * a.Hkv + h) * V * D;
-    for (int e = tid; e < V * H; e += blockDim.x) {
-        const int v = e / H, k = e % H, g = v % G;
-        const double den = s_ss[v];
-        const double gam = den == 0.0 ? 0.0 : sqrt(s_ss[V + g] / D) / sqrt(den / D);
-        const double x1 = gam * s_q[v][k], x2 = gam * s_q[v][k + H];
-        out[(size_t)v * D + k] = x1 * s_cos[k] - x2 * s_sin[k];
-        out[(size_t)v * D + k + H] = x2 * s_cos[k] + x1 * s_sin[k];
-    }
-}
 
 // ------------------------------------------------------------------- logits --
 // Grid (KV head, split / kLogitsWaves, boundary request); each wave of a
@@ -253,51 +181,78 @@ __global__ __launch_bounds__(64 * kLogitsWaves) void logits_kernel(ScoreArgs a) 
     const int y = blockIdx.y * kLogitsWaves + wave, ny = gridDim.y * kLogitsWaves;
     int *s_pg = s_pgs[wave];
     const int k = lane >> 4, cand = lane & 15;      // contraction / output row; candidate 4 b + j
-    int r, P, slot;
-    if (!boundary_of(a, i, r, P, &slot)) return;   // uniform over the workgroup
-    const int C = (P - 1) * kPage;
-    const int nblk = cdiv(C, kStatBlock);
-    if (blockIdx.y * kLogitsWaves >= nblk) return;  // no wave of the workgroup has a block
-    const bool active = y < nblk;
-    const int nit = active ? min(cdiv(nblk - y, ny), min(a.lg_iters, kLogitsMaxIters)) : 0;
-
-    // the page ids of this wave's blocks (-1: no candidates there or an
-    // invalid id) and the aligned summaries (all waves), all requested at
-    // once (clamped indices, values dropped afterwards where unused)
+    // Round trips are slow beside decode attention, so the prologue takes
+    // three: the request index; then, together, everything that needs only
+    // the request (its page count, length and summary slot, the page ids of
+    // this wave's blocks, the query and the position; clamped indices, values
+    // dropped afterwards where unused); then the summaries, which need the
+    // slot, beside the first keys.  The candidate count of the event goes to
+    // the workspace for the kernels that follow.
     constexpr int PPL = 4 * kLogitsMaxIters / 64;               // page ids per lane
     static_assert(4 * kLogitsMaxIters % 64 == 0, "page ids per lane");
     constexpr int NT = 64 * kLogitsWaves;
-    constexpr int NA = (4 * VR * S + NT - 1) / NT;              // summary elements per thread
+    const bool writer = h == 0 && blockIdx.y == 0 && threadIdx.x == 0;
+    if (a.R <= 0) {
+        if (writer) a.cand[i] = 0;
+        return;
+    }
+    const int r = a.bnd[i];
+    const int rc = min(max(r, 0), a.R - 1);
+    const int P = a.num_pages[rc], m_r = a.seq_lens[rc], slot = a.slot_ids[rc];
     int pev[PPL];
 #pragma unroll
     for (int j = 0; j < PPL; ++j) {
         const int e = lane + 64 * j, pg = 4 * (y + ny * (e / 4)) + e % 4;
-        pev[j] = a.page_table[(size_t)r * a.max_pages + min(pg, P - 2)];
+        pev[j] = a.page_table[(size_t)rc * a.max_pages + min(pg, a.max_pages - 1)];
     }
-    const double *qt = a.qt + ((size_t)i * a.Hkv + h) * V * D;
-    double av[NA];
+    // The 2G summaries of the workgroup's GQA group (Sec. 3.2, App. E.1):
+    // thread (view row vr, lane lr of TPR) holds the rotation pairs (k, k +
+    // D/2), k = lr, lr + TPR, ...; each row is scaled to the RMS of its query
+    // head (RMS calibration) and rotated at the current position (angles pos *
+    // theta^(-2k/D), sine and cosine in fp64 on the device).
+    constexpr int H = D / 2;
+    constexpr int TPR = NT / V;                                 // threads per view row
+    constexpr int PP = (H + TPR - 1) / TPR;                     // rotation pairs per thread
+    static_assert(NT % V == 0 && TPR <= 64 && H <= NT, "summary prologue layout");
+    __shared__ double s_cs[2][H];
+    const int Hq = a.Hkv * G;
+    const int vrow = threadIdx.x / TPR, lr = threadIdx.x % TPR;
+    const T *qrow = reinterpret_cast<const T *>(a.q_pre) + ((size_t)rc * Hq + h * G + vrow % G) * D;
+    double q1[PP], q2[PP];
 #pragma unroll
-    for (int j = 0; j < NA; ++j) {
-        const int e = min((int)threadIdx.x + NT * j, 4 * VR * S - 1);
-        const int q = e / (VR * S), rem = e % (VR * S), v = rem / S, s2 = rem % S;
-        const int d = 4 * EPU * (s2 / EPU) + EPU * q + s2 % EPU;
-        av[j] = qt[(size_t)min(v, V - 1) * D + d];
+    for (int j = 0; j < PP; ++j) {
+        const int kk = min(lr + TPR * j, H - 1);
+        q1[j] = ld<T>(qrow + kk);
+        q2[j] = ld<T>(qrow + kk + H);
     }
+    const double pos = (double)a.positions[rc];
+    const bool ok = (r >= 0) & (r < a.R) & (slot >= 0) & (slot < a.M) & (P >= 2) & (P <= a.max_pages) &
+                    (m_r == P * kPage);
+    const int C = ok ? (P - 1) * kPage : 0;
+    const int nblk = cdiv(C, kStatBlock);
+    const bool active = y < nblk;
+    const int nit = active ? min(cdiv(nblk - y, ny), min(a.lg_iters, kLogitsMaxIters)) : 0;
+    // (everything the second round trip brought is used before the first branch)
 #pragma unroll
     for (int j = 0; j < PPL; ++j) {
         const int e = lane + 64 * j, pg = 4 * (y + ny * (e / 4)) + e % 4;
         if (e < 4 * nit) s_pg[e] = pg < P - 1 && pev[j] >= 0 && pev[j] < a.pool_pages ? pev[j] : -1;
     }
+    if ((int)threadIdx.x < H) {
+        const double ang = pos * pow(a.theta, (-2.0 * (int)threadIdx.x) / D);
+        s_cs[0][threadIdx.x] = cos(ang);
+        s_cs[1][threadIdx.x] = sin(ang);
+    }
+    double qq = 0.0;
 #pragma unroll
-    for (int j = 0; j < NA; ++j) {
-        const int e = threadIdx.x + NT * j;
-        if (e < 4 * VR * S) {
-            const int q = e / (VR * S), rem = e % (VR * S), v = rem / S, s2 = rem % S;
-            s_a[q * KS + v * SP + s2] = v < V ? av[j] : 0.0;
+    for (int j = 0; j < PP; ++j) {
+        if (lr + TPR * j < H) {
+            qq += q1[j] * q1[j];
+            qq += q2[j] * q2[j];
         }
     }
-    __syncthreads();
-    if (!active) return;
+    if (writer) a.cand[i] = C;
+    if (blockIdx.y * kLogitsWaves >= nblk) return;  // no wave of the workgroup has a block (or no event)
 
     // keys of half `hf` of block `it`: lane (k, cand) reads units k, 4 + k,
     // ... of token cand of the block's pages 2 hf and 2 hf + 1.  The loads are
@@ -334,7 +289,56 @@ __global__ __launch_bounds__(64 * kLogitsWaves) void logits_kernel(ScoreArgs a) 
     };
     float *lgv = a.expz + ((size_t)i * a.Hkv + h) * V * a.cmax;
     uint4 k0[2][NU], k1[2][NU];
-    load_keys(0, 0, k0);
+    // the first keys of an active wave (its page ids are in its own LDS row),
+    // then the summaries
+    wave_lds_sync();
+    if (active) load_keys(0, 0, k0);
+    const float *srow = a.qstate + ((size_t)slot * 2 * Hq + (size_t)(vrow / G) * Hq + h * G + vrow % G) * D;
+    double s1[PP], s2[PP];
+#pragma unroll
+    for (int j = 0; j < PP; ++j) {
+        const int kk = min(lr + TPR * j, H - 1);
+        s1[j] = (double)srow[kk];
+        s2[j] = (double)srow[kk + H];
+    }
+    double ss = 0.0;
+#pragma unroll
+    for (int j = 0; j < PP; ++j) {
+        if (lr + TPR * j < H) {
+            ss += s1[j] * s1[j];
+            ss += s2[j] * s2[j];
+        }
+    }
+#pragma unroll
+    for (int off = TPR / 2; off >= 1; off >>= 1) {
+        ss += __shfl_xor(ss, off, TPR);
+        qq += __shfl_xor(qq, off, TPR);
+    }
+    const double gam = ss == 0.0 ? 0.0 : sqrt(qq / D) / sqrt(ss / D);
+    // rows V .. VR - 1 of the MFMA operand are zero
+    for (int e = threadIdx.x; e < 4 * (VR - V) * S; e += NT) {
+        const int q = e / ((VR - V) * S), rem = e % ((VR - V) * S);
+        s_a[q * KS + (V + rem / S) * SP + rem % S] = 0.0;
+    }
+    __syncthreads();
+    // head dimension d of view row vr goes to s_a[q][vr][s] with d = 4 E (s / E)
+    // + E q + s % E (the lane-group layout of the product below)
+    auto put = [&](int d, double val) {
+        const int q = (d / EPU) % 4, s2i = (d / (4 * EPU)) * EPU + d % EPU;
+        s_a[q * KS + vrow * SP + s2i] = val;
+    };
+#pragma unroll
+    for (int j = 0; j < PP; ++j) {
+        const int kk = lr + TPR * j;
+        if (kk < H) {
+            const double x1 = gam * s1[j], x2 = gam * s2[j];
+            const double c = s_cs[0][kk], sn = s_cs[1][kk];
+            put(kk, x1 * c - x2 * sn);
+            put(kk + H, x2 * c + x1 * sn);
+        }
+    }
+    __syncthreads();
+    if (!active) return;
     for (int it = 0; it < nit; ++it) {
         const int blk = y + ny * it;
         double acc[VH][4];
@@ -407,39 +411,51 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G >= 8 ? 4 
     __shared__ double s_M[V], s_L[V];
     __shared__ double s_f[BPC][V];
     const int h = blockIdx.x, chunk = blockIdx.y, i = blockIdx.z;
-    int r, P;
-    if (!boundary_of(a, i, r, P)) return;
-    const int C = (P - 1) * kPage;
     const int t0 = chunk * kProbChunk;
-    if (t0 >= C) return;
+    if (t0 >= a.cmax) return;
     const int tid = threadIdx.x;
-    const int used = cdiv(C, kStatBlock);
     const int b0 = t0 / kStatBlock;
     const double *pt = a.part + (((size_t)i * a.Hkv + h) * a.nch) * V * 2;
     const float *lg = a.expz + ((size_t)i * a.Hkv + h) * V * a.cmax;
 
     // The kernel runs beside decode attention, where every memory round trip
-    // is slow: the exponentials of this thread's tokens and the statistics
-    // are all requested before any of them is used.
+    // is slow: the event's candidate count (which the logits left in the
+    // workspace), the exponentials of this thread's tokens and the first
+    // statistics are all requested at once (clamped indices: values beyond
+    // the candidates are dropped), in one round trip.
+    const int C = a.cand[i];
     float e[TPT][V];
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
         const int t = t0 + k * 256 + tid;
 #pragma unroll
-        for (int v = 0; v < V; ++v) e[k][v] = lg[(size_t)v * a.cmax + min(t, C - 1)];
+        for (int v = 0; v < V; ++v) e[k][v] = lg[(size_t)v * a.cmax + min(t, a.cmax - 1)];
     }
+    double mk0[(V + 7) / 8][NPL], sk0[(V + 7) / 8][NPL];
+#pragma unroll
+    for (int vb = 0; vb < V; vb += 8) {
+        const int v = min(vb + tid / 32, V - 1), c0 = tid % 32;
+#pragma unroll
+        for (int k = 0; k < NPL; ++k) {
+            const double *pc = pt + ((size_t)min(c0 + 32 * k, a.nch - 1) * V + v) * 2;
+            mk0[vb / 8][k] = pc[0];
+            sk0[vb / 8][k] = pc[1];
+        }
+    }
+    if (t0 >= C) return;        // (C = 0: not a boundary)
+    const int used = cdiv(C, kStatBlock);
     // merge the block statistics: 32 lanes per view, views 8 at a time; lane
     // c0 holds blocks c0, c0 + 32, ... (the first NPL of them in registers)
+#pragma unroll
     for (int vb = 0; vb < V; vb += 8) {
         const int v = vb + tid / 32, c0 = tid % 32;
         if (v < V) {
             double mk[NPL], sk[NPL];
 #pragma unroll
             for (int k = 0; k < NPL; ++k) {
-                const int c = c0 + 32 * k;
-                const double *pc = pt + ((size_t)min(c, used - 1) * V + v) * 2;
-                mk[k] = pc[0];
-                sk[k] = pc[1];
+                const bool in = c0 + 32 * k < used;       // (blocks past the candidates: stale values)
+                mk[k] = in ? mk0[vb / 8][k] : -__builtin_huge_val();
+                sk[k] = in ? sk0[vb / 8][k] : 0.0;
             }
             double M = -__builtin_huge_val();
 #pragma unroll
@@ -517,29 +533,27 @@ __global__ __launch_bounds__(kTopPThreads, 5) void top_p_kernel(ScoreArgs a) {
     const int h = blockIdx.x, x = blockIdx.y, i = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63;
     int32_t *out = a.k_counts + ((size_t)i * a.Hkv + h) * 2 + x;
-    int r, P;
-    if (!boundary_of(a, i, r, P)) {
+    if (a.cmax == 0) {                     // no request can have candidates
         if (tid == 0) *out = 0;
         return;
     }
-    const int C = (P - 1) * kPage;
     const float *wv = a.weights + (((size_t)i * a.Hkv + h) * 2 + x) * a.cmax;
     const unsigned long long target = (unsigned long long)ldexp(a.p, 60);
 
     // the first CW * NT weights stay in registers across the passes (every
-    // candidate set up to 4096 tokens); longer ones re-read the rest
-    // (loads at clamped indices, so that all of them are in flight at once)
+    // candidate set up to 4096 tokens); longer ones re-read the rest.  They
+    // are requested with the event's candidate count (which the logits left
+    // in the workspace), at clamped indices, in one round trip.
+    const int C = a.cand[i];
     uint32_t cached[CW];
 #pragma unroll
-    for (int k = 0; k < CW; ++k) cached[k] = 0xffffffffu;
-    if (C > 0) {
-#pragma unroll
-        for (int k = 0; k < CW; ++k) {
-            const int t = k * NT + tid;
-            const uint32_t u = __float_as_uint(wv[min(t, C - 1)]);
-            cached[k] = t < C ? u : 0xffffffffu;
-        }
+    for (int k = 0; k < CW; ++k) cached[k] = __float_as_uint(wv[min(k * NT + tid, a.cmax - 1)]);
+    if (C == 0) {                          // not a boundary
+        if (tid == 0) *out = 0;
+        return;
     }
+#pragma unroll
+    for (int k = 0; k < CW; ++k) cached[k] = k * NT + tid < C ? cached[k] : 0xffffffffu;
     uint32_t prefix = 0;
     unsigned long long above_mass = 0;
     unsigned int above_cnt = 0;
@@ -704,7 +718,7 @@ hipError_t launch_gd(int G, const ScoreArgs &a, int stages, hipStream_t s) {
     ScoreArgs b = a;
     const int nblocks = a.Hkv * a.nch * a.Rb;
     b.lg_iters = std::min(kLogitsMaxIters, std::max(1, cdiv(nblocks, 16384)));
-    dim3 g0(a.Hkv, a.Rb), g1(a.Hkv, cdiv(cdiv(a.nch, b.lg_iters), kLogitsWaves), a.Rb), g2(a.Hkv, cdiv(a.cmax, kProbChunk), a.Rb), g3(a.Hkv, 2, a.Rb);
+    dim3 g1(a.Hkv, cdiv(cdiv(a.nch, b.lg_iters), kLogitsWaves), a.Rb), g2(a.Hkv, cdiv(a.cmax, kProbChunk), a.Rb), g3(a.Hkv, 2, a.Rb);
     const bool weights = stages & GP_SCORE_WEIGHTS, counts = stages & GP_SCORE_COUNTS;
     if (a.cmax == 0) {
         // no request can have candidates: the counts are written as zero
@@ -715,7 +729,6 @@ hipError_t launch_gd(int G, const ScoreArgs &a, int stages, hipStream_t s) {
     switch (G) {
 #define GP_CASE(GG)                                                   \
     case GG:                                                          \
-        prep_kernel<T, D, GG><<<g0, 256, 0, s>>>(a);                  \
         logits_kernel<T, D, GG><<<g1, 64 * kLogitsWaves, 0, s>>>(b);  \
         weights_kernel<GG><<<g2, 256, 0, s>>>(a);                     \
         break;
