@@ -6,8 +6,9 @@ A step is one pass of the whole path over the batch: restore the page metadata
 to the step's starting state (one device-to-device copy), update both query summaries of every request, paged decode attention
 for every request, then boundary scoring, selection, the decision and compaction for the
 requests at a capacity boundary.  Inputs are seeded synthetic tensors resident
-in HBM before timing starts.  The step is captured once as a HIP graph and
-replayed (``--eager`` launches every call directly).  Decode attention reads
+in HBM before timing starts.  The step is captured as a HIP graph and
+replayed (``--graph-steps S`` captures S consecutive steps per graph;
+``--eager`` launches every call directly).  Decode attention reads
 a snapshot of the request metadata (written by the restore, in the same
 launch), so the summary update, scoring, selection and the decision (which
 updates the live metadata) run on a second stream beside it; the compaction,
@@ -71,6 +72,11 @@ def parse():
     ap.add_argument("--ceiling-mib", type=int, default=4096, help="buffer of the streaming-read ceiling")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "decode_traffic_qwen3_8b.json"))
     ap.add_argument("--eager", action="store_true", help="launch every call directly (no HIP graphs)")
+    ap.add_argument("--graph-steps", type=int, default=1,
+                    help="steps captured per HIP graph (a divisor of --steps is used)")
+    ap.add_argument("--layout", default="boundary-first",
+                    choices=["boundary-first", "decode-first", "summaries-first"],
+                    help="capture order of the two branches of a step (see step())")
     ap.add_argument("--serial", action="store_true",
                     help="run boundary scoring after decode attention on one stream")
     ap.add_argument("--loop-steps", type=int, default=50,
@@ -226,15 +232,28 @@ def main():
         else:
             # decode attention needs only the snapshot of the request metadata
             # (written by the restore): it forks right after it, beside the
-            # summary update, scoring, selection and the decision
-            side.wait_stream(cur)
-            with torch.cuda.stream(side):
+            # summary update, scoring, selection and the decision.  The
+            # layouts differ in the order of capture (the graph runs the first
+            # branch captured on the launch queue) and in where the summary
+            # update runs
+            if args.layout == "summaries-first":
                 phase["summaries"]()
-                phase["score"]()
-                phase["decide"]()
+            side.wait_stream(cur)
+
+            def boundary_branch():
+                with torch.cuda.stream(side):
+                    if args.layout != "summaries-first":
+                        phase["summaries"]()
+                    phase["score"]()
+                    phase["decide"]()
+
+            if args.layout == "boundary-first":
+                boundary_branch()
             mark("d0")
             phase["decode_snapshot"]()
             mark("d1")
+            if args.layout != "boundary-first":
+                boundary_branch()
             cur.wait_stream(side)
             phase["compact"]()
         mark("b1")
@@ -243,24 +262,30 @@ def main():
     for _ in range(2):
         step()
     torch.cuda.synchronize()
+    # steps per launch: with HIP graphs, S consecutive steps are captured into
+    # one graph (as a serving loop captures its decode steps), so that the
+    # graph's launch cost is paid once per S steps; every step still does all
+    # of its work, the restore included
+    S = 1 if args.eager else max(1, math.gcd(args.graph_steps, args.steps))
     if args.eager:
         run_step = step
     else:
-        # the whole step is one HIP graph: no launch gaps between its kernels
+        # S whole steps are one HIP graph: no launch gaps between their kernels
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
-            step()
+            for _ in range(S):
+                step()
         run_step = graph.replay
 
-    for _ in range(args.warmup):
+    for _ in range(max(1, args.warmup // S)):
         run_step()
     torch.cuda.synchronize()
     counters.zero_()
-    # timed region: K whole steps, nothing else on the streams
+    # timed region: K whole steps (K / S launches), nothing else on the streams
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record(stream)
-    for _ in range(args.steps):
+    for _ in range(args.steps // S):
         run_step()
     t1.record(stream)
     torch.cuda.synchronize()
@@ -511,7 +536,8 @@ def main():
         "config": {"workload": WORKLOADS[args.workload][1],
                    "resident_tokens": int(m.sum()), "boundary_requests": Rb},
         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
-        "launch": "eager" if args.eager else "one HIP graph per step",
+        "launch": ("eager" if args.eager else f"one HIP graph per {S} step{'s' if S > 1 else ''}") +
+                  ("" if args.serial else f", {args.layout}"),
         "decode_attention": {"ms": round(decode_ms, 4), "GB/s": round(dec_gbs, 1),
                              "hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4), "bytes": decode_bytes,
                              "unique_kv_bytes": unique_bytes,
