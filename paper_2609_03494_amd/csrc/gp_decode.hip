@@ -503,8 +503,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_
 
     // gp_decode_step: the summaries of query heads [h G, h G + G) are updated
     // by the first chunk's workgroup (with a new token: only if the request
-    // takes it).  The old values and the query are requested here, with the
-    // other loads of the prologue; the update is stored when the workgroup ends.
+    // takes it).  The slot is looked up here; the old values and the query are
+    // requested when the workgroup's pages are done (held in registers across
+    // the page loop they would push it past its register budget), and the
+    // update is stored when the workgroup ends.
     float f_q[FE], f_s[FE], f_l[FE];
     float *fS = nullptr;
     bool f_init = false;
@@ -514,6 +516,12 @@ __global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_
             if (slot >= 0 && slot < a.M) {
                 fS = a.qstate + (size_t)slot * 2 * Hq * D + (size_t)h * G * D;
                 f_init = a.init[r] != 0;
+            }
+        }
+    }
+    auto load_fold = [&]() {
+        if constexpr (STEP) {
+            if (fS) {
                 const uint16_t *qp = reinterpret_cast<const uint16_t *>(a.q_pre) + ((size_t)r * Hq + (size_t)h * G) * D;
 #pragma unroll
                 for (int e = 0; e < FE; ++e) {
@@ -524,7 +532,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_
                 }
             }
         }
-    }
+    };
     auto finish_fold = [&]() {
         if constexpr (STEP) {
             if (fS) {
@@ -549,6 +557,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_
     if (mt == 0) {
         if (chunk == 0 && !pmatch)
             for (int i = tid; i < G * D; i += blockDim.x) out[i] = 0;
+        load_fold();
         finish_fold();
         return;
     }
@@ -885,6 +894,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_
     } else {
         for (; p < page_end; p += NW) page(p, phys);
     }
+    load_fold();          // (in flight while the waves merge)
 
     // merge the waves: per-wave (max, sum) of each head, o of every dim (o
     // goes where the stages were, once every wave is done with them)
