@@ -18,9 +18,12 @@ stream, decode on the live metadata).
 Prints one JSON line.  ``value`` is GB/s of the every-step traffic (summaries
 and decode attention, algorithmic bytes) over the whole step's time, boundary
 work included in the time but not in the bytes; the timed region holds the K
-steps and nothing else.  The ``roofline`` object covers the dominant kernel
-(decode attention: split kernel + merge), timed with HIP events around K
-back-to-back launches on its stream after the timed steps.  A last,
+steps and nothing else.  With a shared prefix (``--workload prefix_shared``)
+the step decodes with the shared-prefix call and its bytes count each
+resident page once.  The ``roofline`` object covers the dominant kernel
+(decode attention: split kernel + merge; the shared-prefix call with a shared
+prefix), timed with HIP events around K back-to-back launches on its stream
+after the timed steps.  A last,
 instrumented pass of K eager steps with events between the phases gives the
 time the boundary work adds after decode attention.  ``cpu_baseline`` times
 the CPU oracle on a bounded sample of the same workload.
@@ -171,8 +174,17 @@ def main():
     def phase_decode():
         gp.gp_decode_attention(kv, ps, q_post, params.scale, out, ws_d)
 
+    # a workload whose requests share a prefix of pages (App. E.2) decodes in
+    # the step with the shared-prefix call, which reads each shared page once
+    # per block of requests (its three stages in order on one stream)
+    prefix_pages = int(w.meta.get("prefix_len", 0)) // b
+    groups = [(0, R, prefix_pages)] if prefix_pages else []
+
     def phase_decode_snapshot():
-        gp.gp_decode_attention(kv, ps_dec, q_post, params.scale, out, ws_d)
+        if prefix_pages:
+            gp.gp_decode_attention_shared(kv, ps_dec, q_post, params.scale, out, groups, ws_d)
+        else:
+            gp.gp_decode_attention(kv, ps_dec, q_post, params.scale, out, ws_d)
 
     bargs = ([kv], ps, bnd, counts, scores, params, decisions, delta, counters, ws_a)
     # Decode attention reads a per-step snapshot of the request metadata
@@ -395,9 +407,7 @@ def main():
     # pages once per block of requests (the prefix pass on a second stream
     # beside the private tails, then the merge), K back-to-back calls
     shared = None
-    prefix_pages = int(w.meta.get("prefix_len", 0)) // b
     if prefix_pages:
-        groups = [(0, R, prefix_pages)]
         side2 = torch.cuda.Stream()
 
         def shared_call():
@@ -415,7 +425,9 @@ def main():
         for _ in range(2):
             shared_call()
         shared_ms = timed_loop(shared_call)
-        shared = {"ms": shared_ms, "groups": groups}
+        shared_one_ms = timed_loop(lambda: gp.gp_decode_attention_shared(kv, ps, q_post, params.scale, out,
+                                                                        groups, ws_d))
+        shared = {"ms": shared_ms, "one_stream_ms": shared_one_ms, "groups": groups}
 
     # instrumented pass (eager launches, events between phases): how much of a
     # step the boundary work adds after decode attention has finished
@@ -480,25 +492,38 @@ def main():
     m = w.seq_lens.astype(np.int64)
     decode_bytes = int(m.sum()) * Hkv * d * e * 2 + int(w.num_pages.sum()) * 4 + 2 * R * Hq * d * e
     summary_bytes = R * Hq * d * e + 2 * 2 * R * Hq * d * 4
-    step_bytes = decode_bytes + summary_bytes
-    gbs = step_bytes / (step_ms * 1e-3) / 1e9
-    dec_gbs = decode_bytes / (decode_ms * 1e-3) / 1e9
 
     # resident (page, slot) pairs counted once: pages shared by a common prefix
     # are read by every request that holds them, but held in HBM once
     slots_all = np.concatenate([w.page_table[r][np.arange(int(w.seq_lens[r])) // b].astype(np.int64) * b
                                 + np.arange(int(w.seq_lens[r])) % b for r in range(R)])
     unique_bytes = int(np.unique(slots_all).size) * Hkv * d * e * 2
+    # the step's decode bytes: with a shared prefix, the shared pages once
+    # (the call the step makes reads them once per block of requests)
+    step_decode_bytes = (unique_bytes + decode_bytes - int(m.sum()) * Hkv * d * e * 2) if prefix_pages \
+        else decode_bytes
+    step_bytes = step_decode_bytes + summary_bytes
+    gbs = step_bytes / (step_ms * 1e-3) / 1e9
+    dec_gbs = decode_bytes / (decode_ms * 1e-3) / 1e9
 
     if shared is not None:
         sh_gbs = unique_bytes / (shared["ms"] * 1e-3) / 1e9
         shared = {"ms": round(shared["ms"], 4), "unique_GB/s": round(sh_gbs, 1),
                   "unique_hbm_frac": round(sh_gbs / HBM_PEAK_GBS, 4),
+                  "one_stream_ms": round(shared["one_stream_ms"], 4),
+                  "one_stream_unique_hbm_frac": round(unique_bytes / (shared["one_stream_ms"] * 1e-3) / 1e9
+                                                      / HBM_PEAK_GBS, 4),
                   "plain_call_unique_hbm_frac": round(unique_bytes / (decode_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                   "groups": shared["groups"],
                   "note": "gp_decode_attention_shared: the prefix pass (shared pages read once per block of "
                           "requests, on the matrix cores) on a second stream beside the private tails, then "
-                          "the merge"}
+                          "the merge; one_stream: the three stages in order on one stream, as the step "
+                          "calls it"}
+        # the step decodes with the one-stream shared call: it is the roofline's kernel here
+        rf_bytes = step_decode_bytes
+        rf_gbs = rf_bytes / (shared_one_ms * 1e-3) / 1e9
+    else:
+        rf_bytes, rf_gbs = decode_bytes, dec_gbs
 
     traffic = None
     if args.workload == "qwen3_8b" and os.path.exists(args.traffic_json):
@@ -540,7 +565,7 @@ def main():
                   ("" if args.serial else f", {args.layout}"),
         "decode_attention": {"ms": round(decode_ms, 4), "GB/s": round(dec_gbs, 1),
                              "hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4), "bytes": decode_bytes,
-                             "unique_kv_bytes": unique_bytes,
+                             "unique_kv_bytes": unique_bytes, "step_decode_bytes": step_decode_bytes,
                              "ms_inside_step": round(inline_decode_ms, 4),
                              "ms_caches_flushed": round(decode_cold_ms, 4),
                              "ms_caches_flushed_p10_p50_p90": decode_cold_pct,
@@ -559,8 +584,8 @@ def main():
                                "score_bytes": score_bytes,
                                "score_GB/s": round(score_bytes / (t_score * 1e-3) / 1e9, 1)}},
         "serving_loop": loop,
-        "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
+        "roofline": {"bound": "hbm", "achieved": round(rf_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(rf_gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
         "stream_read_ceiling": {"GB/s": round(ceiling_gbs, 1), "hbm_frac": round(ceiling_gbs / HBM_PEAK_GBS, 4),
                                 "bytes": args.ceiling_mib << 20,
                                 "decode_over_ceiling": round(dec_gbs / ceiling_gbs, 4),
