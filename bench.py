@@ -146,7 +146,9 @@ def main():
     bnd = i32(w.boundary)
     Rb = int(bnd.shape[0])
     max_cand = (w.max_pages - 1) * b
-    params = gp.Params(scale=float(np.float32(1 / math.sqrt(d))))
+    # (the selection runs after the scoring on one stream: the counts are final,
+    # so it may skip the requests that can only grow)
+    params = gp.Params(scale=float(np.float32(1 / math.sqrt(d))), select_skip_grows=1)
     counts = torch.zeros((Rb, Hkv, 2), dtype=torch.int32, device=dev)
     scores = torch.zeros((Rb, Hkv, max_cand), device=dev)
     decisions = torch.zeros(Rb, dtype=torch.int32, device=dev)

@@ -163,7 +163,9 @@ typedef struct {
  * tokens), compress_prob 0.7, shrink_threshold -0.005, min_capacity_pages 64
  * (1024 tokens).  draws: DEVICE [num_bnd] float32 uniform in [0, 1), one per
  * boundary request, read by GP_POLICY_RANDOM only (may be NULL otherwise).
- * layout: GP_LAYOUT_SHIFT (0, the method) or GP_LAYOUT_FILL. */
+ * layout: GP_LAYOUT_SHIFT (0, the method) or GP_LAYOUT_FILL.
+ * select_skip_grows: nonzero tells gp_boundary_select that k_counts are
+ * final when it runs (see the split calls below). */
 typedef struct {
     float beta_s, beta_l;
     float p;
@@ -180,6 +182,7 @@ typedef struct {
     float shrink_threshold;
     const float *draws;
     int32_t layout;              /* GP_LAYOUT_*                                 */
+    int32_t select_skip_grows;   /* gp_boundary_select only, see there          */
 } gp_params_t;
 
 /* Dual-timescale summaries (Sec. 3.2, EMA equation; App. E.1).
@@ -405,7 +408,20 @@ gp_status_t gp_boundary_apply(const gp_kv_layer_t *layers, int32_t n_layers,
  *  - select:  the eviction lists of every boundary request (selection needs
  *             only the scores) and the rows compaction will read.  Reads the
  *             page state, K/V and scores; writes only the workspace, so it may
- *             run beside decode attention.
+ *             run beside decode attention.  With params->select_skip_grows
+ *             != 0 the caller guarantees that k_counts are final (e.g. select
+ *             is stream-ordered after the scoring): select then also reads
+ *             k_counts and *free_count and skips the lists and rows of every
+ *             request whose decision can only be a grow -- it wants to grow
+ *             (the decision rule on its counts, as decide applies it), P_r <
+ *             max_pages, and *free_count - i * max_pages > reserve_pages for
+ *             its list index i, so that no earlier request of the event can
+ *             leave it short of a page.  No call may take pages from the free
+ *             stack between an event's select and its decide.  Should decide
+ *             nevertheless not grow such a request (counts changed after
+ *             select, the stack shrank), it preempts it instead (state
+ *             untouched, counted as PREEMPT).  gp_boundary_apply always skips
+ *             (its k_counts are inputs).
  *  - decide:  decisions, delta, counters, page allocation and table updates.
  *             With hold != 0 a request that compresses or shrinks is left HELD
  *             (seq_lens[r] = -(new m) - 1) so that a decode step launched while

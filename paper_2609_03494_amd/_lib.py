@@ -65,7 +65,8 @@ class _Params(ctypes.Structure):
                 ("k_loc", ctypes.c_int32), ("reserve_pages", ctypes.c_int32),
                 ("policy", ctypes.c_int32), ("metric", ctypes.c_int32), ("fixed_pages", ctypes.c_int32),
                 ("min_capacity_pages", ctypes.c_int32), ("compress_prob", ctypes.c_float),
-                ("shrink_threshold", ctypes.c_float), ("draws", ctypes.c_void_p), ("layout", ctypes.c_int32)]
+                ("shrink_threshold", ctypes.c_float), ("draws", ctypes.c_void_p), ("layout", ctypes.c_int32),
+                ("select_skip_grows", ctypes.c_int32)]
 
 
 _lib = None
@@ -202,6 +203,7 @@ class Params:
     shrink_threshold: float = -0.005
     draws: torch.Tensor | None = None   # [num_bnd] float32 on the device (RANDOM only)
     layout: int = 0                 # GP_LAYOUT_*
+    select_skip_grows: int = 0      # gp_boundary_select: k_counts are final (see the header)
 
     def c(self) -> _Params:
         if self.draws is not None and (self.draws.dtype != torch.float32 or not self.draws.is_contiguous()):
@@ -209,7 +211,7 @@ class Params:
         return _Params(self.beta_s, self.beta_l, self.p, self.tau, self.scale, self.rope_theta,
                        self.k_loc, self.reserve_pages, self.policy, self.metric, self.fixed_pages,
                        self.min_capacity_pages, self.compress_prob, self.shrink_threshold,
-                       _ptr(self.draws), self.layout)
+                       _ptr(self.draws), self.layout, self.select_skip_grows)
 
 
 def gp_workspace_bytes(op: int, num_reqs: int, num_bnd: int, num_q_heads: int, num_kv_heads: int,

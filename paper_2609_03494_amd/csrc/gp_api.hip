@@ -424,6 +424,8 @@ gp_status_t apply_call(const gp_kv_layer_t *layers, int32_t n_layers, const gp_p
     a.draws = params->draws;
     a.layout = params->layout;
     a.hold = hold;
+    // the whole apply takes its counts as inputs: they are final when it runs
+    a.skip_grows = stages == (kStageSelect | kStageDecide | kStageCompact) ? 1 : params->select_skip_grows != 0;
     LayerPtrs lp[kMaxLayers];
     for (int l = 0; l < n_layers; ++l) {
         lp[l].k = layers[l].k;

@@ -46,6 +46,30 @@ struct LayerTable {
 
 __device__ inline bool compressing(int dec) { return dec == GP_COMPRESS || dec == GP_FALLBACK; }
 
+// The action boundary request i (P >= 2 pages) wants (Sec. 3.2 aggregation
+// and threshold; the policy variants): grow, and under the Shrink policy
+// shrink.  D = sum over layers and KV heads of K^S - K^L; Delta = D / denom
+// with denom = |C| * Hkv * layers, and thresholds compare exactly as D
+// against t * denom (t is a float and denom < 2^29, so the product is exact
+// in fp64).  The decision and the selection's grow prediction both use it.
+__device__ inline void wanted_action(const ApplyArgs &a, int i, int P, long long D, bool &grow, bool &shrink,
+                                     float &dl) {
+    const long long denom = (long long)(P - 1) * kPage * a.Hkv * a.n_layers;
+    dl = (float)((double)D / (double)denom);
+    const bool above = (double)D > a.tau * (double)denom;      // Delta > tau
+    shrink = false;
+    switch (a.policy) {
+        case GP_POLICY_INVERSE: grow = !above; break;
+        case GP_POLICY_FIXED: grow = P < a.fixed_pages; break;
+        case GP_POLICY_RANDOM: grow = !(a.draws[i] < a.compress_prob); break;
+        case GP_POLICY_SHRINK:
+            grow = above;
+            shrink = (double)D < a.shrink_threshold * (double)denom && P - 1 >= max(a.min_cap, 2);
+            break;
+        default: grow = above; break;
+    }
+}
+
 // ----------------------------------------------------------------- select --
 // Per (boundary request, KV head, layer): every candidate page keeps its q
 // best tokens (score descending, slot ascending); the nev remaining candidates
@@ -238,6 +262,19 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
     const int x = blockIdx.y, i = blockIdx.z;
     const int h = blockIdx.x % a.Hkv, l = blockIdx.x / a.Hkv;
     const int tid = threadIdx.x;
+    __shared__ unsigned long long s_D;
+    __shared__ int s_fc;
+    // the request's counts and the free count (skip_grows only) are requested
+    // with the request index
+    long long dpart = 0;
+    if (a.skip_grows) {
+        for (int e = tid; e < a.n_layers * a.Hkv; e += blockDim.x) {
+            const int ll = e / a.Hkv, hh = e % a.Hkv;
+            const int32_t *kc = a.k_counts + (((size_t)ll * a.Rb + i) * a.Hkv + hh) * 2;
+            dpart += (long long)kc[0] - (long long)kc[1];
+        }
+        if (tid == 0) s_fc = *a.free_count;
+    }
     const int r = a.bnd[i];
     int P = 0;
     bool at_boundary = false;
@@ -248,8 +285,28 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
         at_boundary = (r >= 0) & (r < a.R) & (Pr >= 2) & (Pr <= a.max_pages) & (m == Pr * kPage);
         P = at_boundary ? Pr : 0;
     }
-    if (x == 0) {
+    // A request whose decision can only be a grow needs no eviction lists and
+    // no border rows: it wants to grow, has room for one more page, and even
+    // if every request before it in the list took max_pages pages the free
+    // stack would keep more than reserve_pages (the decision pops only; the
+    // stack can only have grown by the time it runs).
+    bool skip = false;
+    if (a.skip_grows) {
+        if (tid == 0) s_D = 0ull;
+        __syncthreads();
+        if (dpart != 0) atomicAdd(&s_D, (unsigned long long)dpart);
+        __syncthreads();
         if (at_boundary) {
+            bool grow, shrink;
+            float dl;
+            wanted_action(a, i, P, (long long)s_D, grow, shrink, dl);
+            const long long fc = min(max(s_fc, 0), a.pool_pages);
+            skip = grow && P < a.max_pages && fc - (long long)i * a.max_pages > (long long)a.reserve;
+        }
+    }
+    if (blockIdx.x == 0 && x == 0 && tid == 0) a.req[(size_t)i * RQ_STRIDE + RQ_SKIP] = skip ? 1 : 0;
+    if (x == 0) {
+        if (at_boundary && !skip) {
             select_tokens(a, i, h, l, P, kPage, 1, 0);
             if (a.policy == GP_POLICY_SHRINK && P - 1 >= max(a.min_cap, 2))
                 select_tokens(a, i, h, l, P, kShrinkEvict, 2, kPage);
@@ -276,7 +333,7 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
         if (tid == 0) a.nshc[(size_t)i * a.npc + col] = s_n;
     }
     // the fill layout never overwrites a row that another chunk still reads
-    if (!at_boundary || a.layout == GP_LAYOUT_FILL) return;
+    if (!at_boundary || skip || a.layout == GP_LAYOUT_FILL) return;
     // Border rows of the chunk boundaries cc in [col * kBordersPerGroup, +kBordersPerGroup)
     // (cc >= 1, below the resident length): the rows just below slot
     // cc * kCompactChunk that the chunk above may overwrite.  Rows move down
@@ -308,7 +365,7 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
 // ----------------------------------------------------------------- decide --
 // Flags per boundary request: bit 0 at a boundary, bit 1 wants to grow, bit 2
 // wants to shrink.
-enum { F_BOUNDARY = 1, F_GROW = 2, F_SHRINK = 4 };
+enum { F_BOUNDARY = 1, F_GROW = 2, F_SHRINK = 4, F_SKIPPED = 8 };
 
 __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
     __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
@@ -370,24 +427,7 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
                 flags = F_BOUNDARY;
                 bool grow, shrink = false;
                 if (P >= 2) {
-                    const long long D = (long long)s_D[i];
-                    // Delta = D / denom, denom = |C| * Hkv * layers.  Thresholds
-                    // compare exactly as D against t * denom: t is a float and
-                    // denom < 2^29, so the product is exact in fp64.
-                    const long long denom = (long long)(P - 1) * kPage * a.Hkv * a.n_layers;
-                    dl = (float)((double)D / (double)denom);
-                    const bool above = (double)D > a.tau * (double)denom;      // Delta > tau
-                    switch (a.policy) {
-                        case GP_POLICY_INVERSE: grow = !above; break;
-                        case GP_POLICY_FIXED: grow = P < a.fixed_pages; break;
-                        case GP_POLICY_RANDOM: grow = !(a.draws[i] < a.compress_prob); break;
-                        case GP_POLICY_SHRINK:
-                            grow = above;
-                            shrink = (double)D < a.shrink_threshold * (double)denom &&
-                                     P - 1 >= max(a.min_cap, 2);
-                            break;
-                        default: grow = above; break;
-                    }
+                    wanted_action(a, i, P, (long long)s_D[i], grow, shrink, dl);
                     nsh = s_nsh[i];
                     last_shared = a.shflag[(size_t)i * a.max_pages + P - 1];
                 } else {
@@ -395,6 +435,7 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
                 }
                 if (grow) flags |= F_GROW;
                 if (shrink) flags |= F_SHRINK;
+                if (a.req[(size_t)i * RQ_STRIDE + RQ_SKIP] != 0) flags |= F_SKIPPED;
             }
         }
         a.delta[i] = dl;
@@ -422,7 +463,9 @@ __global__ __launch_bounds__(1024) void decide_kernel(ApplyArgs a) {
                     dec = GP_GROW;
                     pop = popped;
                     popped += 1;
-                } else if (P <= 1 || nsh > avail) {
+                } else if (P <= 1 || nsh > avail || (fl & F_SKIPPED)) {
+                    // (a request the selection skipped as a certain grow has
+                    // no eviction lists: it is left as it is)
                     dec = GP_PREEMPT;
                 } else {
                     dec = shrink ? GP_SHRINK : (want ? GP_FALLBACK : GP_COMPRESS);

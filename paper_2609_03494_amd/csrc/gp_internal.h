@@ -112,7 +112,9 @@ struct ApplyWs {
 };
 
 // Per boundary request scratch (int32 fields).
-enum { RQ_R = 0, RQ_P, RQ_FLAGS, RQ_NSH, RQ_POP, RQ_DEC, RQ_STRIDE = 8 };
+// RQ_SKIP: written by the selection, 1 if it skipped the request as a
+// certain grow (its lists and border rows were not made).
+enum { RQ_R = 0, RQ_P, RQ_FLAGS, RQ_NSH, RQ_POP, RQ_DEC, RQ_SKIP, RQ_STRIDE = 8 };
 // Call header (int32): free count before pops, after pops, released pages.
 enum { HDR_FC0 = 0, HDR_FC1, HDR_NREL, HDR_SIZE = 4 };
 constexpr int kPageBlock = 1024;  // pages per work item when walking a page-table row
@@ -243,6 +245,7 @@ struct ApplyArgs {
     const float *draws;
     int layout;       // GP_LAYOUT_*
     int hold;         // mark compressing requests held (negative seq_len)
+    int skip_grows;   // the selection may skip requests whose decision can only be a grow
 };
 
 struct LayerPtrs {

@@ -4,6 +4,7 @@ gp_boundary_apply, held requests in decode attention, the step prologue
 (KV append + summaries) against the oracle, and whole multi-step loops run
 the asynchronous way on the GPU (compaction on a second stream beside the
 next step's decode) against the oracle's decode loop, step by step."""
+import dataclasses
 import math
 
 import numpy as np
@@ -43,18 +44,29 @@ def _bytes(t):
 
 # ------------------------------------------------------ split == apply --
 
-@pytest.mark.parametrize("case", ["tau0", "compress", "shrink_fill"])
+@pytest.mark.parametrize("case", ["tau0", "compress", "shrink_fill", "tau0_big_pool", "grow_big_pool",
+                                  "random_big_pool"])
 def test_split_calls_equal_apply(case):
     """select + decide + compact (hold 0), and with hold 1 then release, give
-    the bytes of one gp_boundary_apply."""
+    the bytes of one gp_boundary_apply; so does the split with the selection
+    told that the counts are final (it then skips the requests that can only
+    grow, as gp_boundary_apply always does).  With a big free pool most or
+    all grows are skipped; with 30 free pages none can be."""
+    big = case.endswith("big_pool")
     w = W.qwen3_8b(seed=7, num_reqs=12, len_lo=300, len_hi=4000, budget_choices=(8, 60, 200),
-                   boundary_frac=0.5, free_pages=30)
+                   boundary_frac=0.5, free_pages=5000 if big else 30)
+    Rb = len(w.boundary)
+    draws = torch.from_numpy(np.random.default_rng(3).random(Rb).astype(np.float32)).to(DEV)
     p = {"tau0": O.Params(), "compress": O.Params(tau=math.inf),
          "shrink_fill": O.Params(tau=math.inf, policy="shrink", shrink_threshold=10.0, min_capacity_pages=2,
-                                 layout="fill")}[case]
+                                 layout="fill"),
+         "tau0_big_pool": O.Params(), "grow_big_pool": O.Params(tau=-math.inf),
+         "random_big_pool": O.Params(policy="random", compress_prob=0.5)}[case]
     gparams = library_params(p, w.head_dim)
+    if case == "random_big_pool":
+        gparams = dataclasses.replace(gparams, draws=draws)
     results = []
-    for mode in ("apply", "split", "split_hold"):
+    for mode in ("apply", "split", "split_hold", "split_skip"):
         _say(f"split: {case}, {mode}")
         dc = DeviceCase(w)
         Rb = len(w.boundary)
@@ -72,7 +84,8 @@ def test_split_calls_equal_apply(case):
         dec = torch.full((Rb,), -1, dtype=torch.int32, device=DEV)
         delta = torch.zeros(Rb, device=DEV)
         ctr = torch.zeros(4, dtype=torch.int64, device=DEV)
-        args = (dc.layers, dc.ps, bnd, counts, scores, gparams, dec, delta, ctr, ws_a)
+        mp = dataclasses.replace(gparams, select_skip_grows=1) if mode == "split_skip" else gparams
+        args = (dc.layers, dc.ps, bnd, counts, scores, mp, dec, delta, ctr, ws_a)
         if mode == "apply":
             gp.gp_boundary_apply(*args)
         else:
@@ -96,6 +109,45 @@ def test_split_calls_equal_apply(case):
     for other in results[1:]:
         for n, a, b in zip(names, results[0], other):
             assert a == b, f"{case}: {n} differs from gp_boundary_apply"
+
+
+def test_skipped_request_that_does_not_grow_is_preempted():
+    """The selection skips requests whose counts say they grow (a big free
+    pool); if the decision then gets counts that say compress -- the caller
+    broke the contract that the counts are final -- every skipped request is
+    preempted: decisions PREEMPT, counters [0, 0, 0, Rb], and the page state
+    and the cache rows untouched by the decision and the compaction."""
+    w = W.qwen3_8b(seed=9, num_reqs=10, len_lo=300, len_hi=3000, budget_choices=(8, 60, 200),
+                   boundary_frac=0.5, free_pages=5000)
+    dc = DeviceCase(w)
+    Rb = len(w.boundary)
+    gparams = dataclasses.replace(library_params(O.Params(), w.head_dim), select_skip_grows=1)
+    bnd = torch.from_numpy(w.boundary.astype(np.int32)).to(DEV)
+    max_cand = (w.max_pages - 1) * w.page_size
+    grow_counts = torch.zeros((1, Rb, w.num_kv_heads, 2), dtype=torch.int32, device=DEV)
+    grow_counts[..., 0] = 16                      # K^S > K^L: Delta > 0, wants to grow
+    compress_counts = grow_counts.flip(-1).contiguous()   # K^S < K^L: wants to compress
+    scores = torch.rand((1, Rb, w.num_kv_heads, max_cand), device=DEV)
+    ws_a = gp.workspace(gp.GP_OP_APPLY, w.num_reqs, Rb, w.num_q_heads, w.num_kv_heads, w.head_dim,
+                        w.max_pages, torch_dtype(w))
+    dec = torch.full((Rb,), -1, dtype=torch.int32, device=DEV)
+    delta = torch.zeros(Rb, device=DEV)
+    ctr = torch.zeros(4, dtype=torch.int64, device=DEV)
+    before = [_bytes(t) for t in (dc.ps.page_table, dc.ps.num_pages, dc.ps.seq_lens, dc.ps.refcount,
+                                  dc.ps.free_list, dc.ps.free_count, dc.layers[0].k, dc.layers[0].v)]
+    _say("skip safety: select with grow counts, decide and compact with compress counts")
+    gp.gp_boundary_select(dc.layers, dc.ps, bnd, grow_counts, scores, gparams, dec, delta, ctr, ws_a)
+    args = (dc.layers, dc.ps, bnd, compress_counts, scores, gparams, dec, delta, ctr, ws_a)
+    gp.gp_boundary_decide(*args, hold=False)
+    gp.gp_boundary_compact(*args)
+    torch.cuda.synchronize()
+    assert (dec.cpu().numpy() == gp.GP_PREEMPT).all()
+    assert ctr.cpu().numpy().tolist() == [0, 0, 0, Rb]
+    after = [_bytes(t) for t in (dc.ps.page_table, dc.ps.num_pages, dc.ps.seq_lens, dc.ps.refcount,
+                                 dc.ps.free_list, dc.ps.free_count, dc.layers[0].k, dc.layers[0].v)]
+    names = ("page_table", "num_pages", "seq_lens", "refcount", "free_list", "free_count", "k", "v")
+    for n, a, b in zip(names, before, after):
+        assert a == b, f"{n} changed"
 
 
 # ------------------------------------------------------- held requests --
