@@ -82,10 +82,12 @@ __device__ inline void wanted_action(const ApplyArgs &a, int i, int P, long long
 // pass a histogram of the keys that share the prefix found so far, scanned by
 // wave 0.  The two slot digits are only resolved when candidates tie on the
 // threshold score and not all of them are evicted.  Each thread keeps the
-// scores of its first two pages in registers and re-reads the rest.
-constexpr int kSelThreads = 1024;
-constexpr int kSelCached = 2;                           // pages per thread held in registers
-constexpr int kSelMaxPages = 4 * kSelThreads;
+// scores of its first page in registers and re-reads the rest (masks in
+// LDS).  The workgroup is one wave per SIMD at no more than 128 registers, so
+// that it starts where a decode attention workgroup has retired.
+constexpr int kSelThreads = 256;
+constexpr int kSelCached = 1;                           // pages per thread held in registers
+constexpr int kSelMaxPages = 16 * kSelThreads;
 
 __device__ inline void load_page_scores(const float *s, int j, uint32_t (&v)[kPage]) {
 #pragma unroll
@@ -104,32 +106,55 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
     const int q = Kt > 0 ? min(a.k_loc, Kt / (P - 1)) : 0;
     const float *s = a.scores + (((size_t)l * a.Rb + i) * a.Hkv + h) * a.max_cand;
 
+    // the first kSelCached pages of this thread stay in registers with their
+    // keep masks; the others (long candidate sets) are re-read in every pass,
+    // their masks kept in LDS
+    __shared__ uint16_t s_keep[kSelMaxPages];
     uint32_t cache[kSelCached][kPage];
-    uint32_t keep[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int j = tid + u * kSelThreads;
-        uint32_t v[kPage];
+    uint32_t keep_c[kSelCached];
+    auto keep_mask = [&](const uint32_t (&v)[kPage]) {
         uint32_t mask = 0;
-        if (j < npages) {
-            load_page_scores(s, j, v);
 #pragma unroll
-            for (int t = 0; t < kPage; ++t) {
-                int rank = 0;
+        for (int t = 0; t < kPage; ++t) {
+            int rank = 0;
 #pragma unroll
-                for (int w = 0; w < kPage; ++w) {
-                    const float x = __uint_as_float(v[w]), y = __uint_as_float(v[t]);
-                    rank += (x > y || (x == y && w < t)) ? 1 : 0;
-                }
-                mask |= (rank < q ? 1u : 0u) << t;
+            for (int w = 0; w < kPage; ++w) {
+                const float x = __uint_as_float(v[w]), y = __uint_as_float(v[t]);
+                rank += (x > y || (x == y && w < t)) ? 1 : 0;
             }
+            mask |= (rank < q ? 1u : 0u) << t;
         }
-        keep[u] = mask;
-        if (u < kSelCached) {
+        return mask;
+    };
 #pragma unroll
-            for (int t = 0; t < kPage; ++t) cache[u < kSelCached ? u : 0][t] = v[t];
+    for (int u = 0; u < kSelCached; ++u) {
+        const int j = tid + u * kSelThreads;
+        keep_c[u] = 0;
+        if (j < npages) {
+            load_page_scores(s, j, cache[u]);
+            keep_c[u] = keep_mask(cache[u]);
         }
     }
+#pragma unroll 1
+    for (int j = tid + kSelCached * kSelThreads; j < npages; j += kSelThreads) {
+        uint32_t v[kPage];
+        load_page_scores(s, j, v);
+        s_keep[j] = (uint16_t)keep_mask(v);
+    }
+    // every candidate page of this thread: fn(page, its 16 scores, keep mask)
+    auto visit = [&](auto &&fn) {
+#pragma unroll
+        for (int u = 0; u < kSelCached; ++u) {
+            const int j = tid + u * kSelThreads;
+            if (j < npages) fn(j, cache[u], keep_c[u]);
+        }
+#pragma unroll 1
+        for (int j = tid + kSelCached * kSelThreads; j < npages; j += kSelThreads) {
+            uint32_t v[kPage];
+            load_page_scores(s, j, v);
+            fn(j, v, (uint32_t)s_keep[j]);
+        }
+    };
 
     // the 48-bit key has 6 digits: 4 of the score, 2 of the inverted slot
     unsigned long long prefix = 0;
@@ -139,25 +164,15 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
         const int sh = 40 - 8 * pass;
         for (int b = tid; b < NB; b += blockDim.x) s_hist[b] = 0;
         __syncthreads();
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int j = tid + u * kSelThreads;
-            if (j >= npages) continue;
-            uint32_t v[kPage];
-            if (u < kSelCached) {
-#pragma unroll
-                for (int t = 0; t < kPage; ++t) v[t] = cache[u < kSelCached ? u : 0][t];
-            } else {
-                load_page_scores(s, j, v);
-            }
+        visit([&](int j, const uint32_t (&v)[kPage], uint32_t keep) {
 #pragma unroll
             for (int t = 0; t < kPage; ++t) {
-                if (keep[u] & (1u << t)) continue;
+                if (keep & (1u << t)) continue;
                 const unsigned long long key = ((unsigned long long)v[t] << 16) |
                                                (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
                 if ((key >> (sh + 8)) == prefix) atomicAdd(&s_hist[(key >> sh) & 0xff], 1u);
             }
-        }
+        });
         __syncthreads();
         if (tid < 64) {
             // lane owns 4 consecutive buckets, lane 0 the lowest
@@ -205,20 +220,10 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
     if (tid == 0) s_nev = 0;
     if (tid < kShrinkEvict) s_ev[tid] = -1;
     __syncthreads();
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int j = tid + u * kSelThreads;
-        if (j >= npages) continue;
-        uint32_t v[kPage];
-        if (u < kSelCached) {
-#pragma unroll
-            for (int t = 0; t < kPage; ++t) v[t] = cache[u < kSelCached ? u : 0][t];
-        } else {
-            load_page_scores(s, j, v);
-        }
+    visit([&](int j, const uint32_t (&v)[kPage], uint32_t keep) {
 #pragma unroll
         for (int t = 0; t < kPage; ++t) {
-            if (keep[u] & (1u << t)) continue;
+            if (keep & (1u << t)) continue;
             const unsigned long long key = ((unsigned long long)v[t] << 16) |
                                            (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
             if (key <= hi) {
@@ -226,7 +231,7 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
                 if (at < nev) s_ev[at] = j * kPage + t;
             }
         }
-    }
+    });
     __syncthreads();
     if (tid == 0) {
         int ev[kShrinkEvict];
@@ -256,7 +261,7 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
 
 // -------------------------------------------------------------------- pre --
 template <int D, int E>
-__global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
+__global__ __launch_bounds__(kSelThreads) __attribute__((amdgpu_waves_per_eu(4))) void pre_kernel(ApplyArgs a, LayerTable lt) {
     __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     __shared__ int s_n;
     const int x = blockIdx.y, i = blockIdx.z;
@@ -319,8 +324,7 @@ __global__ __launch_bounds__(1024) void pre_kernel(ApplyArgs a, LayerTable lt) {
         // shared pages of block col of the table row, as the call starts
         if (tid == 0) s_n = 0;
         __syncthreads();
-        const int j = col * kPageBlock + tid;
-        if (j < a.max_pages) {
+        for (int j = col * kPageBlock + tid; j < min((col + 1) * kPageBlock, a.max_pages); j += blockDim.x) {
             int shared = 0;
             if (at_boundary && j < P) {
                 const int pid = row[j];
@@ -739,7 +743,7 @@ hipError_t launch_de(const ApplyArgs &a, const LayerTable &lt, int stages, hipSt
     // (KV head, layer) is the fastest grid index: each head stays on one XCD
     dim3 gpre(a.Hkv * a.n_layers, 1 + max(a.npc, cdiv(a.ncc, kBordersPerGroup)), a.Rb),
         gcomp(2 * a.Hkv * a.n_layers, a.ncc, a.Rb);
-    if (stages & kStageSelect) pre_kernel<D, E><<<gpre, 1024, 0, s>>>(a, lt);
+    if (stages & kStageSelect) pre_kernel<D, E><<<gpre, kSelThreads, 0, s>>>(a, lt);
     if (stages & kStageDecide) decide_kernel<<<1, 1024, 0, s>>>(a);
     if (stages & kStageCompact) compact_kernel<D, E><<<gcomp, 256, 0, s>>>(a, lt);
     return hipGetLastError();
