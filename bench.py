@@ -10,10 +10,11 @@ in HBM before timing starts.  The step is captured as a HIP graph and
 replayed (``--graph-steps S`` captures S consecutive steps per graph;
 ``--eager`` launches every call directly).  Decode attention reads
 a snapshot of the request metadata (written by the restore, in the same
-launch), so the summary update, scoring, selection and the decision (which
-updates the live metadata) run on a second stream beside it; the compaction,
-which moves cached rows, waits for both (``--serial`` runs everything on one
-stream, decode on the live metadata).
+launch), so scoring, selection and the decision (which updates the live
+metadata) run on a second stream beside it; the summary update runs before
+the fork (``--layout``); the compaction, which moves cached rows, waits for
+both (``--serial`` runs everything on one stream, decode on the live
+metadata).
 
 Prints one JSON line.  ``value`` is GB/s of the every-step traffic (summaries
 and decode attention, algorithmic bytes) over the whole step's time, boundary
@@ -77,7 +78,7 @@ def parse():
     ap.add_argument("--eager", action="store_true", help="launch every call directly (no HIP graphs)")
     ap.add_argument("--graph-steps", type=int, default=1,
                     help="steps captured per HIP graph (a divisor of --steps is used)")
-    ap.add_argument("--layout", default="boundary-first",
+    ap.add_argument("--layout", default="summaries-first",
                     choices=["boundary-first", "decode-first", "summaries-first"],
                     help="capture order of the two branches of a step (see step())")
     ap.add_argument("--serial", action="store_true",
