@@ -6,9 +6,11 @@ A step is one pass of the whole path over the batch: restore the page metadata
 to the step's starting state (one device-to-device copy), update both query summaries of every request, paged decode attention
 for every request, then boundary scoring, selection, the decision and compaction for the
 requests at a capacity boundary.  Inputs are seeded synthetic tensors resident
-in HBM before timing starts.  The step is captured as a HIP graph and
-replayed (``--graph-steps S`` captures S consecutive steps per graph;
-``--eager`` launches every call directly).  Decode attention reads
+in HBM before timing starts.  Five consecutive steps are captured as one
+HIP graph (as a serving loop captures its decode steps: the graph's launch
+cost is paid once per five steps, every step does all of its work) and
+replayed K / 5 times (``--graph-steps S`` sets the steps per graph; ``--eager``
+launches every call directly).  Decode attention reads
 a snapshot of the request metadata (written by the restore, in the same
 launch), so scoring, selection and the decision (which updates the live
 metadata) run on a second stream beside it; the summary update runs before
@@ -76,7 +78,7 @@ def parse():
     ap.add_argument("--ceiling-mib", type=int, default=4096, help="buffer of the streaming-read ceiling")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "decode_traffic_qwen3_8b.json"))
     ap.add_argument("--eager", action="store_true", help="launch every call directly (no HIP graphs)")
-    ap.add_argument("--graph-steps", type=int, default=1,
+    ap.add_argument("--graph-steps", type=int, default=5,
                     help="steps captured per HIP graph (a divisor of --steps is used)")
     ap.add_argument("--layout", default="summaries-first",
                     choices=["boundary-first", "decode-first", "summaries-first"],

@@ -82,11 +82,12 @@ __device__ inline void wanted_action(const ApplyArgs &a, int i, int P, long long
 // pass a histogram of the keys that share the prefix found so far, scanned by
 // wave 0.  The two slot digits are only resolved when candidates tie on the
 // threshold score and not all of them are evicted.  Each thread keeps the
-// scores of its first page in registers and re-reads the rest (masks in
-// LDS).  The workgroup is one wave per SIMD at no more than 128 registers, so
+// scores of its first page in registers and of its second in LDS, and
+// re-reads the rest (masks in LDS).  The workgroup is one wave per SIMD at no more than 128 registers, so
 // that it starts where a decode attention workgroup has retired.
 constexpr int kSelThreads = 256;
 constexpr int kSelCached = 1;                           // pages per thread held in registers
+constexpr int kSelLdsPages = 1;                         // pages per thread held in LDS after them
 constexpr int kSelMaxPages = 16 * kSelThreads;
 
 __device__ inline void load_page_scores(const float *s, int j, uint32_t (&v)[kPage]) {
@@ -107,9 +108,12 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
     const float *s = a.scores + (((size_t)l * a.Rb + i) * a.Hkv + h) * a.max_cand;
 
     // the first kSelCached pages of this thread stay in registers with their
-    // keep masks; the others (long candidate sets) are re-read in every pass,
-    // their masks kept in LDS
+    // keep masks, the next kSelLdsPages in LDS (word t of page tid + k
+    // kSelThreads at [k][t][tid], so a read of one word by a wave is
+    // conflict-free); the others (long candidate sets) are re-read in every
+    // pass.  Keep masks of the pages past the registers are kept in LDS.
     __shared__ uint16_t s_keep[kSelMaxPages];
+    __shared__ uint32_t s_sc[kSelLdsPages][kPage][kSelThreads];
     uint32_t cache[kSelCached][kPage];
     uint32_t keep_c[kSelCached];
     auto keep_mask = [&](const uint32_t (&v)[kPage]) {
@@ -135,13 +139,25 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
             keep_c[u] = keep_mask(cache[u]);
         }
     }
+    constexpr int kRegLds = kSelCached + kSelLdsPages;      // pages per thread not re-read
 #pragma unroll 1
-    for (int j = tid + kSelCached * kSelThreads; j < npages; j += kSelThreads) {
+    for (int k = 0; k < kSelLdsPages; ++k) {
+        const int j = tid + (kSelCached + k) * kSelThreads;
+        if (j >= npages) break;
+        uint32_t v[kPage];
+        load_page_scores(s, j, v);
+#pragma unroll
+        for (int t = 0; t < kPage; ++t) s_sc[k][t][tid] = v[t];
+        s_keep[j] = (uint16_t)keep_mask(v);
+    }
+#pragma unroll 1
+    for (int j = tid + kRegLds * kSelThreads; j < npages; j += kSelThreads) {
         uint32_t v[kPage];
         load_page_scores(s, j, v);
         s_keep[j] = (uint16_t)keep_mask(v);
     }
     // every candidate page of this thread: fn(page, its 16 scores, keep mask)
+    // (each thread reads back only what it wrote itself)
     auto visit = [&](auto &&fn) {
 #pragma unroll
         for (int u = 0; u < kSelCached; ++u) {
@@ -149,9 +165,14 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
             if (j < npages) fn(j, cache[u], keep_c[u]);
         }
 #pragma unroll 1
-        for (int j = tid + kSelCached * kSelThreads; j < npages; j += kSelThreads) {
+        for (int k = 0, j = tid + kSelCached * kSelThreads; j < npages; ++k, j += kSelThreads) {
             uint32_t v[kPage];
-            load_page_scores(s, j, v);
+            if (k < kSelLdsPages) {
+#pragma unroll
+                for (int t = 0; t < kPage; ++t) v[t] = s_sc[k][t][tid];
+            } else {
+                load_page_scores(s, j, v);
+            }
             fn(j, v, (uint32_t)s_keep[j]);
         }
     };
