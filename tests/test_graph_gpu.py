@@ -1,5 +1,6 @@
 """The decode step captured in HIP graphs gives the same bytes as eager calls,
 on every replay, with eager work and synchronisations between replays."""
+import dataclasses
 import math
 
 import numpy as np
@@ -13,19 +14,22 @@ from _harness import DeviceCase
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("fork", [False, True, "bench"], ids=["one_stream", "score_on_side_stream",
-                                                         "bench_step_layout"])
-def test_graph_replays_match_eager(fork):
-    """fork="bench" is the benchmark's step: decode attention reads a snapshot
-    of the request metadata while the summary update, scoring, selection and
-    the decision run on a side stream beside it, then the compaction; its eager
-    result must also equal the plain one-stream sequence."""
+@pytest.mark.parametrize("fork,free", [(False, 40), (True, 40), ("bench", 40), ("bench", 5000)],
+                         ids=["one_stream", "score_on_side_stream", "bench_step_layout",
+                              "bench_step_layout_big_pool"])
+def test_graph_replays_match_eager(fork, free):
+    """fork="bench" is the benchmark's step: after the summary update, decode
+    attention reads a snapshot of the request metadata while scoring, the
+    selection (told that the counts are final, so it skips the certain grows;
+    with the big pool it does) and the decision run on a side stream beside
+    it, then the compaction; its eager result must also equal the plain
+    one-stream sequence."""
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     import paper_2609_03494_amd as gp
     print(f"graph: capture decode + boundary step of a reduced Qwen3-8B batch, fork={fork}", flush=True)
     w = W.qwen3_8b(seed=17, num_reqs=10, len_lo=200, len_hi=3000, budget_choices=(20, 100, 200),
-                   boundary_frac=0.4, free_pages=40)
+                   boundary_frac=0.4, free_pages=free)
     dc = DeviceCase(w)
     p32 = O.Params().as_f32(w.head_dim)
     params = gp.Params(p32.beta_s, p32.beta_l, p32.p, p32.tau, p32.scale, p32.rope_theta, p32.k_loc, 0)
@@ -62,21 +66,26 @@ def test_graph_replays_match_eager(fork):
                                                                 dc.ps.seq_lens))
     ps_dec = gp.PageState(snap_pt, snap_np, snap_sl, dc.ps.refcount, dc.ps.free_list, dc.ps.free_count)
 
+    # the selection runs after the scoring on the side stream: the counts are
+    # final, so it may skip the requests that can only grow
+    bargs_skip = (dc.layers, dc.ps, bnd, counts, scores, dataclasses.replace(params, select_skip_grows=1), dec,
+                  delta, ctr, ws_a)
+
     def step_bench():
         reset()
         cur = torch.cuda.current_stream()
         for t, t0 in ((snap_pt, dc.ps.page_table), (snap_np, dc.ps.num_pages), (snap_sl, dc.ps.seq_lens)):
             torch.mul(t0, 1, out=t)
+        gp.gp_update_summaries(dc.q_pre, dc.slot_ids, init, dc.qstate, p32.beta_s, p32.beta_l)
         aux.wait_stream(cur)
+        gp.gp_decode_attention(dc.layers[0], ps_dec, dc.q_post, p32.scale, out, dc.ws_decode)
         with torch.cuda.stream(aux):
-            gp.gp_update_summaries(dc.q_pre, dc.slot_ids, init, dc.qstate, p32.beta_s, p32.beta_l)
             gp.gp_boundary_score(dc.layers[0], dc.ps, dc.q_pre, dc.qstate, dc.slot_ids, dc.positions,
                                  bnd, params, counts, scores, ws_s)
-            gp.gp_boundary_select(*bargs)
-            gp.gp_boundary_decide(*bargs, hold=False)      # updates the live metadata only
-        gp.gp_decode_attention(dc.layers[0], ps_dec, dc.q_post, p32.scale, out, dc.ws_decode)
+            gp.gp_boundary_select(*bargs_skip)
+            gp.gp_boundary_decide(*bargs_skip, hold=False)      # updates the live metadata only
         cur.wait_stream(aux)
-        gp.gp_boundary_compact(*bargs)
+        gp.gp_boundary_compact(*bargs_skip)
 
     def step():
         if fork == "bench":
