@@ -72,52 +72,74 @@ __device__ inline void wanted_action(const ApplyArgs &a, int i, int P, long long
 
 // ----------------------------------------------------------------- select --
 // Per (boundary request, KV head, layer): every candidate page keeps its q
-// best tokens (score descending, slot ascending); the nev remaining candidates
-// that come last in that order are evicted (nev = 16 for Compress & Hold, 32
+// best tokens (score descending, slot ascending); the NEV remaining candidates
+// that come last in that order are evicted (NEV = 16 for Compress & Hold, 32
 // for a shrink, which keeps K_t = (P - 1 - drop) * 16 tokens).
 // Eviction order is the ascending order of the 48-bit key
 // (score bits << 16) | (0xffff - slot): scores are non-negative floats, so
-// their bit patterns sort like their values, and a later slot loses a tie.
-// The nev-th smallest key is found by a radix select over 8-bit digits, each
-// pass a histogram of the keys that share the prefix found so far, scanned by
-// wave 0.  The two slot digits are only resolved when candidates tie on the
-// threshold score and not all of them are evicted.  Each thread keeps the
-// scores of its first page in registers and of its second in LDS, and
-// re-reads the rest (masks in LDS).  The workgroup is one wave per SIMD at no more than 128 registers, so
-// that it starts where a decode attention workgroup has retired.
+// their bit patterns sort like their values, and a later slot loses a tie;
+// keys are distinct, so the NEV smallest are one set.  They are found by
+// merging sorted lists, with no atomics and one read of every score: each
+// thread sorts the candidates of each of its pages (a sorting network over
+// the 16 keys, kept tokens as the largest key) and keeps the NEV smallest of
+// its pages; the lanes of a wave then merge their lists pairwise over six
+// exchange rounds (each merge keeps the NEV smallest of two sorted lists: the
+// element-wise minimum of one list and the other reversed, then a bitonic
+// clean-up), and wave 0 merges the waves' lists.  The workgroup is one wave
+// per SIMD at no more than 128 registers, so that it starts where a decode
+// attention workgroup has retired.
 constexpr int kSelThreads = 256;
-constexpr int kSelCached = 1;                           // pages per thread held in registers
-constexpr int kSelLdsPages = 1;                         // pages per thread held in LDS after them
 constexpr int kSelMaxPages = 16 * kSelThreads;
+constexpr unsigned long long kNoKey = ~0ull;
 
 __device__ inline void load_page_scores(const float *s, int j, uint32_t (&v)[kPage]) {
 #pragma unroll
     for (int t = 0; t < kPage; ++t) v[t] = __float_as_uint(s[j * kPage + t]);
 }
 
-__device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, int nev, int drop,
-                              int out_offset) {
-    constexpr int NB = 256;
-    __shared__ unsigned int s_hist[NB];
-    __shared__ int s_bucket, s_below, s_in_bucket, s_nev;
-    __shared__ int s_ev[kShrinkEvict];
-    const int tid = threadIdx.x, lane = tid & 63;
+__device__ inline void cas_asc(unsigned long long &x, unsigned long long &y) {
+    const unsigned long long lo = x < y ? x : y, hi = x < y ? y : x;
+    x = lo;
+    y = hi;
+}
+
+// c (a bitonic sequence of N keys) sorted ascending
+template <int N>
+__device__ inline void bitonic_clean(unsigned long long (&c)[N]) {
+#pragma unroll
+    for (int st = N / 2; st > 0; st >>= 1)
+#pragma unroll
+        for (int x = 0; x < N; ++x)
+            if ((x & st) == 0) cas_asc(c[x], c[x + st]);
+}
+
+// a := the N smallest keys of a and b (both sorted ascending), sorted ascending
+template <int N>
+__device__ inline void merge_keep(unsigned long long (&a)[N], const unsigned long long (&b)[N]) {
+#pragma unroll
+    for (int k = 0; k < N; ++k) a[k] = a[k] < b[N - 1 - k] ? a[k] : b[N - 1 - k];
+    bitonic_clean<N>(a);
+}
+
+template <int NEV>
+__device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, int drop, int out_offset) {
+    constexpr int NW = kSelThreads / 64;
+    __shared__ unsigned long long s_wl[NW][NEV];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int npages = min(P - 1, kSelMaxPages);
     const int Kt = (P - 1 - drop) * kPage;
     const int q = Kt > 0 ? min(a.k_loc, Kt / (P - 1)) : 0;
     const float *s = a.scores + (((size_t)l * a.Rb + i) * a.Hkv + h) * a.max_cand;
 
-    // the first kSelCached pages of this thread stay in registers with their
-    // keep masks, the next kSelLdsPages in LDS (word t of page tid + k
-    // kSelThreads at [k][t][tid], so a read of one word by a wave is
-    // conflict-free); the others (long candidate sets) are re-read in every
-    // pass.  Keep masks of the pages past the registers are kept in LDS.
-    __shared__ uint16_t s_keep[kSelMaxPages];
-    __shared__ uint32_t s_sc[kSelLdsPages][kPage][kSelThreads];
-    uint32_t cache[kSelCached][kPage];
-    uint32_t keep_c[kSelCached];
-    auto keep_mask = [&](const uint32_t (&v)[kPage]) {
-        uint32_t mask = 0;
+    unsigned long long best[NEV];
+#pragma unroll
+    for (int k = 0; k < NEV; ++k) best[k] = kNoKey;
+#pragma unroll 1
+    for (int j = tid; j < npages; j += kSelThreads) {
+        uint32_t v[kPage];
+        load_page_scores(s, j, v);
+        // the page's candidates: its q best tokens are kept (no key)
+        unsigned long long pk[NEV];
 #pragma unroll
         for (int t = 0; t < kPage; ++t) {
             int rank = 0;
@@ -126,146 +148,57 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
                 const float x = __uint_as_float(v[w]), y = __uint_as_float(v[t]);
                 rank += (x > y || (x == y && w < t)) ? 1 : 0;
             }
-            mask |= (rank < q ? 1u : 0u) << t;
+            pk[t] = rank < q ? kNoKey
+                             : ((unsigned long long)v[t] << 16) | (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
         }
-        return mask;
-    };
 #pragma unroll
-    for (int u = 0; u < kSelCached; ++u) {
-        const int j = tid + u * kSelThreads;
-        keep_c[u] = 0;
-        if (j < npages) {
-            load_page_scores(s, j, cache[u]);
-            keep_c[u] = keep_mask(cache[u]);
-        }
-    }
-    constexpr int kRegLds = kSelCached + kSelLdsPages;      // pages per thread not re-read
-#pragma unroll 1
-    for (int k = 0; k < kSelLdsPages; ++k) {
-        const int j = tid + (kSelCached + k) * kSelThreads;
-        if (j >= npages) break;
-        uint32_t v[kPage];
-        load_page_scores(s, j, v);
+        for (int t = kPage; t < NEV; ++t) pk[t] = kNoKey;
+        // sort the page's 16 keys ascending (the padding is already largest)
 #pragma unroll
-        for (int t = 0; t < kPage; ++t) s_sc[k][t][tid] = v[t];
-        s_keep[j] = (uint16_t)keep_mask(v);
-    }
-#pragma unroll 1
-    for (int j = tid + kRegLds * kSelThreads; j < npages; j += kSelThreads) {
-        uint32_t v[kPage];
-        load_page_scores(s, j, v);
-        s_keep[j] = (uint16_t)keep_mask(v);
-    }
-    // every candidate page of this thread: fn(page, its 16 scores, keep mask)
-    // (each thread reads back only what it wrote itself)
-    auto visit = [&](auto &&fn) {
+        for (int k = 2; k <= kPage; k <<= 1)
 #pragma unroll
-        for (int u = 0; u < kSelCached; ++u) {
-            const int j = tid + u * kSelThreads;
-            if (j < npages) fn(j, cache[u], keep_c[u]);
-        }
-#pragma unroll 1
-        for (int k = 0, j = tid + kSelCached * kSelThreads; j < npages; ++k, j += kSelThreads) {
-            uint32_t v[kPage];
-            if (k < kSelLdsPages) {
+            for (int jj = k >> 1; jj > 0; jj >>= 1)
 #pragma unroll
-                for (int t = 0; t < kPage; ++t) v[t] = s_sc[k][t][tid];
-            } else {
-                load_page_scores(s, j, v);
-            }
-            fn(j, v, (uint32_t)s_keep[j]);
-        }
-    };
-
-    // the 48-bit key has 6 digits: 4 of the score, 2 of the inverted slot
-    unsigned long long prefix = 0;
-    int need = nev;
-    int digits = 0;
-    for (int pass = 0; pass < 6; ++pass) {
-        const int sh = 40 - 8 * pass;
-        for (int b = tid; b < NB; b += blockDim.x) s_hist[b] = 0;
-        __syncthreads();
-        visit([&](int j, const uint32_t (&v)[kPage], uint32_t keep) {
-#pragma unroll
-            for (int t = 0; t < kPage; ++t) {
-                if (keep & (1u << t)) continue;
-                const unsigned long long key = ((unsigned long long)v[t] << 16) |
-                                               (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
-                if ((key >> (sh + 8)) == prefix) atomicAdd(&s_hist[(key >> sh) & 0xff], 1u);
-            }
-        });
-        __syncthreads();
-        if (tid < 64) {
-            // lane owns 4 consecutive buckets, lane 0 the lowest
-            const unsigned int c0 = s_hist[4 * lane], c1 = s_hist[4 * lane + 1];
-            const unsigned int c2 = s_hist[4 * lane + 2], c3 = s_hist[4 * lane + 3];
-            const unsigned int cc = c0 + c1 + c2 + c3;
-            unsigned int ic = cc;
-            for (int off = 1; off < 64; off <<= 1) {
-                const unsigned int y = __shfl_up(ic, off, 64);
-                if (lane >= off) ic += y;
-            }
-            const unsigned int ec = ic - cc;
-            if (ec < (unsigned)need && ic >= (unsigned)need) {
-                const unsigned int cs[4] = {c0, c1, c2, c3};
-                unsigned int cum = ec;
-                for (int k = 0; k < 4; ++k) {
-                    if (cum + cs[k] >= (unsigned)need) {
-                        s_bucket = 4 * lane + k;
-                        s_below = (int)cum;
-                        s_in_bucket = (int)cs[k];
-                        break;
+                for (int x = 0; x < kPage; ++x) {
+                    const int y = x ^ jj;
+                    if (y > x) {
+                        if ((x & k) == 0) cas_asc(pk[x], pk[y]);
+                        else cas_asc(pk[y], pk[x]);
                     }
-                    cum += cs[k];
                 }
-            }
-            if (lane == 63 && ic < (unsigned)need) {   // fewer candidates than nev
-                s_bucket = NB - 1;
-                s_below = (int)ic;
-                s_in_bucket = 0;
-            }
-        }
-        __syncthreads();
-        need -= s_below;
-        prefix = (prefix << 8) | (unsigned long long)s_bucket;
-        const int in_bucket = s_in_bucket;
-        digits = pass + 1;
-        __syncthreads();
-        // every key in the bucket is evicted: no later digit is needed
-        if (in_bucket == need) break;
+        merge_keep<NEV>(best, pk);
     }
-    const int rest = 48 - 8 * digits;      // key bits not fixed by the prefix
-    const unsigned long long hi = ((prefix + 1ull) << rest) - 1ull;   // largest key in the bucket
-
-    // evict every candidate whose key is at most the threshold
-    if (tid == 0) s_nev = 0;
-    if (tid < kShrinkEvict) s_ev[tid] = -1;
-    __syncthreads();
-    visit([&](int j, const uint32_t (&v)[kPage], uint32_t keep) {
+    // the lanes of the wave: six exchange rounds (both partners keep the merge)
+#pragma unroll 1
+    for (int off = 1; off < 64; off <<= 1) {
+        unsigned long long other[NEV];
 #pragma unroll
-        for (int t = 0; t < kPage; ++t) {
-            if (keep & (1u << t)) continue;
-            const unsigned long long key = ((unsigned long long)v[t] << 16) |
-                                           (unsigned long long)(0xffffu - (uint32_t)(j * kPage + t));
-            if (key <= hi) {
-                const int at = atomicAdd(&s_nev, 1);
-                if (at < nev) s_ev[at] = j * kPage + t;
-            }
-        }
-    });
+        for (int k = 0; k < NEV; ++k) other[k] = __shfl_xor(best[k], off, 64);
+        merge_keep<NEV>(best, other);
+    }
+    if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < NEV; ++k) s_wl[wave][k] = best[k];
+    }
     __syncthreads();
     if (tid == 0) {
-        int ev[kShrinkEvict];
+        for (int w = 1; w < NW; ++w) {
+            unsigned long long other[NEV];
 #pragma unroll
-        for (int k = 0; k < kShrinkEvict; ++k) ev[k] = s_ev[k] < 0 ? 0x7fffffff : s_ev[k];
-        // ascending slot order (bitonic sorting network, static indices)
+            for (int k = 0; k < NEV; ++k) other[k] = s_wl[w][k];
+            merge_keep<NEV>(best, other);
+        }
+        // the evicted slots, ascending (bitonic sorting network, static indices)
+        int ev[NEV];
 #pragma unroll
-        for (int k = 2; k <= kShrinkEvict; k <<= 1)
+        for (int k = 0; k < NEV; ++k) ev[k] = best[k] == kNoKey ? 0x7fffffff : (int)(0xffffu - (uint32_t)(best[k] & 0xffffu));
 #pragma unroll
-            for (int j = k >> 1; j > 0; j >>= 1)
+        for (int k = 2; k <= NEV; k <<= 1)
 #pragma unroll
-                for (int x = 0; x < kShrinkEvict; ++x) {
-                    const int y = x ^ j;
+            for (int jj = k >> 1; jj > 0; jj >>= 1)
+#pragma unroll
+                for (int x = 0; x < NEV; ++x) {
+                    const int y = x ^ jj;
                     if (y > x) {
                         const bool up = (x & k) == 0;
                         const int lo = ev[x] < ev[y] ? ev[x] : ev[y];
@@ -275,13 +208,15 @@ __device__ void select_tokens(const ApplyArgs &a, int i, int h, int l, int P, in
                     }
                 }
         int32_t *out = a.evict + (((size_t)l * a.Rb + i) * a.Hkv + h) * kEvictSlots + out_offset;
-        for (int k = 0; k < nev; ++k) out[k] = ev[k] == 0x7fffffff ? -1 : ev[k];
+        for (int k = 0; k < NEV; ++k) out[k] = ev[k] == 0x7fffffff ? -1 : ev[k];
     }
     __syncthreads();
 }
 
 // -------------------------------------------------------------------- pre --
-template <int D, int E>
+// SHRINK: the Shrink policy's variant, which also selects the 32 tokens a
+// shrink would evict
+template <int D, int E, bool SHRINK>
 __global__ __launch_bounds__(kSelThreads) __attribute__((amdgpu_waves_per_eu(4))) void pre_kernel(ApplyArgs a, LayerTable lt) {
     __builtin_amdgcn_s_setprio(3);   // issue ahead of co-resident decode waves
     __shared__ int s_n;
@@ -333,9 +268,10 @@ __global__ __launch_bounds__(kSelThreads) __attribute__((amdgpu_waves_per_eu(4))
     if (blockIdx.x == 0 && x == 0 && tid == 0) a.req[(size_t)i * RQ_STRIDE + RQ_SKIP] = skip ? 1 : 0;
     if (x == 0) {
         if (at_boundary && !skip) {
-            select_tokens(a, i, h, l, P, kPage, 1, 0);
-            if (a.policy == GP_POLICY_SHRINK && P - 1 >= max(a.min_cap, 2))
-                select_tokens(a, i, h, l, P, kShrinkEvict, 2, kPage);
+            select_tokens<kPage>(a, i, h, l, P, 1, 0);
+            if constexpr (SHRINK) {
+                if (P - 1 >= max(a.min_cap, 2)) select_tokens<kShrinkEvict>(a, i, h, l, P, 2, kPage);
+            }
         }
         return;
     }
@@ -373,17 +309,39 @@ __global__ __launch_bounds__(kSelThreads) __attribute__((amdgpu_waves_per_eu(4))
     if (cc0 >= cc1) return;
     const int per_cc = 2 * nbp * UPP;                 // units saved per boundary
     unsigned char *bd0 = a.border + (((size_t)l * a.Rb + i) * a.Hkv + h) * a.ncc * 2 * kBorderRows * D * E;
-    const unsigned char *pools[2] = {reinterpret_cast<const unsigned char *>(lt.k[l]),
-                                     reinterpret_cast<const unsigned char *>(lt.v[l])};
-    for (int u = tid; u < (cc1 - cc0) * per_cc; u += blockDim.x) {
-        const int cc = cc0 + u / per_cc, uu = u % per_cc;
+    const unsigned char *kpool = reinterpret_cast<const unsigned char *>(lt.k[l]);
+    const unsigned char *vpool = reinterpret_cast<const unsigned char *>(lt.v[l]);
+    // the page ids of the saved pages first (one round trip), then each
+    // thread's units in batches whose loads are all in flight before their
+    // stores (beside decode attention every round trip costs microseconds)
+    __shared__ int s_bp[kBordersPerGroup * NBP];
+    for (int k = tid; k < (cc1 - cc0) * nbp; k += blockDim.x) {
+        const int cc = cc0 + k / nbp, pg = k % nbp;
+        const int phys = row[cc * kCompactChunk / kPage - nbp + pg];
+        s_bp[k] = phys >= 0 && phys < a.pool_pages ? phys : -1;
+    }
+    __syncthreads();
+    // (four units per thread per batch, in named registers: as an array the
+    // compiler moved them to LDS)
+    const int total = (cc1 - cc0) * per_cc;
+    auto unit = [&](int u, int &at) -> const uint4 * {
+        const int uc = min(u, total - 1);
+        const int c = uc / per_cc, uu = uc % per_cc;
         const int kv = uu / (nbp * UPP), rem = uu % (nbp * UPP), pg = rem / UPP, w = rem % UPP;
-        const int lp = cc * kCompactChunk / kPage - nbp + pg;
-        const int phys = row[lp];
-        if (phys < 0 || phys >= a.pool_pages) continue;
-        const size_t src_off = (size_t)phys * a.Hkv * kPage * D * E + (size_t)h * kPage * D * E;
-        const size_t at = (((size_t)cc * 2 + kv) * NBP + (NBP - nbp + pg)) * UPP + w;
-        *reinterpret_cast<uint4 *>(bd0 + at * 16) = *reinterpret_cast<const uint4 *>(pools[kv] + src_off + (size_t)w * 16);
+        const int phys = s_bp[c * nbp + pg];
+        at = u < total && phys >= 0 ? (((cc0 + c) * 2 + kv) * NBP + (NBP - nbp + pg)) * UPP + w : -1;
+        const size_t src_off = (size_t)max(phys, 0) * a.Hkv * kPage * D * E + (size_t)h * kPage * D * E;
+        return reinterpret_cast<const uint4 *>((kv ? vpool : kpool) + src_off + (size_t)w * 16);
+    };
+    const int nt = blockDim.x;
+    for (int base = tid; base < total; base += 4 * nt) {
+        int a0, a1, a2, a3;
+        const uint4 v0 = *unit(base, a0), v1 = *unit(base + nt, a1);
+        const uint4 v2 = *unit(base + 2 * nt, a2), v3 = *unit(base + 3 * nt, a3);
+        if (a0 >= 0) *reinterpret_cast<uint4 *>(bd0 + (size_t)a0 * 16) = v0;
+        if (a1 >= 0) *reinterpret_cast<uint4 *>(bd0 + (size_t)a1 * 16) = v1;
+        if (a2 >= 0) *reinterpret_cast<uint4 *>(bd0 + (size_t)a2 * 16) = v2;
+        if (a3 >= 0) *reinterpret_cast<uint4 *>(bd0 + (size_t)a3 * 16) = v3;
     }
 }
 
@@ -764,7 +722,12 @@ hipError_t launch_de(const ApplyArgs &a, const LayerTable &lt, int stages, hipSt
     // (KV head, layer) is the fastest grid index: each head stays on one XCD
     dim3 gpre(a.Hkv * a.n_layers, 1 + max(a.npc, cdiv(a.ncc, kBordersPerGroup)), a.Rb),
         gcomp(2 * a.Hkv * a.n_layers, a.ncc, a.Rb);
-    if (stages & kStageSelect) pre_kernel<D, E><<<gpre, kSelThreads, 0, s>>>(a, lt);
+    if (stages & kStageSelect) {
+        if (a.policy == GP_POLICY_SHRINK)
+            pre_kernel<D, E, true><<<gpre, kSelThreads, 0, s>>>(a, lt);
+        else
+            pre_kernel<D, E, false><<<gpre, kSelThreads, 0, s>>>(a, lt);
+    }
     if (stages & kStageDecide) decide_kernel<<<1, 1024, 0, s>>>(a);
     if (stages & kStageCompact) compact_kernel<D, E><<<gcomp, 256, 0, s>>>(a, lt);
     return hipGetLastError();

@@ -123,7 +123,7 @@ constexpr int kPageBlock = 1024;  // pages per work item when walking a page-tab
 constexpr int kShrinkEvict = 2 * kPage;
 constexpr int kEvictSlots = kPage + kShrinkEvict;
 constexpr int kBorderRows = kShrinkEvict;
-constexpr int kBordersPerGroup = 16;  // chunk boundaries whose border rows one workgroup saves
+constexpr int kBordersPerGroup = 4;   // chunk boundaries whose border rows one workgroup saves
 
 __host__ __device__ inline ApplyWs apply_ws(int Rb, int Hkv, int D, int elem, int max_pages,
                                             int n_layers) {
