@@ -159,6 +159,9 @@ constexpr int kLogitsMaxIters = 32;
 #define GP_LOGITS_WAVES 2
 #endif
 constexpr int kLogitsWaves = GP_LOGITS_WAVES;   // waves per workgroup, sharing the summaries in LDS
+#ifndef GP_LOGITS_TARGET_WAVES
+#define GP_LOGITS_TARGET_WAVES 16384
+#endif
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(64 * kLogitsWaves) void logits_kernel(ScoreArgs a) {
@@ -717,7 +720,7 @@ hipError_t launch_gd(int G, const ScoreArgs &a, int stages, hipStream_t s) {
     // block each when they are short
     ScoreArgs b = a;
     const int nblocks = a.Hkv * a.nch * a.Rb;
-    b.lg_iters = std::min(kLogitsMaxIters, std::max(1, cdiv(nblocks, 16384)));
+    b.lg_iters = std::min(kLogitsMaxIters, std::max(1, cdiv(nblocks, GP_LOGITS_TARGET_WAVES)));
     dim3 g1(a.Hkv, cdiv(cdiv(a.nch, b.lg_iters), kLogitsWaves), a.Rb), g2(a.Hkv, cdiv(a.cmax, kProbChunk), a.Rb), g3(a.Hkv, 2, a.Rb);
     const bool weights = stages & GP_SCORE_WEIGHTS, counts = stages & GP_SCORE_COUNTS;
     if (a.cmax == 0) {
