@@ -906,11 +906,11 @@ def _full_size_check(w, n_sample, seed=0):
 
 @pytest.mark.parametrize("name", ["qwen3_8b", "high_concurrency", "prefix_shared", "long_reasoning"])
 def test_full_size_sampled(name):
-    """The four large workloads at their full shapes (the long-reasoning one
-    with 6 of its 32 requests, at full lengths: generating all 32 takes most of
-    a minute).  qwen3_8b is exactly the benchmark's input."""
+    """The four large workloads at their full shapes, every boundary event in
+    full (all 32 requests of the long-reasoning one); each is exactly the
+    benchmark's input for that workload."""
     _say(f"full {name}: generating inputs")
-    w = W.long_reasoning(num_reqs=6) if name == "long_reasoning" else W.make(name)
+    w = W.make(name)
     _full_size_check(w, n_sample=6)
 
 
