@@ -422,8 +422,8 @@ __device__ inline float row_sum16(float x) {
 // the vector ALUs, each lane owning D/64 head dimensions for all 16 tokens of
 // the page (accumulators G * D / 64 registers).  The waves merge through LDS
 // at the end.
-// MODE 0: decode attention; 1: gp_decode_step (summaries and/or the new token
-// folded in); 2: the private tails of gp_decode_attention_shared (a request
+// MODE 0: decode attention; 1: gp_decode_step with the step's new token (its
+// summary update is in the merge pass); 2: the private tails of gp_decode_attention_shared (a request
 // that reads its group's shared prefix pass covers the pages after the prefix
 // only, and its partials follow the prefix's).
 template <int D, int G, int MODE>
@@ -437,7 +437,6 @@ __global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_
     constexpr int GI = G < 4 ? G : 4;     // heads per lane row
     constexpr int NW = kDecodeWaves;
     constexpr int NT = 64 * NW;
-    constexpr int FE = STEP ? (G * D + NT - 1) / NT : 1;   // summary elements per thread
     constexpr int UPP = kPage * D / 8;                // 16-byte units of one page of one head (keys or values)
     constexpr int STAGE_BYTES = NW * 2 * UPP * 16, MERGE_BYTES = NW * G * D * 4;
     __shared__ float s_m[NW][G], s_l[NW][G];
@@ -501,54 +500,6 @@ __global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_
     const StepView sv = step_view(a, r, m_in);
     const int CHUNK = a.chunk_pages * kPage;
 
-    // gp_decode_step: the summaries of query heads [h G, h G + G) are updated
-    // by the first chunk's workgroup (with a new token: only if the request
-    // takes it).  The slot is looked up here; the old values and the query are
-    // requested when the workgroup's pages are done (held in registers across
-    // the page loop they would push it past its register budget), and the
-    // update is stored when the workgroup ends.
-    float f_q[FE], f_s[FE], f_l[FE];
-    float *fS = nullptr;
-    bool f_init = false;
-    if constexpr (STEP) {
-        if (chunk == 0 && a.qstate && (a.k_new == nullptr || sv.room)) {
-            const int slot = a.slot_ids[r];
-            if (slot >= 0 && slot < a.M) {
-                fS = a.qstate + (size_t)slot * 2 * Hq * D + (size_t)h * G * D;
-                f_init = a.init[r] != 0;
-            }
-        }
-    }
-    auto load_fold = [&]() {
-        if constexpr (STEP) {
-            if (fS) {
-                const uint16_t *qp = reinterpret_cast<const uint16_t *>(a.q_pre) + ((size_t)r * Hq + (size_t)h * G) * D;
-#pragma unroll
-                for (int e = 0; e < FE; ++e) {
-                    const int i = min(tid + e * NT, G * D - 1);
-                    f_q[e] = bf16_to_f32(qp[i]);
-                    f_s[e] = fS[i];
-                    f_l[e] = fS[(size_t)Hq * D + i];
-                }
-            }
-        }
-    };
-    auto finish_fold = [&]() {
-        if constexpr (STEP) {
-            if (fS) {
-                const double cs_ = 1.0 - a.beta_s, cl_ = 1.0 - a.beta_l;
-#pragma unroll
-                for (int e = 0; e < FE; ++e) {
-                    const int i = tid + e * NT;
-                    if (i < G * D) {
-                        fS[i] = f_init ? f_q[e] : ema_step(f_s[e], f_q[e], a.beta_s, cs_);
-                        fS[(size_t)Hq * D + i] = f_init ? f_q[e] : ema_step(f_l[e], f_q[e], a.beta_l, cl_);
-                    }
-                }
-            }
-        }
-    };
-
     const int m = sv.m_attn;
     const int mt = m - base_page * kPage;         // tokens this pass covers
     const int nchunks = cdiv(mt, CHUNK);
@@ -557,8 +508,6 @@ __global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_
     if (mt == 0) {
         if (chunk == 0 && !pmatch)
             for (int i = tid; i < G * D; i += blockDim.x) out[i] = 0;
-        load_fold();
-        finish_fold();
         return;
     }
     if (chunk >= nchunks) return;
@@ -894,7 +843,6 @@ __global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_
     } else {
         for (; p < page_end; p += NW) page(p, phys);
     }
-    load_fold();          // (in flight while the waves merge)
 
     // merge the waves: per-wave (max, sum) of each head, o of every dim (o
     // goes where the stages were, once every wave is done with them)
@@ -956,7 +904,6 @@ __global__ __launch_bounds__(64 * kDecodeWaves) __attribute__((amdgpu_waves_per_
             }
         }
     }
-    finish_fold();
 }
 
 // Second pass for requests that span several chunks: one workgroup per
@@ -974,6 +921,58 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
     const int h = blockIdx.x, r = blockIdx.y;
     const int tid = threadIdx.x;
     const int kmax = a.max_chunks + (a.ngroups > 0 ? 1 : 0);   // slots any request can fill
+
+    // gp_decode_step, bfloat16: the summaries of query heads [h G, h G + G)
+    // are updated here (Sec. 4.1) rather than in the chunk pass, where the
+    // memory round trip it adds lengthened the workgroups that end the grid.
+    // The slot is requested first, the query and the old values after the
+    // partials (one more round trip at most), and the update is stored after
+    // the output.  A held request, or with a new token one without room, keeps
+    // its summaries, as in the float32 kernel.
+    constexpr bool FOLD = sizeof(T) == 2;
+    constexpr int FE = (G * D + 255) / 256;          // summary elements per thread
+    float f_q[FE], f_s[FE], f_l[FE];
+    float *fS = nullptr;
+    int f_slot = -1;
+    bool f_init = false;
+    if constexpr (FOLD) {
+        if (a.qstate) {
+            f_slot = a.slot_ids[r];
+            f_init = a.init[r] != 0;
+        }
+    }
+    auto load_fold = [&]() {
+        if constexpr (FOLD) {
+            if (a.qstate && f_slot >= 0 && f_slot < a.M) {
+                const size_t Hq = (size_t)a.Hkv * G;
+                const uint16_t *qp = reinterpret_cast<const uint16_t *>(a.q_pre) + ((size_t)r * Hq + (size_t)h * G) * D;
+                fS = a.qstate + (size_t)f_slot * 2 * Hq * D + (size_t)h * G * D;
+#pragma unroll
+                for (int e = 0; e < FE; ++e) {
+                    const int i = min(tid + 256 * e, G * D - 1);
+                    f_q[e] = bf16_to_f32(qp[i]);
+                    f_s[e] = fS[i];
+                    f_l[e] = fS[Hq * D + i];
+                }
+            }
+        }
+    };
+    auto fold = [&](int took) {
+        if constexpr (FOLD) {
+            if (fS && (a.k_new == nullptr || took)) {
+                const size_t Hq = (size_t)a.Hkv * G;
+                const double cs_ = 1.0 - a.beta_s, cl_ = 1.0 - a.beta_l;
+#pragma unroll
+                for (int e = 0; e < FE; ++e) {
+                    const int i = tid + 256 * e;
+                    if (i < G * D) {
+                        fS[i] = f_init ? f_q[e] : ema_step(f_s[e], f_q[e], a.beta_s, cs_);
+                        fS[Hq * D + i] = f_init ? f_q[e] : ema_step(f_l[e], f_q[e], a.beta_l, cl_);
+                    }
+                }
+            }
+        }
+    };
     if (kmax <= kFastMerge) {
         // few slots: every thread requests its elements of every slot a
         // request can fill together with the lengths (one round trip; the
@@ -998,13 +997,17 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
                 }
             }
         }
+        load_fold();
         const int m = a.lens[r], took = a.lens[a.R + r], nslots = a.lens[2 * a.R + r];
         if (m < 0) return;
         if (a.advance && h == 0 && tid == 0 && took) {
             a.seq_lens_w[r] = m;
             if (a.positions) a.positions[r] += 1;
         }
-        if (nslots == 0) return;
+        if (nslots == 0) {
+            fold(took);
+            return;
+        }
         T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * a.Hkv * G + (size_t)h * G) * D;
 #pragma unroll
         for (int e = 0; e < EPT; ++e) {
@@ -1025,19 +1028,25 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
             }
             if (i < G * D) Tr::store(out + i, L > 0.0f ? Os / L : 0.0f);
         }
+        fold(took);
         return;
     }
     // tokens attended and partial slots, as the chunk pass recorded them
     // (-1: held; 0 slots: the chunk pass wrote the output)
+    load_fold();
     const int m = a.lens[r];
     if (m < 0) return;
-    if (a.advance && h == 0 && threadIdx.x == 0 && a.lens[a.R + r]) {
+    const int took = a.lens[a.R + r];
+    if (a.advance && h == 0 && threadIdx.x == 0 && took) {
         // gp_decode_step: the request took the step's token
         a.seq_lens_w[r] = m;
         if (a.positions) a.positions[r] += 1;
     }
     const int nchunks = a.lens[2 * a.R + r];
-    if (nchunks == 0) return;
+    if (nchunks == 0) {
+        fold(took);
+        return;
+    }
     const int Hq = a.Hkv * G;
     T *out = reinterpret_cast<T *>(a.out) + ((size_t)r * Hq + (size_t)h * G) * D;
     const float *base = a.partial + ((size_t)r * a.Hkv + h) * a.slots * G * (D + 2);
@@ -1072,6 +1081,7 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
             }
             Tr::store(out + (size_t)g * D + dd, L > 0.0f ? Os / L : 0.0f);
         }
+        fold(took);
         return;
     }
     // all (max, sum) pairs at once, then one thread per head folds them
@@ -1102,6 +1112,7 @@ __global__ __launch_bounds__(256) void merge_kernel(DecodeArgs a) {
         for (int k = 0; k < nc; ++k) Os += base[((size_t)k * G + g) * (D + 2) + dd] * s_f[k][g];
         Tr::store(out + (size_t)g * D + dd, Os);
     }
+    fold(took);
 }
 
 // ---------------------------------------------------------------------------
@@ -1327,14 +1338,17 @@ template <typename T, int D>
 hipError_t launch_g(int G, const DecodeArgs &a, dim3 grid, int stages, hipStream_t s) {
     dim3 mgrid(a.Hkv, a.R);
     constexpr bool bf16 = sizeof(T) == 2;
-    // the step variant (summaries and/or the new token folded in) and the
-    // tails of the shared-prefix decode are their own instantiations, so plain
-    // decode attention carries none of their code
-    const int mode = a.ngroups > 0 ? 2 : (a.qstate != nullptr || a.k_new != nullptr) ? 1 : 0;
-    // the merge pass also advances the lengths when a token went in, and folds
-    // the prefix partials of a shared-prefix call
+    // the step variant with a new token and the tails of the shared-prefix
+    // decode are their own instantiations, so plain decode attention carries
+    // none of their code (a step call's summary update is in the merge pass:
+    // without a new token its chunk pass is plain decode attention)
+    const int mode = a.ngroups > 0 ? 2 : a.k_new != nullptr ? 1 : 0;
+    // the merge pass also advances the lengths when a token went in, updates
+    // the summaries of a bfloat16 step call, and folds the prefix partials of a
+    // shared-prefix call
     const bool chunks = stages & GP_DECODE_CHUNKS, prefix = (stages & GP_DECODE_PREFIX) && mode == 2,
-               merge = (stages & GP_DECODE_MERGE) && (a.max_chunks > 1 || (a.k_new && a.advance) || mode == 2);
+               merge = (stages & GP_DECODE_MERGE) &&
+                       (a.max_chunks > 1 || (a.k_new && a.advance) || mode == 2 || (bf16 && a.qstate));
     // prefix pass grid: (KV head, prefix chunk, request block)
     int max_pc = 0;
     for (int g = 0; g < a.ngroups; ++g) max_pc = max(max_pc, cdiv(a.g_pages[g], a.chunk_pages));
